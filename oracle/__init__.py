@@ -1,0 +1,237 @@
+"""Oracle for the microscaled-FP4 linear layer -- TEST INFRASTRUCTURE ONLY.
+
+A ctypes front end to ``reqat_oracle.c`` (plain single-threaded C, FP64,
+exact decisions).  Only the test suite, the smoke check and the benchmark's
+CPU-baseline leg may import this package; the GPU library never does, and
+this package imports nothing from it.
+
+Formats and readings: see the header of ``reqat_oracle.c`` (ReQAT App. A,
+Tab. mx_configs; the E2M1 layout of Sec. 1).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+FMT_NVFP4 = 0
+FMT_MXFP4 = 1
+BLOCK = {FMT_NVFP4: 16, FMT_MXFP4: 32}
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "reqat_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lock = threading.Lock()
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc -O2 (no OpenMP, no intrinsics)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-ffp-contract=off",
+                               "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        build(force=False)
+        lib = ctypes.CDLL(_LIB)
+        u8p = ctypes.POINTER(ctypes.c_uint8)
+        u16p = ctypes.POINTER(ctypes.c_uint16)
+        dp = ctypes.POINTER(ctypes.c_double)
+        i64 = ctypes.c_int64
+        i64p = ctypes.POINTER(ctypes.c_int64)
+        sig = {
+            "orc_e2m1_value": (ctypes.c_double, [ctypes.c_uint8]),
+            "orc_e4m3_value": (ctypes.c_double, [ctypes.c_uint8]),
+            "orc_e8m0_value": (ctypes.c_double, [ctypes.c_uint8]),
+            "orc_bf16_value": (ctypes.c_double, [ctypes.c_uint16]),
+            "orc_bf16_from_double": (ctypes.c_uint16, [ctypes.c_double]),
+            "orc_mx_scale_byte": (ctypes.c_uint8, [ctypes.c_double]),
+            "orc_nv_global_scale": (ctypes.c_float, [ctypes.c_double]),
+            "orc_nv_scale_byte": (ctypes.c_uint8, [ctypes.c_double, ctypes.c_double]),
+            "orc_e2m1_encode": (ctypes.c_uint8, [ctypes.c_double, ctypes.c_double]),
+            "orc_tensor_amax": (ctypes.c_double, [u16p, i64, i64, i64]),
+            "orc_quantize": (ctypes.c_int, [ctypes.c_int, u16p, i64, i64, i64, u8p, u8p, ctypes.c_double]),
+            "orc_dequantize": (None, [ctypes.c_int, u8p, u8p, ctypes.c_double, i64, i64, dp]),
+            "orc_fakequant": (ctypes.c_int, [ctypes.c_int, u16p, i64, i64, i64, u16p, i64,
+                                             ctypes.c_double, u8p, u8p]),
+            "orc_gemm_rows": (None, [ctypes.c_int, i64, i64, i64, u8p, u8p, ctypes.c_double,
+                                     u8p, u8p, ctypes.c_double, i64, i64, dp]),
+            "orc_gemm_points": (None, [ctypes.c_int, i64, u8p, u8p, ctypes.c_double,
+                                       u8p, u8p, ctypes.c_double, i64p, i64p, i64, dp, dp]),
+            "orc_e2m1_encode_array": (None, [dp, i64, ctypes.c_double, u8p]),
+            "orc_bf16_from_double_array": (None, [dp, i64, u16p]),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(lib, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = lib
+        return lib
+
+
+def _p(a: np.ndarray, ctype):
+    return a.ctypes.data_as(ctypes.POINTER(ctype))
+
+
+# ----------------------------------------------------------------- scalars
+
+def e2m1_value(code: int) -> float:
+    return _load().orc_e2m1_value(code)
+
+
+def e4m3_value(b: int) -> float:
+    return _load().orc_e4m3_value(b)
+
+
+def e8m0_value(b: int) -> float:
+    return _load().orc_e8m0_value(b)
+
+
+def bf16_value(h: int) -> float:
+    return _load().orc_bf16_value(h)
+
+
+def bf16_from_double(v: float) -> int:
+    return _load().orc_bf16_from_double(v)
+
+
+def mx_scale_byte(amax: float) -> int:
+    return _load().orc_mx_scale_byte(amax)
+
+
+def nv_global_scale(amax: float) -> float:
+    return _load().orc_nv_global_scale(amax)
+
+
+def nv_scale_byte(amax: float, g: float) -> int:
+    return _load().orc_nv_scale_byte(amax, g)
+
+
+def e2m1_encode(x: float, S: float) -> int:
+    return _load().orc_e2m1_encode(x, S)
+
+
+def e2m1_encode_array(x: np.ndarray, S: float) -> np.ndarray:
+    """E2M1 codes (sign included) of each x[i] / S."""
+    x = np.ascontiguousarray(x, np.float64)
+    out = np.empty(x.shape, np.uint8)
+    _load().orc_e2m1_encode_array(_p(x, ctypes.c_double), x.size, S, _p(out, ctypes.c_uint8))
+    return out
+
+
+def bf16_from_double_array(v: np.ndarray) -> np.ndarray:
+    v = np.ascontiguousarray(v, np.float64)
+    out = np.empty(v.shape, np.uint16)
+    _load().orc_bf16_from_double_array(_p(v, ctypes.c_double), v.size, _p(out, ctypes.c_uint16))
+    return out
+
+
+# ----------------------------------------------------------------- tensors
+
+def _as_u16(x: np.ndarray) -> np.ndarray:
+    x = np.ascontiguousarray(x)
+    if x.dtype != np.uint16:
+        raise TypeError("oracle takes bfloat16 bit patterns as uint16")
+    if x.ndim != 2:
+        raise ValueError("2-D input expected")
+    return x
+
+
+def tensor_amax(x: np.ndarray) -> float:
+    x = _as_u16(x)
+    return _load().orc_tensor_amax(_p(x, ctypes.c_uint16), x.shape[0], x.shape[1], x.shape[1])
+
+
+def global_scale(fmt: int, x: np.ndarray, given: float | None = None) -> float:
+    """NVFP4: the given global scale, or the computed power of two.  MXFP4: 1."""
+    if fmt == FMT_MXFP4:
+        return 1.0
+    if given is not None:
+        return float(np.float32(given))
+    return float(nv_global_scale(tensor_amax(x)))
+
+
+def quantize(fmt: int, x: np.ndarray, g: float | None = None):
+    """Return (codes uint8 [R, C/2], scales uint8 [R, C/B], g float)."""
+    x = _as_u16(x)
+    R, C = x.shape
+    B = BLOCK[fmt]
+    if C % B:
+        raise ValueError("cols must be a multiple of the block size")
+    g = global_scale(fmt, x, g)
+    codes = np.zeros((R, C // 2), np.uint8)
+    scales = np.zeros((R, C // B), np.uint8)
+    rc = _load().orc_quantize(fmt, _p(x, ctypes.c_uint16), R, C, C,
+                              _p(codes, ctypes.c_uint8), _p(scales, ctypes.c_uint8), g)
+    assert rc == 0
+    return codes, scales, g
+
+
+def dequantize(fmt: int, codes: np.ndarray, scales: np.ndarray, g: float) -> np.ndarray:
+    codes = np.ascontiguousarray(codes, np.uint8)
+    scales = np.ascontiguousarray(scales, np.uint8)
+    R, C = codes.shape[0], codes.shape[1] * 2
+    out = np.empty((R, C), np.float64)
+    _load().orc_dequantize(fmt, _p(codes, ctypes.c_uint8), _p(scales, ctypes.c_uint8), g, R, C,
+                           _p(out, ctypes.c_double))
+    return out
+
+
+def fakequant(fmt: int, x: np.ndarray, g: float | None = None):
+    """Return (y bfloat16 bits uint16 [R, C], g)."""
+    x = _as_u16(x)
+    R, C = x.shape
+    B = BLOCK[fmt]
+    g = global_scale(fmt, x, g)
+    y = np.zeros((R, C), np.uint16)
+    ct = np.zeros((R, C // 2), np.uint8)
+    st = np.zeros((R, C // B), np.uint8)
+    rc = _load().orc_fakequant(fmt, _p(x, ctypes.c_uint16), R, C, C, _p(y, ctypes.c_uint16), C, g,
+                               _p(ct, ctypes.c_uint8), _p(st, ctypes.c_uint8))
+    assert rc == 0
+    return y, g
+
+
+def gemm(fmt, a_codes, a_scales, ga, b_codes, b_scales, gb, rows=None) -> np.ndarray:
+    """FP64 Y[m, n] = sum_k A^[m, k] B^[n, k] (rows = optional (m0, m1) slice)."""
+    a_codes = np.ascontiguousarray(a_codes, np.uint8)
+    b_codes = np.ascontiguousarray(b_codes, np.uint8)
+    a_scales = np.ascontiguousarray(a_scales, np.uint8)
+    b_scales = np.ascontiguousarray(b_scales, np.uint8)
+    M, K = a_codes.shape[0], a_codes.shape[1] * 2
+    N = b_codes.shape[0]
+    m0, m1 = rows if rows is not None else (0, M)
+    y = np.empty((m1 - m0, N), np.float64)
+    _load().orc_gemm_rows(fmt, M, N, K, _p(a_codes, ctypes.c_uint8), _p(a_scales, ctypes.c_uint8), ga,
+                          _p(b_codes, ctypes.c_uint8), _p(b_scales, ctypes.c_uint8), gb, m0, m1,
+                          _p(y, ctypes.c_double))
+    return y
+
+
+def gemm_points(fmt, a_codes, a_scales, ga, b_codes, b_scales, gb, ms, ns):
+    """FP64 Y at the (ms[i], ns[i]) pairs, and sum_k |A^ B^| at each."""
+    a_codes = np.ascontiguousarray(a_codes, np.uint8)
+    b_codes = np.ascontiguousarray(b_codes, np.uint8)
+    a_scales = np.ascontiguousarray(a_scales, np.uint8)
+    b_scales = np.ascontiguousarray(b_scales, np.uint8)
+    ms = np.ascontiguousarray(ms, np.int64)
+    ns = np.ascontiguousarray(ns, np.int64)
+    K = a_codes.shape[1] * 2
+    y = np.empty(len(ms), np.float64)
+    ay = np.empty(len(ms), np.float64)
+    _load().orc_gemm_points(fmt, K, _p(a_codes, ctypes.c_uint8), _p(a_scales, ctypes.c_uint8), ga,
+                            _p(b_codes, ctypes.c_uint8), _p(b_scales, ctypes.c_uint8), gb,
+                            _p(ms, ctypes.c_int64), _p(ns, ctypes.c_int64), len(ms),
+                            _p(y, ctypes.c_double), _p(ay, ctypes.c_double))
+    return y, ay

@@ -1,0 +1,353 @@
+/*
+ * reqat_oracle.c -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, single-threaded CPU statement of what the microscaled-FP4
+ * linear layer computes: E2M1 element codes with per-block scales (MXFP4 and
+ * NVFP4), the quantize-dequantize ("fake-quant") output, and the block-scaled
+ * FP4 x FP4 product.  Only the test suite, the smoke check and the CPU
+ * baseline leg of the benchmark may load this file's library.  It shares no
+ * code, header, table or constant with the GPU library, and the GPU library
+ * never calls it.
+ *
+ * Formats follow the ReQAT paper, App. A ("Microscaling Formats",
+ * Tab. mx_configs) and the E2M1 layout named in its Sec. 1 (Introduction):
+ *   MXFP4: E2M1 elements, E8M0 block scale, block of 32, no global scale.
+ *   NVFP4: E2M1 elements, E4M3 block scale, block of 16, FP32 global scale.
+ * The paper states no rounding, scale-selection or layout rule; the readings
+ * used here are listed with each function (and in the design notes):
+ *   - blocks run along the contiguous (reduction) dimension;
+ *   - element rounding is round-to-nearest, ties to the even code, of the
+ *     exact quotient |x| / (block scale * global scale), saturating at 6;
+ *   - the block scale is the SMALLEST representable scale with
+ *     block_absmax <= 6 * scale * global  ("ceil" rule), so no element clips;
+ *   - the computed NVFP4 global scale is the smallest power of two 2^k,
+ *     k >= -126, with tensor_absmax <= 6 * 448 * 2^k;
+ *   - a block holding NaN or Inf gets a NaN scale and zero codes;
+ *   - codes are packed two per byte, element 2i in bits 3:0.
+ * Arithmetic is FP64 throughout, and every product formed is exact in FP64
+ * (at most 30 significant bits), so every decision below is the decision of
+ * exact real arithmetic.
+ *
+ * Parity status: every function here is pinned by a CPU test against an
+ * independent statement (brute-force nearest search, torch's float8 and
+ * bfloat16 conversions, closed forms, numpy matmul).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#define ORC_FMT_NVFP4 0
+#define ORC_FMT_MXFP4 1
+
+/* ---------- element and scale formats (App. A, Tab. mx_configs) ---------- */
+
+/* E2M1: sign bit 3, exponent bits 2:1 (bias 1), mantissa bit 0.
+ * Exponent field 0 is subnormal: value = 0.5 * mantissa. */
+double orc_e2m1_value(uint8_t code)
+{
+    int s = (code >> 3) & 1, e = (code >> 1) & 3, m = code & 1;
+    double mag = (e == 0) ? 0.5 * m : ldexp(1.0 + 0.5 * m, e - 1);
+    return s ? -mag : mag;
+}
+
+/* E4M3 as in the OCP FP8 "E4M3FN" encoding: bias 7, no infinities,
+ * S.1111.111 is NaN, largest finite 448, smallest subnormal 2^-9. */
+double orc_e4m3_value(uint8_t b)
+{
+    int s = b >> 7, e = (b >> 3) & 15, m = b & 7;
+    double mag;
+    if (e == 15 && m == 7) return NAN;
+    mag = (e == 0) ? ldexp((double)m, -9) : ldexp(1.0 + m / 8.0, e - 7);
+    return s ? -mag : mag;
+}
+
+/* E8M0: an exponent only, value 2^(b - 127); 0xFF is NaN. */
+double orc_e8m0_value(uint8_t b)
+{
+    if (b == 0xFF) return NAN;
+    return ldexp(1.0, (int)b - 127);
+}
+
+/* bfloat16 bit pattern -> value (exact). */
+double orc_bf16_value(uint16_t h)
+{
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return (double)f;
+}
+
+/* Round a double to bfloat16, nearest with ties to even, with gradual
+ * underflow and overflow to infinity.  Written from the IEEE-754 definition:
+ * find the two neighbouring bfloat16 values and pick the nearer one. */
+uint16_t orc_bf16_from_double(double v)
+{
+    uint16_t sign;
+    double a, q, lo, r;
+    int ex;
+    if (isnan(v)) return 0x7FC0;
+    sign = signbit(v) ? 0x8000 : 0x0000;
+    a = fabs(v);
+    if (a == 0.0) return sign;
+    /* bfloat16: 8 significant bits, exponent range of binary32.  The spacing
+     * of representable values around a is 2^(max(floor(log2 a), -126) - 7). */
+    frexp(a, &ex);               /* a = f * 2^ex, f in [0.5, 1) */
+    ex -= 1;                     /* a in [2^ex, 2^(ex+1)) */
+    if (ex < -126) ex = -126;
+    q = ldexp(1.0, ex - 7);      /* spacing */
+    lo = floor(a / q);           /* exact: a/q is a scaling by a power of two */
+    r = a / q - lo;              /* exact */
+    if (r > 0.5 || (r == 0.5 && fmod(lo, 2.0) != 0.0)) lo += 1.0;
+    a = lo * q;
+    if (a >= ldexp(1.0, 128)) return sign | 0x7F80;   /* overflow -> inf */
+    {
+        float f = (float)a;      /* exact: a has at most 8 significant bits */
+        uint32_t u;
+        memcpy(&u, &f, 4);
+        return sign | (uint16_t)((u >> 16) & 0x7FFF);
+    }
+}
+
+/* ---------- scale rules ---------- */
+
+/* MXFP4 block scale, "ceil" reading: the smallest e in [-127, 127] with
+ * amax <= 6 * 2^e.  Closed form: with amax = 1.f * 2^E, 6 * 2^(E-2) = 1.5 * 2^E,
+ * so e = E - 2 when 1.f <= 1.5 and E - 1 otherwise.  Returns the E8M0 byte. */
+uint8_t orc_mx_scale_byte(double amax)
+{
+    int ex, e;
+    double f;
+    if (isnan(amax) || isinf(amax)) return 0xFF;
+    if (amax == 0.0) return 0x00;
+    f = frexp(amax, &ex);        /* amax = f * 2^ex, f in [0.5,1); 1.f = 2f, E = ex-1 */
+    e = (2.0 * f <= 1.5) ? (ex - 1) - 2 : (ex - 1) - 1;
+    if (e < -127) e = -127;
+    if (e > 127) e = 127;
+    return (uint8_t)(e + 127);
+}
+
+/* NVFP4 computed global scale: g = 2^k with k the smallest integer >= -126
+ * such that amax <= 6 * 448 * 2^k = 2688 * 2^k.  2688 = 1.3125 * 2^11, so with
+ * amax = 1.f * 2^E, k = E - 11 when 1.f <= 1.3125, else E - 10.  A tensor with
+ * no nonzero finite value gets g = 1. */
+float orc_nv_global_scale(double amax)
+{
+    int ex, k;
+    double f;
+    if (!(amax > 0.0) || isinf(amax)) return 1.0f;
+    f = frexp(amax, &ex);
+    k = (2.0 * f <= 1.3125) ? (ex - 1) - 11 : (ex - 1) - 10;
+    if (k < -126) k = -126;
+    return (float)ldexp(1.0, k);
+}
+
+/* Ascending table of the 126 positive finite E4M3 values and their bytes. */
+static double e4m3_pos_val[126];
+static uint8_t e4m3_pos_byte[126];
+static int e4m3_ready = 0;
+static void e4m3_init(void)
+{
+    int n = 0, b;
+    if (e4m3_ready) return;
+    for (b = 0x01; b <= 0x7E; b++) {       /* positive bytes are monotone in value */
+        e4m3_pos_val[n] = orc_e4m3_value((uint8_t)b);
+        e4m3_pos_byte[n] = (uint8_t)b;
+        n++;
+    }
+    e4m3_ready = 1;
+}
+
+/* NVFP4 block scale, "ceil" reading: the smallest positive finite E4M3 value
+ * s with amax <= 6 * s * g.  amax == 0 gives byte 0x00.  When even s = 448 is
+ * too small (only possible with a caller-chosen g), 448 is used and the
+ * elements saturate.
+ * Computed as the first E4M3 value >= q = amax / (6 g).  The FP64 quotient is
+ * within 2^-53 (relative) of the true one, while the true quotient is either
+ * exactly an E4M3 value v (then FP64 returns v exactly) or at least 2^-31 away
+ * from every such v (amax has 8 significant bits and 6 v g at most 30), so the
+ * search on the rounded quotient finds the same value as on the true one. */
+uint8_t orc_nv_scale_byte(double amax, double g)
+{
+    int i;
+    double q;
+    if (isnan(amax) || isinf(amax)) return 0x7F;
+    if (amax == 0.0) return 0x00;
+    e4m3_init();
+    q = amax / (6.0 * g);
+    for (i = 0; i < 126 && e4m3_pos_val[i] < q; i++) {}
+    if (i >= 126) return 0x7E;  /* above 448: saturate */
+    return e4m3_pos_byte[i];
+}
+
+/* ---------- element rounding ---------- */
+
+/* E2M1 magnitude code of |x| / S, round to nearest with ties to the even code,
+ * saturating at 6.  Decided by exact comparisons of |x| with the midpoints
+ * between neighbouring grid values times S (each product exact in FP64). */
+static int e2m1_mag_code(double ax, double S)
+{
+    static const double mid[7] = {0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0};
+    int i;
+    for (i = 0; i < 7; i++) {
+        double t = mid[i] * S;
+        if (ax < t) return i;
+        if (ax == t) return (i % 2 == 0) ? i : i + 1;   /* tie: the even code */
+    }
+    return 7;
+}
+
+/* Full E2M1 code (sign copied from x, also for magnitude 0). */
+uint8_t orc_e2m1_encode(double x, double S)
+{
+    int m = (S > 0.0) ? e2m1_mag_code(fabs(x), S) : 0;
+    return (uint8_t)((signbit(x) ? 8 : 0) | m);
+}
+
+/* ---------- tensor operations ---------- */
+
+static int block_of(int fmt) { return fmt == ORC_FMT_MXFP4 ? 32 : 16; }
+
+/* Largest finite |x| over a rows x cols bfloat16 matrix (row stride ldx). */
+double orc_tensor_amax(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx)
+{
+    double m = 0.0;
+    int64_t r, c;
+    for (r = 0; r < rows; r++)
+        for (c = 0; c < cols; c++) {
+            double v = fabs(orc_bf16_value(x[r * ldx + c]));
+            if (!isnan(v) && !isinf(v) && v > m) m = v;
+        }
+    return m;
+}
+
+/* Quantize a rows x cols bfloat16 matrix along its rows.
+ *   codes : rows x cols/2 bytes, element 2i in bits 3:0 of byte i
+ *   scales: rows x cols/B bytes (E8M0 for MXFP4, E4M3 for NVFP4)
+ *   g     : NVFP4 global scale (ignored for MXFP4); the caller computes it
+ *           with orc_nv_global_scale or chooses it.
+ * Returns 0, or -1 when cols is not a multiple of the block size. */
+int orc_quantize(int fmt, const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                 uint8_t *codes, uint8_t *scales, double g)
+{
+    int B = block_of(fmt);
+    int64_t r, b, j, nb;
+    if (cols % B) return -1;
+    nb = cols / B;
+    for (r = 0; r < rows; r++) {
+        for (b = 0; b < nb; b++) {
+            const uint16_t *xb = x + r * ldx + b * B;
+            double amax = 0.0, S;
+            int bad = 0;
+            uint8_t sb;
+            for (j = 0; j < B; j++) {
+                double v = orc_bf16_value(xb[j]);
+                if (isnan(v) || isinf(v)) bad = 1;
+                else if (fabs(v) > amax) amax = fabs(v);
+            }
+            if (bad) sb = (fmt == ORC_FMT_MXFP4) ? 0xFF : 0x7F;
+            else sb = (fmt == ORC_FMT_MXFP4) ? orc_mx_scale_byte(amax) : orc_nv_scale_byte(amax, g);
+            scales[r * nb + b] = sb;
+            S = (fmt == ORC_FMT_MXFP4) ? orc_e8m0_value(sb) : orc_e4m3_value(sb) * g;
+            for (j = 0; j < B; j++) {
+                uint8_t c = bad ? 0 : orc_e2m1_encode(orc_bf16_value(xb[j]), S);
+                int64_t k = b * B + j;
+                uint8_t *p = &codes[r * (cols / 2) + k / 2];
+                if (k % 2 == 0) *p = (uint8_t)((*p & 0xF0) | c);
+                else *p = (uint8_t)((*p & 0x0F) | (c << 4));
+            }
+        }
+    }
+    return 0;
+}
+
+/* Dequantized value of element (r, k) from codes/scales/g. */
+static double deq(int fmt, const uint8_t *codes, const uint8_t *scales, double g,
+                  int64_t cols, int64_t r, int64_t k)
+{
+    int B = block_of(fmt);
+    uint8_t byte = codes[r * (cols / 2) + k / 2];
+    uint8_t c = (k % 2 == 0) ? (byte & 0xF) : (byte >> 4);
+    uint8_t sb = scales[r * (cols / B) + k / B];
+    double S = (fmt == ORC_FMT_MXFP4) ? orc_e8m0_value(sb) : orc_e4m3_value(sb) * g;
+    return orc_e2m1_value(c) * S;
+}
+
+/* Dequantize to doubles (rows x cols, dense). */
+void orc_dequantize(int fmt, const uint8_t *codes, const uint8_t *scales, double g,
+                    int64_t rows, int64_t cols, double *out)
+{
+    int64_t r, k;
+    for (r = 0; r < rows; r++)
+        for (k = 0; k < cols; k++)
+            out[r * cols + k] = deq(fmt, codes, scales, g, cols, r, k);
+}
+
+/* Fake-quant (the QAT forward's quantize-dequantize): quantize, then round
+ * each dequantized value once to bfloat16.  y has row stride ldy. */
+int orc_fakequant(int fmt, const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                  uint16_t *y, int64_t ldy, double g, uint8_t *codes_tmp, uint8_t *scales_tmp)
+{
+    int64_t r, k;
+    if (orc_quantize(fmt, x, rows, cols, ldx, codes_tmp, scales_tmp, g)) return -1;
+    for (r = 0; r < rows; r++)
+        for (k = 0; k < cols; k++)
+            y[r * ldy + k] = orc_bf16_from_double(deq(fmt, codes_tmp, scales_tmp, g, cols, r, k));
+    return 0;
+}
+
+/* Block-scaled FP4 x FP4 product, Y[m][n] = sum_k A^[m][k] * B^[n][k], with
+ * A^, B^ the exact dequantized operands (global scales included), summed in
+ * FP64 in k order.  rows [m0, m1) of Y only, so that a slice of a large
+ * problem can be evaluated; y is (m1 - m0) x N, dense. */
+void orc_gemm_rows(int fmt, int64_t M, int64_t N, int64_t K,
+                   const uint8_t *a_codes, const uint8_t *a_scales, double ga,
+                   const uint8_t *b_codes, const uint8_t *b_scales, double gb,
+                   int64_t m0, int64_t m1, double *y)
+{
+    int64_t m, n, k;
+    (void)M;
+    for (m = m0; m < m1; m++)
+        for (n = 0; n < N; n++) {
+            double acc = 0.0;
+            for (k = 0; k < K; k++)
+                acc += deq(fmt, a_codes, a_scales, ga, K, m, k) *
+                       deq(fmt, b_codes, b_scales, gb, K, n, k);
+            y[(m - m0) * N + n] = acc;
+        }
+}
+
+/* Same product for a list of (m, n) pairs (sampled checks at large sizes),
+ * plus the sum of |products| for each pair (the scale of FP32 rounding). */
+void orc_gemm_points(int fmt, int64_t K,
+                     const uint8_t *a_codes, const uint8_t *a_scales, double ga,
+                     const uint8_t *b_codes, const uint8_t *b_scales, double gb,
+                     const int64_t *ms, const int64_t *ns, int64_t npts,
+                     double *y, double *absy)
+{
+    int64_t p, k;
+    for (p = 0; p < npts; p++) {
+        double acc = 0.0, aacc = 0.0;
+        for (k = 0; k < K; k++) {
+            double t = deq(fmt, a_codes, a_scales, ga, K, ms[p], k) *
+                       deq(fmt, b_codes, b_scales, gb, K, ns[p], k);
+            acc += t;
+            aacc += fabs(t);
+        }
+        y[p] = acc;
+        absy[p] = aacc;
+    }
+}
+
+/* ---------- array forms of the scalar rules (for exhaustive sweeps) ---------- */
+
+void orc_e2m1_encode_array(const double *x, int64_t n, double S, uint8_t *out)
+{
+    int64_t i;
+    for (i = 0; i < n; i++) out[i] = orc_e2m1_encode(x[i], S);
+}
+
+void orc_bf16_from_double_array(const double *v, int64_t n, uint16_t *out)
+{
+    int64_t i;
+    for (i = 0; i < n; i++) out[i] = orc_bf16_from_double(v[i]);
+}
