@@ -1,0 +1,154 @@
+/*
+ * reqat.h -- C ABI of libreqat, the microscaled-FP4 linear layer for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The operations are those of the W4A4 linear layer of ReQAT (QAT of large
+ * reasoning models with FP4 weights and activations):
+ *   - block quantization of bfloat16 tensors to E2M1 codes with per-block
+ *     scales, in the two microscaled formats of App. A, Tab. mx_configs:
+ *       MXFP4: E2M1 elements, one E8M0 scale per 32 elements, no global scale;
+ *       NVFP4: E2M1 elements, one E4M3 scale per 16 elements, plus one FP32
+ *              global (tensor) scale;
+ *   - the quantize-dequantize ("fake-quant", simulated quantization noise,
+ *     Sec. 2.2 and Sec. 4 Stage-2 QAT) forward, emitting bfloat16;
+ *   - the block-scaled FP4 x FP4 product with FP32 accumulation that the
+ *     quantized weights and activations feed (the 4-bit GEMM of Sec. 5.3).
+ *
+ * Numerics (the paper names the formats only; these are the library's rules):
+ *   - Blocks run along the contiguous dimension (the reduction dimension K of
+ *     the product), for activations X[M][K] and weights W[N][K] alike.
+ *   - Block scale: the smallest representable scale s with
+ *     block_absmax <= 6 * s * g (g = 1 for MXFP4), so no element clips.
+ *     A block of zeros gets scale byte 0x00.  NVFP4 with a caller-given g so
+ *     small that even s = 448 fails: s = 448 and elements saturate at +-6.
+ *   - Element code: round to nearest, ties to the even code, of the exact
+ *     quotient |x| / (s * g), saturating at 6; the sign bit of x is copied
+ *     (so -0 and tiny negatives give code 0x8).
+ *   - Computed NVFP4 global scale (REQAT_TS_COMPUTE): g = 2^k with k the
+ *     smallest integer >= -126 such that tensor_absmax <= 6 * 448 * 2^k
+ *     (absmax over finite values; g = 1 for a tensor with none nonzero).
+ *   - A block containing NaN or Inf: scale byte NaN (MXFP4 0xFF, NVFP4 0x7F),
+ *     codes 0; fake-quant writes bfloat16 NaN (0x7FC0) for that block, and
+ *     the product propagates NaN.
+ *   - E4M3 is the OCP "E4M3FN" encoding (bias 7, max 448, NaN 0x7F/0xFF).
+ *   - Fake-quant output: the dequantized value code * s * g rounded once to
+ *     bfloat16 (nearest, ties to even).
+ *
+ * Layouts (all row-major, all pointers DEVICE pointers unless stated):
+ *   x      : bfloat16 [rows][ldx], the first `cols` of each row are used.
+ *   codes  : uint8 [rows][cols/2]; element 2i in bits 3:0 of byte i,
+ *            element 2i+1 in bits 7:4.
+ *   scales : uint8 [rows][cols/B], B = 16 (NVFP4) or 32 (MXFP4).
+ *   tensor_scale : one float (NVFP4 only); NULL for MXFP4.
+ *   y (product): [M][ldy] float32 or bfloat16 (round to nearest even).
+ *
+ * Ownership and concurrency: the caller allocates and frees every buffer;
+ * the library allocates nothing and keeps no mutable global state.  Every
+ * call only enqueues work on `stream` (a hipStream_t passed as void*; NULL
+ * means the null stream) and returns without waiting.  Calls on different
+ * streams that share a workspace race.
+ *
+ * Errors: arguments are validated on the host before any HIP call; a bad
+ * argument returns a status != REQAT_OK and enqueues nothing.  A failed
+ * launch returns REQAT_E_HIP.  Faults during execution surface at the
+ * caller's next synchronisation of `stream`.
+ */
+#ifndef REQAT_H
+#define REQAT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define REQAT_ABI_VERSION 1
+
+typedef enum {
+    REQAT_FMT_NVFP4 = 0, /* B = 16, E4M3 block scale, FP32 global scale */
+    REQAT_FMT_MXFP4 = 1  /* B = 32, E8M0 block scale */
+} reqat_format;
+
+typedef enum {
+    REQAT_DT_F32 = 0,
+    REQAT_DT_BF16 = 1
+} reqat_dtype;
+
+typedef enum {
+    REQAT_TS_COMPUTE = 0, /* library computes g from the tensor and writes *tensor_scale */
+    REQAT_TS_GIVEN = 1    /* *tensor_scale holds the caller's g (finite, > 0) */
+} reqat_tscale_mode;
+
+typedef enum {
+    REQAT_OK = 0,
+    REQAT_E_NULL = 1,        /* a required pointer is NULL */
+    REQAT_E_SHAPE = 2,       /* negative size, cols/K not a multiple of the block, ld too small */
+    REQAT_E_ALIGN = 3,       /* a pointer or leading dimension breaks the alignment rule */
+    REQAT_E_ENUM = 4,        /* unknown format, dtype or tensor-scale mode */
+    REQAT_E_UNSUPPORTED = 5, /* valid but not implemented (e.g. MXFP4 with a tensor scale) */
+    REQAT_E_HIP = 6          /* a HIP launch failed */
+} reqat_status;
+
+/*
+ * Quantize x[rows][cols] (App. A, Tab. mx_configs; element rounding and
+ * scale rule as above).
+ *   fmt          : REQAT_FMT_NVFP4 or REQAT_FMT_MXFP4.
+ *   x, ldx       : bfloat16 input, row stride ldx >= cols elements.
+ *   codes        : out, [rows][cols/2] bytes.
+ *   scales       : out, [rows][cols/B] bytes.
+ *   tensor_scale : NVFP4: device float; written (COMPUTE) or read (GIVEN).
+ *                  MXFP4: must be NULL.
+ *   ts           : REQAT_TS_COMPUTE or REQAT_TS_GIVEN (ignored for MXFP4).
+ *   workspace    : device scratch of reqat_workspace_bytes() bytes, needed for
+ *                  NVFP4 with REQAT_TS_COMPUTE (may be NULL otherwise).
+ * Requirements: cols % B == 0; x, codes, scales 16-byte aligned; ldx % 8 == 0.
+ * rows == 0 or cols == 0 is a no-op (COMPUTE still writes g = 1).
+ */
+reqat_status reqat_quantize_fp4(reqat_format fmt, const void *x, int64_t rows, int64_t cols,
+                                int64_t ldx, uint8_t *codes, uint8_t *scales, float *tensor_scale,
+                                reqat_tscale_mode ts, void *workspace, void *stream);
+
+/*
+ * Fake-quant: y = bfloat16(dequantize(quantize(x))) (QAT forward, Sec. 2.2,
+ * Sec. 4 Stage-2 QAT; every linear layer, App. D.1).  Same rules and
+ * tensor-scale handling as reqat_quantize_fp4; y[rows][ldy] bfloat16.
+ * Requirements: cols % B == 0; x, y 16-byte aligned; ldx % 8 == 0, ldy % 8 == 0.
+ * y may alias x only when ldy == ldx (in-place).
+ */
+reqat_status reqat_fakequant_fp4(reqat_format fmt, const void *x, int64_t rows, int64_t cols,
+                                 int64_t ldx, void *y, int64_t ldy, float *tensor_scale,
+                                 reqat_tscale_mode ts, void *workspace, void *stream);
+
+/*
+ * Block-scaled FP4 x FP4 product (the W4A4 GEMM of Sec. 5.3):
+ *   Y[m][n] = g_a * g_b * sum_k A^[m][k] * B^[n][k]
+ * with A^ = E2M1(a_codes) * block scale (and likewise B^), FP32 accumulation.
+ *   a_codes [M][K/2], a_scales [M][K/B], a_tensor_scale (NVFP4: device float; MXFP4: NULL)
+ *   b_codes [N][K/2], b_scales [N][K/B], b_tensor_scale (same rule)
+ *   y [M][ldy] of y_dtype.
+ * Requirements: K % 128 == 0 (so every row pitch, K/2 and K/B bytes, is a
+ * multiple of 4); code and scale pointers 16-byte aligned; y aligned to its
+ * element size; ldy >= N.  M == 0 or N == 0 is a no-op; K == 0 writes zeros.
+ */
+reqat_status reqat_gemm_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K,
+                             const uint8_t *a_codes, const uint8_t *a_scales,
+                             const float *a_tensor_scale,
+                             const uint8_t *b_codes, const uint8_t *b_scales,
+                             const float *b_tensor_scale,
+                             void *y, reqat_dtype y_dtype, int64_t ldy, void *stream);
+
+/* Bytes of device workspace that a quantize / fake-quant call may use. */
+size_t reqat_workspace_bytes(void);
+
+/* Static, human-readable name of a status code. */
+const char *reqat_status_str(reqat_status s);
+
+/* REQAT_ABI_VERSION of the built library. */
+int reqat_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* REQAT_H */

@@ -1,0 +1,130 @@
+// C ABI of libreqat: host-side argument validation and dispatch to the kernels.
+// Validation happens before any HIP call, so a bad argument is reported without
+// touching the device (and can be tested on a host without a GPU).
+#include "../../include/reqat.h"
+#include "internal.h"
+
+namespace {
+
+using namespace reqat;
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int block_of(reqat_format f) { return f == REQAT_FMT_MXFP4 ? 32 : 16; }
+
+bool fmt_ok(reqat_format f) { return f == REQAT_FMT_NVFP4 || f == REQAT_FMT_MXFP4; }
+
+// Shared validation of quantize / fake-quant arguments.
+reqat_status check_quant(reqat_format fmt, const void *x, int64_t rows, int64_t cols, int64_t ldx,
+                         const void *out0, const void *out1, int64_t ldy, const float *ts_ptr,
+                         reqat_tscale_mode ts, const void *workspace, bool fake) {
+    if (!fmt_ok(fmt)) return REQAT_E_ENUM;
+    if (fmt == REQAT_FMT_NVFP4 && ts != REQAT_TS_COMPUTE && ts != REQAT_TS_GIVEN) return REQAT_E_ENUM;
+    if (rows < 0 || cols < 0) return REQAT_E_SHAPE;
+    if (cols % block_of(fmt)) return REQAT_E_SHAPE;
+    if (ldx < cols || (fake && ldy < cols)) return REQAT_E_SHAPE;
+    if (fmt == REQAT_FMT_MXFP4 && ts_ptr != nullptr) return REQAT_E_UNSUPPORTED;
+    if (fmt == REQAT_FMT_NVFP4 && ts_ptr == nullptr) return REQAT_E_NULL;
+    if (fmt == REQAT_FMT_NVFP4 && ts == REQAT_TS_COMPUTE && workspace == nullptr) return REQAT_E_NULL;
+    if (rows == 0 || cols == 0) return REQAT_OK;
+    if (!x || !out0 || (!fake && !out1)) return REQAT_E_NULL;
+    if (!aligned16(x) || !aligned16(out0) || (!fake && !aligned16(out1))) return REQAT_E_ALIGN;
+    if (ldx % 8 || (fake && ldy % 8)) return REQAT_E_ALIGN;
+    if (fmt == REQAT_FMT_NVFP4 && (reinterpret_cast<uintptr_t>(ts_ptr) & 3u)) return REQAT_E_ALIGN;
+    if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 3u)) return REQAT_E_ALIGN;
+    return REQAT_OK;
+}
+
+reqat_status run_quant(reqat_format fmt, const void *x, int64_t rows, int64_t cols, int64_t ldx,
+                       uint8_t *codes, uint8_t *scales, void *y, int64_t ldy, float *tensor_scale,
+                       reqat_tscale_mode ts, void *workspace, void *stream, bool fake) {
+    reqat_status st = check_quant(fmt, x, rows, cols, ldx, fake ? y : codes, scales, ldy,
+                                  tensor_scale, ts, workspace, fake);
+    if (st != REQAT_OK) return st;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const bool nv = fmt == REQAT_FMT_NVFP4;
+    const bool compute = nv && ts == REQAT_TS_COMPUTE;
+    if (rows == 0 || cols == 0) {
+        if (compute && launch_unit_scale(tensor_scale, s) != hipSuccess) return REQAT_E_HIP;
+        return REQAT_OK;
+    }
+    int nparts = 0;
+    uint32_t *partials = reinterpret_cast<uint32_t *>(workspace);
+    if (compute) {
+        if (launch_absmax(reinterpret_cast<const uint16_t *>(x), rows, cols, ldx, partials, &nparts,
+                          s) != hipSuccess)
+            return REQAT_E_HIP;
+    }
+    GSrc gsrc = !nv ? kGNone : (compute ? kGComputed : kGGiven);
+    hipError_t e = launch_quantize(nv ? kNV : kMX, fake ? kFakeQuant : kCodes,
+                                   reinterpret_cast<const uint16_t *>(x), rows, cols, ldx, codes,
+                                   scales, reinterpret_cast<uint16_t *>(y), ldy, tensor_scale, gsrc,
+                                   partials, nparts, s);
+    return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+reqat_status reqat_quantize_fp4(reqat_format fmt, const void *x, int64_t rows, int64_t cols,
+                                int64_t ldx, uint8_t *codes, uint8_t *scales, float *tensor_scale,
+                                reqat_tscale_mode ts, void *workspace, void *stream) {
+    return run_quant(fmt, x, rows, cols, ldx, codes, scales, nullptr, 0, tensor_scale, ts,
+                     workspace, stream, false);
+}
+
+reqat_status reqat_fakequant_fp4(reqat_format fmt, const void *x, int64_t rows, int64_t cols,
+                                 int64_t ldx, void *y, int64_t ldy, float *tensor_scale,
+                                 reqat_tscale_mode ts, void *workspace, void *stream) {
+    return run_quant(fmt, x, rows, cols, ldx, nullptr, nullptr, y, ldy, tensor_scale, ts,
+                     workspace, stream, true);
+}
+
+reqat_status reqat_gemm_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K,
+                             const uint8_t *a_codes, const uint8_t *a_scales,
+                             const float *a_tensor_scale, const uint8_t *b_codes,
+                             const uint8_t *b_scales, const float *b_tensor_scale, void *y,
+                             reqat_dtype y_dtype, int64_t ldy, void *stream) {
+    if (!fmt_ok(fmt)) return REQAT_E_ENUM;
+    if (y_dtype != REQAT_DT_F32 && y_dtype != REQAT_DT_BF16) return REQAT_E_ENUM;
+    if (M < 0 || N < 0 || K < 0) return REQAT_E_SHAPE;
+    if (K % 128) return REQAT_E_SHAPE;
+    if (ldy < N) return REQAT_E_SHAPE;
+    const bool nv = fmt == REQAT_FMT_NVFP4;
+    if (!nv && (a_tensor_scale || b_tensor_scale)) return REQAT_E_UNSUPPORTED;
+    if (nv && (!a_tensor_scale || !b_tensor_scale)) return REQAT_E_NULL;
+    if (M == 0 || N == 0) return REQAT_OK;
+    if (!y) return REQAT_E_NULL;
+    if (K > 0 && (!a_codes || !a_scales || !b_codes || !b_scales)) return REQAT_E_NULL;
+    if (reinterpret_cast<uintptr_t>(y) & (y_dtype == REQAT_DT_BF16 ? 1u : 3u)) return REQAT_E_ALIGN;
+    if (K > 0 && (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(a_scales) ||
+                  !aligned16(b_scales)))
+        return REQAT_E_ALIGN;
+    if (nv && ((reinterpret_cast<uintptr_t>(a_tensor_scale) & 3u) ||
+               (reinterpret_cast<uintptr_t>(b_tensor_scale) & 3u)))
+        return REQAT_E_ALIGN;
+    hipError_t e = launch_gemm(nv ? kNV : kMX, M, N, K, a_codes, a_scales, a_tensor_scale, b_codes,
+                               b_scales, b_tensor_scale, y, y_dtype == REQAT_DT_BF16, ldy,
+                               reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
+}
+
+size_t reqat_workspace_bytes(void) { return sizeof(uint32_t) * kMaxPartials; }
+
+const char *reqat_status_str(reqat_status s) {
+    switch (s) {
+    case REQAT_OK: return "REQAT_OK";
+    case REQAT_E_NULL: return "REQAT_E_NULL: a required pointer is NULL";
+    case REQAT_E_SHAPE: return "REQAT_E_SHAPE: invalid size or leading dimension";
+    case REQAT_E_ALIGN: return "REQAT_E_ALIGN: pointer or leading dimension misaligned";
+    case REQAT_E_ENUM: return "REQAT_E_ENUM: unknown format, dtype or tensor-scale mode";
+    case REQAT_E_UNSUPPORTED: return "REQAT_E_UNSUPPORTED: combination not supported";
+    case REQAT_E_HIP: return "REQAT_E_HIP: HIP launch failed";
+    }
+    return "unknown reqat_status";
+}
+
+int reqat_abi_version(void) { return REQAT_ABI_VERSION; }
+
+}  // extern "C"

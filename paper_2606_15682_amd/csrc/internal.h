@@ -1,0 +1,38 @@
+// Internal launcher interface between the C ABI layer and the kernels.
+// Every launcher only enqueues work on `stream` and returns hipGetLastError().
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace reqat {
+
+// Maximum number of partial maxima the absmax pass produces; the workspace
+// holds one uint32 per partial.
+constexpr int kMaxPartials = 1024;
+
+// Format selector shared by the launchers (same values as the C ABI enum).
+enum Fmt : int { kNV = 0, kMX = 1 };
+
+// Output selector for the block quantizer.
+enum QuantOut : int { kCodes = 0, kFakeQuant = 1 };
+
+// Global-scale source for NVFP4.
+enum GSrc : int { kGComputed = 0, kGGiven = 1, kGNone = 2 };
+
+hipError_t launch_unit_scale(float *gptr, hipStream_t stream);
+
+hipError_t launch_absmax(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                         uint32_t *partials, int *nparts_out, hipStream_t stream);
+
+hipError_t launch_quantize(Fmt fmt, QuantOut out, const uint16_t *x, int64_t rows, int64_t cols,
+                           int64_t ldx, uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy,
+                           float *gptr, GSrc gsrc, const uint32_t *partials, int nparts,
+                           hipStream_t stream);
+
+hipError_t launch_gemm(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *a_codes,
+                       const uint8_t *a_scales, const float *ga, const uint8_t *b_codes,
+                       const uint8_t *b_scales, const float *gb, void *y, bool y_bf16, int64_t ldy,
+                       hipStream_t stream);
+
+}  // namespace reqat

@@ -1,0 +1,196 @@
+"""ctypes binding of libreqat (C ABI in include/reqat.h).
+
+Two layers:
+  * ``reqat_quantize_fp4``, ``reqat_fakequant_fp4``, ``reqat_gemm_w4a4``, ... --
+    the C entry points under the same names, taking raw device pointers
+    (ints) and sizes; they return the C status code.
+  * ``quantize``, ``fakequant``, ``gemm`` -- torch-tensor conveniences that
+    allocate outputs with torch, pass ``data_ptr()`` and the current HIP
+    stream, and raise ``ReqatError`` on a non-OK status.
+
+Every step of the computation runs in the HIP library; this module only
+marshals arguments.  It raises at load time when the library is missing.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+NVFP4 = 0
+MXFP4 = 1
+BLOCK = {NVFP4: 16, MXFP4: 32}
+DT_F32 = 0
+DT_BF16 = 1
+TS_COMPUTE = 0
+TS_GIVEN = 1
+
+STATUS = {0: "REQAT_OK", 1: "REQAT_E_NULL", 2: "REQAT_E_SHAPE", 3: "REQAT_E_ALIGN",
+          4: "REQAT_E_ENUM", 5: "REQAT_E_UNSUPPORTED", 6: "REQAT_E_HIP"}
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libreqat.so")
+
+# every symbol include/reqat.h declares, with its ctypes signature
+_VP = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_INT = ctypes.c_int
+SIGNATURES = {
+    "reqat_quantize_fp4": (_INT, [_INT, _VP, _I64, _I64, _I64, _VP, _VP, _VP, _INT, _VP, _VP]),
+    "reqat_fakequant_fp4": (_INT, [_INT, _VP, _I64, _I64, _I64, _VP, _I64, _VP, _INT, _VP, _VP]),
+    "reqat_gemm_w4a4": (_INT, [_INT, _I64, _I64, _I64, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _INT,
+                               _I64, _VP]),
+    "reqat_workspace_bytes": (ctypes.c_size_t, []),
+    "reqat_status_str": (ctypes.c_char_p, [_INT]),
+    "reqat_abi_version": (_INT, []),
+}
+
+_lib = None
+
+
+class ReqatError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__("%s failed: %s" % (where, STATUS.get(status, status)))
+        self.status = status
+
+
+def load(path: str = LIB_PATH):
+    """Load libreqat.so once; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError("libreqat.so is not built (%s); run python -m paper_2606_15682_amd.build"
+                           % path)
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in SIGNATURES.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+# ------------------------------------------------------------------ raw C entry points
+
+def reqat_quantize_fp4(fmt, x, rows, cols, ldx, codes, scales, tensor_scale, ts, workspace, stream):
+    return load().reqat_quantize_fp4(fmt, x, rows, cols, ldx, codes, scales, tensor_scale, ts,
+                                     workspace, stream)
+
+
+def reqat_fakequant_fp4(fmt, x, rows, cols, ldx, y, ldy, tensor_scale, ts, workspace, stream):
+    return load().reqat_fakequant_fp4(fmt, x, rows, cols, ldx, y, ldy, tensor_scale, ts, workspace,
+                                      stream)
+
+
+def reqat_gemm_w4a4(fmt, M, N, K, a_codes, a_scales, a_ts, b_codes, b_scales, b_ts, y, y_dtype,
+                    ldy, stream):
+    return load().reqat_gemm_w4a4(fmt, M, N, K, a_codes, a_scales, a_ts, b_codes, b_scales, b_ts, y,
+                                  y_dtype, ldy, stream)
+
+
+def reqat_workspace_bytes() -> int:
+    return load().reqat_workspace_bytes()
+
+
+def reqat_status_str(s: int) -> str:
+    return load().reqat_status_str(s).decode()
+
+
+def reqat_abi_version() -> int:
+    return load().reqat_abi_version()
+
+
+# ------------------------------------------------------------------ torch conveniences
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _check(st: int, where: str):
+    if st != 0:
+        raise ReqatError(st, where)
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _x2d(x: torch.Tensor):
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or not x.is_cuda:
+        raise TypeError("expected a 2-D bfloat16 CUDA tensor")
+    if x.stride(1) != 1:
+        raise ValueError("rows must be contiguous")
+    return x.shape[0], x.shape[1], x.stride(0)
+
+
+_workspaces: dict = {}
+
+
+def workspace(device) -> torch.Tensor:
+    """A per-device workspace tensor (cached; calls on different streams must not share it)."""
+    device = torch.device(device)
+    key = (device.index if device.index is not None else torch.cuda.current_device())
+    ws = _workspaces.get(key)
+    if ws is None:
+        ws = torch.empty(reqat_workspace_bytes(), dtype=torch.uint8, device=device)
+        _workspaces[key] = ws
+    return ws
+
+
+def _gscale(fmt, x, tensor_scale):
+    """(tensor_scale tensor or None, ts mode)."""
+    if fmt == MXFP4:
+        if tensor_scale is not None:
+            raise ValueError("MXFP4 has no global scale")
+        return None, TS_COMPUTE
+    if tensor_scale is None:
+        return torch.empty(1, dtype=torch.float32, device=x.device), TS_COMPUTE
+    if isinstance(tensor_scale, torch.Tensor):
+        return tensor_scale, TS_GIVEN
+    return torch.tensor([float(tensor_scale)], dtype=torch.float32, device=x.device), TS_GIVEN
+
+
+def quantize(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out=None):
+    """Quantize a 2-D bfloat16 CUDA tensor.  Returns (codes, scales, g) with g a
+    1-element float32 tensor (NVFP4: computed unless given) or None (MXFP4)."""
+    rows, cols, ldx = _x2d(x)
+    B = BLOCK[fmt]
+    if out is not None:
+        codes, scales = out
+    else:
+        codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=x.device)
+        scales = torch.empty((rows, cols // B), dtype=torch.uint8, device=x.device)
+    g, ts = _gscale(fmt, x, tensor_scale)
+    ws = workspace(x.device)
+    st = reqat_quantize_fp4(fmt, x.data_ptr(), rows, cols, ldx, codes.data_ptr(), scales.data_ptr(),
+                            _ptr(g), ts, ws.data_ptr(), _stream(x.device))
+    _check(st, "reqat_quantize_fp4")
+    return codes, scales, g
+
+
+def fakequant(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out=None):
+    """Quantize-dequantize to bfloat16.  Returns (y, g)."""
+    rows, cols, ldx = _x2d(x)
+    y = out if out is not None else torch.empty((rows, cols), dtype=torch.bfloat16, device=x.device)
+    g, ts = _gscale(fmt, x, tensor_scale)
+    ws = workspace(x.device)
+    st = reqat_fakequant_fp4(fmt, x.data_ptr(), rows, cols, ldx, y.data_ptr(), y.stride(0), _ptr(g),
+                             ts, ws.data_ptr(), _stream(x.device))
+    _check(st, "reqat_fakequant_fp4")
+    return y, g
+
+
+def gemm(fmt, a_codes, a_scales, a_g, b_codes, b_scales, b_g, out_dtype=torch.float32, out=None):
+    """Y[M, N] = A^ B^T with FP32 accumulation; Y float32 or bfloat16."""
+    M, K = a_codes.shape[0], a_codes.shape[1] * 2
+    N = b_codes.shape[0]
+    if b_codes.shape[1] * 2 != K:
+        raise ValueError("K mismatch")
+    dt = DT_F32 if out_dtype == torch.float32 else DT_BF16
+    y = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=a_codes.device)
+    st = reqat_gemm_w4a4(fmt, M, N, K, a_codes.data_ptr(), a_scales.data_ptr(), _ptr(a_g),
+                         b_codes.data_ptr(), b_scales.data_ptr(), _ptr(b_g), y.data_ptr(), dt,
+                         y.stride(0), _stream(a_codes.device))
+    _check(st, "reqat_gemm_w4a4")
+    return y

@@ -1,0 +1,121 @@
+"""The C-ABI library loads, exports every symbol include/reqat.h declares, and
+rejects bad arguments on the host before any HIP call (CPU only: no call here
+reaches a kernel launch)."""
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2606_15682_amd import reqat
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "reqat.h")
+
+NV, MX = reqat.NVFP4, reqat.MXFP4
+P = 1 << 20          # a 16-byte aligned, never dereferenced fake pointer value
+OK, E_NULL, E_SHAPE, E_ALIGN, E_ENUM, E_UNSUP = 0, 1, 2, 3, 4, 5
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(reqat_[a-z0-9_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(reqat.LIB_PATH):
+        pytest.skip("libreqat.so not built")
+    return reqat.load()
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ("reqat_quantize_fp4", "reqat_fakequant_fp4", "reqat_gemm_w4a4",
+              "reqat_workspace_bytes", "reqat_status_str", "reqat_abi_version"):
+        assert n in names
+    assert set(names) == set(reqat.SIGNATURES), "binding and header disagree"
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", reqat.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\sT\s(\S+)", out))
+    for n in declared_functions():
+        assert n in exported, n
+        assert hasattr(lib, n)
+
+
+def test_small_queries(lib):
+    assert reqat.reqat_abi_version() == 1
+    assert reqat.reqat_workspace_bytes() >= 4
+    for s in range(7):
+        assert reqat.reqat_status_str(s).startswith(reqat.STATUS[s])
+    assert "unknown" in reqat.reqat_status_str(99)
+
+
+def q(fmt=NV, x=P, rows=4, cols=64, ldx=64, codes=P, scales=P, ts_ptr=P, ts=0, ws=P):
+    return reqat.reqat_quantize_fp4(fmt, x, rows, cols, ldx, codes, scales, ts_ptr, ts, ws, None)
+
+
+def fq(fmt=NV, x=P, rows=4, cols=64, ldx=64, y=P, ldy=64, ts_ptr=P, ts=0, ws=P):
+    return reqat.reqat_fakequant_fp4(fmt, x, rows, cols, ldx, y, ldy, ts_ptr, ts, ws, None)
+
+
+def gm(fmt=NV, M=4, N=8, K=128, ac=P, as_=P, ag=P, bc=P, bs=P, bg=P, y=P, dt=0, ldy=8):
+    return reqat.reqat_gemm_w4a4(fmt, M, N, K, ac, as_, ag, bc, bs, bg, y, dt, ldy, None)
+
+
+def test_quantize_validation(lib):
+    assert q(fmt=7) == E_ENUM
+    assert q(ts=5) == E_ENUM
+    assert q(rows=-1) == E_SHAPE
+    assert q(cols=40) == E_SHAPE                 # not a multiple of 16
+    assert q(fmt=MX, cols=48, ldx=48, ts_ptr=None) == E_SHAPE   # not a multiple of 32
+    assert q(ldx=32) == E_SHAPE
+    assert q(fmt=MX, ts_ptr=P) == E_UNSUP        # MXFP4 has no global scale
+    assert q(ts_ptr=None) == E_NULL
+    assert q(ws=None) == E_NULL                  # computed g needs the workspace
+    assert q(x=None) == E_NULL
+    assert q(codes=None) == E_NULL
+    assert q(scales=None) == E_NULL
+    assert q(x=P + 2) == E_ALIGN
+    assert q(codes=P + 8) == E_ALIGN
+    assert q(ldx=68) == E_ALIGN
+    assert q(ts_ptr=P + 2) == E_ALIGN
+
+
+def test_fakequant_validation(lib):
+    assert fq(fmt=3) == E_ENUM
+    assert fq(cols=24, ldx=24, ldy=24) == E_SHAPE
+    assert fq(ldy=32) == E_SHAPE
+    assert fq(y=None) == E_NULL
+    assert fq(y=P + 4) == E_ALIGN
+    assert fq(ldy=68) == E_ALIGN
+    assert fq(fmt=MX) == E_UNSUP
+
+
+def test_gemm_validation(lib):
+    assert gm(fmt=2) == E_ENUM
+    assert gm(dt=9) == E_ENUM
+    assert gm(M=-1) == E_SHAPE
+    assert gm(K=64) == E_SHAPE                   # K % 128
+    assert gm(ldy=4) == E_SHAPE
+    assert gm(fmt=MX) == E_UNSUP                 # MXFP4 with tensor scales
+    assert gm(ag=None) == E_NULL
+    assert gm(y=None) == E_NULL
+    assert gm(ac=None) == E_NULL
+    assert gm(ac=P + 1) == E_ALIGN
+    assert gm(y=P + 2) == E_ALIGN               # float32 output needs 4-byte alignment
+    assert gm(y=P + 1, dt=1) == E_ALIGN         # bf16 output needs 2-byte alignment
+
+
+def test_binding_raises_when_library_missing(tmp_path):
+    saved = reqat._lib
+    reqat._lib = None
+    try:
+        with pytest.raises(RuntimeError, match="not built"):
+            reqat.load(str(tmp_path / "missing.so"))
+    finally:
+        reqat._lib = saved

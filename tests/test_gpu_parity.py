@@ -1,0 +1,277 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle.
+
+Codes, scales, global scales and fake-quant outputs must match bit for bit;
+GEMM outputs must satisfy |Y - Yref| <= 1e-3 * sum_k |A^ B^| (FP32 output;
+Yref is the FP64 product of the exactly dequantized operands), and a bf16
+output must additionally be within one bf16 ulp of round(Yref).  Outputs are
+pre-filled with two different poison patterns, so an element the kernel does
+not write, or a run-to-run difference, fails the comparison.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_15682_amd import reqat
+from paper_2606_15682_amd import workloads as wl
+from tests import indep
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+NV, MX = reqat.NVFP4, reqat.MXFP4
+GEMM_TOL = 1e-3
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def gpu_quant(fmt, xb, g=None, poison=0, ldx_pad=0):
+    R, C = xb.shape
+    B = reqat.BLOCK[fmt]
+    if ldx_pad:
+        big = np.zeros((R, C + ldx_pad), np.uint16)
+        big[:, :C] = xb
+        xt = wl.from_bits(big).to(DEV)[:, :C]
+    else:
+        xt = wl.from_bits(xb).to(DEV)
+    codes = torch.full((R, C // 2), poison, dtype=torch.uint8, device=DEV)
+    scales = torch.full((R, C // B), poison, dtype=torch.uint8, device=DEV)
+    gt = None if (g is None or fmt == MX) else torch.tensor([g], dtype=torch.float32, device=DEV)
+    _, _, gg = reqat.quantize(xt, fmt, tensor_scale=gt, out=(codes, scales))
+    torch.cuda.synchronize()
+    return codes.cpu().numpy(), scales.cpu().numpy(), (1.0 if gg is None else float(gg.cpu()[0]))
+
+
+def gpu_fakequant(fmt, xb, g=None, poison=0x7FFF):
+    R, C = xb.shape
+    xt = wl.from_bits(xb).to(DEV)
+    y = wl.from_bits(np.full((R, C), poison, np.uint16)).to(DEV)
+    gt = None if (g is None or fmt == MX) else torch.tensor([g], dtype=torch.float32, device=DEV)
+    _, gg = reqat.fakequant(xt, fmt, tensor_scale=gt, out=y)
+    torch.cuda.synchronize()
+    return wl.bf16_bits(y.cpu()), (1.0 if gg is None else float(gg.cpu()[0]))
+
+
+def assert_quant_parity(fmt, xb, g=None, ldx_pad=0):
+    oc, os_, og = oracle.quantize(fmt, xb, g)
+    for poison in (0x00, 0xFF):
+        c, s, gg = gpu_quant(fmt, xb, g, poison, ldx_pad)
+        if fmt == NV:
+            assert gg == np.float32(og), (gg, og)
+        bad = np.argwhere(s != os_)
+        assert bad.size == 0, ("scales differ", bad[:4], s[tuple(bad[0])], os_[tuple(bad[0])])
+        bad = np.argwhere(c != oc)
+        assert bad.size == 0, ("codes differ", bad[:4], c[tuple(bad[0])], oc[tuple(bad[0])])
+
+
+def assert_fq_parity(fmt, xb, g=None):
+    oy, og = oracle.fakequant(fmt, xb, g)
+    for poison in (0x7FFF, 0x0000):
+        y, gg = gpu_fakequant(fmt, xb, g, poison)
+        bad = np.argwhere(y != oy)
+        assert bad.size == 0, ("fake-quant differs", bad[:4], hex(y[tuple(bad[0])]), hex(oy[tuple(bad[0])]))
+
+
+def _rand(R, C, seed, dist="normal", std=1.0, outliers=0):
+    t = wl.random_bf16(R, C, seed, std, dist)
+    xb = wl.bf16_bits(t).copy()
+    if outliers:
+        rng = np.random.default_rng(seed + 1)
+        idx = rng.choice(C, outliers, replace=False)
+        xb[:, idx] = indep.to_bf16_bits(indep.bf16_values(xb[:, idx]) * 20.0)
+    return xb
+
+
+SHAPES = [(16, 256), (37, 224), (1, 32), (129, 512), (300, 96)]
+
+
+@pytest.mark.parametrize("fmt", [NV, MX])
+@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("dist", ["normal", "student_t"])
+def test_quantize_parity_random(fmt, shape, dist):
+    R, C = shape
+    log("quantize parity fmt=%d shape=%s dist=%s" % (fmt, shape, dist))
+    xb = _rand(R, C, 100 + R + C, dist, outliers=max(1, C // 100))
+    assert_quant_parity(fmt, xb)
+    assert_fq_parity(fmt, xb)
+
+
+@pytest.mark.parametrize("g", [2.0 ** -7, 1.0, 0.0123456789, 3.0, 1e-30, 2.0 ** -140])
+def test_nvfp4_given_global_scale(g):
+    log("NVFP4 given g=%r" % g)
+    xb = _rand(33, 256, 7, "student_t", outliers=3)
+    g = float(np.float32(g))
+    assert_quant_parity(NV, xb, g)
+    assert_fq_parity(NV, xb, g)
+
+
+@pytest.mark.parametrize("fmt", [NV, MX])
+def test_strided_rows(fmt):
+    log("strided rows fmt=%d" % fmt)
+    xb = _rand(45, 320, 9, "normal")
+    assert_quant_parity(fmt, xb, ldx_pad=40)
+
+
+@pytest.mark.parametrize("fmt", [NV, MX])
+@pytest.mark.parametrize("order", ["sorted", "shuffled"])
+def test_exhaustive_bf16_patterns(fmt, order):
+    """Every bfloat16 bit pattern (NaN/Inf make NaN blocks when shuffled in)."""
+    log("exhaustive bf16 fmt=%d order=%s" % (fmt, order))
+    allp = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    if order == "sorted":
+        v = indep.bf16_values(allp)
+        allp = allp[np.isfinite(v)]
+        allp = allp[np.argsort(np.abs(indep.bf16_values(allp)), kind="stable")]
+        allp = allp[: (allp.size // 512) * 512]
+    else:
+        allp = np.random.default_rng(3).permutation(allp)
+    xb = allp.reshape(-1, 512)
+    assert_quant_parity(fmt, xb)
+    assert_fq_parity(fmt, xb)
+    if fmt == NV:
+        for g in (2.0 ** -20, 0.3):
+            assert_quant_parity(NV, xb, float(np.float32(g)))
+            assert_fq_parity(NV, xb, float(np.float32(g)))
+
+
+@pytest.mark.parametrize("fmt", [NV, MX])
+def test_exact_ties_and_neighbours(fmt):
+    """Blocks whose elements sit exactly on rounding midpoints (and one bf16
+    step either side), for many scales across the exponent range."""
+    log("ties fmt=%d" % fmt)
+    B = reqat.BLOCK[fmt]
+    rows = []
+    mids = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0])
+    e4 = indep.e4m3_table()
+    for e in range(-130, 126, 3):
+        if fmt == MX:
+            S = 2.0 ** e
+        else:
+            S = e4[(e * 7) % 0x7E + 1] * 2.0 ** (e // 2)
+        vals = np.concatenate([[6.0 * S], mids * S, -mids * S])
+        vals = np.resize(vals, B)
+        b = indep.to_bf16_bits(vals)
+        rows.append(b)
+        rows.append(np.where(b & 0x7FFF, b + 1, b).astype(np.uint16))
+        rows.append(np.where(b & 0x7FFF, b - 1, b).astype(np.uint16))
+    xb = np.concatenate(rows).reshape(-1, 2 * B)
+    assert_quant_parity(fmt, xb)
+    assert_fq_parity(fmt, xb)
+    if fmt == NV:
+        assert_quant_parity(NV, xb, 2.0 ** -3)
+        assert_fq_parity(NV, xb, 2.0 ** -3)
+
+
+@pytest.mark.parametrize("fmt", [NV, MX])
+def test_special_values(fmt):
+    log("special values fmt=%d" % fmt)
+    B = reqat.BLOCK[fmt]
+    x = np.zeros((6, 2 * B), np.uint16)
+    x[0, :] = 0x8000
+    x[1, 0] = 0x7FC0
+    x[1, B] = 0x3F80
+    x[2, 3] = 0xFF80
+    x[2, B:] = np.arange(1, B + 1)
+    x[3, :B] = 0x7F7F
+    x[3, B] = 0x0001
+    x[4, :] = 0x0001
+    x[5, :B] = 0x7F80
+    assert_quant_parity(fmt, x)
+    assert_fq_parity(fmt, x)
+    assert_quant_parity(fmt, x[[0, 4]])           # tensor of only zeros / subnormals
+
+
+def test_empty_tensor_writes_unit_global_scale():
+    log("empty tensor")
+    x = torch.empty((0, 64), dtype=torch.bfloat16, device=DEV)
+    g = torch.full((1,), 7.0, dtype=torch.float32, device=DEV)
+    c, s, gg = reqat.quantize(x, NV, out=(torch.empty((0, 32), dtype=torch.uint8, device=DEV),
+                                          torch.empty((0, 4), dtype=torch.uint8, device=DEV)))
+    torch.cuda.synchronize()
+    assert float(gg.cpu()[0]) == 1.0
+
+
+# ------------------------------------------------------------------ GEMM
+
+def gpu_gemm(fmt, ac, as_, ga, bc, bs, gb, out_dtype, poison):
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    gat = None if fmt == MX else torch.tensor([ga], dtype=torch.float32, device=DEV)
+    gbt = None if fmt == MX else torch.tensor([gb], dtype=torch.float32, device=DEV)
+    M, N = ac.shape[0], bc.shape[0]
+    y = torch.full((M, N), poison, dtype=out_dtype, device=DEV)
+    reqat.gemm(fmt, t(ac), t(as_), gat, t(bc), t(bs), gbt, out_dtype=out_dtype, out=y)
+    torch.cuda.synchronize()
+    return y.float().cpu().numpy().astype(np.float64)
+
+
+def check_gemm_points(fmt, ac, as_, ga, bc, bs, gb, y32, ybf, ms, ns):
+    ref, aref = oracle.gemm_points(fmt, ac, as_, ga, bc, bs, gb, ms, ns)
+    got = y32[ms, ns]
+    nanref = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nanref)
+    ok = ~nanref
+    err = np.abs(got[ok] - ref[ok])
+    assert np.all(err <= GEMM_TOL * aref[ok]), float(np.max(err / np.maximum(aref[ok], 1e-300)))
+    if ybf is not None:
+        gb_ = ybf[ms, ns][ok]
+        rb = indep.bf16_values(oracle.bf16_from_double_array(ref[ok]))
+        ulp = np.maximum(np.abs(rb), 2.0 ** -133) * 2.0 ** -7
+        assert np.all(np.abs(gb_ - rb) <= ulp + GEMM_TOL * aref[ok])
+
+
+def run_gemm_case(fmt, M, N, K, seed, dist="normal", wstd=0.02, g=(None, None), all_points=True):
+    xa = _rand(M, K, seed, dist, outliers=max(1, K // 100))
+    xb = _rand(N, K, seed + 7, "normal", std=wstd)
+    ac, as_, ga = oracle.quantize(fmt, xa, g[0])
+    bc, bs, gb = oracle.quantize(fmt, xb, g[1])
+    y1 = gpu_gemm(fmt, ac, as_, ga, bc, bs, gb, torch.float32, float("nan"))
+    y2 = gpu_gemm(fmt, ac, as_, ga, bc, bs, gb, torch.float32, 0.0)
+    assert np.array_equal(y1, y2, equal_nan=True), "poison visible or nondeterministic"
+    yb = gpu_gemm(fmt, ac, as_, ga, bc, bs, gb, torch.bfloat16, float("nan"))
+    if all_points:
+        ms, ns = np.arange(M).repeat(N), np.tile(np.arange(N), M)
+    else:
+        rng = np.random.default_rng(seed)
+        ms = np.concatenate([rng.integers(0, M, 3000), [0, M - 1, M - 1, 0]])
+        ns = np.concatenate([rng.integers(0, N, 3000), [0, N - 1, 0, N - 1]])
+    check_gemm_points(fmt, ac, as_, ga, bc, bs, gb, y1, yb, ms, ns)
+
+
+@pytest.mark.parametrize("fmt", [NV, MX])
+@pytest.mark.parametrize("M,N,K", [(16, 256, 256), (37, 200, 384), (1, 1, 128), (130, 129, 512),
+                                   (256, 384, 1024), (5, 300, 128)])
+def test_gemm_parity(fmt, M, N, K):
+    log("gemm parity fmt=%d M=%d N=%d K=%d" % (fmt, M, N, K))
+    run_gemm_case(fmt, M, N, K, seed=M * 31 + N * 7 + K, dist="student_t")
+
+
+def test_gemm_given_scales_nv():
+    log("gemm NV given scales")
+    run_gemm_case(NV, 64, 96, 256, seed=5, g=(0.0123, 3.5))
+
+
+@pytest.mark.parametrize("fmt", [NV, MX])
+def test_gemm_nan_block_propagates(fmt):
+    log("gemm NaN fmt=%d" % fmt)
+    B = reqat.BLOCK[fmt]
+    xa = _rand(8, 256, 1)
+    xa[3, B + 2] = 0x7FC0
+    xb = _rand(16, 256, 2)
+    ac, as_, ga = oracle.quantize(fmt, xa)
+    bc, bs, gb = oracle.quantize(fmt, xb)
+    y = gpu_gemm(fmt, ac, as_, ga, bc, bs, gb, torch.float32, 0.0)
+    assert np.all(np.isnan(y[3])) and not np.any(np.isnan(np.delete(y, 3, axis=0)))
+
+
+def test_gemm_k_zero_writes_zeros():
+    log("gemm K=0")
+    y = torch.full((4, 8), float("nan"), dtype=torch.float32, device=DEV)
+    z = torch.zeros(16, dtype=torch.uint8, device=DEV)
+    st = reqat.reqat_gemm_w4a4(MX, 4, 8, 0, z.data_ptr(), z.data_ptr(), None, z.data_ptr(),
+                               z.data_ptr(), None, y.data_ptr(), reqat.DT_F32, 8,
+                               torch.cuda.current_stream().cuda_stream)
+    assert st == 0
+    torch.cuda.synchronize()
+    assert torch.all(y == 0).item()
