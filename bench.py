@@ -1,0 +1,193 @@
+#!/usr/bin/env python3
+"""Benchmark of the microscaled-FP4 linear layer on one MI355X.
+
+One step = one pass of the whole hot path over the 14B-like NVFP4 MLP gate/up
+projection (X[4096 x 5120] activations with 1% outlier channels, W[27648 x 5120]
+= gate || up weights, both bfloat16, seeded synthetic):
+  quantize X (dynamic global scale: absmax pass + quantize),
+  quantize W (dynamic global scale),
+  W4A4 GEMM Y = X^ W^T (FP32 accumulation, bfloat16 output),
+  fake-quant X and W (the QAT forward's quantize-dequantize, bfloat16 out).
+All inputs are resident in HBM before timing starts.  Prints ONE JSON line.
+
+value = 2*M*N*K / step time (TFLOP/s of the layer, whole step).  The roofline
+entry is for the dominant kernel (the GEMM), timed with HIP events on the
+stream the kernels run on.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "W4A4 GEMM TFLOPS & % FP4 MFMA peak (prefill); quantize/decode HBM GB/s"
+PEAK = {"fp4": 10100.0, "f16": 2500.0, "hbm": 8000.0}   # TFLOP/s, TFLOP/s, GB/s (MI355X published)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=4, help="workload number (4 = 14B gate/up)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, xb, wb):
+    """Time the CPU oracle (single thread, as it stands) on a bounded sample of
+    the same step and scale its per-element / per-MAC rates to the full step."""
+    import numpy as np
+    import oracle
+    fmt = oracle.FMT_NVFP4 if w.fmt == "nvfp4" else oracle.FMT_MXFP4
+    rows_x = 256
+    t0 = time.perf_counter()
+    wc, ws_, wg = oracle.quantize(fmt, wb)
+    t_qw = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    xc, xs, xg = oracle.quantize(fmt, np.ascontiguousarray(xb[:rows_x]))
+    t_qx = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.fakequant(fmt, np.ascontiguousarray(xb[:rows_x]))
+    t_fq = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.gemm(fmt, xc[:1], xs[:1], xg, wc, ws_, wg)
+    t_mm = time.perf_counter() - t0
+    per_q = (t_qw + t_qx) / ((w.N + rows_x) * w.K)
+    per_fq = t_fq / (rows_x * w.K)
+    per_mac = t_mm / (1 * w.N * w.K)
+    full = per_q * (w.M + w.N) * w.K + per_fq * (w.M + w.N) * w.K + per_mac * w.M * w.N * w.K
+    return {
+        "value": round(2.0 * w.M * w.N * w.K / full / 1e12, 9),
+        "unit": "TFLOP/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": ("oracle quantize of all of W and of 256 rows of X, fake-quant of 256 rows of X, "
+                   "FP64 GEMM of 1 row of X against all of W; per-element and per-MAC rates "
+                   "scaled to the full step (%.1f s of CPU work; full step would take %.0f s)"
+                   % (t_qw + t_qx + t_fq + t_mm, full)),
+        "host_threads_available": len(os.sched_getaffinity(0)),
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2606_15682_amd import reqat
+    from paper_2606_15682_amd import workloads as wl
+
+    reqat.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = wl.WORKLOADS[args.workload]
+    fmt = reqat.NVFP4 if w.fmt == "nvfp4" else reqat.MXFP4
+    B = reqat.BLOCK[fmt]
+    x_cpu, w_cpu = wl.make_x(w), wl.make_w(w)
+    x = x_cpu.to(dev)
+    wt = w_cpu.to(dev)
+    M, N, K = w.M, w.N, w.K
+
+    xc = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
+    xs = torch.empty((M, K // B), dtype=torch.uint8, device=dev)
+    wc = torch.empty((N, K // 2), dtype=torch.uint8, device=dev)
+    wsc = torch.empty((N, K // B), dtype=torch.uint8, device=dev)
+    gx = torch.empty(1, dtype=torch.float32, device=dev) if fmt == reqat.NVFP4 else None
+    gw = torch.empty(1, dtype=torch.float32, device=dev) if fmt == reqat.NVFP4 else None
+    gfx = torch.empty(1, dtype=torch.float32, device=dev) if fmt == reqat.NVFP4 else None
+    gfw = torch.empty(1, dtype=torch.float32, device=dev) if fmt == reqat.NVFP4 else None
+    y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    fx = torch.empty_like(x)
+    fw = torch.empty_like(wt)
+    names = ["quantize_x", "quantize_w", "gemm", "fakequant_x", "fakequant_w"]
+
+    def step(ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record()
+        mark(0)
+        reqat.quantize(x, fmt, out=(xc, xs), g_out=gx)
+        mark(1)
+        reqat.quantize(wt, fmt, out=(wc, wsc), g_out=gw)
+        mark(2)
+        reqat.gemm(fmt, xc, xs, gx, wc, wsc, gw, out_dtype=torch.bfloat16, out=y)
+        mark(3)
+        reqat.fakequant(x, fmt, out=fx, g_out=gfx)
+        mark(4)
+        reqat.fakequant(wt, fmt, out=fw, g_out=gfw)
+        mark(5)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    per = {n: float(np.mean([events[i][j].elapsed_time(events[i][j + 1]) for i in range(args.steps)]))
+           for j, n in enumerate(names)}
+
+    flops = 2.0 * M * N * K
+    q_bytes = lambda rows: rows * K * (2 + 0.5 + 1.0 / B)        # read bf16, write codes + scales
+    fq_bytes = lambda rows: rows * K * 4.0                        # read bf16, write bf16
+    gemm_tflops = flops / (per["gemm"] * 1e-3) / 1e12
+    mfma_dtype = "f16" if fmt == reqat.NVFP4 else "fp4"
+    kern = {
+        "gemm": {"ms": round(per["gemm"], 4), "TFLOP/s": round(gemm_tflops, 1),
+                 "frac_fp4_peak": round(gemm_tflops / PEAK["fp4"], 4),
+                 "frac_own_mfma_peak": round(gemm_tflops / PEAK[mfma_dtype], 4)},
+    }
+    for n, rows, fn in (("quantize_x", M, q_bytes), ("quantize_w", N, q_bytes),
+                        ("fakequant_x", M, fq_bytes), ("fakequant_w", N, fq_bytes)):
+        gbs = fn(rows) / (per[n] * 1e-3) / 1e9
+        kern[n] = {"ms": round(per[n], 4), "GB/s": round(gbs, 1),
+                   "frac_hbm_peak": round(gbs / PEAK["hbm"], 4),
+                   "note": "includes the absmax pass (its bytes not credited)"}
+
+    out = {
+        "metric": METRIC,
+        "value": round(flops / (ms_step * 1e-3) / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": mfma_dtype,
+        "data": "synthetic (seeded; Gaussian activations with 1% x20 outlier channels, N(0,0.02) weights)",
+        "config": {"workload": w.name, "M": M, "N": N, "K": K, "format": w.fmt,
+                   "gemm_out": "bf16", "global_batch": M, "parallelism": "single GPU",
+                   "step": "quantize X + quantize W (dynamic global scales) + W4A4 GEMM + "
+                           "fake-quant X and W"},
+        "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": PEAK[mfma_dtype],
+                     "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK[mfma_dtype], 4),
+                     "traffic": None,
+                     "kernel": "gemm_w4a4_kernel (%s)" % w.fmt},
+        "kernels": kern,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, wl.bf16_bits(x_cpu), wl.bf16_bits(w_cpu))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

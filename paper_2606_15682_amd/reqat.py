@@ -138,20 +138,23 @@ def workspace(device) -> torch.Tensor:
     return ws
 
 
-def _gscale(fmt, x, tensor_scale):
-    """(tensor_scale tensor or None, ts mode)."""
+def _gscale(fmt, x, tensor_scale, g_out=None):
+    """(tensor_scale tensor or None, ts mode).  g_out: preallocated 1-element
+    float32 tensor that receives the computed NVFP4 global scale."""
     if fmt == MXFP4:
         if tensor_scale is not None:
             raise ValueError("MXFP4 has no global scale")
         return None, TS_COMPUTE
     if tensor_scale is None:
+        if g_out is not None:
+            return g_out, TS_COMPUTE
         return torch.empty(1, dtype=torch.float32, device=x.device), TS_COMPUTE
     if isinstance(tensor_scale, torch.Tensor):
         return tensor_scale, TS_GIVEN
     return torch.tensor([float(tensor_scale)], dtype=torch.float32, device=x.device), TS_GIVEN
 
 
-def quantize(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out=None):
+def quantize(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out=None, g_out=None):
     """Quantize a 2-D bfloat16 CUDA tensor.  Returns (codes, scales, g) with g a
     1-element float32 tensor (NVFP4: computed unless given) or None (MXFP4)."""
     rows, cols, ldx = _x2d(x)
@@ -161,7 +164,7 @@ def quantize(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out=None):
     else:
         codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=x.device)
         scales = torch.empty((rows, cols // B), dtype=torch.uint8, device=x.device)
-    g, ts = _gscale(fmt, x, tensor_scale)
+    g, ts = _gscale(fmt, x, tensor_scale, g_out)
     ws = workspace(x.device)
     st = reqat_quantize_fp4(fmt, x.data_ptr(), rows, cols, ldx, codes.data_ptr(), scales.data_ptr(),
                             _ptr(g), ts, ws.data_ptr(), _stream(x.device))
@@ -169,11 +172,11 @@ def quantize(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out=None):
     return codes, scales, g
 
 
-def fakequant(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out=None):
+def fakequant(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out=None, g_out=None):
     """Quantize-dequantize to bfloat16.  Returns (y, g)."""
     rows, cols, ldx = _x2d(x)
     y = out if out is not None else torch.empty((rows, cols), dtype=torch.bfloat16, device=x.device)
-    g, ts = _gscale(fmt, x, tensor_scale)
+    g, ts = _gscale(fmt, x, tensor_scale, g_out)
     ws = workspace(x.device)
     st = reqat_fakequant_fp4(fmt, x.data_ptr(), rows, cols, ldx, y.data_ptr(), y.stride(0), _ptr(g),
                              ts, ws.data_ptr(), _stream(x.device))
