@@ -1,0 +1,100 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+benchmark uses.  Quantize outputs of the full X and W are compared with the
+oracle bit for bit; the GEMM is checked on sampled (m, n) outputs that the
+oracle evaluates one by one (plus the corners), against
+|Y - Yref| <= 1e-3 * sum_k |A^ B^|.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_15682_amd import reqat
+from paper_2606_15682_amd import workloads as wl
+from tests import indep
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def _quant_both(w):
+    fmt = reqat.NVFP4 if w.fmt == "nvfp4" else reqat.MXFP4
+    ofmt = oracle.FMT_NVFP4 if fmt == reqat.NVFP4 else oracle.FMT_MXFP4
+    x, wt = wl.make_x(w), wl.make_w(w)
+    out = {}
+    for name, t in (("x", x), ("w", wt)):
+        c, s, g = reqat.quantize(t.to(DEV), fmt)
+        torch.cuda.synchronize()
+        bits = wl.bf16_bits(t)
+        oc, os_, og = oracle.quantize(ofmt, bits)
+        assert np.array_equal(s.cpu().numpy(), os_), "%s scales differ" % name
+        assert np.array_equal(c.cpu().numpy(), oc), "%s codes differ" % name
+        if fmt == reqat.NVFP4:
+            assert float(g.cpu()[0]) == og
+        out[name] = (c, s, g, oc, os_, og, bits)
+        log("  %s quantize bit-exact (%d x %d)" % (name, t.shape[0], t.shape[1]))
+    return fmt, ofmt, out
+
+
+def _check_gemm(w, fmt, ofmt, q, out_dtype, npts=2000, seed=0):
+    xc, xs, xg, oxc, oxs, oxg, _ = q["x"]
+    wc, ws, wg, owc, ows, owg, _ = q["w"]
+    y = torch.full((w.M, w.N), float("nan"), dtype=out_dtype, device=DEV)
+    reqat.gemm(fmt, xc, xs, xg, wc, ws, wg, out_dtype=out_dtype, out=y)
+    torch.cuda.synchronize()
+    assert not torch.isnan(y).any().item(), "unwritten or NaN outputs"
+    rng = np.random.default_rng(seed)
+    ms = np.concatenate([rng.integers(0, w.M, npts), [0, 0, w.M - 1, w.M - 1]])
+    ns = np.concatenate([rng.integers(0, w.N, npts), [0, w.N - 1, 0, w.N - 1]])
+    ref, aref = oracle.gemm_points(ofmt, oxc, oxs, oxg, owc, ows, owg, ms, ns)
+    got = y[torch.from_numpy(ms).to(DEV), torch.from_numpy(ns).to(DEV)].float().cpu().numpy()
+    got = got.astype(np.float64)
+    if out_dtype == torch.float32:
+        err = np.abs(got - ref) / np.maximum(aref, 1e-300)
+        assert float(err.max()) <= 1e-3, float(err.max())
+    else:
+        rb = indep.bf16_values(oracle.bf16_from_double_array(ref))
+        ulp = np.maximum(np.abs(rb), 2.0 ** -133) * 2.0 ** -7
+        assert np.all(np.abs(got - rb) <= ulp + 1e-3 * aref)
+    log("  gemm %s sampled parity ok (%d points)" % (out_dtype, len(ms)))
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3])
+def test_fullsize_small_workloads(idx):
+    w = wl.WORKLOADS[idx]
+    log("full-size workload %d: %s" % (idx, w.name))
+    fmt, ofmt, q = _quant_both(w)
+    _check_gemm(w, fmt, ofmt, q, torch.float32, seed=idx)
+    _check_gemm(w, fmt, ofmt, q, torch.bfloat16, seed=idx + 10)
+
+
+def test_fullsize_14b_gate_up_nvfp4():
+    w = wl.WORKLOADS[4]
+    log("full-size workload 4: %s" % w.name)
+    fmt, ofmt, q = _quant_both(w)
+    _check_gemm(w, fmt, ofmt, q, torch.bfloat16, seed=4)
+    _check_gemm(w, fmt, ofmt, q, torch.float32, seed=5, npts=1000)
+
+
+def test_fullsize_14b_fakequant():
+    """Fake-quant (QAT forward) of the full X and a 4096-row slice of W, bit-exact."""
+    w = wl.WORKLOADS[4]
+    log("full-size fake-quant, workload 4")
+    for name, t in (("x", wl.make_x(w)), ("w", wl.make_w(w, rows=4096))):
+        y, g = reqat.fakequant(t.to(DEV), reqat.NVFP4)
+        torch.cuda.synchronize()
+        oy, og = oracle.fakequant(oracle.FMT_NVFP4, wl.bf16_bits(t))
+        assert float(g.cpu()[0]) == og
+        assert np.array_equal(wl.bf16_bits(y.cpu()), oy), "%s fake-quant differs" % name
+        log("  %s fake-quant bit-exact" % name)
+
+
+def test_fullsize_32b_down_mxfp4():
+    w = wl.WORKLOADS[5]
+    log("full-size workload 5: %s" % w.name)
+    fmt, ofmt, q = _quant_both(w)
+    _check_gemm(w, fmt, ofmt, q, torch.float32, seed=7, npts=1000)

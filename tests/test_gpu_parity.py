@@ -186,7 +186,6 @@ def test_special_values(fmt):
 def test_empty_tensor_writes_unit_global_scale():
     log("empty tensor")
     x = torch.empty((0, 64), dtype=torch.bfloat16, device=DEV)
-    g = torch.full((1,), 7.0, dtype=torch.float32, device=DEV)
     c, s, gg = reqat.quantize(x, NV, out=(torch.empty((0, 32), dtype=torch.uint8, device=DEV),
                                           torch.empty((0, 4), dtype=torch.uint8, device=DEV)))
     torch.cuda.synchronize()
@@ -241,7 +240,8 @@ def run_gemm_case(fmt, M, N, K, seed, dist="normal", wstd=0.02, g=(None, None), 
 
 @pytest.mark.parametrize("fmt", [NV, MX])
 @pytest.mark.parametrize("M,N,K", [(16, 256, 256), (37, 200, 384), (1, 1, 128), (130, 129, 512),
-                                   (256, 384, 1024), (5, 300, 128)])
+                                   (256, 384, 1024), (5, 300, 128), (300, 520, 768),
+                                   (257, 256, 2048), (512, 1000, 1280)])
 def test_gemm_parity(fmt, M, N, K):
     log("gemm parity fmt=%d M=%d N=%d K=%d" % (fmt, M, N, K))
     run_gemm_case(fmt, M, N, K, seed=M * 31 + N * 7 + K, dist="student_t")
