@@ -37,7 +37,20 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=4, help="workload number (4 = 14B gate/up)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="only run a plain device copy of this many bytes --steps times "
+                         "(calibrates rocprof FETCH_SIZE/WRITE_SIZE against a known size)")
     return ap.parse_args()
+
+
+def copy_calibration(nbytes: int, steps: int):
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": src.numel() * 4, "steps": steps}), flush=True)
 
 
 def cpu_baseline(w, xb, wb):
@@ -83,6 +96,9 @@ def main():
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
         sys.exit(2)
+    if args.copy_bytes:
+        copy_calibration(args.copy_bytes, args.steps)
+        return
 
     import numpy as np
     import torch

@@ -1,23 +1,31 @@
-// Large-tile W4A4 GEMM for gfx950 (K a multiple of 256).
+// Large-tile W4A4 GEMM for gfx950.
 //
 // Workgroup tile 256 x 256, four waves of 128 x 128 (4 x 4 MFMA tiles of 32 x 32,
-// 256 FP32 accumulators per lane).  K advances 256 elements per stage; each
-// stage's packed codes (128 B per row) and scale bytes go global -> LDS with
-// direct-to-LDS 16-byte loads (global_load_lds_dwordx4), double-buffered, so
-// the next stage streams in while the current one is multiplied.
+// 256 FP32 accumulators per lane, one wave per SIMD).  K advances KS elements
+// per stage; each stage's packed codes (KS/2 bytes per row) and scale bytes go
+// global -> LDS with direct-to-LDS loads (global_load_lds_dwordx4 / _dword)
+// into a ring of NBUF stage buffers: the loads of stage st + NBUF - 1 are
+// issued while stage st is multiplied, and the wait at the top of each stage
+// counts only the loads of the stages still in flight behind it (vmcnt).
 //
-// LDS code layout: one row = 8 chunks of 16 B (32 E2M1 codes each); chunk c of
-// row r is stored at chunk position c ^ (r & 7).  A wave's 16-byte operand read
-// has 8 consecutive rows at the same logical chunk in each group of 8 lanes,
-// which the XOR spreads over all 8 positions: no bank conflicts.  The
-// direct-to-LDS write of one instruction is 1 KB contiguous (8 rows), and each
-// lane fetches whichever 16 global bytes belong at its LDS slot.
+// LDS code layout: one row = CH chunks of 16 B (32 E2M1 codes each); chunk c of
+// row r is stored at chunk position c ^ f(r).  A wave's 16-byte operand read
+// puts consecutive rows at the same logical chunk on consecutive lanes, and f
+// spreads them: any 8 aligned consecutive rows land in 8 distinct 16-byte
+// slots of a 128-byte bank window and any 16 aligned rows in 16 distinct slots
+// of a 256-byte window, so the reads are free of bank conflicts for either 32
+// or 64 four-byte banks.
+//   CH = 8 (128-byte rows): f(r) = (r & 7) ^ ((r >> 3) & 1)
+//   CH = 4 ( 64-byte rows): f(r) = ((r >> 1) & 3) ^ ((r >> 3) & 1)
+// One direct-to-LDS instruction writes 1 KB contiguous, and each lane fetches
+// whichever 16 global bytes belong at its LDS slot.
 //
 // MXFP4 (v_mfma_scale_f32_32x32x64_f8f6f4, E2M1 x E2M1): in substep s of a
-// stage, lanes 0-31 feed 32-block s and lanes 32-63 feed 32-block 4 + s of
-// their row; a lane's four scale bytes for the stage are one dword and the
+// stage, lanes 0-31 feed 32-block s and lanes 32-63 feed 32-block KS/64 + s of
+// their row; the lane's scale bytes for the stage sit in one dword and the
 // instruction's op_sel picks byte s.  A and B use the same K assignment, so
-// the sum over K is unchanged.
+// the sum over K is unchanged.  The next substep's operands are read from LDS
+// before the current substep's MFMAs are issued.
 //
 // NVFP4 (v_mfma_f32_32x32x16_f16): per 64-element chunk a lane loads 32 codes
 // (16 B) and decodes 8 per MFMA step: v_cvt_scalef32_pk_f16_fp4 applies the
@@ -34,6 +42,19 @@
 #include "fp4_device.h"
 #include "internal.h"
 
+#ifndef REQAT_MX_KS
+#define REQAT_MX_KS 128
+#endif
+#ifndef REQAT_MX_NBUF
+#define REQAT_MX_NBUF 4
+#endif
+#ifndef REQAT_NV_KS
+#define REQAT_NV_KS 256
+#endif
+#ifndef REQAT_NV_NBUF
+#define REQAT_NV_NBUF 2
+#endif
+
 namespace reqat {
 
 namespace {
@@ -45,23 +66,32 @@ typedef _Float16 v2h __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kThreads = 256;
-constexpr int TM = 256, TN = 256, KS = 256;
-constexpr int ROW_BYTES = KS / 2;                       // 128
-constexpr int CODE_BYTES = TM * ROW_BYTES;              // 32 KB per operand per stage
+constexpr int TM = 256, TN = 256;
 constexpr int GROUP_M = 8;
 
-template <int FMT>
-struct Layout {
+template <int FMT, int KS, int NBUF>
+struct Cfg {
     static constexpr int B = FMT == kMX ? 32 : 16;
-    static constexpr int SB = KS / B;                   // scale bytes per row per stage (8 | 16)
-    static constexpr int SCALE_BYTES = TM * SB;
-    static constexpr int A_CODES = 0;
-    static constexpr int B_CODES = CODE_BYTES;
-    static constexpr int A_SC = 2 * CODE_BYTES;
-    static constexpr int B_SC = 2 * CODE_BYTES + SCALE_BYTES;
-    static constexpr int STAGE = 2 * CODE_BYTES + 2 * SCALE_BYTES;
-    static constexpr int LUT = 2 * STAGE;               // NVFP4 scale table (256 x 8 B)
-    static constexpr int TOTAL = 2 * STAGE + (FMT == kNV ? 2048 : 0);
+    static constexpr int ROW = KS / 2;                  // code bytes per row per stage
+    static constexpr int CH = ROW / 16;                 // 16-byte chunks per row
+    static constexpr int RPI = 1024 / ROW;              // rows per 1 KB load instruction
+    static constexpr int CODE = TM * ROW;               // code bytes per operand per stage
+    static constexpr int SB = KS / B;                   // scale bytes per row per stage
+    static constexpr int SCALE = TM * SB;
+    static constexpr int LS = SB >= 16 ? 16 : 4;        // bytes per lane of a scale load
+    static constexpr int SRPI = 64 * LS / SB;           // rows per scale load instruction
+    static constexpr int SINS = TM / SRPI;              // scale load instructions per operand
+    static constexpr int A_CODES = 0, B_CODES = CODE;
+    static constexpr int A_SC = 2 * CODE, B_SC = 2 * CODE + SCALE;
+    static constexpr int STAGE = 2 * CODE + 2 * SCALE;
+    static constexpr int LUT = NBUF * STAGE;            // NVFP4 scale table (256 x 8 B)
+    static constexpr int TOTAL = NBUF * STAGE + (FMT == kNV ? 2048 : 0);
+    static constexpr int CODE_LPW = (CODE / 1024) / 4;  // code loads per operand per wave
+    static constexpr int SCALE_LPW = SINS / 4;          // scale loads per operand per wave
+    static constexpr int LPS = 2 * CODE_LPW + 2 * SCALE_LPW;   // loads per wave per stage
+    static_assert(CH == 4 || CH == 8, "row must be 4 or 8 chunks");
+    static_assert(SINS % 4 == 0 && (CODE / 1024) % 4 == 0, "loads must split over 4 waves");
+    static_assert(TOTAL <= 160 * 1024, "LDS budget");
 };
 
 __device__ __forceinline__ void g2l16(const void *g, uint8_t *l) {
@@ -74,70 +104,96 @@ __device__ __forceinline__ void g2l4(const void *g, uint8_t *l) {
 __device__ __forceinline__ uint4 lds16(const uint8_t *p) { return *reinterpret_cast<const uint4 *>(p); }
 __device__ __forceinline__ uint32_t lds4(const uint8_t *p) { return *reinterpret_cast<const uint32_t *>(p); }
 
-// Issue the direct-to-LDS loads of one stage (this wave's share).  a/b point at
-// the first row of the tile and at column k0; full tiles use one per-lane
-// 32-bit offset plus wave-uniform steps, edge tiles clamp every row to the
-// last valid one (those rows are loaded but never stored).
-template <int FMT>
-__device__ __forceinline__ void load_stage(uint8_t *buf, int wave, int lane, bool full_a,
-                                           bool full_b, int64_t rows_a, int64_t rows_b,
-                                           int64_t cpr, int64_t spr,
-                                           const uint8_t *a_codes, const uint8_t *b_codes,
-                                           const uint8_t *a_scales, const uint8_t *b_scales) {
-    using L = Layout<FMT>;
-    const int sub = lane >> 3;                            // row within the 8-row instruction
-    const int c = (lane & 7) ^ sub;                       // logical chunk stored at this slot
-#pragma unroll
-    for (int jj = 0; jj < 8; ++jj) {
-        const int j = wave * 8 + jj;                      // 32 instructions per operand
-        int ra = 8 * j + sub, rb = ra;
-        if (!full_a) ra = ra < rows_a ? ra : (int)rows_a - 1;
-        if (!full_b) rb = rb < rows_b ? rb : (int)rows_b - 1;
-        g2l16(a_codes + (int64_t)ra * cpr + c * 16, buf + L::A_CODES + j * 1024);
-        g2l16(b_codes + (int64_t)rb * cpr + c * 16, buf + L::B_CODES + j * 1024);
-    }
-    if constexpr (FMT == kMX) {
-        // 8 scale bytes per row: 8 instructions of 64 x 4 B per operand, two per wave
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-            const int j = wave * 2 + jj;
-            int ra = 32 * j + (lane >> 1), rb = ra;
-            if (!full_a) ra = ra < rows_a ? ra : (int)rows_a - 1;
-            if (!full_b) rb = rb < rows_b ? rb : (int)rows_b - 1;
-            g2l4(a_scales + (int64_t)ra * spr + (lane & 1) * 4, buf + L::A_SC + j * 256);
-            g2l4(b_scales + (int64_t)rb * spr + (lane & 1) * 4, buf + L::B_SC + j * 256);
-        }
+template <int CH>
+__device__ __forceinline__ int swz(int r) {
+    return CH == 8 ? ((r & 7) ^ ((r >> 3) & 1)) : (((r >> 1) & 3) ^ ((r >> 3) & 1));
+}
+
+// Byte offset of logical 16-byte chunk c of tile row r.
+template <int ROW>
+__device__ __forceinline__ int code_off(int r, int c) {
+    return r * ROW + ((c ^ swz<ROW / 16>(r)) << 4);
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Load number IDX (0 .. LPS-1) of this wave's share of one stage.  a/b point at
+// the first row of the tile and at the stage's first column; edge tiles clamp
+// rows to the last valid one (those rows are loaded but never stored).
+template <class C, int IDX>
+__device__ __forceinline__ void load_one(uint8_t *buf, int wave, int lane, int rows_a, int rows_b,
+                                         int64_t cpr, int64_t spr, const uint8_t *a_codes,
+                                         const uint8_t *b_codes, const uint8_t *a_scales,
+                                         const uint8_t *b_scales) {
+    if constexpr (IDX < 2 * C::CODE_LPW) {
+        constexpr bool isA = IDX < C::CODE_LPW;
+        const int j = wave * C::CODE_LPW + (isA ? IDX : IDX - C::CODE_LPW);
+        const int row = C::RPI * j + lane / C::CH;
+        const int c = (lane % C::CH) ^ swz<C::CH>(row);
+        const int lim = isA ? rows_a : rows_b;
+        const int r = row < lim ? row : lim - 1;
+        g2l16((isA ? a_codes : b_codes) + (int64_t)r * cpr + c * 16,
+              buf + (isA ? C::A_CODES : C::B_CODES) + j * 1024);
     } else {
-        // 16 scale bytes per row: 4 instructions of 64 x 16 B per operand, one per wave
-        int ra = 64 * wave + lane, rb = ra;
-        if (!full_a) ra = ra < rows_a ? ra : (int)rows_a - 1;
-        if (!full_b) rb = rb < rows_b ? rb : (int)rows_b - 1;
-        g2l16(a_scales + (int64_t)ra * spr, buf + L::A_SC + wave * 1024);
-        g2l16(b_scales + (int64_t)rb * spr, buf + L::B_SC + wave * 1024);
+        constexpr int k = IDX - 2 * C::CODE_LPW;
+        constexpr bool isA = k < C::SCALE_LPW;
+        const int j = wave * C::SCALE_LPW + (isA ? k : k - C::SCALE_LPW);
+        constexpr int PPR = C::SB / C::LS;              // lanes per row
+        const int row = C::SRPI * j + lane / PPR;
+        const int piece = lane % PPR;
+        const int lim = isA ? rows_a : rows_b;
+        const int r = row < lim ? row : lim - 1;
+        const uint8_t *src = (isA ? a_scales : b_scales) + (int64_t)r * spr + piece * C::LS;
+        uint8_t *dst = buf + (isA ? C::A_SC : C::B_SC) + j * (64 * C::LS);
+        if constexpr (C::LS == 16) g2l16(src, dst);
+        else g2l4(src, dst);
     }
 }
 
-// Byte address of logical 16-byte chunk c of tile row r.
-__device__ __forceinline__ int code_off(int r, int c) { return r * ROW_BYTES + ((c ^ (r & 7)) << 4); }
+// Loads [LO, HI) of this wave's share of one stage.
+template <class C, int LO, int HI>
+__device__ __forceinline__ void load_range(uint8_t *buf, int wave, int lane, int rows_a, int rows_b,
+                                           int64_t cpr, int64_t spr, const uint8_t *ac,
+                                           const uint8_t *bc, const uint8_t *as_, const uint8_t *bs_) {
+    if constexpr (LO < HI) {
+        load_one<C, LO>(buf, wave, lane, rows_a, rows_b, cpr, spr, ac, bc, as_, bs_);
+        load_range<C, LO + 1, HI>(buf, wave, lane, rows_a, rows_b, cpr, spr, ac, bc, as_, bs_);
+    }
+}
+
+// Issues the loads of one later stage in four parts (part P covers loads
+// [P*LPS/4, (P+1)*LPS/4) of this wave's share), or nothing when no stage is left.
+template <class C>
+struct StageIssue {
+    uint8_t *buf;
+    bool active;
+    int wave, lane, rows_a, rows_b;
+    int64_t cpr, spr;
+    const uint8_t *ac, *bc, *as_, *bs_;
+    template <int P>
+    __device__ __forceinline__ void part() {
+        if (active)
+            load_range<C, P * C::LPS / 4, (P + 1) * C::LPS / 4>(buf, wave, lane, rows_a, rows_b, cpr,
+                                                                 spr, ac, bc, as_, bs_);
+    }
+};
+
+__device__ __forceinline__ v8i as_v8i(uint4 q) {
+    return v8i{(int)q.x, (int)q.y, (int)q.z, (int)q.w, 0, 0, 0, 0};
+}
 
 template <int S>
-__device__ __forceinline__ void mx_substep(v16f (&acc)[4][4], const uint8_t *buf, int rA0, int rB0,
-                                           int h, const uint32_t (&sa)[4], const uint32_t (&sb)[4]) {
-    using L = Layout<kMX>;
-    v8i av[4], bv[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        uint4 q = lds16(buf + L::A_CODES + code_off(rA0 + 32 * i, 4 * h + S));
-        av[i] = v8i{(int)q.x, (int)q.y, (int)q.z, (int)q.w, 0, 0, 0, 0};
-        uint4 p = lds16(buf + L::B_CODES + code_off(rB0 + 32 * i, 4 * h + S));
-        bv[i] = v8i{(int)p.x, (int)p.y, (int)p.z, (int)p.w, 0, 0, 0, 0};
-    }
+__device__ __forceinline__ void mx_mfma16(v16f (&acc)[4][4], const uint4 (&a)[4], const uint4 (&b)[4],
+                                          const uint32_t (&sa)[4], const uint32_t (&sb)[4]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                av[i], bv[j], acc[i][j], 4, 4, S, (int)sa[i], S, (int)sb[j]);
+                as_v8i(a[i]), as_v8i(b[j]), acc[i][j], 4, 4, S, (int)sa[i], S, (int)sb[j]);
 }
 
 // Eight codes (one dword) times an NVFP4 block scale -> FP16 (exact).
@@ -149,13 +205,131 @@ __device__ __forceinline__ v8h nv_decode8(uint32_t c, float pow2, v2h mant) {
     return v8h{p0[0], p0[1], p1[0], p1[1], p2[0], p2[1], p3[0], p3[1]};
 }
 
-template <int FMT>
+__device__ __forceinline__ uint32_t pick(const uint4 &q, int s) {
+    return s == 0 ? q.x : s == 1 ? q.y : s == 2 ? q.z : q.w;
+}
+
+// MXFP4: one stage from LDS buffer `buf`, with the loads of a later stage
+// issued in parts between the substeps.
+template <class C, class Issue>
+__device__ __forceinline__ void mx_stage(v16f (&acc)[4][4], const uint8_t *buf, int rA0, int rB0,
+                                         int h, Issue &issue) {
+    constexpr int NSUB = C::CH / 2;                     // K=64 substeps per stage
+    uint32_t sa[4], sb[4];
+    uint4 a0[4], b0[4], a1[4], b1[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int ra = rA0 + 32 * i, rb = rB0 + 32 * i;
+        if constexpr (C::SB == 8) {
+            sa[i] = lds4(buf + C::A_SC + ra * 8 + 4 * h);
+            sb[i] = lds4(buf + C::B_SC + rb * 8 + 4 * h);
+        } else {
+            sa[i] = lds4(buf + C::A_SC + ra * 4) >> (16 * h);
+            sb[i] = lds4(buf + C::B_SC + rb * 4) >> (16 * h);
+        }
+        a0[i] = lds16(buf + C::A_CODES + code_off<C::ROW>(ra, NSUB * h));
+        b0[i] = lds16(buf + C::B_CODES + code_off<C::ROW>(rb, NSUB * h));
+    }
+#define REQAT_MX_READ(A, B, S)                                                           \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                      \
+        A[i] = lds16(buf + C::A_CODES + code_off<C::ROW>(rA0 + 32 * i, NSUB * h + (S))); \
+        B[i] = lds16(buf + C::B_CODES + code_off<C::ROW>(rB0 + 32 * i, NSUB * h + (S))); \
+    }
+    REQAT_MX_READ(a1, b1, 1);
+    issue.template part<0>();
+    __builtin_amdgcn_sched_barrier(0);
+    mx_mfma16<0>(acc, a0, b0, sa, sb);
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (NSUB == 4) {
+        REQAT_MX_READ(a0, b0, 2);
+        issue.template part<1>();
+        __builtin_amdgcn_sched_barrier(0);
+        mx_mfma16<1>(acc, a1, b1, sa, sb);
+        __builtin_amdgcn_sched_barrier(0);
+        REQAT_MX_READ(a1, b1, 3);
+        issue.template part<2>();
+        __builtin_amdgcn_sched_barrier(0);
+        mx_mfma16<2>(acc, a0, b0, sa, sb);
+        __builtin_amdgcn_sched_barrier(0);
+        issue.template part<3>();
+        __builtin_amdgcn_sched_barrier(0);
+        mx_mfma16<3>(acc, a1, b1, sa, sb);
+    } else {
+        issue.template part<1>();
+        issue.template part<2>();
+        issue.template part<3>();
+        __builtin_amdgcn_sched_barrier(0);
+        mx_mfma16<1>(acc, a1, b1, sa, sb);
+    }
+#undef REQAT_MX_READ
+}
+
+// NVFP4: one stage from LDS buffer `buf`.
+template <class C, class Issue>
+__device__ __forceinline__ void nv_stage(v16f (&acc)[4][4], const uint8_t *buf, const uint2 *lut,
+                                         int rA0, int rB0, int h, Issue &issue) {
+    constexpr int NQ = C::CH / 2;                       // 64-element chunks per stage
+    uint4 ca[2][4], cb[2][4];
+    uint2 ea[2][4][2], eb[2][4][2];
+#define REQAT_NV_READ(Q, D)                                                                    \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                            \
+        const int ra = rA0 + 32 * i, rb = rB0 + 32 * i;                                        \
+        ca[D][i] = lds16(buf + C::A_CODES + code_off<C::ROW>(ra, 2 * (Q) + h));                \
+        cb[D][i] = lds16(buf + C::B_CODES + code_off<C::ROW>(rb, 2 * (Q) + h));                \
+        const uint32_t wa = lds4(buf + C::A_SC + ra * C::SB + 4 * (Q));                        \
+        const uint32_t wb = lds4(buf + C::B_SC + rb * C::SB + 4 * (Q));                        \
+        _Pragma("unroll") for (int hb = 0; hb < 2; ++hb) {                                     \
+            ea[D][i][hb] = lut[(wa >> (8 * (2 * h + hb))) & 0xFFu];                            \
+            eb[D][i][hb] = lut[(wb >> (8 * (2 * h + hb))) & 0xFFu];                            \
+        }                                                                                      \
+    }
+    REQAT_NV_READ(0, 0);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+        const int d = q & 1;
+        if (q + 1 < NQ) { REQAT_NV_READ(q + 1, d ^ 1); }
+        if (NQ == 4) {
+            switch (q) {
+            case 0: issue.template part<0>(); break;
+            case 1: issue.template part<1>(); break;
+            case 2: issue.template part<2>(); break;
+            default: issue.template part<3>(); break;
+            }
+        } else if (q == 0) {
+            issue.template part<0>();
+            issue.template part<1>();
+        } else {
+            issue.template part<2>();
+            issue.template part<3>();
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) {
+            v8h av[4], bv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint2 e = ea[d][i][s2 >> 1], f = eb[d][i][s2 >> 1];
+                av[i] = nv_decode8(pick(ca[d][i], s2), f32_from_bits(e.x), __builtin_bit_cast(v2h, e.y));
+                bv[i] = nv_decode8(pick(cb[d][i], s2), f32_from_bits(f.x), __builtin_bit_cast(v2h, f.y));
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i], bv[j], acc[i][j], 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+#undef REQAT_NV_READ
+}
+
+template <int FMT, int KS, int NBUF>
 __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(
     int64_t M, int64_t N, int64_t K, const uint8_t *__restrict__ a_codes,
     const uint8_t *__restrict__ a_scales, const float *__restrict__ ga,
     const uint8_t *__restrict__ b_codes, const uint8_t *__restrict__ b_scales,
     const float *__restrict__ gb, void *__restrict__ y, int y_bf16, int64_t ldy) {
-    using L = Layout<FMT>;
+    using C = Cfg<FMT, KS, NBUF>;
     extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -172,18 +346,18 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(
     const int64_t gsz = (tm_n - first_m) < GROUP_M ? (tm_n - first_m) : GROUP_M;
     const int64_t tm = first_m + (t % width) % gsz, tn = (t % width) / gsz;
     const int64_t m0 = tm * TM, n0 = tn * TN;
-    const int64_t cpr = K / 2, spr = K / L::B;
+    const int64_t cpr = K / 2, spr = K / C::B;
 
     if constexpr (FMT == kNV) {
         // (pow2 operand for the convert, mantissa pair for the multiply) per E4M3 byte
-        uint32_t b = tid;
-        float s = e4m3_value(b);
-        uint32_t sb = bits_from_f32(s);
+        const uint32_t b = tid;
+        const float s = e4m3_value(b);
+        const uint32_t sbits = bits_from_f32(s);
         _Float16 mh;
         if (s != s) mh = __builtin_bit_cast(_Float16, (uint16_t)0x7E00);
-        else mh = (_Float16)f32_from_bits((sb & 0x807FFFFFu) | 0x3F800000u);
-        uint32_t mm = (uint32_t)__builtin_bit_cast(uint16_t, mh);
-        reinterpret_cast<uint2 *>(smem + L::LUT)[b] = make_uint2(sb, mm | (mm << 16));
+        else mh = (_Float16)f32_from_bits((sbits & 0x807FFFFFu) | 0x3F800000u);
+        const uint32_t mm = (uint32_t)__builtin_bit_cast(uint16_t, mh);
+        reinterpret_cast<uint2 *>(smem + C::LUT)[b] = make_uint2(sbits, mm | (mm << 16));
     }
 
     v16f acc[4][4];
@@ -194,76 +368,40 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-    const int64_t nst = K / KS;
-    const int64_t rows_a = M - m0, rows_b = N - n0;
-    const bool full_a = rows_a >= TM, full_b = rows_b >= TN;
+    const int nst = (int)(K / KS);
+    const int rows_a = (int)(M - m0 < TM ? M - m0 : TM), rows_b = (int)(N - n0 < TN ? N - n0 : TN);
     const uint8_t *ac = a_codes + m0 * cpr, *bc = b_codes + n0 * cpr;
     const uint8_t *as_ = a_scales + m0 * spr, *bs_ = b_scales + n0 * spr;
-    load_stage<FMT>(smem, wave, lane, full_a, full_b, rows_a, rows_b, cpr, spr, ac, bc, as_, bs_);
+
+    // prologue: the first NBUF - 1 stages
+#pragma unroll
+    for (int p = 0; p < NBUF - 1; ++p) {
+        if (p < nst)
+            load_range<C, 0, C::LPS>(smem + p * C::STAGE, wave, lane, rows_a, rows_b, cpr, spr,
+                                     ac + (int64_t)p * KS / 2, bc + (int64_t)p * KS / 2,
+                                     as_ + (int64_t)p * KS / C::B, bs_ + (int64_t)p * KS / C::B);
+    }
 
     const int rA0 = wm * 128 + (lane & 31);               // this lane's A row in tile i: rA0 + 32 i
     const int rB0 = wn * 128 + (lane & 31);
 
-    for (int64_t st = 0; st < nst; ++st) {
-        uint8_t *buf = smem + (st & 1) * L::STAGE;
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    for (int st = 0; st < nst; ++st) {
+        // stage st has landed once no more than (stages issued after it) x LPS loads remain
+        const int behind = (nst - 1 - st) < (NBUF - 2) ? (nst - 1 - st) : (NBUF - 2);
+        if (NBUF >= 3 && behind == NBUF - 2) wait_vmcnt<(NBUF >= 3 ? NBUF - 2 : 0) * C::LPS>();
+        else if (NBUF >= 4 && behind == 1) wait_vmcnt<C::LPS>();
+        else wait_vmcnt<0>();
         __syncthreads();
-        if (st + 1 < nst) {
-            const int64_t k1 = (st + 1) * KS;
-            load_stage<FMT>(smem + ((st + 1) & 1) * L::STAGE, wave, lane, full_a, full_b, rows_a,
-                            rows_b, cpr, spr, ac + k1 / 2, bc + k1 / 2, as_ + k1 / L::B,
-                            bs_ + k1 / L::B);
-        }
 
+        const uint8_t *buf = smem + (st % NBUF) * C::STAGE;
+        const int nx = st + NBUF - 1;                      // stage whose loads go out now
+        const int64_t kx = (int64_t)nx * KS;
+        StageIssue<C> issue{smem + (nx % NBUF) * C::STAGE, nx < nst, wave, lane, rows_a, rows_b,
+                            cpr, spr, ac + kx / 2, bc + kx / 2, as_ + kx / C::B, bs_ + kx / C::B};
         if constexpr (FMT == kMX) {
-            uint32_t sa[4], sb[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                sa[i] = lds4(buf + L::A_SC + (rA0 + 32 * i) * 8 + 4 * h);
-                sb[i] = lds4(buf + L::B_SC + (rB0 + 32 * i) * 8 + 4 * h);
-            }
-            mx_substep<0>(acc, buf, rA0, rB0, h, sa, sb);
-            mx_substep<1>(acc, buf, rA0, rB0, h, sa, sb);
-            mx_substep<2>(acc, buf, rA0, rB0, h, sa, sb);
-            mx_substep<3>(acc, buf, rA0, rB0, h, sa, sb);
+            mx_stage<C>(acc, buf, rA0, rB0, h, issue);
         } else {
-            const uint2 *lut = reinterpret_cast<const uint2 *>(smem + L::LUT);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {               // 64-element chunks
-                uint4 ca[4], cb[4];
-                uint2 ea[4][2], eb[4][2];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int ra = rA0 + 32 * i, rb = rB0 + 32 * i;
-                    ca[i] = lds16(buf + L::A_CODES + code_off(ra, 2 * q + h));
-                    cb[i] = lds16(buf + L::B_CODES + code_off(rb, 2 * q + h));
-                    uint32_t wa = lds4(buf + L::A_SC + ra * 16 + 4 * q);
-                    uint32_t wb = lds4(buf + L::B_SC + rb * 16 + 4 * q);
-#pragma unroll
-                    for (int hb = 0; hb < 2; ++hb) {
-                        ea[i][hb] = lut[(wa >> (8 * (2 * h + hb))) & 0xFFu];
-                        eb[i][hb] = lut[(wb >> (8 * (2 * h + hb))) & 0xFFu];
-                    }
-                }
-#pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    v8h av[4], bv[4];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const uint32_t wa = s == 0 ? ca[i].x : s == 1 ? ca[i].y : s == 2 ? ca[i].z : ca[i].w;
-                        const uint32_t wb = s == 0 ? cb[i].x : s == 1 ? cb[i].y : s == 2 ? cb[i].z : cb[i].w;
-                        const uint2 e = ea[i][s >> 1], f = eb[i][s >> 1];
-                        av[i] = nv_decode8(wa, f32_from_bits(e.x), __builtin_bit_cast(v2h, e.y));
-                        bv[i] = nv_decode8(wb, f32_from_bits(f.x), __builtin_bit_cast(v2h, f.y));
-                    }
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-#pragma unroll
-                        for (int j = 0; j < 4; ++j)
-                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i], bv[j], acc[i][j],
-                                                                                0, 0, 0);
-                }
-            }
+            nv_stage<C>(acc, buf, reinterpret_cast<const uint2 *>(smem + C::LUT), rA0, rB0, h, issue);
         }
     }
 
@@ -289,33 +427,37 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(
         }
 }
 
+template <int FMT, int KS, int NBUF>
+hipError_t launch_cfg(int64_t M, int64_t N, int64_t K, const uint8_t *a_codes, const uint8_t *a_scales,
+                      const float *ga, const uint8_t *b_codes, const uint8_t *b_scales,
+                      const float *gb, void *y, bool y_bf16, int64_t ldy, hipStream_t stream) {
+    const int64_t tiles = ((M + TM - 1) / TM) * ((N + TN - 1) / TN);
+    const size_t lds = Cfg<FMT, KS, NBUF>::TOTAL;
+    hipError_t e = hipFuncSetAttribute((const void *)gemm_tile256_kernel<FMT, KS, NBUF>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((gemm_tile256_kernel<FMT, KS, NBUF>), dim3((unsigned)tiles), dim3(kThreads), lds,
+                       stream, M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, (int)y_bf16,
+                       ldy);
+    return hipGetLastError();
+}
+
 }  // namespace
 
-bool gemm_tile256_supported(int64_t M, int64_t N, int64_t K) {
-    return K > 0 && K % KS == 0 && M > 0 && N > 0;
+bool gemm_tile256_supported(Fmt fmt, int64_t M, int64_t N, int64_t K) {
+    const int ks = fmt == kMX ? REQAT_MX_KS : REQAT_NV_KS;
+    return K > 0 && K % ks == 0 && M > 0 && N > 0 && K / ks < (int64_t(1) << 30);
 }
 
 hipError_t launch_gemm_tile256(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *a_codes,
                                const uint8_t *a_scales, const float *ga, const uint8_t *b_codes,
                                const uint8_t *b_scales, const float *gb, void *y, bool y_bf16,
                                int64_t ldy, hipStream_t stream) {
-    const int64_t tiles = ((M + TM - 1) / TM) * ((N + TN - 1) / TN);
-    if (fmt == kMX) {
-        const size_t lds = Layout<kMX>::TOTAL;
-        hipError_t e = hipFuncSetAttribute((const void *)gemm_tile256_kernel<kMX>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(gemm_tile256_kernel<kMX>, dim3((unsigned)tiles), dim3(kThreads), lds, stream,
-                           M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, (int)y_bf16, ldy);
-    } else {
-        const size_t lds = Layout<kNV>::TOTAL;
-        hipError_t e = hipFuncSetAttribute((const void *)gemm_tile256_kernel<kNV>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(gemm_tile256_kernel<kNV>, dim3((unsigned)tiles), dim3(kThreads), lds, stream,
-                           M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, (int)y_bf16, ldy);
-    }
-    return hipGetLastError();
+    if (fmt == kMX)
+        return launch_cfg<kMX, REQAT_MX_KS, REQAT_MX_NBUF>(M, N, K, a_codes, a_scales, ga, b_codes,
+                                                           b_scales, gb, y, y_bf16, ldy, stream);
+    return launch_cfg<kNV, REQAT_NV_KS, REQAT_NV_NBUF>(M, N, K, a_codes, a_scales, ga, b_codes,
+                                                       b_scales, gb, y, y_bf16, ldy, stream);
 }
 
 }  // namespace reqat
