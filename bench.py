@@ -27,6 +27,38 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "W4A4 GEMM TFLOPS & % FP4 MFMA peak (prefill); quantize/decode HBM GB/s"
+GEMM_SOURCES = ["paper_2606_15682_amd/csrc/gemm_tile256.hip", "paper_2606_15682_amd/csrc/gemm.hip",
+                "paper_2606_15682_amd/csrc/fp4_device.h", "paper_2606_15682_amd/csrc/internal.h"]
+
+
+def gemm_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in GEMM_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def profiled_traffic(fmt_name: str, workload: int):
+    """HBM bytes per GEMM launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    summary (each counter scaled by its reading for a plain copy of known size);
+    None when there is no summary or the GEMM sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "gemm_%s_workload%d_traffic.txt" % (fmt_name, workload))
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("gemm_source_sha256") != gemm_source_hash():
+        return None
+    try:
+        return float(kv["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 PEAK = {"fp4": 10100.0, "f16": 2500.0, "hbm": 8000.0}   # TFLOP/s, TFLOP/s, GB/s (MI355X published)
 
 
@@ -69,12 +101,13 @@ def cpu_baseline(w, xb, wb):
     t0 = time.perf_counter()
     oracle.fakequant(fmt, np.ascontiguousarray(xb[:rows_x]))
     t_fq = time.perf_counter() - t0
+    gemm_rows = 4
     t0 = time.perf_counter()
-    oracle.gemm(fmt, xc[:1], xs[:1], xg, wc, ws_, wg)
+    oracle.gemm(fmt, xc[:gemm_rows], xs[:gemm_rows], xg, wc, ws_, wg)
     t_mm = time.perf_counter() - t0
     per_q = (t_qw + t_qx) / ((w.N + rows_x) * w.K)
     per_fq = t_fq / (rows_x * w.K)
-    per_mac = t_mm / (1 * w.N * w.K)
+    per_mac = t_mm / (gemm_rows * w.N * w.K)
     full = per_q * (w.M + w.N) * w.K + per_fq * (w.M + w.N) * w.K + per_mac * w.M * w.N * w.K
     return {
         "value": round(2.0 * w.M * w.N * w.K / full / 1e12, 9),
@@ -82,7 +115,7 @@ def cpu_baseline(w, xb, wb):
         "cores": 1,
         "kind": "oracle",
         "sample": ("oracle quantize of all of W and of 256 rows of X, fake-quant of 256 rows of X, "
-                   "FP64 GEMM of 1 row of X against all of W; per-element and per-MAC rates "
+                   "FP64 GEMM of 4 rows of X against all of W; per-element and per-MAC rates "
                    "scaled to the full step (%.1f s of CPU work; full step would take %.0f s)"
                    % (t_qw + t_qx + t_fq + t_mm, full)),
         "host_threads_available": len(os.sched_getaffinity(0)),
@@ -196,7 +229,7 @@ def main():
                            "fake-quant X and W"},
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": PEAK[mfma_dtype],
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK[mfma_dtype], 4),
-                     "traffic": None,
+                     "traffic": profiled_traffic(w.fmt, args.workload),
                      "kernel": "gemm_w4a4_kernel (%s)" % w.fmt},
         "kernels": kern,
     }
