@@ -230,7 +230,7 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": PEAK[mfma_dtype],
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK[mfma_dtype], 4),
                      "traffic": profiled_traffic(w.fmt, args.workload),
-                     "kernel": "gemm_w4a4_kernel (%s)" % w.fmt},
+                     "kernel": "gemm_tile256_kernel (%s W4A4 GEMM)" % w.fmt},
         "kernels": kern,
     }
     if not args.no_cpu_baseline:

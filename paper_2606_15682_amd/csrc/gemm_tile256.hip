@@ -6,7 +6,8 @@
 // global -> LDS with direct-to-LDS loads (global_load_lds_dwordx4 / _dword)
 // into a ring of NBUF stage buffers: the loads of stage st + NBUF - 1 are
 // issued while stage st is multiplied, and the wait at the top of each stage
-// counts only the loads of the stages still in flight behind it (vmcnt).
+// counts only the loads of the stages still in flight behind it (vmcnt) and is
+// followed by a bare s_barrier (no fence that would drain those loads).
 //
 // LDS code layout: one row = CH chunks of 16 B (32 E2M1 codes each); chunk c of
 // row r is stored at chunk position c ^ f(r).  A wave's 16-byte operand read
@@ -28,12 +29,13 @@
 // before the current substep's MFMAs are issued.
 //
 // NVFP4 (v_mfma_f32_32x32x16_f16): per 64-element chunk a lane loads 32 codes
-// (16 B) and decodes 8 per MFMA step: v_cvt_scalef32_pk_f16_fp4 applies the
-// power-of-two part of the E4M3 block scale (the instruction reads only the
-// exponent of its FP32 scale operand) and v_pk_mul_f16 the 4-bit mantissa
-// part; code * scale has <= 6 significant bits within FP16's normal range, so
-// both steps are exact.  The per-byte (scale, mantissa) pairs come from a
-// 256-entry table built in LDS at kernel start.
+// (16 B) and the two E4M3 scale bytes of its two 16-blocks (one 16-bit LDS
+// read).  v_cvt_scalef32_pk_f16_fp8 turns the two scale bytes into FP16 (every
+// E4M3 value, subnormals and NaN included, is exact in FP16), and each step
+// decodes 8 codes with v_cvt_scalef32_pk_f16_fp4 (unit scale) and multiplies
+// them by their block's scale with v_pk_mul_f16 (op_sel picks the half).
+// code * scale has <= 6 significant bits and lies in [2^-10, 2688], so the
+// product is exact and the FP16 MFMA sums exactly the terms of the definition.
 //
 // Tile order: workgroups are dealt round-robin to the 8 XCDs, so workgroup b
 // is mapped to the (b % 8)-th contiguous range of tiles, and tiles are walked
@@ -84,8 +86,7 @@ struct Cfg {
     static constexpr int A_CODES = 0, B_CODES = CODE;
     static constexpr int A_SC = 2 * CODE, B_SC = 2 * CODE + SCALE;
     static constexpr int STAGE = 2 * CODE + 2 * SCALE;
-    static constexpr int LUT = NBUF * STAGE;            // NVFP4 scale table (256 x 8 B)
-    static constexpr int TOTAL = NBUF * STAGE + (FMT == kNV ? 2048 : 0);
+    static constexpr int TOTAL = NBUF * STAGE;
     static constexpr int CODE_LPW = (CODE / 1024) / 4;  // code loads per operand per wave
     static constexpr int SCALE_LPW = SINS / 4;          // scale loads per operand per wave
     static constexpr int LPS = 2 * CODE_LPW + 2 * SCALE_LPW;   // loads per wave per stage
@@ -135,7 +136,8 @@ __device__ __forceinline__ void load_one(uint8_t *buf, int wave, int lane, int r
         const int c = (lane % C::CH) ^ swz<C::CH>(row);
         const int lim = isA ? rows_a : rows_b;
         const int r = row < lim ? row : lim - 1;
-        g2l16((isA ? a_codes : b_codes) + (int64_t)r * cpr + c * 16,
+        // 32-bit lane offset from a wave-uniform base (the launcher bounds 256 * K / 2 below 2^32)
+        g2l16((isA ? a_codes : b_codes) + (uint32_t)(r * (uint32_t)cpr + c * 16),
               buf + (isA ? C::A_CODES : C::B_CODES) + j * 1024);
     } else {
         constexpr int k = IDX - 2 * C::CODE_LPW;
@@ -146,7 +148,7 @@ __device__ __forceinline__ void load_one(uint8_t *buf, int wave, int lane, int r
         const int piece = lane % PPR;
         const int lim = isA ? rows_a : rows_b;
         const int r = row < lim ? row : lim - 1;
-        const uint8_t *src = (isA ? a_scales : b_scales) + (int64_t)r * spr + piece * C::LS;
+        const uint8_t *src = (isA ? a_scales : b_scales) + (uint32_t)(r * (uint32_t)spr + piece * C::LS);
         uint8_t *dst = buf + (isA ? C::A_SC : C::B_SC) + j * (64 * C::LS);
         if constexpr (C::LS == 16) g2l16(src, dst);
         else g2l4(src, dst);
@@ -174,11 +176,16 @@ struct StageIssue {
     int64_t cpr, spr;
     const uint8_t *ac, *bc, *as_, *bs_;
     template <int P>
-    __device__ __forceinline__ void part() {
+    __device__ __forceinline__ void part() { region<P, 4>(); }
+    // Region R of NR: loads [R*LPS/NR, (R+1)*LPS/NR).
+    template <int R, int NR>
+    __device__ __forceinline__ void region() {
         if (active)
-            load_range<C, P * C::LPS / 4, (P + 1) * C::LPS / 4>(buf, wave, lane, rows_a, rows_b, cpr,
-                                                                 spr, ac, bc, as_, bs_);
+            load_range<C, R * C::LPS / NR, (R + 1) * C::LPS / NR>(buf, wave, lane, rows_a, rows_b, cpr,
+                                                                   spr, ac, bc, as_, bs_);
     }
+    template <int R, int NR>
+    static constexpr int count() { return (R + 1) * C::LPS / NR - R * C::LPS / NR; }
 };
 
 __device__ __forceinline__ v8i as_v8i(uint4 q) {
@@ -196,12 +203,12 @@ __device__ __forceinline__ void mx_mfma16(v16f (&acc)[4][4], const uint4 (&a)[4]
                 as_v8i(a[i]), as_v8i(b[j]), acc[i][j], 4, 4, S, (int)sa[i], S, (int)sb[j]);
 }
 
-// Eight codes (one dword) times an NVFP4 block scale -> FP16 (exact).
-__device__ __forceinline__ v8h nv_decode8(uint32_t c, float pow2, v2h mant) {
-    v2h p0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, pow2, 0) * mant;
-    v2h p1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, pow2, 1) * mant;
-    v2h p2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, pow2, 2) * mant;
-    v2h p3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, pow2, 3) * mant;
+// Eight codes (one dword) times an NVFP4 block scale (FP16, in both halves) -> FP16 (exact).
+__device__ __forceinline__ v8h nv_decode8(uint32_t c, v2h s) {
+    v2h p0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, 1.0f, 0) * s;
+    v2h p1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, 1.0f, 1) * s;
+    v2h p2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, 1.0f, 2) * s;
+    v2h p3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, 1.0f, 3) * s;
     return v8h{p0[0], p0[1], p1[0], p1[1], p2[0], p2[1], p3[0], p3[1]};
 }
 
@@ -264,63 +271,134 @@ __device__ __forceinline__ void mx_stage(v16f (&acc)[4][4], const uint8_t *buf, 
 #undef REQAT_MX_READ
 }
 
-// NVFP4: one stage from LDS buffer `buf`.
-template <class C, class Issue>
-__device__ __forceinline__ void nv_stage(v16f (&acc)[4][4], const uint8_t *buf, const uint2 *lut,
-                                         int rA0, int rB0, int h, Issue &issue) {
-    constexpr int NQ = C::CH / 2;                       // 64-element chunks per stage
-    uint4 ca[2][4], cb[2][4];
-    uint2 ea[2][4][2], eb[2][4][2];
-#define REQAT_NV_READ(Q, D)                                                                    \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                            \
-        const int ra = rA0 + 32 * i, rb = rB0 + 32 * i;                                        \
-        ca[D][i] = lds16(buf + C::A_CODES + code_off<C::ROW>(ra, 2 * (Q) + h));                \
-        cb[D][i] = lds16(buf + C::B_CODES + code_off<C::ROW>(rb, 2 * (Q) + h));                \
-        const uint32_t wa = lds4(buf + C::A_SC + ra * C::SB + 4 * (Q));                        \
-        const uint32_t wb = lds4(buf + C::B_SC + rb * C::SB + 4 * (Q));                        \
-        _Pragma("unroll") for (int hb = 0; hb < 2; ++hb) {                                     \
-            ea[D][i][hb] = lut[(wa >> (8 * (2 * h + hb))) & 0xFFu];                            \
-            eb[D][i][hb] = lut[(wb >> (8 * (2 * h + hb))) & 0xFFu];                            \
-        }                                                                                      \
-    }
-    REQAT_NV_READ(0, 0);
+// NVFP4: one stage from LDS buffer `buf`, software-pipelined by MFMA step.
+// K assignment: a stage's row holds 2*NQ units of 32 codes (16 B, two
+// 16-blocks each); in chunk q (64 elements) lane half h takes unit NQ*h + q,
+// so over the stage a lane half covers one contiguous half of the row and
+// its 2*NQ scale bytes are contiguous too (one 4- or 8-byte LDS read per tile
+// and stage; chunk q's pair is 16-bit word q of them).  A and B use the same
+// assignment, so the sum over K is unchanged.
+// A step is one 16-element slice of K for all 4 x 4 tiles of the wave: 16
+// MFMAs fed by 8 decoded operands (4 A tiles, 4 B tiles; 8 VALU each).  The
+// operands of step t+1 are decoded while the MFMAs of step t run, and
+// sched_group_barrier interleaves them as one MFMA then four VALU, so the
+// decode hides under the matrix pipe.  Chunk q+1's codes are read from LDS in
+// the first step of chunk q and its scales converted in the third.
+template <class C>
+struct NvLane {
+    static constexpr int NQ = C::CH / 2;
+    int codeA[NQ], codeB[NQ];                           // byte offset of this lane's unit in chunk q (tile 0)
+    int scA, scB;                                       // byte offset of this lane's scale bytes (tile 0)
+    __device__ __forceinline__ NvLane(int rA0, int rB0, int h) {
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-        const int d = q & 1;
-        if (q + 1 < NQ) { REQAT_NV_READ(q + 1, d ^ 1); }
-        if (NQ == 4) {
-            switch (q) {
-            case 0: issue.template part<0>(); break;
-            case 1: issue.template part<1>(); break;
-            case 2: issue.template part<2>(); break;
-            default: issue.template part<3>(); break;
-            }
-        } else if (q == 0) {
-            issue.template part<0>();
-            issue.template part<1>();
+        for (int q = 0; q < NQ; ++q) {
+            codeA[q] = C::A_CODES + code_off<C::ROW>(rA0, NQ * h + q);
+            codeB[q] = C::B_CODES + code_off<C::ROW>(rB0, NQ * h + q);
+        }
+        scA = C::A_SC + rA0 * C::SB + NQ * 2 * h;
+        scB = C::B_SC + rB0 * C::SB + NQ * 2 * h;
+    }
+};
+
+template <class C>
+struct NvState {
+    static constexpr int NW = C::CH / 4;                // scale dwords per tile and stage
+    uint4 ca[2][4], cb[2][4];                           // codes of chunks q (even/odd)
+    uint32_t wa[4][NW], wb[4][NW];                      // this stage's scale bytes
+    v2h sa[2][4], sb[2][4];                             // FP16 scales of chunk q's two 16-blocks
+    v8h av[2][4], bv[2][4];                             // decoded operands of steps t (even/odd)
+};
+
+template <class C, int Q, int D>
+__device__ __forceinline__ void nv_read_codes(NvState<C> &st, const uint8_t *buf, const NvLane<C> &ln) {
+    const uint8_t *pa = buf + ln.codeA[Q], *pb = buf + ln.codeB[Q];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        st.ca[D][i] = lds16(pa + 32 * C::ROW * i);
+        st.cb[D][i] = lds16(pb + 32 * C::ROW * i);
+    }
+}
+
+template <class C>
+__device__ __forceinline__ void nv_read_scales(NvState<C> &st, const uint8_t *buf, const NvLane<C> &ln) {
+    const uint8_t *pa = buf + ln.scA, *pb = buf + ln.scB;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        if constexpr (NvState<C>::NW == 2) {
+            const uint2 x = *reinterpret_cast<const uint2 *>(pa + 32 * C::SB * i);
+            const uint2 y = *reinterpret_cast<const uint2 *>(pb + 32 * C::SB * i);
+            st.wa[i][0] = x.x; st.wa[i][1] = x.y;
+            st.wb[i][0] = y.x; st.wb[i][1] = y.y;
         } else {
-            issue.template part<2>();
-            issue.template part<3>();
+            st.wa[i][0] = lds4(pa + 32 * C::SB * i);
+            st.wb[i][0] = lds4(pb + 32 * C::SB * i);
         }
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int s2 = 0; s2 < 4; ++s2) {
-            v8h av[4], bv[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const uint2 e = ea[d][i][s2 >> 1], f = eb[d][i][s2 >> 1];
-                av[i] = nv_decode8(pick(ca[d][i], s2), f32_from_bits(e.x), __builtin_bit_cast(v2h, e.y));
-                bv[i] = nv_decode8(pick(cb[d][i], s2), f32_from_bits(f.x), __builtin_bit_cast(v2h, f.y));
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i], bv[j], acc[i][j], 0, 0, 0);
-        }
-        __builtin_amdgcn_sched_barrier(0);
     }
-#undef REQAT_NV_READ
+}
+
+template <class C, int Q, int D>
+__device__ __forceinline__ void nv_scales(NvState<C> &st) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        st.sa[D][i] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(st.wa[i][Q >> 1], 1.0f, (Q & 1) != 0);
+        st.sb[D][i] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(st.wb[i][Q >> 1], 1.0f, (Q & 1) != 0);
+    }
+}
+
+template <class C, int T>
+__device__ __forceinline__ void nv_decode(NvState<C> &st) {
+    constexpr int D = (T >> 2) & 1, S = T & 3, HB = S >> 1, E = T & 1;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        st.av[E][i] = nv_decode8(pick(st.ca[D][i], S), __builtin_shufflevector(st.sa[D][i], st.sa[D][i], HB, HB));
+        st.bv[E][i] = nv_decode8(pick(st.cb[D][i], S), __builtin_shufflevector(st.sb[D][i], st.sb[D][i], HB, HB));
+    }
+}
+
+template <class C, int T, int NT, class Issue>
+__device__ __forceinline__ void nv_region(v16f (&acc)[4][4], NvState<C> &st, const uint8_t *buf,
+                                          const NvLane<C> &ln, Issue &issue) {
+    constexpr int NQ = NT / 4, Q = T >> 2, S = T & 3, E = T & 1;
+    constexpr bool READ = S == 0 && Q + 1 < NQ;
+    constexpr int ND = READ ? 8 : 0;                    // LDS reads in this region
+    // the next stage's loads go out in the first half of the stage
+    constexpr int NG = T < NT / 2 ? Issue::template count<T, NT / 2>() : 0;
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (READ) nv_read_codes<C, Q + 1, (Q + 1) & 1>(st, buf, ln);
+    if constexpr (S == 2 && Q + 1 < NQ) nv_scales<C, Q + 1, (Q + 1) & 1>(st);
+    if constexpr (T < NT / 2) issue.template region<T, NT / 2>();
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(st.av[E][i], st.bv[E][j], acc[i][j], 0, 0, 0);
+    if constexpr (T + 1 < NT) nv_decode<C, T + 1>(st);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // one MFMA
+        if (T + 1 < NT) __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   // four VALU
+        if (k < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);       // one LDS read
+        if (k < NG) __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);       // one global load
+    }
+    if constexpr (T + 1 < NT) {
+        // pin the decoded operands to this region (otherwise they are sunk next to their MFMAs)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(st.av[E ^ 1][i]), "+v"(st.bv[E ^ 1][i]));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (T + 1 < NT) nv_region<C, T + 1, NT>(acc, st, buf, ln, issue);
+}
+
+template <class C, class Issue>
+__device__ __forceinline__ void nv_stage(v16f (&acc)[4][4], const uint8_t *buf, const NvLane<C> &ln,
+                                         Issue &issue) {
+    constexpr int NT = 2 * C::CH;                       // 16-element steps per stage
+    NvState<C> st;
+    nv_read_codes<C, 0, 0>(st, buf, ln);
+    nv_read_scales<C>(st, buf, ln);
+    nv_scales<C, 0, 0>(st);
+    nv_decode<C, 0>(st);
+    nv_region<C, 0, NT>(acc, st, buf, ln, issue);
 }
 
 template <int FMT, int KS, int NBUF>
@@ -332,7 +410,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(
     using C = Cfg<FMT, KS, NBUF>;
     extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int h = lane >> 5;
     const int wm = wave >> 1, wn = wave & 1;
 
@@ -347,18 +426,6 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(
     const int64_t tm = first_m + (t % width) % gsz, tn = (t % width) / gsz;
     const int64_t m0 = tm * TM, n0 = tn * TN;
     const int64_t cpr = K / 2, spr = K / C::B;
-
-    if constexpr (FMT == kNV) {
-        // (pow2 operand for the convert, mantissa pair for the multiply) per E4M3 byte
-        const uint32_t b = tid;
-        const float s = e4m3_value(b);
-        const uint32_t sbits = bits_from_f32(s);
-        _Float16 mh;
-        if (s != s) mh = __builtin_bit_cast(_Float16, (uint16_t)0x7E00);
-        else mh = (_Float16)f32_from_bits((sbits & 0x807FFFFFu) | 0x3F800000u);
-        const uint32_t mm = (uint32_t)__builtin_bit_cast(uint16_t, mh);
-        reinterpret_cast<uint2 *>(smem + C::LUT)[b] = make_uint2(sbits, mm | (mm << 16));
-    }
 
     v16f acc[4][4];
 #pragma unroll
@@ -384,6 +451,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(
 
     const int rA0 = wm * 128 + (lane & 31);               // this lane's A row in tile i: rA0 + 32 i
     const int rB0 = wn * 128 + (lane & 31);
+    const NvLane<C> nvl(rA0, rB0, h);
 
     for (int st = 0; st < nst; ++st) {
         // stage st has landed once no more than (stages issued after it) x LPS loads remain
@@ -391,7 +459,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(
         if (NBUF >= 3 && behind == NBUF - 2) wait_vmcnt<(NBUF >= 3 ? NBUF - 2 : 0) * C::LPS>();
         else if (NBUF >= 4 && behind == 1) wait_vmcnt<C::LPS>();
         else wait_vmcnt<0>();
-        __syncthreads();
+        // A bare barrier: __syncthreads() would also drain every load still in
+        // flight for later stages.  This wave's loads of stage st are done (vmcnt
+        // above) and its LDS reads of the buffer about to be refilled are done
+        // (lgkmcnt), so after the barrier stage st is complete for every wave.
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
         const uint8_t *buf = smem + (st % NBUF) * C::STAGE;
         const int nx = st + NBUF - 1;                      // stage whose loads go out now
@@ -401,7 +473,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(
         if constexpr (FMT == kMX) {
             mx_stage<C>(acc, buf, rA0, rB0, h, issue);
         } else {
-            nv_stage<C>(acc, buf, reinterpret_cast<const uint2 *>(smem + C::LUT), rA0, rB0, h, issue);
+            nv_stage<C>(acc, buf, nvl, issue);
         }
     }
 
@@ -446,7 +518,8 @@ hipError_t launch_cfg(int64_t M, int64_t N, int64_t K, const uint8_t *a_codes, c
 
 bool gemm_tile256_supported(Fmt fmt, int64_t M, int64_t N, int64_t K) {
     const int ks = fmt == kMX ? REQAT_MX_KS : REQAT_NV_KS;
-    return K > 0 && K % ks == 0 && M > 0 && N > 0 && K / ks < (int64_t(1) << 30);
+    // lane offsets into a tile's rows are 32-bit: 256 rows * K/2 bytes < 2^32
+    return K > 0 && K % ks == 0 && M > 0 && N > 0 && K <= (int64_t(1) << 24);
 }
 
 hipError_t launch_gemm_tile256(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *a_codes,
