@@ -197,7 +197,7 @@ hipError_t launch_gemm(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *
                        const uint8_t *b_scales, const float *gb, void *y, bool y_bf16, int64_t ldy,
                        hipStream_t stream) {
     if (M == 0 || N == 0) return hipSuccess;
-    if (M > 64 && gemm_tile256_supported(fmt, M, N, K))
+    if (M > 64 && gemm_tile256_supported(fmt, M, N, K, ldy))
         return launch_gemm_tile256(fmt, M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y,
                                    y_bf16, ldy, stream);
     dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)), block(kThreads);

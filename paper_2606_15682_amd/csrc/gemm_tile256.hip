@@ -56,6 +56,9 @@
 #ifndef REQAT_NV_NBUF
 #define REQAT_NV_NBUF 2
 #endif
+#ifndef REQAT_NV_LEAD
+#define REQAT_NV_LEAD 3
+#endif
 
 namespace reqat {
 
@@ -310,95 +313,264 @@ struct NvState {
 };
 
 template <class C, int Q, int D>
-__device__ __forceinline__ void nv_read_codes(NvState<C> &st, const uint8_t *buf, const NvLane<C> &ln) {
-    const uint8_t *pa = buf + ln.codeA[Q], *pb = buf + ln.codeB[Q];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        st.ca[D][i] = lds16(pa + 32 * C::ROW * i);
-        st.cb[D][i] = lds16(pb + 32 * C::ROW * i);
-    }
+__device__ __forceinline__ void nv_read_codes1(NvState<C> &st, const uint8_t *buf, const NvLane<C> &ln, int i) {
+    st.ca[D][i] = lds16(buf + ln.codeA[Q] + 32 * C::ROW * i);
+    st.cb[D][i] = lds16(buf + ln.codeB[Q] + 32 * C::ROW * i);
 }
 
 template <class C>
-__device__ __forceinline__ void nv_read_scales(NvState<C> &st, const uint8_t *buf, const NvLane<C> &ln) {
-    const uint8_t *pa = buf + ln.scA, *pb = buf + ln.scB;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        if constexpr (NvState<C>::NW == 2) {
-            const uint2 x = *reinterpret_cast<const uint2 *>(pa + 32 * C::SB * i);
-            const uint2 y = *reinterpret_cast<const uint2 *>(pb + 32 * C::SB * i);
-            st.wa[i][0] = x.x; st.wa[i][1] = x.y;
-            st.wb[i][0] = y.x; st.wb[i][1] = y.y;
-        } else {
-            st.wa[i][0] = lds4(pa + 32 * C::SB * i);
-            st.wb[i][0] = lds4(pb + 32 * C::SB * i);
-        }
+__device__ __forceinline__ void nv_read_scales1(NvState<C> &st, const uint8_t *buf, const NvLane<C> &ln, int i) {
+    if constexpr (NvState<C>::NW == 2) {
+        const uint2 x = *reinterpret_cast<const uint2 *>(buf + ln.scA + 32 * C::SB * i);
+        const uint2 y = *reinterpret_cast<const uint2 *>(buf + ln.scB + 32 * C::SB * i);
+        st.wa[i][0] = x.x; st.wa[i][1] = x.y;
+        st.wb[i][0] = y.x; st.wb[i][1] = y.y;
+    } else {
+        st.wa[i][0] = lds4(buf + ln.scA + 32 * C::SB * i);
+        st.wb[i][0] = lds4(buf + ln.scB + 32 * C::SB * i);
     }
 }
 
 template <class C, int Q, int D>
-__device__ __forceinline__ void nv_scales(NvState<C> &st) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        st.sa[D][i] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(st.wa[i][Q >> 1], 1.0f, (Q & 1) != 0);
-        st.sb[D][i] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(st.wb[i][Q >> 1], 1.0f, (Q & 1) != 0);
-    }
+__device__ __forceinline__ void nv_scales1(NvState<C> &st, int i) {
+    st.sa[D][i] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(st.wa[i][Q >> 1], 1.0f, (Q & 1) != 0);
+    st.sb[D][i] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(st.wb[i][Q >> 1], 1.0f, (Q & 1) != 0);
 }
 
+// Decodes step T's operands of A tile i and B tile i.
 template <class C, int T>
-__device__ __forceinline__ void nv_decode(NvState<C> &st) {
+__device__ __forceinline__ void nv_decode1(NvState<C> &st, int i) {
     constexpr int D = (T >> 2) & 1, S = T & 3, HB = S >> 1, E = T & 1;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        st.av[E][i] = nv_decode8(pick(st.ca[D][i], S), __builtin_shufflevector(st.sa[D][i], st.sa[D][i], HB, HB));
-        st.bv[E][i] = nv_decode8(pick(st.cb[D][i], S), __builtin_shufflevector(st.sb[D][i], st.sb[D][i], HB, HB));
+    st.av[E][i] = nv_decode8(pick(st.ca[D][i], S), __builtin_shufflevector(st.sa[D][i], st.sa[D][i], HB, HB));
+    st.bv[E][i] = nv_decode8(pick(st.cb[D][i], S), __builtin_shufflevector(st.sb[D][i], st.sb[D][i], HB, HB));
+}
+
+// Region T of a stage (NT regions; buffer `buf`, next stage in `nbuf`), in
+// four fenced parts: part k issues the MFMAs of A tile k (4) and decodes A
+// tile k and B tile k for step T + 1 (16 VALU), one MFMA to four VALU, plus
+// its share of LDS reads and loads.  The stage's LDS reads all happen by
+// region NT-4; at its end the wave waits for its loads of the next stage and
+// meets the others at a barrier.  Past that point every wave is done with
+// `buf`, so regions NT-3 .. NT-1 issue the loads of stage + 2 into it, read
+// the next stage's first chunk and scales from `nbuf`, and decode its first
+// step: the next stage starts with its operands ready.
+template <class C, int T, int NT, int K, class Issue>
+__device__ __forceinline__ void nv_part(v16f (&acc)[4][4], NvState<C> &st, const uint8_t *buf,
+                                        const uint8_t *nbuf, const NvLane<C> &ln, Issue &issue) {
+    constexpr int NQ = NT / 4, Q = T >> 2, S = T & 3, E = T & 1;
+    constexpr bool READ = S == 0 && Q + 1 < NQ;
+    constexpr int L = REQAT_NV_LEAD;                    // regions after the stage's barrier
+    static_assert(L >= 3 && L <= 5, "the barrier follows chunk NQ-1's reads and conversions");
+    constexpr bool NEXT_READ = T == NT - L, NEXT_CVT = T == NT - L + 1;
+    constexpr int LP = (T - (NT - L)) * 4 + K;          // load part (0..4L-1) in the last L regions
+    constexpr int NG = LP >= 0 ? Issue::template count<(LP >= 0 ? LP : 0), 4 * L>() : 0;
+    constexpr int ND = READ ? 2 : NEXT_READ ? 4 : 0;    // LDS reads in this part
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (READ) nv_read_codes1<C, Q + 1, (Q + 1) & 1>(st, buf, ln, K);
+    if constexpr (S == 2 && Q + 1 < NQ) nv_scales1<C, Q + 1, (Q + 1) & 1>(st, K);
+    if constexpr (NEXT_READ) {
+        nv_read_codes1<C, 0, 0>(st, nbuf, ln, K);
+        nv_read_scales1<C>(st, nbuf, ln, K);
     }
+    if constexpr (NEXT_CVT) nv_scales1<C, 0, 0>(st, K);
+    if constexpr (LP >= 0) issue.template region<(LP >= 0 ? LP : 0), 4 * L>();
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        acc[K][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(st.av[E][K], st.bv[E][j], acc[K][j], 0, 0, 0);
+    nv_decode1<C, T + 1>(st, K);                        // T + 1 == NT: the next stage's step 0
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);     // four VALU
+        if (k < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);       // one LDS read
+    }
+    if (NG > 0) __builtin_amdgcn_sched_group_barrier(0x010, NG, 0);          // the part's loads
+    // pin the decoded operands to this part (otherwise they are sunk next to their MFMAs)
+    asm volatile("" : "+v"(st.av[E ^ 1][K]), "+v"(st.bv[E ^ 1][K]));
+    __builtin_amdgcn_sched_barrier(0);
 }
 
 template <class C, int T, int NT, class Issue>
 __device__ __forceinline__ void nv_region(v16f (&acc)[4][4], NvState<C> &st, const uint8_t *buf,
-                                          const NvLane<C> &ln, Issue &issue) {
-    constexpr int NQ = NT / 4, Q = T >> 2, S = T & 3, E = T & 1;
-    constexpr bool READ = S == 0 && Q + 1 < NQ;
-    constexpr int ND = READ ? 8 : 0;                    // LDS reads in this region
-    // the next stage's loads go out in the first half of the stage
-    constexpr int NG = T < NT / 2 ? Issue::template count<T, NT / 2>() : 0;
-    __builtin_amdgcn_sched_barrier(0);
-    if constexpr (READ) nv_read_codes<C, Q + 1, (Q + 1) & 1>(st, buf, ln);
-    if constexpr (S == 2 && Q + 1 < NQ) nv_scales<C, Q + 1, (Q + 1) & 1>(st);
-    if constexpr (T < NT / 2) issue.template region<T, NT / 2>();
+                                          const uint8_t *nbuf, const NvLane<C> &ln, Issue &issue) {
+    nv_part<C, T, NT, 0>(acc, st, buf, nbuf, ln, issue);
+    nv_part<C, T, NT, 1>(acc, st, buf, nbuf, ln, issue);
+    nv_part<C, T, NT, 2>(acc, st, buf, nbuf, ln, issue);
+    nv_part<C, T, NT, 3>(acc, st, buf, nbuf, ln, issue);
+    if constexpr (T == NT - REQAT_NV_LEAD - 1) {
+        // this wave's loads of the next stage have landed and its reads of `buf`
+        // are done; after the barrier both hold for every wave
+        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    }
+    if constexpr (T + 1 < NT) nv_region<C, T + 1, NT>(acc, st, buf, nbuf, ln, issue);
+}
+
+// Output tile of virtual tile id v: workgroups are dealt round-robin to the 8
+// XCDs, so id v is mapped into the (v % 8)-th contiguous range of tiles, and
+// tiles are walked in groups of GROUP_M tile-rows, keeping the A and B panels
+// a group reuses in the L2 of the XCD that owns it.  With a persistent grid
+// of G workgroups (G a multiple of 8), workgroup w takes ids w, w + G, ...,
+// which stay on its XCD and walk that XCD's range in order.
+struct TileGeo {
+    int64_t m0, n0;
+    int rows_a, rows_b;
+};
+
+__device__ __forceinline__ TileGeo tile_geo(int64_t v, int64_t M, int64_t N) {
+    const int64_t tm_n = (M + TM - 1) / TM, tn_n = (N + TN - 1) / TN, T = tm_n * tn_n;
+    const int64_t xcd = v % 8, local = v / 8, per = T / 8, rem = T % 8;
+    const int64_t t = xcd * per + (xcd < rem ? xcd : rem) + local;
+    const int64_t width = GROUP_M * tn_n;
+    const int64_t first_m = (t / width) * GROUP_M;
+    const int64_t gsz = (tm_n - first_m) < GROUP_M ? (tm_n - first_m) : GROUP_M;
+    const int64_t tm = first_m + (t % width) % gsz, tn = (t % width) / gsz;
+    TileGeo g;
+    g.m0 = tm * TM;
+    g.n0 = tn * TN;
+    g.rows_a = (int)(M - g.m0 < TM ? M - g.m0 : TM);
+    g.rows_b = (int)(N - g.n0 < TN ? N - g.n0 : TN);
+    return g;
+}
+
+// Stores the wave's 128 x 128 block of a finished tile (times `scale`).
+// D[i][j] of a 32 x 32 MFMA tile is in lane j + 32*((i/4)%2), register (i/8)*4 + i%4:
+// a row base per (i, register) is wave-uniform and the lane adds a 32-bit
+// offset (the launcher bounds ldy), so each store needs no address VALU.
+template <bool BF16, bool FULL>
+__device__ __forceinline__ void store_tile_as(const v16f (&acc)[4][4], const TileGeo &g, int64_t M, int64_t N,
+                                              int wm, int wn, int lane, float scale, void *y, int64_t ldy) {
+    typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+    constexpr int ES = BF16 ? 2 : 4;
+    const int h = lane >> 5;
+    const int64_t row0 = g.m0 + wm * 128, col0 = g.n0 + wn * 128;
+    const uint32_t voff = (uint32_t)((4 * h) * ldy + (lane & 31)) * ES;
+    const int lrow = 4 * h, lcol = lane & 31;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(st.av[E][i], st.bv[E][j], acc[i][j], 0, 0, 0);
-    if constexpr (T + 1 < NT) nv_decode<C, T + 1>(st);
+        for (int r = 0; r < 16; r += 2) {
+            // registers r and r + 1 are consecutive rows of the same column
+            const int ro = i * 32 + 8 * (r >> 2) + (r & 3);
+            uint8_t *p0 = reinterpret_cast<uint8_t *>(y) + ((row0 + ro) * ldy + col0) * ES;
+            uint8_t *p1 = p0 + ldy * ES;
+            const bool r0 = FULL || row0 + ro + lrow < M, r1 = FULL || row0 + ro + lrow + 1 < M;
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // one MFMA
-        if (T + 1 < NT) __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   // four VALU
-        if (k < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);       // one LDS read
-        if (k < NG) __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);       // one global load
-    }
-    if constexpr (T + 1 < NT) {
-        // pin the decoded operands to this region (otherwise they are sunk next to their MFMAs)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(st.av[E ^ 1][i]), "+v"(st.bv[E ^ 1][i]));
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    if constexpr (T + 1 < NT) nv_region<C, T + 1, NT>(acc, st, buf, ln, issue);
+            for (int j = 0; j < 4; ++j) {
+                float v0 = acc[i][j][r], v1 = acc[i][j][r + 1];
+                // keep each pair's copy out of the accumulators next to its store
+                asm volatile("" : "+v"(v0), "+v"(v1));
+                v0 *= scale;
+                v1 *= scale;
+                const bool c = FULL || col0 + 32 * j + lcol < N;
+                if (BF16) {
+                    const v2bf b = {(__bf16)v0, (__bf16)v1};
+                    const uint32_t u = __builtin_bit_cast(uint32_t, b);
+                    if (r0 && c) *reinterpret_cast<uint16_t *>(p0 + voff + 32 * ES * j) = (uint16_t)u;
+                    if (r1 && c) *reinterpret_cast<uint16_t *>(p1 + voff + 32 * ES * j) = (uint16_t)(u >> 16);
+                } else {
+                    if (r0 && c) *reinterpret_cast<float *>(p0 + voff + 32 * ES * j) = v0;
+                    if (r1 && c) *reinterpret_cast<float *>(p1 + voff + 32 * ES * j) = v1;
+                }
+            }
+        }
 }
 
-template <class C, class Issue>
-__device__ __forceinline__ void nv_stage(v16f (&acc)[4][4], const uint8_t *buf, const NvLane<C> &ln,
-                                         Issue &issue) {
-    constexpr int NT = 2 * C::CH;                       // 16-element steps per stage
+__device__ __forceinline__ void store_tile(const v16f (&acc)[4][4], const TileGeo &g, int64_t M, int64_t N,
+                                           int wm, int wn, int lane, float scale, void *y, int y_bf16,
+                                           int64_t ldy) {
+    const bool full = g.rows_a == TM && g.rows_b == TN;
+    if (y_bf16) {
+        if (full) store_tile_as<true, true>(acc, g, M, N, wm, wn, lane, scale, y, ldy);
+        else store_tile_as<true, false>(acc, g, M, N, wm, wn, lane, scale, y, ldy);
+    } else {
+        if (full) store_tile_as<false, true>(acc, g, M, N, wm, wn, lane, scale, y, ldy);
+        else store_tile_as<false, false>(acc, g, M, N, wm, wn, lane, scale, y, ldy);
+    }
+}
+
+// Position of the load stream: stage s of virtual tile v.
+template <class C>
+struct LoadPos {
+    int64_t v;
+    int s;
+    TileGeo g;
+    __device__ __forceinline__ void advance(int nst, int64_t G, int64_t M, int64_t N) {
+        if (++s == nst) {
+            s = 0;
+            v += G;
+            g = tile_geo(v, M, N);
+        }
+    }
+};
+
+// NVFP4, persistent: the workgroup runs the stages of all its tiles as one
+// stream over two stage buffers (stage g in buffer g % 2; stages 0 and 1 are
+// loaded up front and stage g + 2 during stage g), so the next tile's first
+// stages are loaded, and its first step decoded, while the current tile ends;
+// a finished tile is stored and its accumulators cleared between two stages.
+template <class C>
+__device__ __forceinline__ void nv_persistent(uint8_t *smem, int64_t M, int64_t N, int64_t K,
+                                              const uint8_t *a_codes, const uint8_t *a_scales, float scale,
+                                              const uint8_t *b_codes, const uint8_t *b_scales, void *y,
+                                              int y_bf16, int64_t ldy, int wave, int lane) {
+    constexpr int KS = 2 * C::ROW, NT = 2 * C::CH;
+    static_assert(C::TOTAL == 2 * C::STAGE, "two stage buffers");
+    const int h = lane >> 5, wm = wave >> 1, wn = wave & 1;
+    const int64_t tm_n = (M + TM - 1) / TM, tn_n = (N + TN - 1) / TN, T = tm_n * tn_n;
+    const int64_t G = gridDim.x, w = blockIdx.x;
+    const int nst = (int)(K / KS);
+    const int64_t cpr = K / 2, spr = K / C::B;
+    const int64_t total = ((T - w + G - 1) / G) * nst;  // stages this workgroup runs (grid <= T)
+
+    auto issue_at = [&](const LoadPos<C> &p, uint8_t *buf) {
+        const int64_t k0 = (int64_t)p.s * KS;
+        return StageIssue<C>{buf, p.v < T, wave, lane, p.g.rows_a, p.g.rows_b, cpr, spr,
+                             a_codes + p.g.m0 * cpr + k0 / 2, b_codes + p.g.n0 * cpr + k0 / 2,
+                             a_scales + p.g.m0 * spr + k0 / C::B, b_scales + p.g.n0 * spr + k0 / C::B};
+    };
+
+    LoadPos<C> ld{w, 0, tile_geo(w, M, N)};
+    {
+        StageIssue<C> i0 = issue_at(ld, smem);
+        i0.template region<0, 1>();
+        ld.advance(nst, G, M, N);
+        StageIssue<C> i1 = issue_at(ld, smem + C::STAGE);
+        i1.template region<0, 1>();
+        ld.advance(nst, G, M, N);
+        if (total > 1) wait_vmcnt<C::LPS>();
+        else wait_vmcnt<0>();
+    }
+    asm volatile("s_barrier" ::: "memory");
+
+    const NvLane<C> ln(wm * 128 + (lane & 31), wn * 128 + (lane & 31), h);
     NvState<C> st;
-    nv_read_codes<C, 0, 0>(st, buf, ln);
-    nv_read_scales<C>(st, buf, ln);
-    nv_scales<C, 0, 0>(st);
-    nv_decode<C, 0>(st);
-    nv_region<C, 0, NT>(acc, st, buf, ln, issue);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        nv_read_codes1<C, 0, 0>(st, smem, ln, i);
+        nv_read_scales1<C>(st, smem, ln, i);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        nv_scales1<C, 0, 0>(st, i);
+        nv_decode1<C, 0>(st, i);
+    }
+
+    int64_t gs = 0;                                     // stream position (stage buffer gs % 2)
+    for (int64_t v = w; v < T; v += G) {
+        v16f acc[4][4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = v16f{};
+        for (int s = 0; s < nst; ++s, ++gs) {
+            uint8_t *buf = smem + (gs & 1) * C::STAGE;
+            const uint8_t *nbuf = smem + ((gs + 1) & 1) * C::STAGE;
+            StageIssue<C> issue = issue_at(ld, buf);    // stage gs + 2
+            nv_region<C, 0, NT>(acc, st, buf, nbuf, ln, issue);
+            ld.advance(nst, G, M, N);
+        }
+        store_tile(acc, tile_geo(v, M, N), M, N, wm, wn, lane, scale, y, y_bf16, ldy);
+    }
 }
 
 template <int FMT, int KS, int NBUF>
@@ -412,6 +584,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    if constexpr (FMT == kNV) {
+        nv_persistent<C>(smem, M, N, K, a_codes, a_scales, (*ga) * (*gb), b_codes, b_scales, y, y_bf16,
+                         ldy, wave, lane);
+        return;
+    }
     const int h = lane >> 5;
     const int wm = wave >> 1, wn = wave & 1;
 
@@ -440,75 +617,75 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(
     const uint8_t *ac = a_codes + m0 * cpr, *bc = b_codes + n0 * cpr;
     const uint8_t *as_ = a_scales + m0 * spr, *bs_ = b_scales + n0 * spr;
 
-    // prologue: the first NBUF - 1 stages
-#pragma unroll
-    for (int p = 0; p < NBUF - 1; ++p) {
-        if (p < nst)
-            load_range<C, 0, C::LPS>(smem + p * C::STAGE, wave, lane, rows_a, rows_b, cpr, spr,
-                                     ac + (int64_t)p * KS / 2, bc + (int64_t)p * KS / 2,
-                                     as_ + (int64_t)p * KS / C::B, bs_ + (int64_t)p * KS / C::B);
-    }
-
     const int rA0 = wm * 128 + (lane & 31);               // this lane's A row in tile i: rA0 + 32 i
     const int rB0 = wn * 128 + (lane & 31);
-    const NvLane<C> nvl(rA0, rB0, h);
 
-    for (int st = 0; st < nst; ++st) {
-        // stage st has landed once no more than (stages issued after it) x LPS loads remain
-        const int behind = (nst - 1 - st) < (NBUF - 2) ? (nst - 1 - st) : (NBUF - 2);
-        if (NBUF >= 3 && behind == NBUF - 2) wait_vmcnt<(NBUF >= 3 ? NBUF - 2 : 0) * C::LPS>();
-        else if (NBUF >= 4 && behind == 1) wait_vmcnt<C::LPS>();
-        else wait_vmcnt<0>();
-        // A bare barrier: __syncthreads() would also drain every load still in
-        // flight for later stages.  This wave's loads of stage st are done (vmcnt
-        // above) and its LDS reads of the buffer about to be refilled are done
-        // (lgkmcnt), so after the barrier stage st is complete for every wave.
-        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    {
+        // prologue: the first NBUF - 1 stages
+#pragma unroll
+        for (int p = 0; p < NBUF - 1; ++p) {
+            if (p < nst)
+                load_range<C, 0, C::LPS>(smem + p * C::STAGE, wave, lane, rows_a, rows_b, cpr, spr,
+                                         ac + (int64_t)p * KS / 2, bc + (int64_t)p * KS / 2,
+                                         as_ + (int64_t)p * KS / C::B, bs_ + (int64_t)p * KS / C::B);
+        }
+        for (int st = 0; st < nst; ++st) {
+            // stage st has landed once no more than (stages issued after it) x LPS loads remain
+            const int behind = (nst - 1 - st) < (NBUF - 2) ? (nst - 1 - st) : (NBUF - 2);
+            if (NBUF >= 3 && behind == NBUF - 2) wait_vmcnt<(NBUF >= 3 ? NBUF - 2 : 0) * C::LPS>();
+            else if (NBUF >= 4 && behind == 1) wait_vmcnt<C::LPS>();
+            else wait_vmcnt<0>();
+            // A bare barrier: __syncthreads() would also drain every load still in
+            // flight for later stages.  This wave's loads of stage st are done (vmcnt
+            // above) and its LDS reads of the buffer about to be refilled are done
+            // (lgkmcnt), so after the barrier stage st is complete for every wave.
+            asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
-        const uint8_t *buf = smem + (st % NBUF) * C::STAGE;
-        const int nx = st + NBUF - 1;                      // stage whose loads go out now
-        const int64_t kx = (int64_t)nx * KS;
-        StageIssue<C> issue{smem + (nx % NBUF) * C::STAGE, nx < nst, wave, lane, rows_a, rows_b,
-                            cpr, spr, ac + kx / 2, bc + kx / 2, as_ + kx / C::B, bs_ + kx / C::B};
-        if constexpr (FMT == kMX) {
+            const uint8_t *buf = smem + (st % NBUF) * C::STAGE;
+            const int nx = st + NBUF - 1;                      // stage whose loads go out now
+            const int64_t kx = (int64_t)nx * KS;
+            StageIssue<C> issue{smem + (nx % NBUF) * C::STAGE, nx < nst, wave, lane, rows_a, rows_b,
+                                cpr, spr, ac + kx / 2, bc + kx / 2, as_ + kx / C::B, bs_ + kx / C::B};
             mx_stage<C>(acc, buf, rA0, rB0, h, issue);
-        } else {
-            nv_stage<C>(acc, buf, nvl, issue);
         }
     }
 
-    // ---- epilogue: D[i][j] of a 32 x 32 tile is in lane j + 32*((i/4)%2), register (i/8)*4 + i%4
-    float scale = 1.0f;
-    if (FMT == kNV) scale = (*ga) * (*gb);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t gn = n0 + wn * 128 + j * 32 + (lane & 31);
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int64_t gm = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-                if (gm < M && gn < N) {
-                    const float v = acc[i][j][r] * scale;
-                    if (y_bf16)
-                        reinterpret_cast<uint16_t *>(y)[gm * ldy + gn] = (uint16_t)bf16_rne_from_float(v);
-                    else
-                        reinterpret_cast<float *>(y)[gm * ldy + gn] = v;
-                }
-            }
-        }
+    TileGeo geo;
+    geo.m0 = m0;
+    geo.n0 = n0;
+    geo.rows_a = rows_a;
+    geo.rows_b = rows_b;
+    store_tile(acc, geo, M, N, wm, wn, lane, 1.0f, y, y_bf16, ldy);
+}
+
+// Compute units of the current device (cached per device).
+int compute_units() {
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return -1;
+    if (dev < 64 && cache[dev] > 0) return cache[dev];
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
+    if (dev < 64) cache[dev] = n;
+    return n;
 }
 
 template <int FMT, int KS, int NBUF>
 hipError_t launch_cfg(int64_t M, int64_t N, int64_t K, const uint8_t *a_codes, const uint8_t *a_scales,
                       const float *ga, const uint8_t *b_codes, const uint8_t *b_scales,
                       const float *gb, void *y, bool y_bf16, int64_t ldy, hipStream_t stream) {
-    const int64_t tiles = ((M + TM - 1) / TM) * ((N + TN - 1) / TN);
+    int64_t grid = ((M + TM - 1) / TM) * ((N + TN - 1) / TN);
+    if (FMT == kNV) {
+        // persistent: one workgroup per CU (a multiple of 8 keeps each one on its XCD)
+        const int cus = compute_units();
+        if (cus <= 0) return hipErrorInvalidDevice;
+        if (grid > cus) grid = cus;
+    }
     const size_t lds = Cfg<FMT, KS, NBUF>::TOTAL;
     hipError_t e = hipFuncSetAttribute((const void *)gemm_tile256_kernel<FMT, KS, NBUF>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((gemm_tile256_kernel<FMT, KS, NBUF>), dim3((unsigned)tiles), dim3(kThreads), lds,
+    hipLaunchKernelGGL((gemm_tile256_kernel<FMT, KS, NBUF>), dim3((unsigned)grid), dim3(kThreads), lds,
                        stream, M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, (int)y_bf16,
                        ldy);
     return hipGetLastError();
@@ -516,10 +693,11 @@ hipError_t launch_cfg(int64_t M, int64_t N, int64_t K, const uint8_t *a_codes, c
 
 }  // namespace
 
-bool gemm_tile256_supported(Fmt fmt, int64_t M, int64_t N, int64_t K) {
+bool gemm_tile256_supported(Fmt fmt, int64_t M, int64_t N, int64_t K, int64_t ldy) {
     const int ks = fmt == kMX ? REQAT_MX_KS : REQAT_NV_KS;
-    // lane offsets into a tile's rows are 32-bit: 256 rows * K/2 bytes < 2^32
-    return K > 0 && K % ks == 0 && M > 0 && N > 0 && K <= (int64_t(1) << 24);
+    // lane offsets are 32-bit: 256 rows * K/2 bytes and 4 * ldy * 4 bytes stay below 2^31
+    return K > 0 && K % ks == 0 && M > 0 && N > 0 && K <= (int64_t(1) << 24) &&
+           ldy <= (int64_t(1) << 26);
 }
 
 hipError_t launch_gemm_tile256(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *a_codes,

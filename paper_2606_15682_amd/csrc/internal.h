@@ -30,7 +30,7 @@ hipError_t launch_quantize(Fmt fmt, QuantOut out, const uint16_t *x, int64_t row
                            float *gptr, GSrc gsrc, const uint32_t *partials, int nparts,
                            hipStream_t stream);
 
-bool gemm_tile256_supported(Fmt fmt, int64_t M, int64_t N, int64_t K);
+bool gemm_tile256_supported(Fmt fmt, int64_t M, int64_t N, int64_t K, int64_t ldy);
 
 hipError_t launch_gemm_tile256(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *a_codes,
                                const uint8_t *a_scales, const float *ga, const uint8_t *b_codes,
