@@ -56,6 +56,9 @@
 #ifndef REQAT_NV_NBUF
 #define REQAT_NV_NBUF 2
 #endif
+#ifndef REQAT_MX_PERSISTENT
+#define REQAT_MX_PERSISTENT 1
+#endif
 #ifndef REQAT_NV_LEAD
 #define REQAT_NV_LEAD 3
 #endif
@@ -98,11 +101,22 @@ struct Cfg {
     static_assert(TOTAL <= 160 * 1024, "LDS budget");
 };
 
-__device__ __forceinline__ void g2l16(const void *g, uint8_t *l) {
-    __builtin_amdgcn_global_load_lds(g, (lds_void *)l, 16, 0, 0);
+// Direct-to-LDS loads: lane i's 16 (4) bytes at base + voff land at LDS
+// address l + 16 i (4 i); base and l are wave-uniform.  Written as inline asm
+// so the compiler does not track them: it would otherwise wait for every
+// such load in flight (vmcnt(0)) before any later LDS read, since it cannot
+// tell which stage buffer a read touches.  The kernels order these writes
+// against their LDS reads themselves (vmcnt waits and barriers).
+__device__ __forceinline__ void g2l16(const uint8_t *base, uint32_t voff, uint8_t *l) {
+    asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "{m0}"((uint32_t)(uintptr_t)l));
 }
-__device__ __forceinline__ void g2l4(const void *g, uint8_t *l) {
-    __builtin_amdgcn_global_load_lds(g, (lds_void *)l, 4, 0, 0);
+__device__ __forceinline__ void g2l4(const uint8_t *base, uint32_t voff, uint8_t *l) {
+    asm volatile("global_load_lds_dword %0, %1" ::"v"(voff), "s"(base), "{m0}"((uint32_t)(uintptr_t)l));
+}
+
+// A float read through the scalar cache (the pointer is uniform).
+__device__ __forceinline__ float uniform_load(const float *p) {
+    return *(const __attribute__((address_space(4))) float *)p;
 }
 
 __device__ __forceinline__ uint4 lds16(const uint8_t *p) { return *reinterpret_cast<const uint4 *>(p); }
@@ -140,7 +154,7 @@ __device__ __forceinline__ void load_one(uint8_t *buf, int wave, int lane, int r
         const int lim = isA ? rows_a : rows_b;
         const int r = row < lim ? row : lim - 1;
         // 32-bit lane offset from a wave-uniform base (the launcher bounds 256 * K / 2 below 2^32)
-        g2l16((isA ? a_codes : b_codes) + (uint32_t)(r * (uint32_t)cpr + c * 16),
+        g2l16(isA ? a_codes : b_codes, (uint32_t)(r * (uint32_t)cpr + c * 16),
               buf + (isA ? C::A_CODES : C::B_CODES) + j * 1024);
     } else {
         constexpr int k = IDX - 2 * C::CODE_LPW;
@@ -151,10 +165,11 @@ __device__ __forceinline__ void load_one(uint8_t *buf, int wave, int lane, int r
         const int piece = lane % PPR;
         const int lim = isA ? rows_a : rows_b;
         const int r = row < lim ? row : lim - 1;
-        const uint8_t *src = (isA ? a_scales : b_scales) + (uint32_t)(r * (uint32_t)spr + piece * C::LS);
+        const uint8_t *src = isA ? a_scales : b_scales;
+        const uint32_t off = (uint32_t)(r * (uint32_t)spr + piece * C::LS);
         uint8_t *dst = buf + (isA ? C::A_SC : C::B_SC) + j * (64 * C::LS);
-        if constexpr (C::LS == 16) g2l16(src, dst);
-        else g2l4(src, dst);
+        if constexpr (C::LS == 16) g2l16(src, off, dst);
+        else g2l4(src, off, dst);
     }
 }
 
@@ -573,6 +588,221 @@ __device__ __forceinline__ void nv_persistent(uint8_t *smem, int64_t M, int64_t 
     }
 }
 
+// MXFP4, persistent, over a ring of NBUF stage buffers (stage g in buffer
+// g % NBUF).  A stage has NS = KS/64 substeps of 16 scaled MFMAs; the operands
+// of substep s + 1 are read during substep s, and during the last substep the
+// next stage's first operands and scale bytes are read, so stages follow each
+// other without a bubble.  The barrier of stage g sits before its last
+// substep: by then this wave's reads of buffer g % NBUF are done and its loads
+// of stage g + 1 have landed (vmcnt counts only the later stages still in
+// flight); after it, stage g + 1 is readable and buffer g % NBUF is refilled
+// with stage g + NBUF during the last substep.  The first barrier after a
+// tile's stores waits for everything (vmcnt(0)), since the counter is only
+// ordered among loads.
+template <class C>
+struct MxLane {
+    static constexpr int NS = C::CH / 2;
+    int codeA[NS], codeB[NS];                           // byte offset of this lane's unit in substep s (tile 0)
+    int scA, scB;                                       // byte offset of this lane's NS scale bytes (tile 0)
+    __device__ __forceinline__ MxLane(int rA0, int rB0, int h) {
+#pragma unroll
+        for (int q = 0; q < NS; ++q) {
+            codeA[q] = C::A_CODES + code_off<C::ROW>(rA0, NS * h + q);
+            codeB[q] = C::B_CODES + code_off<C::ROW>(rB0, NS * h + q);
+        }
+        scA = C::A_SC + rA0 * C::SB + NS * h;
+        scB = C::B_SC + rB0 * C::SB + NS * h;
+    }
+};
+
+template <class C>
+struct MxState {
+    uint4 a[2][4], b[2][4];                             // operands of substeps (even/odd)
+    uint32_t sa[4], sb[4];                              // scale bytes of the current stage (byte s: substep s)
+    uint32_t na[4], nb[4];                              // scale bytes of the next stage
+};
+
+template <class C>
+__device__ __forceinline__ uint32_t mx_scale_read(const uint8_t *p) {
+    if constexpr (C::CH / 2 == 4) return lds4(p);
+    else return *reinterpret_cast<const uint16_t *>(p);
+}
+
+// Part K of substep S of a stage: the 4 MFMAs of A tile K, the reads of A
+// tile K's and B tile K's operands for the next substep (and, in the last
+// substep, the next stage's scale bytes for them), and a share of the loads.
+// The loads of a stage go out in two halves: the first in the last substep of
+// the stage NB before it (right after the barrier that frees its buffer), the
+// second in substep 0 of the following stage.
+template <class C, int S, int NS, int K, class Issue>
+__device__ __forceinline__ void mx_part(v16f (&acc)[4][4], MxState<C> &st, const uint8_t *buf,
+                                        const uint8_t *nbuf, const MxLane<C> &ln, Issue &prev, Issue &next) {
+    constexpr int E = S & 1, LAST = S == NS - 1;
+    constexpr int ND = LAST ? 4 : 2;
+    // load parts: 8 per half, two per substep part
+    constexpr int NGN = LAST ? Issue::template count<2 * K, 8>() + Issue::template count<2 * K + 1, 8>() : 0;
+    constexpr int HALF2 = S == 0 ? 1 : 0;
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (!LAST) {
+        st.a[E ^ 1][K] = lds16(buf + ln.codeA[S + 1] + 32 * C::ROW * K);
+        st.b[E ^ 1][K] = lds16(buf + ln.codeB[S + 1] + 32 * C::ROW * K);
+    } else {
+        st.a[E ^ 1][K] = lds16(nbuf + ln.codeA[0] + 32 * C::ROW * K);
+        st.b[E ^ 1][K] = lds16(nbuf + ln.codeB[0] + 32 * C::ROW * K);
+        st.na[K] = mx_scale_read<C>(nbuf + ln.scA + 32 * C::SB * K);
+        st.nb[K] = mx_scale_read<C>(nbuf + ln.scB + 32 * C::SB * K);
+    }
+    if constexpr (LAST) {
+        next.template region<2 * K, 16>();
+        next.template region<2 * K + 1, 16>();
+    }
+    if constexpr (HALF2) {
+        prev.template region<8 + 2 * K, 16>();
+        prev.template region<9 + 2 * K, 16>();
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        acc[K][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+            as_v8i(st.a[E][K]), as_v8i(st.b[E][j]), acc[K][j], 4, 4, S, (int)st.sa[K], S, (int)st.sb[j]);
+    constexpr int NG = NGN + (HALF2 ? Issue::template count<8 + 2 * K, 16>() + Issue::template count<9 + 2 * K, 16>() : 0);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // one MFMA
+        if (k < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);       // one LDS read
+        if (k < NG) __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);       // one load
+    }
+    // keep the part's MFMAs in it (they would otherwise be sunk past the
+    // stage's barrier and branches)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) asm volatile("" : "+a"(acc[K][j]));
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+template <class C, int S, int NS, class Issue>
+__device__ __forceinline__ void mx_substep(v16f (&acc)[4][4], MxState<C> &st, const uint8_t *buf,
+                                           const uint8_t *nbuf, const MxLane<C> &ln, Issue &prev,
+                                           Issue &next) {
+    mx_part<C, S, NS, 0>(acc, st, buf, nbuf, ln, prev, next);
+    mx_part<C, S, NS, 1>(acc, st, buf, nbuf, ln, prev, next);
+    mx_part<C, S, NS, 2>(acc, st, buf, nbuf, ln, prev, next);
+    mx_part<C, S, NS, 3>(acc, st, buf, nbuf, ln, prev, next);
+}
+
+template <class C>
+constexpr int half_count() {
+    return StageIssue<C>::template count<0, 2>();       // loads in parts 0..7 of 16
+}
+
+template <class C>
+__device__ __forceinline__ void load_first_half(StageIssue<C> &is) {
+    is.template region<0, 2>();
+}
+
+// One stage of the MXFP4 stream.  Past the end of the workgroup's stages the
+// loads still go out (re-reading its first stage into a buffer nobody reads
+// again), so every stage issues exactly LPS loads and the wait before the
+// barrier is one constant: the NB - 2 stages issued after stage g + 1 may stay
+// in flight.  FIRST (a tile's first stage, after the previous tile's stores)
+// waits for everything instead.
+template <class C, int NB, bool FIRST>
+__device__ __forceinline__ void mx_stage_p(v16f (&acc)[4][4], MxState<C> &st, uint8_t *smem, int64_t gs,
+                                           const MxLane<C> &ln, StageIssue<C> &prev, StageIssue<C> &issue) {
+    constexpr int NS = C::CH / 2;
+    const int bi = (int)(gs % NB);
+    uint8_t *buf = smem + bi * C::STAGE;
+    const uint8_t *nbuf = smem + (bi + 1 == NB ? 0 : bi + 1) * C::STAGE;
+    issue.buf = buf;                                    // stage gs + NB goes where stage gs was
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        st.sa[i] = st.na[i];
+        st.sb[i] = st.nb[i];
+    }
+    mx_substep<C, 0, NS>(acc, st, buf, nbuf, ln, prev, issue);
+    if constexpr (NS == 4) {
+        mx_substep<C, 1, NS>(acc, st, buf, nbuf, ln, prev, issue);
+        mx_substep<C, 2, NS>(acc, st, buf, nbuf, ln, prev, issue);
+    }
+    if constexpr (FIRST) wait_vmcnt<0>();
+    else wait_vmcnt<(NB - 2) * C::LPS>();
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    mx_substep<C, NS - 1, NS>(acc, st, buf, nbuf, ln, prev, issue);
+}
+
+template <class C, int NB>
+__device__ __forceinline__ void mx_persistent(uint8_t *smem, int64_t M, int64_t N, int64_t K,
+                                              const uint8_t *a_codes, const uint8_t *a_scales,
+                                              const uint8_t *b_codes, const uint8_t *b_scales, void *y,
+                                              int y_bf16, int64_t ldy, int wave, int lane) {
+    constexpr int KS = 2 * C::ROW, NS = C::CH / 2;
+    static_assert(NS % 2 == 0 && NB >= 2, "even substeps per stage");
+    static_assert((NB - 1) * C::LPS <= 63, "vmcnt range");
+    const int h = lane >> 5, wm = wave >> 1, wn = wave & 1;
+    const int64_t tm_n = (M + TM - 1) / TM, tn_n = (N + TN - 1) / TN, T = tm_n * tn_n;
+    const int64_t G = gridDim.x, w = blockIdx.x;
+    const int nst = (int)(K / KS);
+    const int64_t cpr = K / 2, spr = K / C::B;
+    const TileGeo g0 = tile_geo(w, M, N);
+
+    // loads of the stream position p (the workgroup's first stage once past its end)
+    auto issue_at = [&](const LoadPos<C> &p, uint8_t *buf) {
+        const bool live = p.v < T;
+        const TileGeo &g = live ? p.g : g0;
+        const int64_t k0 = live ? (int64_t)p.s * KS : 0;
+        return StageIssue<C>{buf, true, wave, lane, g.rows_a, g.rows_b, cpr, spr,
+                             a_codes + g.m0 * cpr + k0 / 2, b_codes + g.n0 * cpr + k0 / 2,
+                             a_scales + g.m0 * spr + k0 / C::B, b_scales + g.n0 * spr + k0 / C::B};
+    };
+
+    // prologue: stages 0 .. NB-1 into buffers 0 .. NB-1 (the second half of
+    // stage NB-1 goes out in substep 0 of stage 0), then wait for stage 0
+    LoadPos<C> ld{w, 0, g0};
+    StageIssue<C> prev = issue_at(ld, smem);
+#pragma unroll
+    for (int p = 0; p < NB; ++p) {
+        prev = issue_at(ld, smem + p * C::STAGE);
+        if (p < NB - 1) prev.template region<0, 1>();
+        else load_first_half(prev);
+        ld.advance(nst, G, M, N);
+    }
+    wait_vmcnt<(NB - 2) * C::LPS + half_count<C>()>();
+    asm volatile("s_barrier" ::: "memory");
+
+    const MxLane<C> ln(wm * 128 + (lane & 31), wn * 128 + (lane & 31), h);
+    MxState<C> st;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        st.a[0][i] = lds16(smem + ln.codeA[0] + 32 * C::ROW * i);
+        st.b[0][i] = lds16(smem + ln.codeB[0] + 32 * C::ROW * i);
+        st.na[i] = mx_scale_read<C>(smem + ln.scA + 32 * C::SB * i);
+        st.nb[i] = mx_scale_read<C>(smem + ln.scB + 32 * C::SB * i);
+    }
+
+    int64_t gs = 0;                                     // stream position (buffer gs % NB)
+    for (int64_t v = w; v < T; v += G) {
+        v16f acc[4][4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = v16f{};
+        {
+            StageIssue<C> issue = issue_at(ld, smem);
+            mx_stage_p<C, NB, true>(acc, st, smem, gs, ln, prev, issue);
+            ld.advance(nst, G, M, N);
+            prev = issue;
+            ++gs;
+        }
+        for (int s = 1; s < nst; ++s, ++gs) {
+            StageIssue<C> issue = issue_at(ld, smem);
+            mx_stage_p<C, NB, false>(acc, st, smem, gs, ln, prev, issue);
+            ld.advance(nst, G, M, N);
+            prev = issue;
+        }
+        store_tile(acc, tile_geo(v, M, N), M, N, wm, wn, lane, 1.0f, y, y_bf16, ldy);
+    }
+    // no load may still be writing this workgroup's LDS when it exits
+    wait_vmcnt<0>();
+}
+
 template <int FMT, int KS, int NBUF>
 __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(
     int64_t M, int64_t N, int64_t K, const uint8_t *__restrict__ a_codes,
@@ -585,8 +815,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     if constexpr (FMT == kNV) {
-        nv_persistent<C>(smem, M, N, K, a_codes, a_scales, (*ga) * (*gb), b_codes, b_scales, y, y_bf16,
-                         ldy, wave, lane);
+        nv_persistent<C>(smem, M, N, K, a_codes, a_scales, uniform_load(ga) * uniform_load(gb), b_codes,
+                         b_scales, y, y_bf16, ldy, wave, lane);
+        return;
+    } else if constexpr (REQAT_MX_PERSISTENT) {
+        mx_persistent<C, NBUF>(smem, M, N, K, a_codes, a_scales, b_codes, b_scales, y, y_bf16, ldy, wave, lane);
         return;
     }
     const int h = lane >> 5;
@@ -675,7 +908,7 @@ hipError_t launch_cfg(int64_t M, int64_t N, int64_t K, const uint8_t *a_codes, c
                       const float *ga, const uint8_t *b_codes, const uint8_t *b_scales,
                       const float *gb, void *y, bool y_bf16, int64_t ldy, hipStream_t stream) {
     int64_t grid = ((M + TM - 1) / TM) * ((N + TN - 1) / TN);
-    if (FMT == kNV) {
+    if (FMT == kNV || REQAT_MX_PERSISTENT) {
         // persistent: one workgroup per CU (a multiple of 8 keeps each one on its XCD)
         const int cus = compute_units();
         if (cus <= 0) return hipErrorInvalidDevice;
