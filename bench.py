@@ -193,6 +193,21 @@ def main():
     per = {n: float(np.mean([events[i][j].elapsed_time(events[i][j + 1]) for i in range(args.steps)]))
            for j, n in enumerate(names)}
 
+    # the same activation quantize + product through the one-call linear entry
+    # point (a kernel right before the product on the same stream), timed apart
+    lws = torch.empty(reqat.reqat_linear_workspace_bytes(fmt, M, K), dtype=torch.uint8, device=dev)
+    gl = torch.empty(1, dtype=torch.float32, device=dev) if fmt == reqat.NVFP4 else None
+    for _ in range(max(1, args.warmup)):
+        reqat.linear(x, fmt, wc, wsc, gw, out_dtype=torch.bfloat16, out=y, g_out=gl, ws=lws)
+    lev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    lev[0].record()
+    for _ in range(args.steps):
+        reqat.linear(x, fmt, wc, wsc, gw, out_dtype=torch.bfloat16, out=y, g_out=gl, ws=lws)
+    lev[1].record()
+    torch.cuda.synchronize()
+    linear_ms = lev[0].elapsed_time(lev[1]) / args.steps
+
     flops = 2.0 * M * N * K
     q_bytes = lambda rows: rows * K * (2 + 0.5 + 1.0 / B)        # read bf16, write codes + scales
     fq_bytes = lambda rows: rows * K * 4.0                        # read bf16, write bf16
@@ -210,6 +225,9 @@ def main():
                    "frac_hbm_peak": round(gbs / PEAK["hbm"], 4),
                    "note": "includes the absmax pass (its bytes not credited)"}
 
+    kern["linear"] = {"ms": round(linear_ms, 4),
+                      "vs_quantize_x_plus_gemm": round(linear_ms / (per["quantize_x"] + per["gemm"]), 4),
+                      "note": "reqat_linear_w4a4: quantize X + GEMM in one call, timed separately"}
     out = {
         "metric": METRIC,
         "value": round(flops / (ms_step * 1e-3) / 1e12, 2),

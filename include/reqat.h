@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define REQAT_ABI_VERSION 1
+#define REQAT_ABI_VERSION 2
 
 typedef enum {
     REQAT_FMT_NVFP4 = 0, /* B = 16, E4M3 block scale, FP32 global scale */
@@ -137,6 +137,36 @@ reqat_status reqat_gemm_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K,
                              const uint8_t *b_codes, const uint8_t *b_scales,
                              const float *b_tensor_scale,
                              void *y, reqat_dtype y_dtype, int64_t ldy, void *stream);
+
+/*
+ * W4A4 linear layer: quantize the activations x[M][K] (bfloat16) and multiply
+ * them by already-quantized weights (the "4-bit GEMM enabled by activation
+ * quantization" of Sec. 5.3):
+ *   Y = gemm_w4a4(quantize(x), W)
+ * The activation quantization follows reqat_quantize_fp4 exactly (same codes,
+ * scales and computed g); it runs as a kernel on `stream` immediately before
+ * the product, with the activation codes and scales kept in `workspace`.
+ *   x, ldx         : bfloat16 activations, ldx >= K, ldx % 8 == 0, 16-byte aligned.
+ *   x_tensor_scale : NVFP4: device float, written (COMPUTE) or read (GIVEN);
+ *                    MXFP4: must be NULL.
+ *   ts             : REQAT_TS_COMPUTE or REQAT_TS_GIVEN (ignored for MXFP4).
+ *   w_codes, w_scales, w_tensor_scale : the weights, as b_* of reqat_gemm_w4a4.
+ *   y, y_dtype, ldy: as reqat_gemm_w4a4.
+ *   workspace      : device scratch of reqat_linear_workspace_bytes(fmt, M, K)
+ *                    bytes, 256-byte aligned; it holds the activation codes
+ *                    and scales until the product has run.
+ * Requirements: K % 128 == 0, plus those of the two operations.  M == 0 is a
+ * no-op except that COMPUTE writes g = 1; N == 0 (M > 0) enqueues nothing.
+ */
+reqat_status reqat_linear_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K,
+                               const void *x, int64_t ldx, float *x_tensor_scale,
+                               reqat_tscale_mode ts, const uint8_t *w_codes,
+                               const uint8_t *w_scales, const float *w_tensor_scale,
+                               void *y, reqat_dtype y_dtype, int64_t ldy, void *workspace,
+                               void *stream);
+
+/* Bytes of workspace reqat_linear_w4a4 needs for M x K activations (0 on bad arguments). */
+size_t reqat_linear_workspace_bytes(reqat_format fmt, int64_t M, int64_t K);
 
 /* Bytes of device workspace that a quantize / fake-quant call may use. */
 size_t reqat_workspace_bytes(void);

@@ -112,6 +112,61 @@ reqat_status reqat_gemm_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K,
 
 size_t reqat_workspace_bytes(void) { return sizeof(uint32_t) * kMaxPartials; }
 
+// Linear workspace: [absmax partials | activation codes | activation scales],
+// each part starting on a 256-byte boundary.
+static size_t round256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+size_t reqat_linear_workspace_bytes(reqat_format fmt, int64_t M, int64_t K) {
+    if (!fmt_ok(fmt) || M < 0 || K < 0 || K % 128) return 0;
+    const size_t codes = (size_t)M * (size_t)(K / 2);
+    const size_t scales = (size_t)M * (size_t)(K / block_of(fmt));
+    return round256(sizeof(uint32_t) * kMaxPartials) + round256(codes) + round256(scales);
+}
+
+reqat_status reqat_linear_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K, const void *x,
+                               int64_t ldx, float *x_tensor_scale, reqat_tscale_mode ts,
+                               const uint8_t *w_codes, const uint8_t *w_scales,
+                               const float *w_tensor_scale, void *y, reqat_dtype y_dtype,
+                               int64_t ldy, void *workspace, void *stream) {
+    if (!fmt_ok(fmt)) return REQAT_E_ENUM;
+    if (y_dtype != REQAT_DT_F32 && y_dtype != REQAT_DT_BF16) return REQAT_E_ENUM;
+    const bool nv = fmt == REQAT_FMT_NVFP4;
+    if (nv && ts != REQAT_TS_COMPUTE && ts != REQAT_TS_GIVEN) return REQAT_E_ENUM;
+    if (M < 0 || N < 0 || K < 0) return REQAT_E_SHAPE;
+    if (K % 128 || ldx < K || ldy < N) return REQAT_E_SHAPE;
+    if (!nv && (x_tensor_scale || w_tensor_scale)) return REQAT_E_UNSUPPORTED;
+    if (nv && (!x_tensor_scale || !w_tensor_scale)) return REQAT_E_NULL;
+    if (!workspace) return REQAT_E_NULL;
+    if (reinterpret_cast<uintptr_t>(workspace) & 255u) return REQAT_E_ALIGN;
+    if (M > 0 && N > 0) {
+        if (!x || !y) return REQAT_E_NULL;
+        if (K > 0 && (!w_codes || !w_scales)) return REQAT_E_NULL;
+        if (!aligned16(x) || ldx % 8) return REQAT_E_ALIGN;
+        if (reinterpret_cast<uintptr_t>(y) & (y_dtype == REQAT_DT_BF16 ? 1u : 3u)) return REQAT_E_ALIGN;
+        if (K > 0 && (!aligned16(w_codes) || !aligned16(w_scales))) return REQAT_E_ALIGN;
+        if (nv && ((reinterpret_cast<uintptr_t>(x_tensor_scale) & 3u) ||
+                   (reinterpret_cast<uintptr_t>(w_tensor_scale) & 3u)))
+            return REQAT_E_ALIGN;
+    }
+    uint8_t *ws = reinterpret_cast<uint8_t *>(workspace);
+    uint8_t *a_codes = ws + round256(sizeof(uint32_t) * kMaxPartials);
+    uint8_t *a_scales = a_codes + round256((size_t)M * (size_t)(K / 2));
+    if (M == 0 || N == 0) {
+        // nothing to multiply; a computed activation scale is still defined
+        if (nv && ts == REQAT_TS_COMPUTE && M == 0 &&
+            launch_unit_scale(x_tensor_scale, reinterpret_cast<hipStream_t>(stream)) != hipSuccess)
+            return REQAT_E_HIP;
+        return REQAT_OK;
+    }
+    reqat_status st = run_quant(fmt, x, M, K, ldx, a_codes, a_scales, nullptr, 0, x_tensor_scale, ts,
+                                workspace, stream, false);
+    if (st != REQAT_OK) return st;
+    hipError_t e = launch_gemm(nv ? kNV : kMX, M, N, K, a_codes, a_scales, x_tensor_scale, w_codes,
+                               w_scales, w_tensor_scale, y, y_dtype == REQAT_DT_BF16, ldy,
+                               reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
+}
+
 const char *reqat_status_str(reqat_status s) {
     switch (s) {
     case REQAT_OK: return "REQAT_OK";

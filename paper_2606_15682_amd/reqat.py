@@ -40,6 +40,9 @@ SIGNATURES = {
     "reqat_fakequant_fp4": (_INT, [_INT, _VP, _I64, _I64, _I64, _VP, _I64, _VP, _INT, _VP, _VP]),
     "reqat_gemm_w4a4": (_INT, [_INT, _I64, _I64, _I64, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _INT,
                                _I64, _VP]),
+    "reqat_linear_w4a4": (_INT, [_INT, _I64, _I64, _I64, _VP, _I64, _VP, _INT, _VP, _VP, _VP, _VP,
+                                 _INT, _I64, _VP, _VP]),
+    "reqat_linear_workspace_bytes": (ctypes.c_size_t, [_INT, _I64, _I64]),
     "reqat_workspace_bytes": (ctypes.c_size_t, []),
     "reqat_status_str": (ctypes.c_char_p, [_INT]),
     "reqat_abi_version": (_INT, []),
@@ -87,6 +90,16 @@ def reqat_gemm_w4a4(fmt, M, N, K, a_codes, a_scales, a_ts, b_codes, b_scales, b_
                     ldy, stream):
     return load().reqat_gemm_w4a4(fmt, M, N, K, a_codes, a_scales, a_ts, b_codes, b_scales, b_ts, y,
                                   y_dtype, ldy, stream)
+
+
+def reqat_linear_w4a4(fmt, M, N, K, x, ldx, x_ts, ts, w_codes, w_scales, w_ts, y, y_dtype, ldy,
+                      workspace, stream):
+    return load().reqat_linear_w4a4(fmt, M, N, K, x, ldx, x_ts, ts, w_codes, w_scales, w_ts, y,
+                                    y_dtype, ldy, workspace, stream)
+
+
+def reqat_linear_workspace_bytes(fmt, M, K) -> int:
+    return load().reqat_linear_workspace_bytes(fmt, M, K)
 
 
 def reqat_workspace_bytes() -> int:
@@ -197,3 +210,23 @@ def gemm(fmt, a_codes, a_scales, a_g, b_codes, b_scales, b_g, out_dtype=torch.fl
                          y.stride(0), _stream(a_codes.device))
     _check(st, "reqat_gemm_w4a4")
     return y
+
+
+def linear(x: torch.Tensor, fmt, w_codes, w_scales, w_g, x_tensor_scale=None, out_dtype=torch.bfloat16,
+           out=None, g_out=None, ws=None):
+    """Y = quantize(x) . W^T for already-quantized weights.  Returns (Y, g_x).
+    ws: optional workspace tensor of reqat_linear_workspace_bytes(fmt, M, K) bytes."""
+    M, K, ldx = _x2d(x)
+    N = w_codes.shape[0]
+    if w_codes.shape[1] * 2 != K:
+        raise ValueError("K mismatch")
+    dt = DT_F32 if out_dtype == torch.float32 else DT_BF16
+    y = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=x.device)
+    g, ts = _gscale(fmt, x, x_tensor_scale, g_out)
+    if ws is None:
+        ws = torch.empty(reqat_linear_workspace_bytes(fmt, M, K), dtype=torch.uint8, device=x.device)
+    st = reqat_linear_w4a4(fmt, M, N, K, x.data_ptr(), ldx, _ptr(g), ts, w_codes.data_ptr(),
+                           w_scales.data_ptr(), _ptr(w_g), y.data_ptr(), dt, y.stride(0), ws.data_ptr(),
+                           _stream(x.device))
+    _check(st, "reqat_linear_w4a4")
+    return y, g

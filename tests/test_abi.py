@@ -48,7 +48,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_small_queries(lib):
-    assert reqat.reqat_abi_version() == 1
+    assert reqat.reqat_abi_version() == 2
     assert reqat.reqat_workspace_bytes() >= 4
     for s in range(7):
         assert reqat.reqat_status_str(s).startswith(reqat.STATUS[s])
@@ -109,6 +109,44 @@ def test_gemm_validation(lib):
     assert gm(ac=P + 1) == E_ALIGN
     assert gm(y=P + 2) == E_ALIGN               # float32 output needs 4-byte alignment
     assert gm(y=P + 1, dt=1) == E_ALIGN         # bf16 output needs 2-byte alignment
+
+
+def ln(fmt=NV, M=4, N=8, K=128, x=P, ldx=128, xg=P, ts=0, wc=P, ws_=P, wg=P, y=P, dt=0, ldy=8, ws=P):
+    return reqat.reqat_linear_w4a4(fmt, M, N, K, x, ldx, xg, ts, wc, ws_, wg, y, dt, ldy, ws, None)
+
+
+def test_linear_workspace_bytes(lib):
+    # partials (1024 words) | codes M*K/2 | scales M*K/B, each rounded up to 256 bytes
+    assert reqat.reqat_linear_workspace_bytes(NV, 4, 128) == 4096 + 256 + 256
+    assert reqat.reqat_linear_workspace_bytes(MX, 300, 1024) == 4096 + 153600 + 9728
+    assert reqat.reqat_linear_workspace_bytes(NV, 4, 64) == 0      # K % 128
+    assert reqat.reqat_linear_workspace_bytes(NV, -1, 128) == 0
+    assert reqat.reqat_linear_workspace_bytes(7, 4, 128) == 0
+
+
+def test_linear_validation(lib):
+    assert ln(fmt=2) == E_ENUM
+    assert ln(dt=9) == E_ENUM
+    assert ln(ts=5) == E_ENUM
+    assert ln(M=-1) == E_SHAPE
+    assert ln(K=64, ldx=64) == E_SHAPE            # K % 128
+    assert ln(ldx=64) == E_SHAPE                  # ldx < K
+    assert ln(ldy=4) == E_SHAPE
+    assert ln(fmt=MX) == E_UNSUP                  # MXFP4 with tensor scales
+    assert ln(xg=None) == E_NULL
+    assert ln(wg=None) == E_NULL
+    assert ln(ws=None) == E_NULL
+    assert ln(ws=P + 16) == E_ALIGN               # workspace 256-byte aligned
+    assert ln(x=None) == E_NULL
+    assert ln(y=None) == E_NULL
+    assert ln(wc=None) == E_NULL
+    assert ln(x=P + 2) == E_ALIGN
+    assert ln(ldx=132) == E_ALIGN                 # ldx % 8
+    assert ln(wc=P + 8) == E_ALIGN
+    assert ln(y=P + 2) == E_ALIGN
+    assert ln(xg=P + 2) == E_ALIGN
+    # nothing to do: N == 0 with M > 0 enqueues nothing and returns OK
+    assert ln(N=0, x=None, y=None) == OK
 
 
 def test_binding_raises_when_library_missing(tmp_path):

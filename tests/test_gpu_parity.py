@@ -275,3 +275,42 @@ def test_gemm_k_zero_writes_zeros():
     assert st == 0
     torch.cuda.synchronize()
     assert torch.all(y == 0).item()
+
+# ------------------------------------------------------------------ linear (quantize X + GEMM)
+
+@pytest.mark.parametrize("fmt", [NV, MX])
+@pytest.mark.parametrize("M,N,K,given", [(16, 256, 256, False), (5, 300, 128, False),
+                                         (300, 520, 768, False), (257, 256, 2048, True)])
+def test_linear_parity(fmt, M, N, K, given):
+    """reqat_linear_w4a4 = quantize X (same codes, scales and g as reqat_quantize_fp4,
+    checked against the oracle) followed by the product, to the GEMM bar."""
+    log("linear fmt=%d M=%d N=%d K=%d given=%s" % (fmt, M, N, K, given))
+    seed = 11 * M + 5 * N + K
+    xa = _rand(M, K, seed, "student_t", outliers=max(1, K // 100))
+    xb = _rand(N, K, seed + 3, "normal", std=0.02)
+    gx = 0.0625 if (given and fmt == NV) else None
+    ac, as_, ga = oracle.quantize(fmt, xa, gx)
+    bc, bs, gb = oracle.quantize(fmt, xb)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    x = wl.from_bits(xa).to(DEV)
+    wg = None if fmt == MX else torch.tensor([gb], dtype=torch.float32, device=DEV)
+    xg_in = None if gx is None else torch.tensor([gx], dtype=torch.float32, device=DEV)
+    outs = []
+    for dt, poison in ((torch.float32, float("nan")), (torch.float32, 0.0), (torch.bfloat16, float("nan"))):
+        y = torch.full((M, N), poison, dtype=dt, device=DEV)
+        ws = torch.full((reqat.reqat_linear_workspace_bytes(fmt, M, K),), 0xAB, dtype=torch.uint8, device=DEV)
+        _, g = reqat.linear(x, fmt, t(bc), t(bs), wg, x_tensor_scale=xg_in, out_dtype=dt, out=y, ws=ws)
+        torch.cuda.synchronize()
+        if fmt == NV:
+            assert float(g.cpu()[0]) == np.float32(ga)
+        # the activation codes and scales the call left in its workspace are the oracle's
+        off = 4096
+        wsn = ws.cpu().numpy()
+        codes = wsn[off:off + M * K // 2].reshape(M, K // 2)
+        off2 = off + ((M * K // 2 + 255) // 256) * 256
+        scales = wsn[off2:off2 + M * (K // reqat.BLOCK[fmt])].reshape(M, K // reqat.BLOCK[fmt])
+        assert np.array_equal(codes, ac) and np.array_equal(scales, as_)
+        outs.append(y.float().cpu().numpy().astype(np.float64))
+    assert np.array_equal(outs[0], outs[1], equal_nan=True), "poison visible or nondeterministic"
+    ms, ns = np.arange(M).repeat(N), np.tile(np.arange(N), M)
+    check_gemm_points(fmt, ac, as_, ga, bc, bs, gb, outs[0], outs[2], ms, ns)
