@@ -225,6 +225,20 @@ def main():
                    "frac_hbm_peak": round(gbs / PEAK["hbm"], 4),
                    "note": "includes the absmax pass (its bytes not credited)"}
 
+    if M <= 64:
+        # decode shape: the product streams the weights once, so it is bounded by HBM
+        gemm_bytes = (N + M) * K * (0.5 + 1.0 / B) + M * N * 2.0
+        gbs = gemm_bytes / (per["gemm"] * 1e-3) / 1e9
+        kern["gemm"]["GB/s"] = round(gbs, 1)
+        kern["gemm"]["algorithmic_bytes"] = int(gemm_bytes)
+        roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK["hbm"], "unit": "GB/s",
+                    "frac": round(gbs / PEAK["hbm"], 4), "traffic": None,
+                    "kernel": "gemm_skinny_kernel (%s W4A4 GEMM, M <= 64)" % w.fmt}
+    else:
+        roofline = {"bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": PEAK[mfma_dtype],
+                    "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK[mfma_dtype], 4),
+                    "traffic": profiled_traffic(w.fmt, args.workload),
+                    "kernel": "gemm_tile256_kernel (%s W4A4 GEMM)" % w.fmt}
     kern["linear"] = {"ms": round(linear_ms, 4),
                       "vs_quantize_x_plus_gemm": round(linear_ms / (per["quantize_x"] + per["gemm"]), 4),
                       "note": "reqat_linear_w4a4: quantize X + GEMM in one call, timed separately"}
@@ -245,10 +259,7 @@ def main():
                    "gemm_out": "bf16", "global_batch": M, "parallelism": "single GPU",
                    "step": "quantize X + quantize W (dynamic global scales) + W4A4 GEMM + "
                            "fake-quant X and W"},
-        "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": PEAK[mfma_dtype],
-                     "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK[mfma_dtype], 4),
-                     "traffic": profiled_traffic(w.fmt, args.workload),
-                     "kernel": "gemm_tile256_kernel (%s W4A4 GEMM)" % w.fmt},
+        "roofline": roofline,
         "kernels": kern,
     }
     if not args.no_cpu_baseline:

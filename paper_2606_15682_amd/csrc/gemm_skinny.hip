@@ -5,14 +5,15 @@
 // every CU, with enough bytes in flight to cover the memory latency.
 //
 // Each 256-thread workgroup owns 32 rows of B (one 32-wide MFMA tile of the
-// output) and all of K; its four waves take interleaved 64-element chunks of
-// K (wave w: chunks w, w + 4, ...) and their partial sums meet in LDS at the
-// end.  A lane loads its operands straight into registers in the MFMA layout
+// output) and all of K; its four waves take contiguous quarters of the K
+// chunks (64 elements each) and their partial sums meet in LDS at the end.
+// A lane loads its operands straight into registers in the MFMA layout
 // (row = lane % 32, 32 consecutive K elements = 16 bytes per lane, lane half
-// h = lane / 32 taking the chunk's second 32 elements), D chunks ahead of the
-// one it multiplies.  The activation tile (M rows padded to 32 or 64, padding
-// rows re-reading the last real row and never stored) is reread by every
-// workgroup from L2.
+// h = lane / 32 taking the chunk's second 32 elements), up to kDepth chunks
+// ahead of the one it multiplies (for decode-sized K that is all of them, so
+// a workgroup's whole share of B is in flight at once).  The activation tile
+// (M rows padded to 32 or 64, padding rows re-reading the last real row and
+// never stored) is reread by every workgroup from L2.
 //
 // MXFP4: v_mfma_scale_f32_32x32x64_f8f6f4 on the codes, the lane's 32
 // elements being one MX block whose E8M0 byte rides along.
@@ -35,7 +36,7 @@ typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef _Float16 v2h __attribute__((ext_vector_type(2)));
 
 constexpr int kThreads = 256;
-constexpr int kDepth = 4;                       // chunks in flight per wave
+constexpr int kDepth = 8;                       // chunks in flight per wave
 
 template <int MT>
 struct Chunk {
@@ -122,7 +123,7 @@ __global__ __launch_bounds__(kThreads) void gemm_skinny_kernel(
     const int64_t n0 = (int64_t)blockIdx.x * 32;
     const int64_t cpr = K / 2, spr = K / B;
     const int64_t nch = K / 64;
-    const int64_t my = nch > wave ? (nch - wave + 3) / 4 : 0;   // chunks of this wave
+    const int64_t c0 = nch * wave / 4, my = nch * (wave + 1) / 4 - c0;   // this wave's chunks
 
     v16f acc[MT];
 #pragma unroll
@@ -132,7 +133,7 @@ __global__ __launch_bounds__(kThreads) void gemm_skinny_kernel(
 #pragma unroll
     for (int j = 0; j < kDepth; ++j)
         if (j < my)
-            load_chunk<FMT, MT>(q[j], wave + 4 * j, r, h, M, N, n0, cpr, spr, a_codes, a_scales, b_codes,
+            load_chunk<FMT, MT>(q[j], c0 + j, r, h, M, N, n0, cpr, spr, a_codes, a_scales, b_codes,
                                 b_scales);
     for (int64_t i0 = 0; i0 < my; i0 += kDepth) {
 #pragma unroll
@@ -141,7 +142,7 @@ __global__ __launch_bounds__(kThreads) void gemm_skinny_kernel(
             if (i < my) {
                 mul_chunk<FMT, MT>(acc, q[j]);
                 if (i + kDepth < my)
-                    load_chunk<FMT, MT>(q[j], wave + 4 * (i + kDepth), r, h, M, N, n0, cpr, spr, a_codes,
+                    load_chunk<FMT, MT>(q[j], c0 + i + kDepth, r, h, M, N, n0, cpr, spr, a_codes,
                                         a_scales, b_codes, b_scales);
             }
         }

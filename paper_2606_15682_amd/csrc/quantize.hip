@@ -63,7 +63,25 @@ __device__ __forceinline__ uint32_t finite_mag2(uint32_t w) {
     return lo > hi ? lo : hi;
 }
 
-// One partial maximum of the finite bfloat16 magnitudes per workgroup.
+// Packed (two 16-bit lanes) maximum of the bfloat16 magnitudes of a 16-byte vector.
+__device__ __forceinline__ us2 mag_max8(uint4 d, us2 m) {
+    m = __builtin_elementwise_max(m, __builtin_bit_cast(us2, d.x & 0x7FFF7FFFu));
+    m = __builtin_elementwise_max(m, __builtin_bit_cast(us2, d.y & 0x7FFF7FFFu));
+    m = __builtin_elementwise_max(m, __builtin_bit_cast(us2, d.z & 0x7FFF7FFFu));
+    m = __builtin_elementwise_max(m, __builtin_bit_cast(us2, d.w & 0x7FFF7FFFu));
+    return m;
+}
+
+__device__ __forceinline__ uint32_t finite_max8(uint4 d, uint32_t m) {
+    uint32_t a = finite_mag2(d.x), b = finite_mag2(d.y), c = finite_mag2(d.z), e = finite_mag2(d.w);
+    a = a > b ? a : b; c = c > e ? c : e; a = a > c ? a : c;
+    return m > a ? m : a;
+}
+
+// One partial maximum of the finite bfloat16 magnitudes per workgroup.  The
+// loop takes the plain packed maximum of all magnitudes (two VALU per dword);
+// only a lane whose maximum reached the non-finite patterns (>= 0x7F80)
+// walks its elements again with the finite filter.
 __global__ __launch_bounds__(kThreads) void absmax_kernel(const uint16_t *__restrict__ x,
                                                           int64_t rows, int64_t cols, int64_t ldx,
                                                           uint32_t *__restrict__ partials) {
@@ -72,37 +90,27 @@ __global__ __launch_bounds__(kThreads) void absmax_kernel(const uint16_t *__rest
         const int64_t total = rows * cols / 8;          // 16-byte vectors
         const uint4 *v = reinterpret_cast<const uint4 *>(x);
         const int64_t stride = (int64_t)gridDim.x * kThreads;
-        int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+        const int64_t i0 = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+        us2 m2 = us2{0, 0};
+        int64_t i = i0;
         for (; i + 3 * stride < total; i += 4 * stride) {
             uint4 d[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) d[u] = v[i + u * stride];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                uint32_t a = finite_mag2(d[u].x), b = finite_mag2(d[u].y);
-                uint32_t c = finite_mag2(d[u].z), e = finite_mag2(d[u].w);
-                a = a > b ? a : b; c = c > e ? c : e; a = a > c ? a : c;
-                m = m > a ? m : a;
-            }
+            for (int u = 0; u < 4; ++u) m2 = mag_max8(d[u], m2);
         }
-        for (; i < total; i += stride) {
-            uint4 d = v[i];
-            uint32_t a = finite_mag2(d.x), b = finite_mag2(d.y);
-            uint32_t c = finite_mag2(d.z), e = finite_mag2(d.w);
-            a = a > b ? a : b; c = c > e ? c : e; a = a > c ? a : c;
-            m = m > a ? m : a;
+        for (; i < total; i += stride) m2 = mag_max8(v[i], m2);
+        m = m2[0] > m2[1] ? m2[0] : m2[1];
+        if (m >= 0x7F80u) {                             // rare: a NaN or Inf among this lane's elements
+            m = 0;
+            for (int64_t j = i0; j < total; j += stride) m = finite_max8(v[j], m);
         }
     } else {
         const int64_t vpr = cols / 8;
         for (int64_t r = blockIdx.x; r < rows; r += gridDim.x) {
             const uint4 *v = reinterpret_cast<const uint4 *>(x + r * ldx);
-            for (int64_t c = threadIdx.x; c < vpr; c += kThreads) {
-                uint4 d = v[c];
-                uint32_t a = finite_mag2(d.x), b = finite_mag2(d.y);
-                uint32_t cc = finite_mag2(d.z), e = finite_mag2(d.w);
-                a = a > b ? a : b; cc = cc > e ? cc : e; a = a > cc ? a : cc;
-                m = m > a ? m : a;
-            }
+            for (int64_t c = threadIdx.x; c < vpr; c += kThreads) m = finite_max8(v[c], m);
         }
     }
     __shared__ uint32_t red[kThreads / 64];
@@ -276,6 +284,7 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
     }
     const uint32_t gb = bits_from_f32(g);
     const bool g_pow2 = (gb & 0x807FFFFFu) == 0u && (gb >> 23) != 0u;
+    const int kg = (int)(gb >> 23) - 127;               // g = 2^kg when g_pow2
 
     const int64_t nb = cols / B;
     const int64_t total = rows * nb;
@@ -283,7 +292,11 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
     const bool narrow = total < (int64_t(1) << 32);
     const int64_t stride = (int64_t)gridDim.x * kThreads;
 
-    for (int64_t blk = (int64_t)blockIdx.x * kThreads + threadIdx.x; blk < total; blk += stride) {
+    // Blocks are walked from the end of the tensor: the absmax pass that
+    // precedes an NVFP4 call with a computed g walks it from the start, so the
+    // tail it read last is still in the Infinity Cache.
+    for (int64_t it = (int64_t)blockIdx.x * kThreads + threadIdx.x; it < total; it += stride) {
+        const int64_t blk = total - 1 - it;
         int64_t xoff, yoff;
         if (contiguous) {
             xoff = blk * B;
@@ -326,13 +339,36 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
             p2 = f32_from_bits(sbyte << 23);
             Sd = __builtin_ldexp(1.0, (int)sbyte - 127);
         } else {
-            sbyte = bad ? 0x7Fu : nv_scale_byte(bf16_mag_value(am), g);
-            const float s = e4m3_value(sbyte);
-            const float S = s * g;
-            fast = !bad && sbyte != 0u && g_pow2 && S >= 0x1p-123f && S <= 0x1p125f;
-            p2 = f32_from_bits(bits_from_f32(S) & 0x7F800000u);
-            mant = f32_from_bits((bits_from_f32(S) & 0x007FFFFFu) | 0x3F800000u);
-            Sd = (double)s * (double)g;
+            // g = 2^kg and a normal bfloat16 amax = A * 2^(Ef - 134) (A = 128..255):
+            // the smallest 4-significant-bit value >= amax / 6 is
+            // Q(A) * 2^(Ef - 134), Q(A) = 2*ceil(A/12) (A <= 180) or 4*ceil(A/24),
+            // = (1 + f/8) * 2^j; when amax / (6g) rounded that way is a normal E4M3
+            // value it is the scale (dividing by g only moves the exponent), and
+            // s * g = Q(A) * 2^(Ef - 134) exactly.
+            fast = false;
+            const uint32_t Ef = am >> 7;
+            if (!bad && g_pow2 && Ef != 0u) {
+                const uint32_t A = 128u + (am & 0x7Fu);
+                const uint32_t j = A <= 180u ? 4u : 5u;
+                const uint32_t f = (A <= 180u ? (A + 11u) / 12u : (A + 23u) / 24u) - 8u;
+                const int ef = (int)(j + Ef) - 127 - kg;
+                const int eS = (int)(j + Ef) - 134;
+                if (ef >= 1 && (ef < 15 || (ef == 15 && f < 7u)) && eS >= -123 && eS <= 125) {
+                    sbyte = ((uint32_t)ef << 3) | f;
+                    p2 = f32_from_bits((uint32_t)(eS + 127) << 23);
+                    mant = f32_from_bits(0x3F800000u | (f << 20));
+                    fast = true;
+                }
+            }
+            if (!fast) {
+                sbyte = bad ? 0x7Fu : nv_scale_byte(bf16_mag_value(am), g);
+                const float s = e4m3_value(sbyte);
+                const float S = s * g;
+                fast = !bad && sbyte != 0u && g_pow2 && S >= 0x1p-123f && S <= 0x1p125f;
+                p2 = f32_from_bits(bits_from_f32(S) & 0x7F800000u);
+                mant = f32_from_bits((bits_from_f32(S) & 0x007FFFFFu) | 0x3F800000u);
+                Sd = (double)s * (double)g;
+            }
         }
 
         if (OUT == kCodes) {
