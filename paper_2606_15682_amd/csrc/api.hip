@@ -35,9 +35,12 @@ reqat_status check_quant(reqat_format fmt, const void *x, int64_t rows, int64_t 
     return REQAT_OK;
 }
 
+// `workspace` holds the kMaxPartials partial maxima; `seg_table` (NVFP4 with
+// a computed g) has room for seg_capacity segments, else the quantizer reads x twice.
 reqat_status run_quant(reqat_format fmt, const void *x, int64_t rows, int64_t cols, int64_t ldx,
                        uint8_t *codes, uint8_t *scales, void *y, int64_t ldy, float *tensor_scale,
-                       reqat_tscale_mode ts, void *workspace, void *stream, bool fake) {
+                       reqat_tscale_mode ts, void *workspace, uint16_t *seg_table, int64_t seg_capacity,
+                       void *stream, bool fake) {
     reqat_status st = check_quant(fmt, x, rows, cols, ldx, fake ? y : codes, scales, ldy,
                                   tensor_scale, ts, workspace, fake);
     if (st != REQAT_OK) return st;
@@ -48,20 +51,27 @@ reqat_status run_quant(reqat_format fmt, const void *x, int64_t rows, int64_t co
         if (compute && launch_unit_scale(tensor_scale, s) != hipSuccess) return REQAT_E_HIP;
         return REQAT_OK;
     }
-    int nparts = 0;
-    uint32_t *partials = reinterpret_cast<uint32_t *>(workspace);
-    if (compute) {
-        if (launch_absmax(reinterpret_cast<const uint16_t *>(x), rows, cols, ldx, partials, &nparts,
-                          s) != hipSuccess)
-            return REQAT_E_HIP;
-    }
     GSrc gsrc = !nv ? kGNone : (compute ? kGComputed : kGGiven);
     hipError_t e = launch_quantize(nv ? kNV : kMX, fake ? kFakeQuant : kCodes,
                                    reinterpret_cast<const uint16_t *>(x), rows, cols, ldx, codes,
                                    scales, reinterpret_cast<uint16_t *>(y), ldy, tensor_scale, gsrc,
-                                   partials, nparts, s);
+                                   reinterpret_cast<uint32_t *>(workspace), compute ? seg_table : nullptr,
+                                   seg_capacity, s);
     return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
 }
+
+// Quantize workspace: [kMaxPartials uint32 partial maxima | kMaxSegments uint16 segment table].
+uint16_t *quant_seg_table(void *workspace) {
+    return workspace ? reinterpret_cast<uint16_t *>(reinterpret_cast<uint8_t *>(workspace) +
+                                                    sizeof(uint32_t) * kMaxPartials)
+                     : nullptr;
+}
+
+size_t round256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+// Segments of 64 blocks in an M x K activation (NVFP4), and whether the linear
+// workspace carries a segment table for them.
+int64_t linear_segments(int64_t M, int64_t K) { return (M * (K / 16) + 63) / 64; }
 
 }  // namespace
 
@@ -71,14 +81,14 @@ reqat_status reqat_quantize_fp4(reqat_format fmt, const void *x, int64_t rows, i
                                 int64_t ldx, uint8_t *codes, uint8_t *scales, float *tensor_scale,
                                 reqat_tscale_mode ts, void *workspace, void *stream) {
     return run_quant(fmt, x, rows, cols, ldx, codes, scales, nullptr, 0, tensor_scale, ts,
-                     workspace, stream, false);
+                     workspace, quant_seg_table(workspace), kMaxSegments, stream, false);
 }
 
 reqat_status reqat_fakequant_fp4(reqat_format fmt, const void *x, int64_t rows, int64_t cols,
                                  int64_t ldx, void *y, int64_t ldy, float *tensor_scale,
                                  reqat_tscale_mode ts, void *workspace, void *stream) {
     return run_quant(fmt, x, rows, cols, ldx, nullptr, nullptr, y, ldy, tensor_scale, ts,
-                     workspace, stream, true);
+                     workspace, quant_seg_table(workspace), kMaxSegments, stream, true);
 }
 
 reqat_status reqat_gemm_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K,
@@ -110,17 +120,20 @@ reqat_status reqat_gemm_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K,
     return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
 }
 
-size_t reqat_workspace_bytes(void) { return sizeof(uint32_t) * kMaxPartials; }
+size_t reqat_workspace_bytes(void) {
+    return sizeof(uint32_t) * kMaxPartials + sizeof(uint16_t) * kMaxSegments;
+}
 
-// Linear workspace: [absmax partials | activation codes | activation scales],
-// each part starting on a 256-byte boundary.
-static size_t round256(size_t n) { return (n + 255) & ~(size_t)255; }
-
+// Linear workspace: [partial maxima | activation codes | activation scales |
+// NVFP4 segment table (when the activation fits kMaxSegments)], each part
+// starting on a 256-byte boundary.
 size_t reqat_linear_workspace_bytes(reqat_format fmt, int64_t M, int64_t K) {
     if (!fmt_ok(fmt) || M < 0 || K < 0 || K % 128) return 0;
     const size_t codes = (size_t)M * (size_t)(K / 2);
     const size_t scales = (size_t)M * (size_t)(K / block_of(fmt));
-    return round256(sizeof(uint32_t) * kMaxPartials) + round256(codes) + round256(scales);
+    const int64_t nseg = fmt == REQAT_FMT_NVFP4 ? linear_segments(M, K) : 0;
+    const size_t table = nseg <= kMaxSegments ? sizeof(uint16_t) * (size_t)nseg : 0;
+    return round256(sizeof(uint32_t) * kMaxPartials) + round256(codes) + round256(scales) + round256(table);
 }
 
 reqat_status reqat_linear_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K, const void *x,
@@ -158,8 +171,10 @@ reqat_status reqat_linear_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K
             return REQAT_E_HIP;
         return REQAT_OK;
     }
+    const int64_t nseg = nv ? linear_segments(M, K) : 0;
+    uint16_t *table = reinterpret_cast<uint16_t *>(a_scales + round256((size_t)M * (size_t)(K / block_of(fmt))));
     reqat_status st = run_quant(fmt, x, M, K, ldx, a_codes, a_scales, nullptr, 0, x_tensor_scale, ts,
-                                workspace, stream, false);
+                                workspace, nseg <= kMaxSegments ? table : nullptr, nseg, stream, false);
     if (st != REQAT_OK) return st;
     hipError_t e = launch_gemm(nv ? kNV : kMX, M, N, K, a_codes, a_scales, x_tensor_scale, w_codes,
                                w_scales, w_tensor_scale, y, y_dtype == REQAT_DT_BF16, ldy,

@@ -9,7 +9,13 @@ namespace reqat {
 
 // Maximum number of partial maxima the absmax pass produces; the workspace
 // holds one uint32 per partial.
-constexpr int kMaxPartials = 1024;
+#ifndef REQAT_MAX_PARTIALS
+#define REQAT_MAX_PARTIALS 4096
+#endif
+constexpr int kMaxPartials = REQAT_MAX_PARTIALS;
+
+// Segment-table capacity of the quantize workspace (segments of 64 blocks).
+constexpr int64_t kMaxSegments = int64_t(1) << 19;
 
 // Format selector shared by the launchers (same values as the C ABI enum).
 enum Fmt : int { kNV = 0, kMX = 1 };
@@ -25,10 +31,12 @@ hipError_t launch_unit_scale(float *gptr, hipStream_t stream);
 hipError_t launch_absmax(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
                          uint32_t *partials, int *nparts_out, hipStream_t stream);
 
+// NVFP4 with a computed g reads x once when the segment table (one uint16 per
+// 64 blocks) has room for the tensor, and twice (absmax pass first) otherwise.
 hipError_t launch_quantize(Fmt fmt, QuantOut out, const uint16_t *x, int64_t rows, int64_t cols,
                            int64_t ldx, uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy,
-                           float *gptr, GSrc gsrc, const uint32_t *partials, int nparts,
-                           hipStream_t stream);
+                           float *gptr, GSrc gsrc, uint32_t *partials, uint16_t *seg_table,
+                           int64_t seg_capacity, hipStream_t stream);
 
 bool gemm_tile256_supported(Fmt fmt, int64_t M, int64_t N, int64_t K, int64_t ldy);
 // Skinny product for M <= 64 (K % 64 == 0, K > 0).

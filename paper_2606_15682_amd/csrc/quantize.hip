@@ -40,7 +40,26 @@ namespace reqat {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kMaxGroups = 4096;      // grid cap of the quantize block loop
+#ifndef REQAT_Q_GROUPS
+#define REQAT_Q_GROUPS 4096
+#endif
+// blocks per lane per step: codes output / fake-quant output
+#ifndef REQAT_Q_UCODES
+#define REQAT_Q_UCODES 1
+#endif
+#ifndef REQAT_Q_UFQ
+#define REQAT_Q_UFQ 2
+#endif
+#ifndef REQAT_Q_BLOCKED
+#define REQAT_Q_BLOCKED 0
+#endif
+#ifndef REQAT_Q_SPW
+#define REQAT_Q_SPW 2
+#endif
+// grid cap of the block loop (one partial maximum per workgroup)
+constexpr int kMaxGroups = REQAT_Q_GROUPS < kMaxPartials ? REQAT_Q_GROUPS : kMaxPartials;
+constexpr int kSeg = 64;                    // blocks per segment: one per lane of a wave
+constexpr int kSegPerWave = REQAT_Q_SPW;    // segments per wave the grid size aims at
 
 typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
 typedef float v2f __attribute__((ext_vector_type(2)));
@@ -149,24 +168,30 @@ __device__ __forceinline__ void codes_general(const uint32_t (&w)[B / 2], const 
     }
 }
 
-// Fake-quant of one block by thresholds; P[m] = bfloat16 pattern of grid value m.
+// Fake-quant of one block by thresholds; P[m] = bfloat16 pattern of grid value
+// m.  Stores 16 bytes at a time, so no more than one vector of results is live.
 template <int B>
 __device__ __forceinline__ void fq_general(const uint32_t (&w)[B / 2], const uint32_t (&U)[7],
-                                           const uint32_t (&P)[8], bool bad,
-                                           uint32_t (&outw)[B / 2]) {
+                                           const uint32_t (&P)[8], bool bad, uint16_t *ydst) {
 #pragma unroll
-    for (int i = 0; i < B / 2; ++i) {
-        uint32_t res[2];
+    for (int q = 0; q < B / 8; ++q) {
+        uint32_t o[4];
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-            uint32_t h = hf ? (w[i] >> 16) : (w[i] & 0xFFFFu);
-            uint32_t mag = h & 0x7FFFu;
-            uint32_t v = P[0];
+        for (int k = 0; k < 4; ++k) {
+            const uint32_t word = w[4 * q + k];
+            uint32_t res[2];
 #pragma unroll
-            for (int t = 0; t < 7; ++t) v = (mag >= U[t]) ? P[t + 1] : v;
-            res[hf] = bad ? 0x7FC0u : (v | (h & 0x8000u));
+            for (int hf = 0; hf < 2; ++hf) {
+                uint32_t h = hf ? (word >> 16) : (word & 0xFFFFu);
+                uint32_t mag = h & 0x7FFFu;
+                uint32_t v = P[0];
+#pragma unroll
+                for (int t = 0; t < 7; ++t) v = (mag >= U[t]) ? P[t + 1] : v;
+                res[hf] = bad ? 0x7FC0u : (v | (h & 0x8000u));
+            }
+            o[k] = res[0] | (res[1] << 16);
         }
-        outw[i] = res[0] | (res[1] << 16);
+        reinterpret_cast<uint4 *>(ydst)[q] = make_uint4(o[0], o[1], o[2], o[3]);
     }
 }
 
@@ -251,166 +276,487 @@ __device__ __forceinline__ void fq_fast_nv(uint32_t word, float p2, float m, uin
     o[3] = fq_pair_nv(__builtin_amdgcn_cvt_scalef32_pk_f32_fp4(word, p2, 3), m);
 }
 
-// ---------------------------------------------------------------- kernel
+// ---------------------------------------------------------------- one block
 
+// The global scale as the block routine needs it.
+struct GScale {
+    float g;
+    bool pow2;      // g = 2^kg exactly
+    int kg;
+};
+
+__device__ __forceinline__ GScale make_gscale(float g) {
+    const uint32_t gb = bits_from_f32(g);
+    return GScale{g, (gb & 0x807FFFFFu) == 0u && (gb >> 23) != 0u, (int)(gb >> 23) - 127};
+}
+
+// Packed maximum of the bfloat16 magnitude patterns of a block (NaN/Inf give >= 0x7F80).
+template <int B>
+__device__ __forceinline__ uint32_t block_mag_max(const uint32_t (&w)[B / 2]) {
+    us2 mx2 = __builtin_bit_cast(us2, w[0] & 0x7FFF7FFFu);
+#pragma unroll
+    for (int i = 1; i < B / 2; ++i)
+        mx2 = __builtin_elementwise_max(mx2, __builtin_bit_cast(us2, w[i] & 0x7FFF7FFFu));
+    return mx2[0] > mx2[1] ? mx2[0] : mx2[1];
+}
+
+template <int B>
+__device__ __forceinline__ uint32_t block_finite_max(const uint32_t (&w)[B / 2]) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int i = 0; i < B / 2; ++i) {
+        const uint32_t f = finite_mag2(w[i]);
+        m = m > f ? m : f;
+    }
+    return m;
+}
+
+template <int B>
+__device__ __forceinline__ void load_block(const uint16_t *src16, uint32_t (&w)[B / 2]) {
+    const uint4 *src = reinterpret_cast<const uint4 *>(src16);
+#pragma unroll
+    for (int i = 0; i < B / 8; ++i) {
+        const uint4 d = src[i];
+        w[4 * i + 0] = d.x; w[4 * i + 1] = d.y; w[4 * i + 2] = d.z; w[4 * i + 3] = d.w;
+    }
+}
+
+// Element offset of block `blk` (row-major blocks, nb per row) in a matrix with leading dimension ld.
+__device__ __forceinline__ int64_t block_offset(int64_t blk, int64_t nb, int64_t cols, int64_t ld, int B,
+                                                bool narrow) {
+    if (ld == cols) return blk * B;
+    const int64_t r = narrow ? (int64_t)((uint32_t)blk / (uint32_t)nb) : blk / nb;
+    return r * ld + (blk - r * nb) * B;
+}
+
+// Scale byte of a block and, when the exact fast conversion applies, its parameters.
+struct BlockPlan {
+    uint32_t sbyte;
+    bool fast;
+    float p2, mant;     // s * g = mant * p2 (mant = 1 for MXFP4)
+};
+
+// FULL = false stops an NVFP4 block after the closed form (fast = false and no
+// scale byte when it does not apply), leaving the rest to emit_general.
+template <int FMT, int OUT, bool FULL = true>
+__device__ __forceinline__ BlockPlan plan_block(uint32_t am, const GScale &G) {
+    const bool bad = am >= 0x7F80u;                      // NaN or Inf somewhere in the block
+    BlockPlan pl{0u, false, 1.0f, 1.0f};
+    if (FMT == kMX) {
+        pl.sbyte = bad ? 0xFFu : mx_scale_byte(am);
+        pl.fast = !bad && pl.sbyte >= (OUT == kCodes ? 1u : 3u);
+        pl.p2 = f32_from_bits(pl.sbyte << 23);
+        return pl;
+    }
+    // g = 2^kg and a normal bfloat16 amax = A * 2^(Ef - 134) (A = 128..255):
+    // the smallest 4-significant-bit value >= amax / 6 is
+    // Q(A) * 2^(Ef - 134), Q(A) = 2*ceil(A/12) (A <= 180) or 4*ceil(A/24),
+    // = (1 + f/8) * 2^j; when amax / (6g) rounded that way is a normal E4M3
+    // value it is the scale (dividing by g only moves the exponent), and
+    // s * g = Q(A) * 2^(Ef - 134) exactly.
+    const uint32_t Ef = am >> 7;
+    if (!bad && G.pow2 && Ef != 0u) {
+        const uint32_t A = 128u + (am & 0x7Fu);
+        const uint32_t j = A <= 180u ? 4u : 5u;
+        const uint32_t f = (A <= 180u ? (A + 11u) / 12u : (A + 23u) / 24u) - 8u;
+        const int ef = (int)(j + Ef) - 127 - G.kg;
+        const int eS = (int)(j + Ef) - 134;
+        if (ef >= 1 && (ef < 15 || (ef == 15 && f < 7u)) && eS >= -123 && eS <= 125) {
+            pl.sbyte = ((uint32_t)ef << 3) | f;
+            pl.p2 = f32_from_bits((uint32_t)(eS + 127) << 23);
+            pl.mant = f32_from_bits(0x3F800000u | (f << 20));
+            pl.fast = true;
+            return pl;
+        }
+    }
+    if (!FULL) return pl;
+    pl.sbyte = bad ? 0x7Fu : nv_scale_byte(bf16_mag_value(am), G.g);
+    const float S = e4m3_value(pl.sbyte) * G.g;
+    pl.fast = !bad && pl.sbyte != 0u && G.pow2 && S >= 0x1p-123f && S <= 0x1p125f;
+    pl.p2 = f32_from_bits(bits_from_f32(S) & 0x7F800000u);
+    pl.mant = f32_from_bits((bits_from_f32(S) & 0x007FFFFFu) | 0x3F800000u);
+    return pl;
+}
+
+// Fast path: codes (and scale byte) or fake-quant values of one block.
 template <int FMT, int OUT>
+__device__ __forceinline__ void emit_fast(const uint32_t (&w)[(FMT == kMX ? 32 : 16) / 2], const BlockPlan &pl,
+                                          int64_t blk, uint8_t *codes, uint8_t *scales, uint16_t *ydst) {
+    constexpr int B = FMT == kMX ? 32 : 16;
+    uint32_t cw[B / 8];
+    if (FMT == kMX) codes_fast_mx<B>(w, pl.p2, cw);
+    else codes_fast_nv<B>(w, pl.p2, __builtin_amdgcn_rcpf(pl.mant), cw);
+    if (OUT == kCodes) {
+        uint8_t *dst = codes + blk * (B / 2);
+        if constexpr (B == 16) *reinterpret_cast<uint2 *>(dst) = make_uint2(cw[0], cw[1]);
+        else *reinterpret_cast<uint4 *>(dst) = make_uint4(cw[0], cw[1], cw[2], cw[3]);
+        scales[blk] = (uint8_t)pl.sbyte;
+    } else {
+        uint4 *dst = reinterpret_cast<uint4 *>(ydst);
+#pragma unroll
+        for (int q = 0; q < B / 8; ++q) {
+            uint32_t o[4];
+            if (FMT == kMX) fq_fast_mx(cw[q], pl.p2, o);
+            else fq_fast_nv(cw[q], pl.p2, pl.mant, o);
+            dst[q] = make_uint4(o[0], o[1], o[2], o[3]);
+        }
+    }
+}
+
+// Blocks the block loop's fast test did not take (NaN/Inf blocks, zero NVFP4
+// blocks, E4M3-subnormal scales, a non-power-of-two g, extreme exponents): the
+// complete scale rule, then the fast conversion when it still applies and the
+// threshold path otherwise.  The block is read from x again rather than kept
+// alive in the caller, so this rarely taken code does not raise the register
+// count of the loop around it.  Returns the scale byte.
+template <int FMT, int OUT>
+__device__ __forceinline__ uint32_t emit_general(const uint16_t *xsrc, const GScale &G, int64_t blk,
+                                                 uint8_t *codes, uint8_t *scales, uint16_t *ydst) {
+    constexpr int B = FMT == kMX ? 32 : 16;
+    asm volatile("" : "+v"(xsrc));                      // a fresh load, not the loop's registers
+    uint32_t w[B / 2];
+    load_block<B>(xsrc, w);
+    const uint32_t am = block_mag_max<B>(w);
+    const bool bad = am >= 0x7F80u;
+    const BlockPlan pl = plan_block<FMT, OUT>(am, G);
+    if (pl.fast) {
+        emit_fast<FMT, OUT>(w, pl, blk, codes, scales, ydst);
+        return pl.sbyte;
+    }
+    const uint32_t sbyte = pl.sbyte;
+    const double Sd = FMT == kMX ? __builtin_ldexp(1.0, (int)sbyte - 127)
+                                 : (double)e4m3_value(sbyte) * (double)G.g;
+    const bool zero = bad || (FMT == kNV && sbyte == 0u);
+    uint32_t U[7], P[8];
+    if (OUT == kCodes) {
+        general_plan<false>(Sd, zero, U, P);
+        uint32_t out[B / 8];
+        codes_general<B>(w, U, bad, out);
+        uint8_t *dst = codes + blk * (B / 2);
+        if constexpr (B == 16) *reinterpret_cast<uint2 *>(dst) = make_uint2(out[0], out[1]);
+        else *reinterpret_cast<uint4 *>(dst) = make_uint4(out[0], out[1], out[2], out[3]);
+        scales[blk] = (uint8_t)sbyte;
+    } else {
+        general_plan<true>(Sd, zero, U, P);
+        fq_general<B>(w, U, P, bad, ydst);
+    }
+    return sbyte;
+}
+
+// ---------------------------------------------------------------- block loop
+
+// How the NVFP4 global scale is obtained.
+enum GMode : int {
+    kGFixed = 0,      // read from *gptr (NVFP4 given g), or none (MXFP4)
+    kGFold = 1,       // folded from the partial maxima of a preceding absmax pass
+    kGDeferred = 2,   // per-segment reference, corrected by nv_fixup_kernel
+};
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        uint32_t o = __shfl_xor(v, off, 64);
+        v = v < o ? v : o;
+    }
+    return v;
+}
+
+// Global scale from the partial maxima.  Every thread issues its (at most
+// kMaxPartials / kThreads) loads at once, so the fold costs one L2 round trip.
+__device__ __forceinline__ float fold_partials(const uint32_t *__restrict__ partials, int nparts) {
+    __shared__ uint32_t red[kThreads / 64];
+    constexpr int kPer = (kMaxPartials + kThreads - 1) / kThreads;
+    uint32_t p[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int i = (int)threadIdx.x + j * kThreads;
+        p[j] = i < nparts ? partials[i] : 0u;
+    }
+    uint32_t m = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) m = m > p[j] ? m : p[j];
+    m = wave_max_u32(m);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    uint32_t r = red[0];
+#pragma unroll
+    for (int i = 1; i < kThreads / 64; ++i) r = r > red[i] ? r : red[i];
+    return nv_global_scale(r);
+}
+
+// Blocks are grouped in segments of kSeg = 64 consecutive blocks, one per lane
+// of a wave.  Workgroup i owns the contiguous segment range
+// [nseg*i/G, nseg*(i+1)/G) and its four waves take every fourth segment of it,
+// U segments per step (loads of all U issued before any is used).
+//
+// kGDeferred (NVFP4, computed g, one pass over x): the final g needs the tensor
+// amax, which is only known once every block has been read.  Each segment is
+// therefore quantized under its own reference g_r = the power-of-two global
+// scale rule applied to the segment's amax (g_r <= g, both powers of two).
+// Dividing g by a power of two only moves the exponent of s, so codes, s*g
+// and fake-quant values under g_r equal those under g for every block whose
+// scale under g is still a normal E4M3 value; nv_fixup_kernel then lowers the
+// scale exponents by log2(g/g_r) and re-quantizes from x only the blocks whose
+// scale would leave the normal range.  The segment table records, per
+// segment, log2(g_r) + 127 (0 when the segment holds no non-zero finite block,
+// whose outputs do not depend on g) and the smallest scale exponent field among
+// its non-zero finite blocks; each workgroup also writes the maximum finite
+// magnitude of its elements to partials[blockIdx.x].
+template <int FMT, int OUT, int GM, int U>
 __global__ __launch_bounds__(kThreads) void quantize_kernel(
     const uint16_t *__restrict__ x, int64_t rows, int64_t cols, int64_t ldx,
     uint8_t *__restrict__ codes, uint8_t *__restrict__ scales, uint16_t *__restrict__ y,
-    int64_t ldy, float *gptr, int gsrc, const uint32_t *__restrict__ partials, int nparts) {
+    int64_t ldy, float *gptr, uint32_t *__restrict__ partials, int nparts,
+    uint16_t *__restrict__ seg_table) {
     constexpr int B = FMT == kMX ? 32 : 16;
-    constexpr int NV4 = B / 8;                          // 16-byte vectors per block
 
-    // ---- global scale (NVFP4)
-    float g = 1.0f;
-    if (FMT == kNV) {
-        if (gsrc == kGComputed) {
-            __shared__ float g_sh;
-            if (threadIdx.x < 64) {
-                uint32_t m = 0;
-                for (int i = threadIdx.x; i < nparts; i += 64) {
-                    uint32_t p = partials[i];
-                    m = m > p ? m : p;
-                }
-                m = wave_max_u32(m);
-                if (threadIdx.x == 0) g_sh = nv_global_scale(m);
-            }
-            __syncthreads();
-            g = g_sh;
-            if (blockIdx.x == 0 && threadIdx.x == 0) *gptr = g;
-        } else {
-            g = *gptr;
-        }
+    GScale G = make_gscale(1.0f);
+    if (FMT == kNV && GM == kGFold) {
+        G = make_gscale(fold_partials(partials, nparts));
+        if (blockIdx.x == 0 && threadIdx.x == 0) *gptr = G.g;
+    } else if (FMT == kNV && GM == kGFixed) {
+        G = make_gscale(*gptr);
     }
-    const uint32_t gb = bits_from_f32(g);
-    const bool g_pow2 = (gb & 0x807FFFFFu) == 0u && (gb >> 23) != 0u;
-    const int kg = (int)(gb >> 23) - 127;               // g = 2^kg when g_pow2
 
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t nb = cols / B;
     const int64_t total = rows * nb;
-    const bool contiguous = ldx == cols;
+    const int64_t nseg = (total + kSeg - 1) / kSeg;
+    const bool narrow = total < (int64_t(1) << 32);
+#if REQAT_Q_BLOCKED
+    const int64_t s_begin = nseg * blockIdx.x / gridDim.x + wave;
+    const int64_t s_end = nseg * (blockIdx.x + 1) / gridDim.x;
+    const int64_t step = 4;
+#else
+    const int64_t s_begin = (int64_t)blockIdx.x * 4 + wave;
+    const int64_t s_end = nseg;
+    const int64_t step = (int64_t)gridDim.x * 4;
+#endif
+
+    // Loads the U blocks of the step starting at segment s.  A lane without a
+    // block there loads the tensor's last block instead (always valid, never
+    // used), so the loads need no branch.
+    auto load_step = [&](int64_t s, uint32_t (&wd)[U][B / 2]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            int64_t b = (s + step * u) * kSeg + lane;
+            b = (s + step * u < s_end && b < total) ? b : total - 1;
+            load_block<B>(x + block_offset(b, nb, cols, ldx, B, narrow), wd[u]);
+        }
+    };
+
+    uint32_t mloc = 0;                                  // kGDeferred: finite max of this lane's elements
+    for (int64_t s = s_begin; s < s_end; s += step * U) {
+        uint32_t wc[U][B / 2];
+        load_step(s, wc);
+        uint32_t am[U];
+        int64_t blk[U];
+        bool act[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            blk[u] = (s + step * u) * kSeg + lane;
+            act[u] = s + step * u < s_end && blk[u] < total;
+            am[u] = act[u] ? block_mag_max<B>(wc[u]) : 0u;
+        }
+
+        GScale Gs[U];
+        uint32_t segmax[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            Gs[u] = G;
+            if (GM == kGDeferred) {
+                const bool bad = am[u] >= 0x7F80u;
+                const uint32_t fm = bad ? block_finite_max<B>(wc[u]) : am[u];
+                mloc = mloc > fm ? mloc : fm;
+                segmax[u] = wave_max_u32(bad ? 0u : am[u]);
+                Gs[u] = make_gscale(nv_global_scale(segmax[u]));
+            }
+        }
+
+        bool general[U];
+        uint32_t sbyte[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            sbyte[u] = 0u;
+            general[u] = false;
+            if (act[u]) {
+                const BlockPlan pl = plan_block<FMT, OUT, false>(am[u], Gs[u]);
+                sbyte[u] = pl.sbyte;
+                general[u] = !pl.fast;
+                if (pl.fast) {
+                    uint16_t *ydst = OUT == kFakeQuant ? y + block_offset(blk[u], nb, cols, ldy, B, narrow) : nullptr;
+                    emit_fast<FMT, OUT>(wc[u], pl, blk[u], codes, scales, ydst);
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (general[u]) {
+                uint16_t *ydst = OUT == kFakeQuant ? y + block_offset(blk[u], nb, cols, ldy, B, narrow) : nullptr;
+                sbyte[u] = emit_general<FMT, OUT>(x + block_offset(blk[u], nb, cols, ldx, B, narrow), Gs[u], blk[u],
+                                                  codes, scales, ydst);
+            }
+            if (GM == kGDeferred && s + step * u < s_end) {
+                const bool live = act[u] && am[u] != 0u && am[u] < 0x7F80u;
+                const uint32_t emin = wave_min_u32(live ? sbyte[u] >> 3 : 0xFFu);
+                if (lane == 0)
+                    seg_table[s + step * u] =
+                        segmax[u] ? (uint16_t)((uint32_t)(Gs[u].kg + 127) | (emin << 8)) : (uint16_t)0;
+            }
+        }
+    }
+
+    if (GM == kGDeferred) {
+        __shared__ uint32_t red[kThreads / 64];
+        mloc = wave_max_u32(mloc);
+        if (lane == 0) red[wave] = mloc;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint32_t r = red[0];
+            for (int i = 1; i < kThreads / 64; ++i) r = r > red[i] ? r : red[i];
+            partials[blockIdx.x] = r;
+        }
+    }
+}
+
+// Subtracts sub (= sh << 3 < 128, a lowering of the exponent field by sh) from
+// each of the four scale bytes in v except 0x00 (zero block) and 0x7F (NaN
+// block), whose meaning does not depend on g.  Every other byte must have an
+// exponent field > sh, so no byte borrows from its neighbour.
+__device__ __forceinline__ uint32_t lower_scale_bytes(uint32_t v, uint32_t sub) {
+    const uint32_t z = ~(((v & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | v | 0x7F7F7F7Fu);   // 0x80 where a byte is 0x00
+    const uint32_t t = v ^ 0x7F7F7F7Fu;
+    const uint32_t n = ~(((t & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | t | 0x7F7F7F7Fu);   // 0x80 where a byte is 0x7F
+    const uint32_t mask = 0x01010101u & ~((z | n) >> 7);
+    return v - mask * sub;
+}
+
+// Second kernel of the one-pass NVFP4 quantizer (see quantize_kernel): folds
+// the partial maxima into g, publishes it, and corrects every segment whose
+// reference scale differs from g by the factor 2^sh.  One lane per segment:
+// when the segment's smallest scale exponent field exceeds sh, every block
+// keeps a normal scale, so codes and fake-quant values stand and only the
+// segment's 64 scale bytes are lowered (codes output).  Otherwise the wave
+// walks such segments together, one lane per block, lowering the bytes that
+// stay normal and re-quantizing the other blocks from x under g (fake-quant:
+// every block of the segment).  The lane's first table entry and scale bytes
+// are requested before the fold, so their latency overlaps it.
+template <int OUT>
+__global__ __launch_bounds__(kThreads) void nv_fixup_kernel(
+    const uint16_t *__restrict__ x, int64_t rows, int64_t cols, int64_t ldx,
+    uint8_t *__restrict__ codes, uint8_t *__restrict__ scales, uint16_t *__restrict__ y,
+    int64_t ldy, float *gptr, const uint32_t *__restrict__ partials, int nparts,
+    const uint16_t *__restrict__ seg_table) {
+    const int lane = threadIdx.x & 63;
+    const int64_t nb = cols / 16;
+    const int64_t total = rows * nb;
+    const int64_t nseg = (total + kSeg - 1) / kSeg;
     const bool narrow = total < (int64_t(1) << 32);
     const int64_t stride = (int64_t)gridDim.x * kThreads;
+    const int64_t first = (int64_t)blockIdx.x * kThreads + (threadIdx.x & ~63);
 
-    // Blocks are walked from the end of the tensor: the absmax pass that
-    // precedes an NVFP4 call with a computed g walks it from the start, so the
-    // tail it read last is still in the Infinity Cache.
-    for (int64_t it = (int64_t)blockIdx.x * kThreads + threadIdx.x; it < total; it += stride) {
-        const int64_t blk = total - 1 - it;
-        int64_t xoff, yoff;
-        if (contiguous) {
-            xoff = blk * B;
-        } else {
-            int64_t r = narrow ? (int64_t)((uint32_t)blk / (uint32_t)nb) : blk / nb;
-            xoff = r * ldx + (blk - r * nb) * B;
-        }
-        if (OUT == kFakeQuant) {
-            if (ldy == cols) {
-                yoff = blk * B;
-            } else {
-                int64_t r = narrow ? (int64_t)((uint32_t)blk / (uint32_t)nb) : blk / nb;
-                yoff = r * ldy + (blk - r * nb) * B;
+    auto fetch = [&](int64_t seg, uint32_t &m, uint4 (&v)[4]) {
+        m = 0u;
+        if (seg < nseg) {
+            m = seg_table[seg];
+            if (OUT == kCodes && total - seg * kSeg >= kSeg) {
+                const uint4 *p = reinterpret_cast<const uint4 *>(scales + seg * kSeg);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) v[i] = p[i];
             }
         }
+    };
+    uint32_t m;
+    uint4 v[4] = {};
+    fetch(first + lane, m, v);
 
-        // ---- load the block and its absmax (packed 16-bit max of magnitudes)
-        uint32_t w[B / 2];
-        const uint4 *src = reinterpret_cast<const uint4 *>(x + xoff);
-#pragma unroll
-        for (int i = 0; i < NV4; ++i) {
-            uint4 d = src[i];
-            w[4 * i + 0] = d.x; w[4 * i + 1] = d.y; w[4 * i + 2] = d.z; w[4 * i + 3] = d.w;
-        }
-        us2 mx2 = __builtin_bit_cast(us2, w[0] & 0x7FFF7FFFu);
-#pragma unroll
-        for (int i = 1; i < B / 2; ++i)
-            mx2 = __builtin_elementwise_max(mx2, __builtin_bit_cast(us2, w[i] & 0x7FFF7FFFu));
-        const uint32_t am = mx2[0] > mx2[1] ? mx2[0] : mx2[1];
-        const bool bad = am >= 0x7F80u;                  // NaN or Inf somewhere in the block
+    const GScale G = make_gscale(fold_partials(partials, nparts));
+    if (blockIdx.x == 0 && threadIdx.x == 0) *gptr = G.g;
 
-        // ---- scale, path choice
-        uint32_t sbyte;
-        bool fast;
-        float p2 = 1.0f, mant = 1.0f;
-        double Sd = 0.0;
-        if (FMT == kMX) {
-            sbyte = bad ? 0xFFu : mx_scale_byte(am);
-            fast = !bad && sbyte >= (OUT == kCodes ? 1u : 3u);
-            p2 = f32_from_bits(sbyte << 23);
-            Sd = __builtin_ldexp(1.0, (int)sbyte - 127);
-        } else {
-            // g = 2^kg and a normal bfloat16 amax = A * 2^(Ef - 134) (A = 128..255):
-            // the smallest 4-significant-bit value >= amax / 6 is
-            // Q(A) * 2^(Ef - 134), Q(A) = 2*ceil(A/12) (A <= 180) or 4*ceil(A/24),
-            // = (1 + f/8) * 2^j; when amax / (6g) rounded that way is a normal E4M3
-            // value it is the scale (dividing by g only moves the exponent), and
-            // s * g = Q(A) * 2^(Ef - 134) exactly.
-            fast = false;
-            const uint32_t Ef = am >> 7;
-            if (!bad && g_pow2 && Ef != 0u) {
-                const uint32_t A = 128u + (am & 0x7Fu);
-                const uint32_t j = A <= 180u ? 4u : 5u;
-                const uint32_t f = (A <= 180u ? (A + 11u) / 12u : (A + 23u) / 24u) - 8u;
-                const int ef = (int)(j + Ef) - 127 - kg;
-                const int eS = (int)(j + Ef) - 134;
-                if (ef >= 1 && (ef < 15 || (ef == 15 && f < 7u)) && eS >= -123 && eS <= 125) {
-                    sbyte = ((uint32_t)ef << 3) | f;
-                    p2 = f32_from_bits((uint32_t)(eS + 127) << 23);
-                    mant = f32_from_bits(0x3F800000u | (f << 20));
-                    fast = true;
+    for (int64_t s0 = first; s0 < nseg; s0 += stride) {
+        if (s0 != first) fetch(s0 + lane, m, v);
+        const int64_t seg = s0 + lane;
+        int sh = 0;
+        bool redo = false;
+        if (m != 0u) sh = G.kg - ((int)(m & 0xFFu) - 127);
+        if (sh > 0) {
+            redo = (int)(m >> 8) <= sh;
+            if (OUT == kCodes && !redo) {
+                const uint32_t sub = (uint32_t)sh << 3;
+                const int64_t n = total - seg * kSeg;
+                if (n >= kSeg) {
+                    uint4 *p = reinterpret_cast<uint4 *>(scales + seg * kSeg);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        p[i] = make_uint4(lower_scale_bytes(v[i].x, sub), lower_scale_bytes(v[i].y, sub),
+                                          lower_scale_bytes(v[i].z, sub), lower_scale_bytes(v[i].w, sub));
+                } else {
+                    for (int64_t i = 0; i < n; ++i) {
+                        const uint32_t b = scales[seg * kSeg + i];
+                        scales[seg * kSeg + i] = (uint8_t)lower_scale_bytes(b, sub);
+                    }
                 }
             }
-            if (!fast) {
-                sbyte = bad ? 0x7Fu : nv_scale_byte(bf16_mag_value(am), g);
-                const float s = e4m3_value(sbyte);
-                const float S = s * g;
-                fast = !bad && sbyte != 0u && g_pow2 && S >= 0x1p-123f && S <= 0x1p125f;
-                p2 = f32_from_bits(bits_from_f32(S) & 0x7F800000u);
-                mant = f32_from_bits((bits_from_f32(S) & 0x007FFFFFu) | 0x3F800000u);
-                Sd = (double)s * (double)g;
-            }
         }
 
-        if (OUT == kCodes) {
-            uint32_t out[B / 8];
-            if (fast) {
-                if (FMT == kMX) codes_fast_mx<B>(w, p2, out);
-                else codes_fast_nv<B>(w, p2, __builtin_amdgcn_rcpf(mant), out);
-            } else {
-                uint32_t U[7], P[8];
-                general_plan<false>(Sd, bad || (FMT == kNV && sbyte == 0u), U, P);
-                codes_general<B>(w, U, bad, out);
-            }
-            uint8_t *dst = codes + blk * (B / 2);
-            if constexpr (B == 16) *reinterpret_cast<uint2 *>(dst) = make_uint2(out[0], out[1]);
-            else *reinterpret_cast<uint4 *>(dst) = make_uint4(out[0], out[1], out[2], out[3]);
-            scales[blk] = (uint8_t)sbyte;
-        } else {
-            uint32_t outw[B / 2];
-            if (fast) {
-                uint32_t cw[B / 8];
-                if (FMT == kMX) codes_fast_mx<B>(w, p2, cw);
-                else codes_fast_nv<B>(w, p2, __builtin_amdgcn_rcpf(mant), cw);
-#pragma unroll
-                for (int q = 0; q < B / 8; ++q) {
-                    if (FMT == kMX) fq_fast_mx(cw[q], p2, &outw[4 * q]);
-                    else fq_fast_nv(cw[q], p2, mant, &outw[4 * q]);
+        uint64_t flags = __ballot(redo);
+        while (flags) {
+            const int l = __builtin_ctzll(flags);
+            flags &= flags - 1;
+            const int lsh = __shfl(sh, l, 64);
+            const int64_t blk = (s0 + l) * kSeg + lane;
+            if (blk < total) {
+                bool requant = true;
+                if (OUT == kCodes) {
+                    const uint32_t b = scales[blk];
+                    if (b == 0u || b == 0x7Fu) {
+                        requant = false;
+                    } else if ((int)(b >> 3) > lsh) {
+                        scales[blk] = (uint8_t)(b - ((uint32_t)lsh << 3));
+                        requant = false;
+                    }
                 }
-            } else {
-                uint32_t U[7], P[8];
-                general_plan<true>(Sd, bad || (FMT == kNV && sbyte == 0u), U, P);
-                fq_general<B>(w, U, P, bad, outw);
+                if (requant) {
+                    const uint16_t *xsrc = x + block_offset(blk, nb, cols, ldx, 16, narrow);
+                    uint16_t *ydst = OUT == kFakeQuant ? y + block_offset(blk, nb, cols, ldy, 16, narrow) : nullptr;
+                    uint32_t w[8];
+                    load_block<16>(xsrc, w);
+                    const BlockPlan pl = plan_block<kNV, OUT, false>(block_mag_max<16>(w), G);
+                    if (pl.fast) emit_fast<kNV, OUT>(w, pl, blk, codes, scales, ydst);
+                    else emit_general<kNV, OUT>(xsrc, G, blk, codes, scales, ydst);
+                }
             }
-            uint4 *dst = reinterpret_cast<uint4 *>(y + yoff);
-#pragma unroll
-            for (int i = 0; i < NV4; ++i)
-                dst[i] = make_uint4(outw[4 * i], outw[4 * i + 1], outw[4 * i + 2], outw[4 * i + 3]);
         }
     }
 }
 
 // Writes g = 1 (the global scale of a tensor with no elements).
 __global__ void unit_scale_kernel(float *gptr) { *gptr = 1.0f; }
+
+template <int FMT, int OUT, int GM, int U>
+hipError_t launch_loop(int grid, const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx, uint8_t *codes,
+                       uint8_t *scales, uint16_t *y, int64_t ldy, float *gptr, uint32_t *partials, int nparts,
+                       uint16_t *seg_table, hipStream_t stream) {
+    hipLaunchKernelGGL((quantize_kernel<FMT, OUT, GM, U>), dim3(grid), dim3(kThreads), 0, stream, x, rows, cols,
+                       ldx, codes, scales, y, ldy, gptr, partials, nparts, seg_table);
+    return hipGetLastError();
+}
+
+template <int FMT, int OUT>
+hipError_t launch_fmt_out(GSrc gsrc, bool deferred, int grid, const uint16_t *x, int64_t rows, int64_t cols,
+                          int64_t ldx, uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy, float *gptr,
+                          uint32_t *partials, int nparts, uint16_t *seg_table, hipStream_t stream) {
+    constexpr int U = OUT == kCodes ? REQAT_Q_UCODES : REQAT_Q_UFQ;
+    if (FMT == kNV && deferred)
+        return launch_loop<FMT, OUT, kGDeferred, U>(grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr,
+                                                   partials, nparts, seg_table, stream);
+    if (FMT == kNV && gsrc == kGComputed)
+        return launch_loop<FMT, OUT, kGFold, U>(grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr, partials,
+                                               nparts, seg_table, stream);
+    return launch_loop<FMT, OUT, kGFixed, U>(grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr, partials,
+                                            nparts, seg_table, stream);
+}
 
 }  // namespace
 
@@ -432,29 +778,46 @@ hipError_t launch_absmax(const uint16_t *x, int64_t rows, int64_t cols, int64_t 
 
 hipError_t launch_quantize(Fmt fmt, QuantOut out, const uint16_t *x, int64_t rows, int64_t cols,
                            int64_t ldx, uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy,
-                           float *gptr, GSrc gsrc, const uint32_t *partials, int nparts,
-                           hipStream_t stream) {
+                           float *gptr, GSrc gsrc, uint32_t *partials, uint16_t *seg_table,
+                           int64_t seg_capacity, hipStream_t stream) {
     const int B = fmt == kMX ? 32 : 16;
-    const int64_t blocks = rows * (cols / B);
-    if (blocks == 0) return hipSuccess;
-    int64_t grid = (blocks + kThreads - 1) / kThreads;
-    if (grid > kMaxGroups) grid = kMaxGroups;
-    dim3 g((unsigned)grid), t(kThreads);
-    if (fmt == kMX) {
-        if (out == kCodes)
-            hipLaunchKernelGGL((quantize_kernel<kMX, kCodes>), g, t, 0, stream, x, rows, cols, ldx,
-                               codes, scales, y, ldy, gptr, (int)gsrc, partials, nparts);
-        else
-            hipLaunchKernelGGL((quantize_kernel<kMX, kFakeQuant>), g, t, 0, stream, x, rows, cols,
-                               ldx, codes, scales, y, ldy, gptr, (int)gsrc, partials, nparts);
-    } else {
-        if (out == kCodes)
-            hipLaunchKernelGGL((quantize_kernel<kNV, kCodes>), g, t, 0, stream, x, rows, cols, ldx,
-                               codes, scales, y, ldy, gptr, (int)gsrc, partials, nparts);
-        else
-            hipLaunchKernelGGL((quantize_kernel<kNV, kFakeQuant>), g, t, 0, stream, x, rows, cols,
-                               ldx, codes, scales, y, ldy, gptr, (int)gsrc, partials, nparts);
+    const int64_t total = rows * (cols / B);
+    if (total == 0) return hipSuccess;
+    const int64_t nseg = (total + kSeg - 1) / kSeg;
+    const bool nv = fmt == kNV;
+    const bool deferred = nv && gsrc == kGComputed && seg_table != nullptr && nseg <= seg_capacity;
+    int nparts = 0;
+    if (nv && gsrc == kGComputed && !deferred) {
+        hipError_t e = launch_absmax(x, rows, cols, ldx, partials, &nparts, stream);
+        if (e != hipSuccess) return e;
     }
+    // about kSegPerWave segments per wave, at most kMaxGroups workgroups
+    int64_t grid = (nseg + 4 * kSegPerWave - 1) / (4 * kSegPerWave);
+    if (grid > kMaxGroups) grid = kMaxGroups;
+    if (grid < 1) grid = 1;
+    if (deferred) nparts = (int)grid;
+    hipError_t e;
+    if (fmt == kMX)
+        e = out == kCodes ? launch_fmt_out<kMX, kCodes>(gsrc, false, (int)grid, x, rows, cols, ldx, codes, scales,
+                                                         y, ldy, gptr, partials, nparts, seg_table, stream)
+                          : launch_fmt_out<kMX, kFakeQuant>(gsrc, false, (int)grid, x, rows, cols, ldx, codes,
+                                                             scales, y, ldy, gptr, partials, nparts, seg_table,
+                                                             stream);
+    else
+        e = out == kCodes ? launch_fmt_out<kNV, kCodes>(gsrc, deferred, (int)grid, x, rows, cols, ldx, codes,
+                                                         scales, y, ldy, gptr, partials, nparts, seg_table, stream)
+                          : launch_fmt_out<kNV, kFakeQuant>(gsrc, deferred, (int)grid, x, rows, cols, ldx, codes,
+                                                             scales, y, ldy, gptr, partials, nparts, seg_table,
+                                                             stream);
+    if (e != hipSuccess || !deferred) return e;
+    int64_t fgrid = (nseg + kThreads - 1) / kThreads;
+    if (fgrid > kMaxGroups) fgrid = kMaxGroups;
+    if (out == kCodes)
+        hipLaunchKernelGGL(nv_fixup_kernel<kCodes>, dim3((unsigned)fgrid), dim3(kThreads), 0, stream, x, rows,
+                           cols, ldx, codes, scales, y, ldy, gptr, partials, nparts, seg_table);
+    else
+        hipLaunchKernelGGL(nv_fixup_kernel<kFakeQuant>, dim3((unsigned)fgrid), dim3(kThreads), 0, stream, x, rows,
+                           cols, ldx, codes, scales, y, ldy, gptr, partials, nparts, seg_table);
     return hipGetLastError();
 }
 

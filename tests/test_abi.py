@@ -49,7 +49,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 def test_small_queries(lib):
     assert reqat.reqat_abi_version() == 2
-    assert reqat.reqat_workspace_bytes() >= 4
+    assert reqat.reqat_workspace_bytes() == 4 * 4096 + 2 * (1 << 19)   # partials + segment table
     for s in range(7):
         assert reqat.reqat_status_str(s).startswith(reqat.STATUS[s])
     assert "unknown" in reqat.reqat_status_str(99)
@@ -117,8 +117,10 @@ def ln(fmt=NV, M=4, N=8, K=128, x=P, ldx=128, xg=P, ts=0, wc=P, ws_=P, wg=P, y=P
 
 def test_linear_workspace_bytes(lib):
     # partials (1024 words) | codes M*K/2 | scales M*K/B, each rounded up to 256 bytes
-    assert reqat.reqat_linear_workspace_bytes(NV, 4, 128) == 4096 + 256 + 256
-    assert reqat.reqat_linear_workspace_bytes(MX, 300, 1024) == 4096 + 153600 + 9728
+    # NVFP4: partials, codes, scales, then one uint16 per 64 blocks of segment table
+    assert reqat.reqat_linear_workspace_bytes(NV, 4, 128) == 16384 + 256 + 256 + 256
+    assert reqat.reqat_linear_workspace_bytes(NV, 2048, 3584) == 16384 + 3670016 + 458752 + 7168 * 2
+    assert reqat.reqat_linear_workspace_bytes(MX, 300, 1024) == 16384 + 153600 + 9728
     assert reqat.reqat_linear_workspace_bytes(NV, 4, 64) == 0      # K % 128
     assert reqat.reqat_linear_workspace_bytes(NV, -1, 128) == 0
     assert reqat.reqat_linear_workspace_bytes(7, 4, 128) == 0

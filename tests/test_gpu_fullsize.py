@@ -98,3 +98,29 @@ def test_fullsize_32b_down_mxfp4():
     log("full-size workload 5: %s" % w.name)
     fmt, ofmt, q = _quant_both(w)
     _check_gemm(w, fmt, ofmt, q, torch.float32, seed=7, npts=1000)
+
+
+def test_nvfp4_computed_scale_beyond_segment_table():
+    """A tensor of more than 2^19 segments of 64 NVFP4 blocks (33000 x 16384
+    bfloat16, 1.08 GB) takes the two-pass quantizer (absmax, then quantize).
+    Values are clipped normals with one planted maximum, so the tensor amax is
+    known exactly; sampled rows are compared with the oracle under that g."""
+    R, C = 33000, 16384
+    log("nvfp4 computed scale, %d x %d (two-pass)" % (R, C))
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(11)
+    x = torch.randn((R, C), generator=gen, device=DEV, dtype=torch.float32).clamp_(-4.0, 4.0)
+    x = x.to(torch.bfloat16)
+    x[R // 3, 777] = 100.0
+    c, s, g = reqat.quantize(x, reqat.NVFP4)
+    torch.cuda.synchronize()
+    og = oracle.nv_global_scale(100.0)
+    assert float(g.cpu()[0]) == og
+    rows = np.array([0, 1, R // 3, R // 2, R - 2, R - 1])
+    idx = torch.from_numpy(rows).to(DEV)
+    bits = wl.bf16_bits(x[idx].cpu())
+    oc, os_, _ = oracle.quantize(oracle.FMT_NVFP4, bits, og)
+    assert np.array_equal(s[idx].cpu().numpy(), os_)
+    assert np.array_equal(c[idx].cpu().numpy(), oc)
+    del x, c, s
+    torch.cuda.empty_cache()

@@ -107,6 +107,34 @@ def test_nvfp4_given_global_scale(g):
     assert_fq_parity(NV, xb, g)
 
 
+def _ramp(R, C, seed, step):
+    """Normal values with row r scaled by 2^(-step*r): segments of very different
+    magnitude, so a computed g differs from most segments' own reference and the
+    smallest rows fall into E4M3-subnormal block scales."""
+    xb = wl.bf16_bits(wl.random_bf16(R, C, seed)).copy()
+    return indep.to_bf16_bits(indep.bf16_values(xb) * (2.0 ** (-step * np.arange(R)))[:, None])
+
+
+@pytest.mark.parametrize("shape,step", [((40, 1040), 1.5), ((48, 1024), 1.0), ((7, 4096), 9.0),
+                                        ((300, 96), 0.25)])
+def test_nvfp4_computed_scale_wide_range(shape, step):
+    """NVFP4 with a computed g over tensors whose rows span many binades: the
+    one-pass quantizer must lower the scale exponents of rows quantized under a
+    smaller reference and re-quantize blocks whose scale leaves the normal range."""
+    R, C = shape
+    log("nvfp4 computed scale, wide range shape=%s step=%g" % (shape, step))
+    xb = _ramp(R, C, 31 + R, step)
+    assert_quant_parity(NV, xb)
+    assert_fq_parity(NV, xb)
+    assert_quant_parity(NV, xb, ldx_pad=24)
+    xs = xb.copy()
+    xs[R // 2, 3] = 0x7FC0                       # NaN block
+    xs[R - 1, :] = 0                             # zero row
+    xs[1, C - 1] = 0xFF80                        # -Inf in the last block of a row
+    assert_quant_parity(NV, xs)
+    assert_fq_parity(NV, xs)
+
+
 @pytest.mark.parametrize("fmt", [NV, MX])
 def test_strided_rows(fmt):
     log("strided rows fmt=%d" % fmt)
@@ -304,7 +332,7 @@ def test_linear_parity(fmt, M, N, K, given):
         if fmt == NV:
             assert float(g.cpu()[0]) == np.float32(ga)
         # the activation codes and scales the call left in its workspace are the oracle's
-        off = 4096
+        off = 16384                                  # after the 4096 partial maxima
         wsn = ws.cpu().numpy()
         codes = wsn[off:off + M * K // 2].reshape(M, K // 2)
         off2 = off + ((M * K // 2 + 255) // 256) * 256
