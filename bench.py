@@ -4,7 +4,7 @@
 One step = one pass of the whole hot path over the 14B-like NVFP4 MLP gate/up
 projection (X[4096 x 5120] activations with 1% outlier channels, W[27648 x 5120]
 = gate || up weights, both bfloat16, seeded synthetic):
-  quantize X (dynamic global scale: absmax pass + quantize),
+  quantize X (dynamic global scale, one pass over X plus a small fix-up kernel),
   quantize W (dynamic global scale),
   W4A4 GEMM Y = X^ W^T (FP32 accumulation, bfloat16 output),
   fake-quant X and W (the QAT forward's quantize-dequantize, bfloat16 out).
@@ -223,7 +223,8 @@ def main():
         gbs = fn(rows) / (per[n] * 1e-3) / 1e9
         kern[n] = {"ms": round(per[n], 4), "GB/s": round(gbs, 1),
                    "frac_hbm_peak": round(gbs / PEAK["hbm"], 4),
-                   "note": "includes the absmax pass (its bytes not credited)"}
+                   "note": ("one pass + scale fix-up kernel (computed g); credited bytes = read x + writes"
+                            if fmt == reqat.NVFP4 else "credited bytes = read x + writes")}
 
     if M <= 64:
         # decode shape: the product streams the weights once, so it is bounded by HBM
