@@ -71,6 +71,11 @@ def _load():
                                        u8p, u8p, ctypes.c_double, i64p, i64p, i64, dp, dp]),
             "orc_e2m1_encode_array": (None, [dp, i64, ctypes.c_double, u8p]),
             "orc_bf16_from_double_array": (None, [dp, i64, u16p]),
+            "orc_rht_norm": (ctypes.c_float, []),
+            "orc_fwht32_f32": (None, [ctypes.POINTER(ctypes.c_float)]),
+            "orc_rht32": (None, [u16p, ctypes.c_uint32, ctypes.POINTER(ctypes.c_float)]),
+            "orc_quantize_mx_rht": (ctypes.c_int, [u16p, i64, i64, i64, ctypes.c_uint32, u8p, u8p]),
+            "orc_fakequant_mx_rht": (ctypes.c_int, [u16p, i64, i64, i64, ctypes.c_uint32, u16p, i64]),
         }
         for name, (res, args) in sig.items():
             f = getattr(lib, name)
@@ -235,3 +240,50 @@ def gemm_points(fmt, a_codes, a_scales, ga, b_codes, b_scales, gb, ms, ns):
                             _p(ms, ctypes.c_int64), _p(ns, ctypes.c_int64), len(ms),
                             _p(y, ctypes.c_double), _p(ay, ctypes.c_double))
     return y, ay
+
+
+# ------------------------------------------------- block rotation (MXFP4)
+
+def rht_norm() -> float:
+    """The FP32 constant 1/sqrt(32) the rotation multiplies by."""
+    return float(np.float32(_load().orc_rht_norm()))
+
+
+def fwht32_f32(v: np.ndarray) -> np.ndarray:
+    """Unnormalized FP32 fast Walsh-Hadamard transform of 32 float32 values."""
+    t = np.array(v, np.float32).reshape(32).copy()
+    _load().orc_fwht32_f32(_p(t, ctypes.c_float))
+    return t
+
+
+def rht32(x: np.ndarray, signs: int) -> np.ndarray:
+    """FP32 rotated block y = H_32 D x / sqrt(32) of 32 bfloat16 bit patterns."""
+    x = np.ascontiguousarray(x, np.uint16).reshape(32)
+    y = np.empty(32, np.float32)
+    _load().orc_rht32(_p(x, ctypes.c_uint16), ctypes.c_uint32(signs), _p(y, ctypes.c_float))
+    return y
+
+
+def quantize_mx_rht(x: np.ndarray, signs: int):
+    """MXFP4 codes and scales of the block-rotated rows: (codes [R, C/2], scales [R, C/32])."""
+    x = _as_u16(x)
+    R, C = x.shape
+    if C % 32:
+        raise ValueError("cols must be a multiple of 32")
+    codes = np.zeros((R, C // 2), np.uint8)
+    scales = np.zeros((R, C // 32), np.uint8)
+    rc = _load().orc_quantize_mx_rht(_p(x, ctypes.c_uint16), R, C, C, ctypes.c_uint32(signs),
+                                     _p(codes, ctypes.c_uint8), _p(scales, ctypes.c_uint8))
+    assert rc == 0
+    return codes, scales
+
+
+def fakequant_mx_rht(x: np.ndarray, signs: int) -> np.ndarray:
+    """bfloat16 bits of the dequantized rotated values (rotated basis), [R, C]."""
+    x = _as_u16(x)
+    R, C = x.shape
+    y = np.zeros((R, C), np.uint16)
+    rc = _load().orc_fakequant_mx_rht(_p(x, ctypes.c_uint16), R, C, C, ctypes.c_uint32(signs),
+                                      _p(y, ctypes.c_uint16), C)
+    assert rc == 0
+    return y

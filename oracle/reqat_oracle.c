@@ -351,3 +351,110 @@ void orc_bf16_from_double_array(const double *v, int64_t n, uint16_t *out)
     int64_t i;
     for (i = 0; i < n; i++) out[i] = orc_bf16_from_double(v[i]);
 }
+
+/* ---------- block rotation before MXFP4 quantization ---------- */
+
+/* MXFP4 activations in ReQAT are rotated block by block before quantization
+ * (Sec. 3.3, "Additional implementation details"; App. C.2, "Challenges in
+ * MXFP4 activation quantization"): a randomized Hadamard transform over each
+ * 32-element block.  The paper fixes neither the normalization, the sign
+ * vector nor the arithmetic; the readings used here:
+ *   - y = (1/sqrt(32)) * H_32 * D * x per block, H_32 the Sylvester Hadamard
+ *     matrix (H[i][j] = (-1)^popcount(i & j)), D = diag(d) with d_j = -1 where
+ *     bit j of the 32-bit `signs` word is set (the random draw is an input);
+ *     the map is orthonormal, so rotating both operands of a product leaves
+ *     the product unchanged;
+ *   - arithmetic is FP32: the fast Walsh-Hadamard transform in stages
+ *     h = 1, 2, 4, 8, 16, each replacing (t[j], t[j+h]) by (t[j] + t[j+h],
+ *     t[j] - t[j+h]) for every j with bit h clear, every sum rounded to
+ *     nearest-even FP32; then each entry times 1/sqrt(32) rounded once to FP32
+ *     (one more rounding);
+ *   - the FP32 results are quantized exactly as a block of MXFP4 values
+ *     (ceil E8M0 scale, RNE codes); a block with a non-finite result (a NaN or
+ *     Inf input, or an FP32 overflow) gets scale 0xFF and zero codes.
+ * FP32 here is the C `float` type with SSE arithmetic (no excess precision),
+ * compiled without contraction of multiply-add. */
+
+/* The FP32 constant 1/sqrt(32): sqrt and the division are correctly rounded
+ * in FP64 and the value is far from an FP32 rounding boundary (pinned). */
+float orc_rht_norm(void) { return (float)(1.0 / sqrt(32.0)); }
+
+/* In-place FP32 fast Walsh-Hadamard transform of 32 values (unnormalized). */
+void orc_fwht32_f32(float *t)
+{
+    int h, i, j;
+    for (h = 1; h < 32; h *= 2)
+        for (i = 0; i < 32; i += 2 * h)
+            for (j = i; j < i + h; j++) {
+                float a = t[j], b = t[j + h];
+                t[j] = a + b;
+                t[j + h] = a - b;
+            }
+}
+
+/* y = rotated block of the 32 bfloat16 values x. */
+void orc_rht32(const uint16_t *x, uint32_t signs, float *y)
+{
+    int j;
+    float c = orc_rht_norm();
+    for (j = 0; j < 32; j++) {
+        float v = (float)orc_bf16_value(x[j]);          /* exact */
+        y[j] = ((signs >> j) & 1u) ? -v : v;
+    }
+    orc_fwht32_f32(y);
+    for (j = 0; j < 32; j++) y[j] = y[j] * c;
+}
+
+/* MXFP4 quantization of the rotated blocks of a rows x cols bfloat16 matrix
+ * (cols % 32 == 0): codes rows x cols/2, scales rows x cols/32.  With fake != 0
+ * it writes instead y_out (row stride ldy): each dequantized rotated value
+ * rounded once to bfloat16 (NaN for a non-finite block). */
+static int quantize_mx_rht(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                           uint32_t signs, uint8_t *codes, uint8_t *scales,
+                           uint16_t *y_out, int64_t ldy, int fake)
+{
+    int64_t r, b, nb;
+    int j;
+    if (cols % 32) return -1;
+    nb = cols / 32;
+    for (r = 0; r < rows; r++) {
+        for (b = 0; b < nb; b++) {
+            float y[32];
+            double amax = 0.0, S;
+            int bad = 0;
+            uint8_t sb;
+            orc_rht32(x + r * ldx + b * 32, signs, y);
+            for (j = 0; j < 32; j++) {
+                if (isnan(y[j]) || isinf(y[j])) bad = 1;
+                else if (fabs((double)y[j]) > amax) amax = fabs((double)y[j]);
+            }
+            sb = bad ? 0xFF : orc_mx_scale_byte(amax);
+            S = orc_e8m0_value(sb);
+            if (!fake) scales[r * nb + b] = sb;
+            for (j = 0; j < 32; j++) {
+                uint8_t c = bad ? 0 : orc_e2m1_encode((double)y[j], S);
+                int64_t k = b * 32 + j;
+                if (fake) {
+                    y_out[r * ldy + k] = bad ? 0x7FC0 : orc_bf16_from_double(orc_e2m1_value(c) * S);
+                } else {
+                    uint8_t *p = &codes[r * (cols / 2) + k / 2];
+                    if (k % 2 == 0) *p = (uint8_t)((*p & 0xF0) | c);
+                    else *p = (uint8_t)((*p & 0x0F) | (c << 4));
+                }
+            }
+        }
+    }
+    return 0;
+}
+
+int orc_quantize_mx_rht(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx, uint32_t signs,
+                        uint8_t *codes, uint8_t *scales)
+{
+    return quantize_mx_rht(x, rows, cols, ldx, signs, codes, scales, 0, 0, 0);
+}
+
+int orc_fakequant_mx_rht(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx, uint32_t signs,
+                         uint16_t *y, int64_t ldy)
+{
+    return quantize_mx_rht(x, rows, cols, ldx, signs, 0, 0, y, ldy, 1);
+}
