@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define REQAT_ABI_VERSION 2
+#define REQAT_ABI_VERSION 3
 
 typedef enum {
     REQAT_FMT_NVFP4 = 0, /* B = 16, E4M3 block scale, FP32 global scale */
@@ -119,6 +119,38 @@ reqat_status reqat_quantize_fp4(reqat_format fmt, const void *x, int64_t rows, i
 reqat_status reqat_fakequant_fp4(reqat_format fmt, const void *x, int64_t rows, int64_t cols,
                                  int64_t ldx, void *y, int64_t ldy, float *tensor_scale,
                                  reqat_tscale_mode ts, void *workspace, void *stream);
+
+/*
+ * MXFP4 quantization of block-rotated rows (the block rotation ReQAT applies
+ * to MXFP4 activations before quantizing them, Sec. 3.3 "Additional
+ * implementation details" and App. C.2): each 32-element block x of a row
+ * becomes
+ *     y = H_32 * D * x / sqrt(32),   D = diag(d), d_j = -1 where bit j of signs is set,
+ * H_32 the Sylvester Hadamard matrix (H[i][j] = (-1)^popcount(i & j)), and y
+ * is quantized as an MXFP4 block (same rules as reqat_quantize_fp4).  The map
+ * is orthonormal: rotating the weights' rows with the same signs leaves the
+ * product X W^T unchanged.  y is evaluated in FP32 in a fixed order: the fast
+ * Walsh-Hadamard transform in stages h = 1, 2, 4, 8, 16, each pair
+ * (t[j], t[j+h]) -> (t[j] + t[j+h], t[j] - t[j+h]) rounded to nearest even,
+ * then each value times 1/sqrt(32) rounded to FP32 (0x3E3504F3).  A block
+ * with a non-finite y (NaN/Inf input or FP32 overflow) gets scale 0xFF and
+ * zero codes.
+ *   x [rows][ldx] bfloat16 (cols % 32 == 0, 16-byte aligned, ldx % 8 == 0);
+ *   signs: the random sign draw, bit j for position j of every block;
+ *   codes [rows][cols/2], scales [rows][cols/32] as reqat_quantize_fp4 (MXFP4).
+ * rows == 0 or cols == 0 is a no-op.  Errors as reqat_quantize_fp4.
+ */
+reqat_status reqat_quantize_mxfp4_rht(const void *x, int64_t rows, int64_t cols, int64_t ldx,
+                                      uint32_t signs, uint8_t *codes, uint8_t *scales, void *stream);
+
+/*
+ * Fake-quant of block-rotated rows: y_out = bfloat16(dequantize(quantize(y)))
+ * with y the rotated blocks of reqat_quantize_mxfp4_rht (values stay in the
+ * rotated basis; NaN for a non-finite block).  y_out [rows][ldy] bfloat16,
+ * 16-byte aligned, ldy % 8 == 0, ldy >= cols.
+ */
+reqat_status reqat_fakequant_mxfp4_rht(const void *x, int64_t rows, int64_t cols, int64_t ldx,
+                                       uint32_t signs, void *y_out, int64_t ldy, void *stream);
 
 /*
  * Block-scaled FP4 x FP4 product (the W4A4 GEMM of Sec. 5.3):

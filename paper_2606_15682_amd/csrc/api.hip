@@ -91,6 +91,27 @@ reqat_status reqat_fakequant_fp4(reqat_format fmt, const void *x, int64_t rows, 
                      workspace, quant_seg_table(workspace), kMaxSegments, stream, true);
 }
 
+static reqat_status run_rht(const void *x, int64_t rows, int64_t cols, int64_t ldx, uint32_t signs,
+                            uint8_t *codes, uint8_t *scales, void *y, int64_t ldy, void *stream, bool fake) {
+    reqat_status st = check_quant(REQAT_FMT_MXFP4, x, rows, cols, ldx, fake ? y : codes, scales, ldy,
+                                  nullptr, REQAT_TS_GIVEN, nullptr, fake);
+    if (st != REQAT_OK || rows == 0 || cols == 0) return st;
+    hipError_t e = launch_quantize_rht(fake ? kFakeQuant : kCodes, reinterpret_cast<const uint16_t *>(x), rows,
+                                       cols, ldx, signs, codes, scales, reinterpret_cast<uint16_t *>(y), ldy,
+                                       reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
+}
+
+reqat_status reqat_quantize_mxfp4_rht(const void *x, int64_t rows, int64_t cols, int64_t ldx, uint32_t signs,
+                                      uint8_t *codes, uint8_t *scales, void *stream) {
+    return run_rht(x, rows, cols, ldx, signs, codes, scales, nullptr, 0, stream, false);
+}
+
+reqat_status reqat_fakequant_mxfp4_rht(const void *x, int64_t rows, int64_t cols, int64_t ldx, uint32_t signs,
+                                       void *y, int64_t ldy, void *stream) {
+    return run_rht(x, rows, cols, ldx, signs, nullptr, nullptr, y, ldy, stream, true);
+}
+
 reqat_status reqat_gemm_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K,
                              const uint8_t *a_codes, const uint8_t *a_scales,
                              const float *a_tensor_scale, const uint8_t *b_codes,

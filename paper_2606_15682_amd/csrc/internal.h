@@ -38,6 +38,11 @@ hipError_t launch_quantize(Fmt fmt, QuantOut out, const uint16_t *x, int64_t row
                            float *gptr, GSrc gsrc, uint32_t *partials, uint16_t *seg_table,
                            int64_t seg_capacity, hipStream_t stream);
 
+// MXFP4 quantize / fake-quant of block-rotated rows (randomized Hadamard of 32).
+hipError_t launch_quantize_rht(QuantOut out, const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                               uint32_t signs, uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy,
+                               hipStream_t stream);
+
 bool gemm_tile256_supported(Fmt fmt, int64_t M, int64_t N, int64_t K, int64_t ldy);
 // Skinny product for M <= 64 (K % 64 == 0, K > 0).
 hipError_t launch_gemm_skinny(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *a_codes,

@@ -731,6 +731,176 @@ __global__ __launch_bounds__(kThreads) void nv_fixup_kernel(
     }
 }
 
+// ---------------------------------------------------------------- block rotation
+
+// MXFP4 activations may be rotated block by block before quantization (a
+// randomized Hadamard transform per 32-element block, Sec. 3.3 and App. C.2):
+// y = H_32 D x / sqrt(32), D = diag(d), d_j = -1 where bit j of `signs` is set,
+// H_32 the Sylvester Hadamard matrix.  Arithmetic is FP32 in a fixed order:
+// the fast Walsh-Hadamard transform in stages h = 1, 2, 4, 8, 16 (each
+// (t[j], t[j+h]) -> (t[j] + t[j+h], t[j] - t[j+h]), rounded to nearest even),
+// then each value times the FP32 constant nearest 1/sqrt(32).  Only adds,
+// subtracts and one multiply per value, none contracted, so the values are
+// fixed bit for bit.  The FP32 values are then quantized as an MXFP4 block.
+
+constexpr uint32_t kInvSqrt32 = 0x3E3504F3u;   // 1/sqrt(32) rounded to nearest FP32
+
+__device__ __forceinline__ void rotate32(const uint32_t (&w)[16], uint32_t signs, float (&t)[32]) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        const uint32_t lo = (w[i] << 16) ^ (((signs >> (2 * i)) & 1u) << 31);
+        const uint32_t hi = (w[i] & 0xFFFF0000u) ^ (((signs >> (2 * i + 1)) & 1u) << 31);
+        t[2 * i] = f32_from_bits(lo);
+        t[2 * i + 1] = f32_from_bits(hi);
+    }
+#pragma unroll
+    for (int h = 1; h < 32; h *= 2)
+#pragma unroll
+        for (int i = 0; i < 32; i += 2 * h)
+#pragma unroll
+            for (int j = i; j < i + h; ++j) {
+                const float a = t[j], b = t[j + h];
+                t[j] = a + b;
+                t[j + h] = a - b;
+            }
+    const float c = f32_from_bits(kInvSqrt32);
+#pragma unroll
+    for (int j = 0; j < 32; ++j) t[j] = t[j] * c;
+}
+
+// E8M0 byte of the smallest e in [-127, 127] with amax <= 6 * 2^e, for an FP32
+// magnitude pattern: with amax = 1.f * 2^E that is E - 2 when 1.f <= 1.5, else E - 1.
+__device__ __forceinline__ uint32_t mx_scale_byte_f32(uint32_t am) {
+    if (am == 0u) return 0u;
+    int E;
+    uint32_t frac;
+    if ((am >> 23) != 0u) {
+        E = (int)(am >> 23) - 127;
+        frac = am & 0x7FFFFFu;
+    } else {                                   // FP32 subnormal: normalize
+        const int p = 31 - __builtin_clz(am);
+        E = p - 149;
+        frac = (am << (23 - p)) & 0x7FFFFFu;
+    }
+    int e = frac <= 0x400000u ? E - 2 : E - 1;
+    e = e < -127 ? -127 : (e > 127 ? 127 : e);
+    return (uint32_t)(e + 127);
+}
+
+// E2M1 code of v / S (S = 2^e), nearest with ties to the even code, saturating
+// at 6, sign copied; decided by exact FP64 comparisons (v is FP32).
+__device__ __forceinline__ uint32_t e2m1_code_exact(float v, double S) {
+    const double a = __builtin_fabs((double)v);
+    const double mids[7] = {0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0};
+    uint32_t m = 7u;
+#pragma unroll
+    for (int i = 6; i >= 0; --i) {
+        const double t = mids[i] * S;
+        if (a < t || (a == t && (i & 1) == 0)) m = (uint32_t)i;
+    }
+    return m | ((bits_from_f32(v) >> 28) & 8u);
+}
+
+// Quantizes (codes) or fake-quantizes one rotated block.  v_cvt_scalef32_pk_fp4_f32
+// rounds FP32 inputs to nearest-even E2M1 exactly for every power-of-two scale
+// 2^-126..2^127 (checked on gfx950 at every midpoint and its neighbouring FP32
+// values); scale byte 0, the fake-quant outputs below 2^-124 and non-finite
+// blocks take the FP64 comparisons instead.
+template <int OUT>
+__device__ __forceinline__ void emit_rotated(const float (&t)[32], int64_t blk, uint8_t *codes,
+                                             uint8_t *scales, uint16_t *ydst) {
+    uint32_t am = 0u;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+        const uint32_t m = bits_from_f32(t[j]) & 0x7FFFFFFFu;
+        am = am > m ? am : m;
+    }
+    const bool bad = am >= 0x7F800000u;
+    const uint32_t sbyte = bad ? 0xFFu : mx_scale_byte_f32(am);
+    const float p2 = f32_from_bits(sbyte << 23);
+    const bool fast = !bad && sbyte >= (OUT == kCodes ? 1u : 3u);
+    uint32_t cw[4];
+    if (fast) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            uint32_t word = 0;
+            word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, t[8 * q + 0], t[8 * q + 1], p2, 0);
+            word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, t[8 * q + 2], t[8 * q + 3], p2, 1);
+            word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, t[8 * q + 4], t[8 * q + 5], p2, 2);
+            word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, t[8 * q + 6], t[8 * q + 7], p2, 3);
+            cw[q] = word;
+        }
+    } else {
+        const double S = __builtin_ldexp(1.0, (int)sbyte - 127);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            uint32_t word = 0;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) word |= (bad ? 0u : e2m1_code_exact(t[8 * q + k], S)) << (4 * k);
+            cw[q] = word;
+        }
+    }
+    if (OUT == kCodes) {
+        *reinterpret_cast<uint4 *>(codes + blk * 16) = make_uint4(cw[0], cw[1], cw[2], cw[3]);
+        scales[blk] = (uint8_t)sbyte;
+        return;
+    }
+    uint4 *dst = reinterpret_cast<uint4 *>(ydst);
+    if (fast) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            uint32_t o[4];
+            fq_fast_mx(cw[q], p2, o);
+            dst[q] = make_uint4(o[0], o[1], o[2], o[3]);
+        }
+    } else {
+        const double S = __builtin_ldexp(1.0, (int)sbyte - 127);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            uint32_t o[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                uint32_t h2[2];
+#pragma unroll
+                for (int hf = 0; hf < 2; ++hf) {
+                    const uint32_t c = (cw[q] >> (8 * k + 4 * hf)) & 0xFu;
+                    const double v = (double)e2m1_mag_value((int)(c & 7u)) * S;
+                    h2[hf] = bad ? 0x7FC0u : (bf16_rne_from_double(v) | ((c & 8u) << 12));
+                }
+                o[k] = h2[0] | (h2[1] << 16);
+            }
+            dst[q] = make_uint4(o[0], o[1], o[2], o[3]);
+        }
+    }
+}
+
+// One lane per 32-element block, blocks in segments of 64 (one per lane of a
+// wave), wave w of workgroup b taking segments b*4 + w + k*(4*grid).
+template <int OUT>
+__global__ __launch_bounds__(kThreads) void quantize_rht_kernel(
+    const uint16_t *__restrict__ x, int64_t rows, int64_t cols, int64_t ldx, uint32_t signs,
+    uint8_t *__restrict__ codes, uint8_t *__restrict__ scales, uint16_t *__restrict__ y, int64_t ldy) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t nb = cols / 32;
+    const int64_t total = rows * nb;
+    const int64_t nseg = (total + kSeg - 1) / kSeg;
+    const bool narrow = total < (int64_t(1) << 32);
+    const int64_t step = (int64_t)gridDim.x * 4;
+    for (int64_t s = (int64_t)blockIdx.x * 4 + wave; s < nseg; s += step) {
+        const int64_t blk = s * kSeg + lane;
+        const int64_t b = blk < total ? blk : total - 1;       // branch-free load, result unused
+        uint32_t w[16];
+        load_block<32>(x + block_offset(b, nb, cols, ldx, 32, narrow), w);
+        float t[32];
+        rotate32(w, signs, t);
+        if (blk < total) {
+            uint16_t *ydst = OUT == kFakeQuant ? y + block_offset(blk, nb, cols, ldy, 32, narrow) : nullptr;
+            emit_rotated<OUT>(t, blk, codes, scales, ydst);
+        }
+    }
+}
+
 // Writes g = 1 (the global scale of a tensor with no elements).
 __global__ void unit_scale_kernel(float *gptr) { *gptr = 1.0f; }
 
@@ -762,6 +932,23 @@ hipError_t launch_fmt_out(GSrc gsrc, bool deferred, int grid, const uint16_t *x,
 
 hipError_t launch_unit_scale(float *gptr, hipStream_t stream) {
     hipLaunchKernelGGL(unit_scale_kernel, dim3(1), dim3(1), 0, stream, gptr);
+    return hipGetLastError();
+}
+
+hipError_t launch_quantize_rht(QuantOut out, const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
+                               uint32_t signs, uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy,
+                               hipStream_t stream) {
+    const int64_t total = rows * (cols / 32);
+    if (total == 0) return hipSuccess;
+    const int64_t nseg = (total + kSeg - 1) / kSeg;
+    int64_t grid = (nseg + 4 * kSegPerWave - 1) / (4 * kSegPerWave);
+    if (grid > kMaxGroups) grid = kMaxGroups;
+    if (out == kCodes)
+        hipLaunchKernelGGL(quantize_rht_kernel<kCodes>, dim3((unsigned)grid), dim3(kThreads), 0, stream, x, rows,
+                           cols, ldx, signs, codes, scales, y, ldy);
+    else
+        hipLaunchKernelGGL(quantize_rht_kernel<kFakeQuant>, dim3((unsigned)grid), dim3(kThreads), 0, stream, x,
+                           rows, cols, ldx, signs, codes, scales, y, ldy);
     return hipGetLastError();
 }
 

@@ -43,6 +43,8 @@ SIGNATURES = {
     "reqat_linear_w4a4": (_INT, [_INT, _I64, _I64, _I64, _VP, _I64, _VP, _INT, _VP, _VP, _VP, _VP,
                                  _INT, _I64, _VP, _VP]),
     "reqat_linear_workspace_bytes": (ctypes.c_size_t, [_INT, _I64, _I64]),
+    "reqat_quantize_mxfp4_rht": (_INT, [_VP, _I64, _I64, _I64, ctypes.c_uint32, _VP, _VP, _VP]),
+    "reqat_fakequant_mxfp4_rht": (_INT, [_VP, _I64, _I64, _I64, ctypes.c_uint32, _VP, _I64, _VP]),
     "reqat_workspace_bytes": (ctypes.c_size_t, []),
     "reqat_status_str": (ctypes.c_char_p, [_INT]),
     "reqat_abi_version": (_INT, []),
@@ -96,6 +98,14 @@ def reqat_linear_w4a4(fmt, M, N, K, x, ldx, x_ts, ts, w_codes, w_scales, w_ts, y
                       workspace, stream):
     return load().reqat_linear_w4a4(fmt, M, N, K, x, ldx, x_ts, ts, w_codes, w_scales, w_ts, y,
                                     y_dtype, ldy, workspace, stream)
+
+
+def reqat_quantize_mxfp4_rht(x, rows, cols, ldx, signs, codes, scales, stream):
+    return load().reqat_quantize_mxfp4_rht(x, rows, cols, ldx, signs, codes, scales, stream)
+
+
+def reqat_fakequant_mxfp4_rht(x, rows, cols, ldx, signs, y, ldy, stream):
+    return load().reqat_fakequant_mxfp4_rht(x, rows, cols, ldx, signs, y, ldy, stream)
 
 
 def reqat_linear_workspace_bytes(fmt, M, K) -> int:
@@ -195,6 +205,31 @@ def fakequant(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out=None, g_
                              ts, ws.data_ptr(), _stream(x.device))
     _check(st, "reqat_fakequant_fp4")
     return y, g
+
+
+def quantize_rht(x: torch.Tensor, signs: int, out=None):
+    """MXFP4 codes and scales of the block-rotated rows of x (randomized Hadamard
+    of 32 with the given 32-bit sign draw).  Returns (codes, scales)."""
+    rows, cols, ldx = _x2d(x)
+    if out is not None:
+        codes, scales = out
+    else:
+        codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=x.device)
+        scales = torch.empty((rows, cols // 32), dtype=torch.uint8, device=x.device)
+    st = reqat_quantize_mxfp4_rht(x.data_ptr(), rows, cols, ldx, signs & 0xFFFFFFFF, codes.data_ptr(),
+                                  scales.data_ptr(), _stream(x.device))
+    _check(st, "reqat_quantize_mxfp4_rht")
+    return codes, scales
+
+
+def fakequant_rht(x: torch.Tensor, signs: int, out=None):
+    """bfloat16 quantize-dequantize of the block-rotated rows (rotated basis)."""
+    rows, cols, ldx = _x2d(x)
+    y = out if out is not None else torch.empty((rows, cols), dtype=torch.bfloat16, device=x.device)
+    st = reqat_fakequant_mxfp4_rht(x.data_ptr(), rows, cols, ldx, signs & 0xFFFFFFFF, y.data_ptr(),
+                                   y.stride(0), _stream(x.device))
+    _check(st, "reqat_fakequant_mxfp4_rht")
+    return y
 
 
 def gemm(fmt, a_codes, a_scales, a_g, b_codes, b_scales, b_g, out_dtype=torch.float32, out=None):

@@ -33,6 +33,7 @@ def lib():
 def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ("reqat_quantize_fp4", "reqat_fakequant_fp4", "reqat_gemm_w4a4",
+              "reqat_quantize_mxfp4_rht", "reqat_fakequant_mxfp4_rht",
               "reqat_workspace_bytes", "reqat_status_str", "reqat_abi_version"):
         assert n in names
     assert set(names) == set(reqat.SIGNATURES), "binding and header disagree"
@@ -48,7 +49,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_small_queries(lib):
-    assert reqat.reqat_abi_version() == 2
+    assert reqat.reqat_abi_version() == 3
     assert reqat.reqat_workspace_bytes() == 4 * 4096 + 2 * (1 << 19)   # partials + segment table
     for s in range(7):
         assert reqat.reqat_status_str(s).startswith(reqat.STATUS[s])
@@ -94,6 +95,21 @@ def test_fakequant_validation(lib):
     assert fq(y=P + 4) == E_ALIGN
     assert fq(ldy=68) == E_ALIGN
     assert fq(fmt=MX) == E_UNSUP
+
+
+def test_rotated_quantize_validation(lib):
+    qr = lambda x=P, rows=4, cols=64, ldx=64, c=P, s=P: reqat.reqat_quantize_mxfp4_rht(
+        x, rows, cols, ldx, 0x12345678, c, s, None)
+    fr = lambda x=P, rows=4, cols=64, ldx=64, y=P, ldy=64: reqat.reqat_fakequant_mxfp4_rht(
+        x, rows, cols, ldx, 0xFFFFFFFF, y, ldy, None)
+    assert qr(rows=-1) == E_SHAPE
+    assert qr(cols=48, ldx=48) == E_SHAPE        # blocks of 32
+    assert qr(ldx=32) == E_SHAPE
+    assert qr(x=None) == E_NULL and qr(c=None) == E_NULL and qr(s=None) == E_NULL
+    assert qr(x=P + 2) == E_ALIGN and qr(c=P + 8) == E_ALIGN and qr(ldx=68) == E_ALIGN
+    assert qr(rows=0, x=None, c=None, s=None) == 0                   # empty: no-op
+    assert fr(ldy=32) == E_SHAPE
+    assert fr(y=None) == E_NULL and fr(y=P + 4) == E_ALIGN and fr(ldy=68) == E_ALIGN
 
 
 def test_gemm_validation(lib):

@@ -124,3 +124,23 @@ def test_nvfp4_computed_scale_beyond_segment_table():
     assert np.array_equal(c[idx].cpu().numpy(), oc)
     del x, c, s
     torch.cuda.empty_cache()
+
+
+def test_fullsize_rotated_mxfp4_activations():
+    """Block-rotated MXFP4 quantization of the full 32B-like down-proj activations
+    (8192 x 27648, Student-t with outlier channels); rows are independent, so 48
+    sampled rows plus the first and last are compared with the oracle bit for bit."""
+    w = wl.WORKLOADS[5]
+    log("full-size rotated mxfp4, workload 5 X")
+    x = wl.make_x(w)
+    signs = 0x6C8E9CF5
+    c, s = reqat.quantize_rht(x.to(DEV), signs)
+    y = reqat.fakequant_rht(x.to(DEV), signs)
+    torch.cuda.synchronize()
+    rows = np.concatenate([[0, w.M - 1], np.random.default_rng(5).choice(w.M, 48, replace=False)])
+    bits = wl.bf16_bits(x)[rows]
+    oc, os_ = oracle.quantize_mx_rht(bits, signs)
+    idx = torch.from_numpy(rows).to(DEV)
+    assert np.array_equal(s[idx].cpu().numpy(), os_)
+    assert np.array_equal(c[idx].cpu().numpy(), oc)
+    assert np.array_equal(wl.bf16_bits(y[idx].cpu()), oracle.fakequant_mx_rht(bits, signs))

@@ -135,6 +135,67 @@ def test_nvfp4_computed_scale_wide_range(shape, step):
     assert_fq_parity(NV, xs)
 
 
+# ------------------------------------------------------- block-rotated MXFP4
+
+def gpu_quant_rht(xb, signs, poison=0, ldx_pad=0):
+    R, C = xb.shape
+    if ldx_pad:
+        big = np.zeros((R, C + ldx_pad), np.uint16)
+        big[:, :C] = xb
+        xt = wl.from_bits(big).to(DEV)[:, :C]
+    else:
+        xt = wl.from_bits(xb).to(DEV)
+    codes = torch.full((R, C // 2), poison, dtype=torch.uint8, device=DEV)
+    scales = torch.full((R, C // 32), poison, dtype=torch.uint8, device=DEV)
+    reqat.quantize_rht(xt, signs, out=(codes, scales))
+    torch.cuda.synchronize()
+    return codes.cpu().numpy(), scales.cpu().numpy()
+
+
+def assert_rht_parity(xb, signs, ldx_pad=0):
+    oc, os_ = oracle.quantize_mx_rht(xb, signs)
+    for poison in (0x00, 0xFF):
+        c, s = gpu_quant_rht(xb, signs, poison, ldx_pad)
+        bad = np.argwhere(s != os_)
+        assert bad.size == 0, ("scales differ", bad[:4], s[tuple(bad[0])], os_[tuple(bad[0])])
+        bad = np.argwhere(c != oc)
+        assert bad.size == 0, ("codes differ", bad[:4], c[tuple(bad[0])], oc[tuple(bad[0])])
+    oy = oracle.fakequant_mx_rht(xb, signs)
+    for poison in (0x7FFF, 0x0000):
+        y = wl.from_bits(np.full(xb.shape, poison, np.uint16)).to(DEV)
+        reqat.fakequant_rht(wl.from_bits(xb).to(DEV), signs, out=y)
+        torch.cuda.synchronize()
+        yb = wl.bf16_bits(y.cpu())
+        bad = np.argwhere(yb != oy)
+        assert bad.size == 0, ("rotated fake-quant differs", bad[:4], hex(yb[tuple(bad[0])]), hex(oy[tuple(bad[0])]))
+
+
+@pytest.mark.parametrize("shape", [(16, 256), (37, 224), (1, 32), (129, 512), (300, 96)])
+@pytest.mark.parametrize("signs", [0x0, 0xFFFFFFFF, 0x9E3779B9])
+def test_rotated_mxfp4_parity_random(shape, signs):
+    R, C = shape
+    log("rotated mxfp4 parity shape=%s signs=%08x" % (shape, signs))
+    xb = _rand(R, C, 300 + R + C, "student_t", outliers=max(1, C // 100))
+    assert_rht_parity(xb, signs)
+
+
+@pytest.mark.parametrize("order", ["sorted", "shuffled"])
+def test_rotated_mxfp4_exhaustive_bf16_patterns(order):
+    """Every bfloat16 pattern (NaN, Inf, subnormals, overflowing sums) through the rotation."""
+    log("rotated mxfp4 exhaustive %s" % order)
+    pats = np.arange(65536, dtype=np.uint16)
+    if order == "shuffled":
+        pats = np.random.default_rng(11).permutation(pats)
+    assert_rht_parity(pats.reshape(64, 1024), 0xA5A5F00F)
+
+
+def test_rotated_mxfp4_tiny_and_strided():
+    log("rotated mxfp4 tiny scales, strided rows")
+    xb = _ramp(24, 320, 77, 6.0)                 # rows down to 2^-138: E8M0 byte 0 and FP32 subnormals
+    assert_rht_parity(xb, 0x13579BDF)
+    assert_rht_parity(_rand(45, 320, 9, "normal"), 0x2468ACE0, ldx_pad=40)
+
+
 @pytest.mark.parametrize("fmt", [NV, MX])
 def test_strided_rows(fmt):
     log("strided rows fmt=%d" % fmt)
