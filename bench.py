@@ -208,6 +208,22 @@ def main():
     torch.cuda.synchronize()
     linear_ms = lev[0].elapsed_time(lev[1]) / args.steps
 
+    # MXFP4: the block-rotated activation quantizer (randomized Hadamard of 32
+    # fused into the quantizer), timed apart from the step
+    rht_ms = None
+    if fmt == reqat.MXFP4:
+        signs = 0x6C8E9CF5
+        for _ in range(max(1, args.warmup)):
+            reqat.quantize_rht(x, signs, out=(xc, xs))
+        rev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        rev[0].record()
+        for _ in range(args.steps):
+            reqat.quantize_rht(x, signs, out=(xc, xs))
+        rev[1].record()
+        torch.cuda.synchronize()
+        rht_ms = rev[0].elapsed_time(rev[1]) / args.steps
+
     flops = 2.0 * M * N * K
     q_bytes = lambda rows: rows * K * (2 + 0.5 + 1.0 / B)        # read bf16, write codes + scales
     fq_bytes = lambda rows: rows * K * 4.0                        # read bf16, write bf16
@@ -240,6 +256,11 @@ def main():
                     "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK[mfma_dtype], 4),
                     "traffic": profiled_traffic(w.fmt, args.workload),
                     "kernel": "gemm_tile256_kernel (%s W4A4 GEMM)" % w.fmt}
+    if rht_ms is not None:
+        gbs = q_bytes(M) / (rht_ms * 1e-3) / 1e9
+        kern["quantize_x_rotated"] = {"ms": round(rht_ms, 4), "GB/s": round(gbs, 1),
+                                      "frac_hbm_peak": round(gbs / PEAK["hbm"], 4),
+                                      "note": "block-rotated MXFP4 quantize of X (Hadamard 32), timed apart"}
     kern["linear"] = {"ms": round(linear_ms, 4),
                       "vs_quantize_x_plus_gemm": round(linear_ms / (per["quantize_x"] + per["gemm"]), 4),
                       "note": "reqat_linear_w4a4: quantize X + GEMM in one call, timed separately"}
