@@ -71,6 +71,7 @@ def _load():
                                        u8p, u8p, ctypes.c_double, i64p, i64p, i64, dp, dp]),
             "orc_e2m1_encode_array": (None, [dp, i64, ctypes.c_double, u8p]),
             "orc_bf16_from_double_array": (None, [dp, i64, u16p]),
+            "orc_gemm_w4a16_points": (None, [i64, u16p, i64, u8p, u8p, i64p, i64p, i64, dp, dp]),
             "orc_rht_norm": (ctypes.c_float, []),
             "orc_fwht32_f32": (None, [ctypes.POINTER(ctypes.c_float)]),
             "orc_rht32": (None, [u16p, ctypes.c_uint32, ctypes.POINTER(ctypes.c_float)]),
@@ -287,3 +288,25 @@ def fakequant_mx_rht(x: np.ndarray, signs: int) -> np.ndarray:
                                       _p(y, ctypes.c_uint16), C)
     assert rc == 0
     return y
+
+
+# ------------------------------------------------------------------ W4A16
+
+def gemm_w4a16_points(x: np.ndarray, w_codes: np.ndarray, w_scales: np.ndarray, ms, ns):
+    """FP64 Y[m, n] = sum_k x[m, k] RN_bf16(w^[n, k]) at the (ms[i], ns[i]) pairs
+    (x bfloat16 bits [M, K]; MXFP4 weights), and sum_k |x w^| at each."""
+    x = _as_u16(x)
+    w_codes = np.ascontiguousarray(w_codes, np.uint8)
+    w_scales = np.ascontiguousarray(w_scales, np.uint8)
+    ms = np.ascontiguousarray(ms, np.int64)
+    ns = np.ascontiguousarray(ns, np.int64)
+    K = x.shape[1]
+    if w_codes.shape[1] * 2 != K or w_scales.shape[1] * 32 != K:
+        raise ValueError("K mismatch")
+    y = np.empty(len(ms), np.float64)
+    ay = np.empty(len(ms), np.float64)
+    _load().orc_gemm_w4a16_points(K, _p(x, ctypes.c_uint16), K, _p(w_codes, ctypes.c_uint8),
+                                  _p(w_scales, ctypes.c_uint8), _p(ms, ctypes.c_int64),
+                                  _p(ns, ctypes.c_int64), len(ms), _p(y, ctypes.c_double),
+                                  _p(ay, ctypes.c_double))
+    return y, ay

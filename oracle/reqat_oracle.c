@@ -458,3 +458,40 @@ int orc_fakequant_mx_rht(const uint16_t *x, int64_t rows, int64_t cols, int64_t 
 {
     return quantize_mx_rht(x, rows, cols, ldx, signs, 0, 0, y, ldy, 1);
 }
+
+/* ---------- W4A16: MXFP4 weights, bfloat16 activations ---------- */
+
+/* The MXFP4 W4A16 deployment setting (Sec. 2, "Microscaled FP4 formats";
+ * Sec. 5.1; App. D.1): weights stored as MXFP4, activations bfloat16.
+ * Readings: the weight is dequantized to the activation type,
+ *     w^[n][k] = RN_bf16(E2M1(c) * 2^e)
+ * (exact for E8M0 bytes 2..252; the bfloat16 rounding, overflow to Inf
+ * included, otherwise; NaN for byte 0xFF), and
+ *     Y[m][n] = sum_k x[m][k] * w^[n][k]
+ * is evaluated here in FP64 in k order (every product is exact in FP64).
+ * For each requested (m, n) pair it also returns sum_k |x w^|, the scale of
+ * FP32 accumulation error. */
+static double w4a16_weight(const uint8_t *w_codes, const uint8_t *w_scales, int64_t K, int64_t n, int64_t k)
+{
+    uint8_t byte = w_codes[n * (K / 2) + k / 2];
+    uint8_t c = (k % 2 == 0) ? (byte & 0xF) : (byte >> 4);
+    double v = orc_e2m1_value(c) * orc_e8m0_value(w_scales[n * (K / 32) + k / 32]);
+    return orc_bf16_value(orc_bf16_from_double(v));
+}
+
+void orc_gemm_w4a16_points(int64_t K, const uint16_t *x, int64_t ldx, const uint8_t *w_codes,
+                           const uint8_t *w_scales, const int64_t *ms, const int64_t *ns, int64_t npts,
+                           double *y, double *absy)
+{
+    int64_t p, k;
+    for (p = 0; p < npts; p++) {
+        double acc = 0.0, aacc = 0.0;
+        for (k = 0; k < K; k++) {
+            double t = orc_bf16_value(x[ms[p] * ldx + k]) * w4a16_weight(w_codes, w_scales, K, ns[p], k);
+            acc += t;
+            aacc += fabs(t);
+        }
+        y[p] = acc;
+        absy[p] = aacc;
+    }
+}
