@@ -67,7 +67,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", type=int, default=4, help="workload number (4 = 14B gate/up)")
+    ap.add_argument("--workload", type=int, default=4,
+                    help="workload number (4 = 14B gate/up; 6, 7 = MXFP4 W4A16 decode)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes --steps times "
@@ -122,6 +123,77 @@ def cpu_baseline(w, xb, wb):
     }
 
 
+def bench_w4a16(args, w):
+    """W4A16 decode step: the product of bfloat16 activations with MXFP4 weights
+    (quantized once, untimed: served weights are stored quantized).  Bound by HBM."""
+    import numpy as np
+    import torch
+
+    from paper_2606_15682_amd import reqat
+    from paper_2606_15682_amd import workloads as wl
+
+    reqat.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    M, N, K = w.M, w.N, w.K
+    x_cpu, w_cpu = wl.make_x(w), wl.make_w(w)
+    x = x_cpu.to(dev)
+    wc, ws, _ = reqat.quantize(w_cpu.to(dev), reqat.MXFP4)
+    y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    for _ in range(args.warmup):
+        reqat.gemm_w4a16(x, wc, ws, out_dtype=torch.bfloat16, out=y)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record()
+    for _ in range(args.steps):
+        reqat.gemm_w4a16(x, wc, ws, out_dtype=torch.bfloat16, out=y)
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms_kernel = ev[0].elapsed_time(ev[1]) / args.steps
+    flops = 2.0 * M * N * K
+    nbytes = N * K * (0.5 + 1.0 / 32) + M * K * 2.0 + M * N * 2.0       # W codes + scales, x, Y (bf16)
+    gbs = nbytes / (ms_kernel * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(flops / (ms_step * 1e-3) / 1e12, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; Student-t or Gaussian-with-outlier activations, N(0,0.02) weights)",
+        "config": {"workload": w.name, "M": M, "N": N, "K": K, "format": "mxfp4 weights, bf16 activations",
+                   "gemm_out": "bf16", "global_batch": M, "parallelism": "single GPU",
+                   "step": "W4A16 GEMM (weights pre-quantized, untimed)"},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK["hbm"], "unit": "GB/s",
+                     "frac": round(gbs / PEAK["hbm"], 4), "traffic": None,
+                     "kernel": "gemm_w4a16_kernel (MXFP4 W4A16, algorithmic bytes %d)" % int(nbytes)},
+        "kernels": {"gemm_w4a16": {"ms": round(ms_kernel, 4), "GB/s": round(gbs, 1),
+                                   "TFLOP/s": round(flops / (ms_kernel * 1e-3) / 1e12, 2)}},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        xb, wb = wl.bf16_bits(x_cpu), wl.bf16_bits(w_cpu)
+        owc, ows, _ = oracle.quantize(oracle.FMT_MXFP4, wb[:64])
+        npts = int(5e8 // K)                        # about 10 s of single-thread CPU work
+        ms_, ns_ = np.arange(npts) % M, np.arange(npts) % 64
+        t0 = time.perf_counter()
+        oracle.gemm_w4a16_points(xb, owc, ows, ms_, ns_)
+        dt = time.perf_counter() - t0
+        per_mac = dt / (npts * K)
+        out["cpu_baseline"] = {
+            "value": round(2.0 / per_mac / 1e12, 9), "unit": "TFLOP/s", "cores": 1, "kind": "oracle",
+            "sample": ("FP64 W4A16 oracle on %d output points (each a %d-term dot product), per-MAC "
+                       "rate scaled to the full product (%.2f s of CPU work)" % (npts, K, dt))}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -143,6 +215,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = wl.WORKLOADS[args.workload]
+    if w.kind == "w4a16":
+        bench_w4a16(args, w)
+        return
     fmt = reqat.NVFP4 if w.fmt == "nvfp4" else reqat.MXFP4
     B = reqat.BLOCK[fmt]
     x_cpu, w_cpu = wl.make_x(w), wl.make_w(w)

@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define REQAT_ABI_VERSION 3
+#define REQAT_ABI_VERSION 4
 
 typedef enum {
     REQAT_FMT_NVFP4 = 0, /* B = 16, E4M3 block scale, FP32 global scale */
@@ -151,6 +151,23 @@ reqat_status reqat_quantize_mxfp4_rht(const void *x, int64_t rows, int64_t cols,
  */
 reqat_status reqat_fakequant_mxfp4_rht(const void *x, int64_t rows, int64_t cols, int64_t ldx,
                                        uint32_t signs, void *y_out, int64_t ldy, void *stream);
+
+/*
+ * W4A16 product (the MXFP4 W4A16 deployment setting, Sec. 2 "Microscaled FP4
+ * formats", Sec. 5.1, App. D.1): MXFP4 weights, bfloat16 activations,
+ *     Y[m][n] = sum_k x[m][k] * w^[n][k],   w^ = RN_bf16(E2M1(c) * 2^e),
+ * i.e. each weight dequantized to bfloat16 (exact for E8M0 bytes 2..252; the
+ * bfloat16 rounding, overflow to Inf included, otherwise; NaN for 0xFF),
+ * products exact, FP32 accumulation.
+ *   x [M][ldx] bfloat16 (16-byte aligned, ldx % 8 == 0, ldx >= K);
+ *   w_codes [N][K/2], w_scales [N][K/32] (as reqat_quantize_fp4, MXFP4);
+ *   y [M][ldy] of y_dtype, ldy >= N.
+ * Requirements: K % 128 == 0.  M == 0 or N == 0 is a no-op; K == 0 writes zeros.
+ * Designed for decode (small M): one pass over the weights.
+ */
+reqat_status reqat_gemm_w4a16(int64_t M, int64_t N, int64_t K, const void *x, int64_t ldx,
+                              const uint8_t *w_codes, const uint8_t *w_scales, void *y, reqat_dtype y_dtype,
+                              int64_t ldy, void *stream);
 
 /*
  * Block-scaled FP4 x FP4 product (the W4A4 GEMM of Sec. 5.3):

@@ -43,6 +43,11 @@ hipError_t launch_quantize_rht(QuantOut out, const uint16_t *x, int64_t rows, in
                                uint32_t signs, uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy,
                                hipStream_t stream);
 
+// W4A16: bfloat16 x [M][ldx] times MXFP4 weights [N][K/2] (+ scales [N][K/32]), K % 128 == 0.
+hipError_t launch_gemm_w4a16(int64_t M, int64_t N, int64_t K, const uint16_t *x, int64_t ldx,
+                             const uint8_t *w_codes, const uint8_t *w_scales, void *y, bool y_bf16,
+                             int64_t ldy, hipStream_t stream);
+
 bool gemm_tile256_supported(Fmt fmt, int64_t M, int64_t N, int64_t K, int64_t ldy);
 // Skinny product for M <= 64 (K % 64 == 0, K > 0).
 hipError_t launch_gemm_skinny(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *a_codes,

@@ -43,6 +43,7 @@ SIGNATURES = {
     "reqat_linear_w4a4": (_INT, [_INT, _I64, _I64, _I64, _VP, _I64, _VP, _INT, _VP, _VP, _VP, _VP,
                                  _INT, _I64, _VP, _VP]),
     "reqat_linear_workspace_bytes": (ctypes.c_size_t, [_INT, _I64, _I64]),
+    "reqat_gemm_w4a16": (_INT, [_I64, _I64, _I64, _VP, _I64, _VP, _VP, _VP, _INT, _I64, _VP]),
     "reqat_quantize_mxfp4_rht": (_INT, [_VP, _I64, _I64, _I64, ctypes.c_uint32, _VP, _VP, _VP]),
     "reqat_fakequant_mxfp4_rht": (_INT, [_VP, _I64, _I64, _I64, ctypes.c_uint32, _VP, _I64, _VP]),
     "reqat_workspace_bytes": (ctypes.c_size_t, []),
@@ -98,6 +99,10 @@ def reqat_linear_w4a4(fmt, M, N, K, x, ldx, x_ts, ts, w_codes, w_scales, w_ts, y
                       workspace, stream):
     return load().reqat_linear_w4a4(fmt, M, N, K, x, ldx, x_ts, ts, w_codes, w_scales, w_ts, y,
                                     y_dtype, ldy, workspace, stream)
+
+
+def reqat_gemm_w4a16(M, N, K, x, ldx, w_codes, w_scales, y, y_dtype, ldy, stream):
+    return load().reqat_gemm_w4a16(M, N, K, x, ldx, w_codes, w_scales, y, y_dtype, ldy, stream)
 
 
 def reqat_quantize_mxfp4_rht(x, rows, cols, ldx, signs, codes, scales, stream):
@@ -244,6 +249,21 @@ def gemm(fmt, a_codes, a_scales, a_g, b_codes, b_scales, b_g, out_dtype=torch.fl
                          b_codes.data_ptr(), b_scales.data_ptr(), _ptr(b_g), y.data_ptr(), dt,
                          y.stride(0), _stream(a_codes.device))
     _check(st, "reqat_gemm_w4a4")
+    return y
+
+
+def gemm_w4a16(x: torch.Tensor, w_codes, w_scales, out_dtype=torch.float32, out=None):
+    """Y = x . W^T with x bfloat16 [M, K] and MXFP4 weights (codes [N, K/2],
+    scales [N, K/32]) dequantized to bfloat16; FP32 accumulation."""
+    M, K, ldx = _x2d(x)
+    N = w_codes.shape[0]
+    if w_codes.shape[1] * 2 != K:
+        raise ValueError("K mismatch")
+    dt = DT_F32 if out_dtype == torch.float32 else DT_BF16
+    y = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=x.device)
+    st = reqat_gemm_w4a16(M, N, K, x.data_ptr(), ldx, w_codes.data_ptr(), w_scales.data_ptr(), y.data_ptr(),
+                          dt, y.stride(0), _stream(x.device))
+    _check(st, "reqat_gemm_w4a16")
     return y
 
 

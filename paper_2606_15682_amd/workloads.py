@@ -41,6 +41,7 @@ class Workload:
     x_dist: str         # "normal" | "normal_outliers" | "student_t"
     n_outliers: int     # outlier channels in X (multiplied by 20)
     w_std: float        # weight standard deviation
+    kind: str = "w4a4"  # "w4a4" (both operands FP4) | "w4a16" (FP4 weights, bfloat16 activations)
 
     @property
     def flops(self) -> int:
@@ -57,6 +58,11 @@ WORKLOADS = {
                 "normal_outliers", 51, 0.02),
     5: Workload(5, "MXFP4 down-proj 32B-like 8192x5120x27648", MXFP4, 8192, 5120, 27648,
                 "student_t", 0, 0.02),
+    # MXFP4 W4A16 decode (weights FP4, activations bfloat16)
+    6: Workload(6, "W4A16 decode MXFP4 down-proj 32B-like 16x5120x27648", MXFP4, 16, 5120, 27648,
+                "student_t", 0, 0.02, "w4a16"),
+    7: Workload(7, "W4A16 decode MXFP4 gate/up 14B-like 16x27648x5120", MXFP4, 16, 27648, 5120,
+                "normal_outliers", 51, 0.02, "w4a16"),
 }
 
 

@@ -33,7 +33,7 @@ def lib():
 def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ("reqat_quantize_fp4", "reqat_fakequant_fp4", "reqat_gemm_w4a4",
-              "reqat_quantize_mxfp4_rht", "reqat_fakequant_mxfp4_rht",
+              "reqat_quantize_mxfp4_rht", "reqat_fakequant_mxfp4_rht", "reqat_gemm_w4a16",
               "reqat_workspace_bytes", "reqat_status_str", "reqat_abi_version"):
         assert n in names
     assert set(names) == set(reqat.SIGNATURES), "binding and header disagree"
@@ -49,7 +49,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_small_queries(lib):
-    assert reqat.reqat_abi_version() == 3
+    assert reqat.reqat_abi_version() == 4
     assert reqat.reqat_workspace_bytes() == 4 * 4096 + 2 * (1 << 19)   # partials + segment table
     for s in range(7):
         assert reqat.reqat_status_str(s).startswith(reqat.STATUS[s])
@@ -110,6 +110,18 @@ def test_rotated_quantize_validation(lib):
     assert qr(rows=0, x=None, c=None, s=None) == 0                   # empty: no-op
     assert fr(ldy=32) == E_SHAPE
     assert fr(y=None) == E_NULL and fr(y=P + 4) == E_ALIGN and fr(ldy=68) == E_ALIGN
+
+
+def test_w4a16_validation(lib):
+    g16 = lambda M=4, N=8, K=128, x=P, ldx=128, wc=P, ws=P, y=P, dt=0, ldy=8: reqat.reqat_gemm_w4a16(
+        M, N, K, x, ldx, wc, ws, y, dt, ldy, None)
+    assert g16(dt=5) == E_ENUM
+    assert g16(M=-1) == E_SHAPE and g16(K=96, ldx=96) == E_SHAPE and g16(ldx=64) == E_SHAPE
+    assert g16(ldy=4) == E_SHAPE
+    assert g16(M=0, x=None, wc=None, ws=None, y=None) == 0 and g16(N=0, y=None) == 0
+    assert g16(y=None) == E_NULL and g16(x=None) == E_NULL and g16(wc=None) == E_NULL and g16(ws=None) == E_NULL
+    assert g16(x=P + 2) == E_ALIGN and g16(ldx=132) == E_ALIGN and g16(wc=P + 8) == E_ALIGN
+    assert g16(y=P + 2) == E_ALIGN and g16(y=P + 1, dt=1) == E_ALIGN
 
 
 def test_gemm_validation(lib):

@@ -144,3 +144,22 @@ def test_fullsize_rotated_mxfp4_activations():
     assert np.array_equal(s[idx].cpu().numpy(), os_)
     assert np.array_equal(c[idx].cpu().numpy(), oc)
     assert np.array_equal(wl.bf16_bits(y[idx].cpu()), oracle.fakequant_mx_rht(bits, signs))
+
+
+@pytest.mark.parametrize("idx", [6, 7])
+def test_fullsize_w4a16_decode(idx):
+    """W4A16 decode shapes at full size: weights quantized to MXFP4 by the oracle,
+    the product checked on sampled outputs (plus corners) against the FP64 oracle."""
+    w = wl.WORKLOADS[idx]
+    log("full-size W4A16 workload %d: %s" % (idx, w.name))
+    xb, wb = wl.bf16_bits(wl.make_x(w)), wl.bf16_bits(wl.make_w(w))
+    wc, ws, _ = oracle.quantize(oracle.FMT_MXFP4, wb)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    y = reqat.gemm_w4a16(wl.from_bits(xb).to(DEV), t(wc), t(ws), out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(idx)
+    ms = np.concatenate([rng.integers(0, w.M, 2000), [0, 0, w.M - 1, w.M - 1]])
+    ns = np.concatenate([rng.integers(0, w.N, 2000), [0, w.N - 1, 0, w.N - 1]])
+    ref, aref = oracle.gemm_w4a16_points(xb, wc, ws, ms, ns)
+    got = y.cpu().numpy().astype(np.float64)[ms, ns]
+    assert float(np.max(np.abs(got - ref) / np.maximum(aref, 1e-300))) <= 1e-3

@@ -354,6 +354,79 @@ def test_gemm_nan_block_propagates(fmt):
     assert np.all(np.isnan(y[3])) and not np.any(np.isnan(np.delete(y, 3, axis=0)))
 
 
+# ------------------------------------------------------------------ W4A16
+
+def run_w4a16(xb, wc, ws):
+    M, K = xb.shape
+    N = wc.shape[0]
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    xt = wl.from_bits(xb).to(DEV)
+    outs = []
+    for dt, poison in ((torch.float32, float("nan")), (torch.float32, 0.0), (torch.bfloat16, float("nan"))):
+        y = torch.full((M, N), poison, dtype=dt, device=DEV)
+        reqat.gemm_w4a16(xt, t(wc), t(ws), out_dtype=dt, out=y)
+        torch.cuda.synchronize()
+        outs.append(y.float().cpu().numpy().astype(np.float64))
+    assert np.array_equal(outs[0], outs[1], equal_nan=True), "poison visible or nondeterministic"
+    ms, ns = np.arange(M).repeat(N), np.tile(np.arange(N), M)
+    ref, aref = oracle.gemm_w4a16_points(xb, wc, ws, ms, ns)
+    got = outs[0].reshape(-1)
+    assert np.array_equal(np.isnan(got), np.isnan(ref))
+    inf = np.isinf(ref)
+    assert np.array_equal(got[inf], ref[inf])
+    ok = ~(np.isnan(ref) | inf)
+    err = np.abs(got[ok] - ref[ok])
+    assert np.all(err <= GEMM_TOL * aref[ok]), float(np.max(err / np.maximum(aref[ok], 1e-300)))
+    gb_ = outs[2].reshape(-1)[ok]
+    rb = indep.bf16_values(oracle.bf16_from_double_array(ref[ok]))
+    ulp = np.maximum(np.abs(rb), 2.0 ** -133) * 2.0 ** -7
+    assert np.all(np.abs(gb_ - rb) <= ulp + GEMM_TOL * aref[ok])
+
+
+def _w4a16_weights(N, K, seed, lo=110, hi=140):
+    rng = np.random.default_rng(seed)
+    return (rng.integers(0, 256, (N, K // 2), dtype=np.uint8),
+            rng.integers(lo, hi, (N, K // 32), dtype=np.uint8))
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 16, 128), (5, 40, 256), (16, 256, 1536), (17, 33, 512),
+                                   (33, 100, 384), (64, 48, 640), (100, 70, 1024)])
+def test_w4a16_parity(M, N, K):
+    log("w4a16 parity M=%d N=%d K=%d" % (M, N, K))
+    xb = _rand(M, K, 40 + M + N, "student_t", outliers=max(1, K // 100))
+    run_w4a16(xb, *_w4a16_weights(N, K, M + N))
+
+
+def test_w4a16_special_scales():
+    log("w4a16 special scale bytes")
+    xb = _rand(8, 512, 91, "student_t", outliers=5)
+    wc, ws = _w4a16_weights(24, 512, 91)
+    ws[0, :] = 0                               # bfloat16-subnormal weights
+    ws[1, 0] = 0xFF                            # a NaN block
+    ws[2, :] = 200                             # large but far from overflow for these x
+    run_w4a16(xb, wc, ws)
+    # every scale byte 0..250, small activations so that no FP32 sum overflows
+    xs = indep.to_bf16_bits(np.random.default_rng(3).normal(0.0, 1e-3, (3, 128)))
+    wc, _ = _w4a16_weights(251, 128, 4)
+    ws = np.repeat(np.arange(251, dtype=np.uint8)[:, None], 4, axis=1)
+    run_w4a16(xs, wc, ws)
+    # scale bytes 253/254 with code 6.0: the bfloat16 weight overflows to +Inf
+    ones = np.full((2, 128), 0x3F80, np.uint16)
+    wc = np.full((3, 64), 0x77, np.uint8)
+    ws = np.array([[253] * 4, [254] * 4, [127] * 4], np.uint8)
+    run_w4a16(ones, wc, ws)
+
+
+def test_w4a16_k_zero_writes_zeros():
+    log("w4a16 K = 0")
+    x = torch.empty((3, 0), dtype=torch.bfloat16, device=DEV)
+    y = torch.full((3, 5), float("nan"), dtype=torch.float32, device=DEV)
+    reqat.gemm_w4a16(x, torch.empty((5, 0), dtype=torch.uint8, device=DEV),
+                     torch.empty((5, 0), dtype=torch.uint8, device=DEV), out=y)
+    torch.cuda.synchronize()
+    assert torch.equal(y.cpu(), torch.zeros(3, 5))
+
+
 def test_gemm_k_zero_writes_zeros():
     log("gemm K=0")
     y = torch.full((4, 8), float("nan"), dtype=torch.float32, device=DEV)
