@@ -72,6 +72,13 @@ def _load():
             "orc_e2m1_encode_array": (None, [dp, i64, ctypes.c_double, u8p]),
             "orc_bf16_from_double_array": (None, [dp, i64, u16p]),
             "orc_gemm_w4a16_points": (None, [i64, u16p, i64, u8p, u8p, i64p, i64p, i64, dp, dp]),
+            "orc_e1m2_value": (ctypes.c_double, [ctypes.c_uint8]),
+            "orc_e1m2_encode": (ctypes.c_uint8, [ctypes.c_double, ctypes.c_double]),
+            "orc_kv4_global_scale": (ctypes.c_float, [ctypes.c_double]),
+            "orc_kv4_scale_byte": (ctypes.c_uint8, [ctypes.c_double, ctypes.c_double]),
+            "orc_kv4_amax": (ctypes.c_double, [u16p, i64, i64, i64, ctypes.POINTER(ctypes.c_float)]),
+            "orc_kv4_quantize": (ctypes.c_int, [u16p, i64, i64, i64, ctypes.POINTER(ctypes.c_float),
+                                                ctypes.c_double, u8p, u8p, u16p, i64]),
             "orc_rht_norm": (ctypes.c_float, []),
             "orc_fwht32_f32": (None, [ctypes.POINTER(ctypes.c_float)]),
             "orc_rht32": (None, [u16p, ctypes.c_uint32, ctypes.POINTER(ctypes.c_float)]),
@@ -310,3 +317,67 @@ def gemm_w4a16_points(x: np.ndarray, w_codes: np.ndarray, w_scales: np.ndarray, 
                                   _p(ns, ctypes.c_int64), len(ms), _p(y, ctypes.c_double),
                                   _p(ay, ctypes.c_double))
     return y, ay
+
+
+# ------------------------------------------------- KV4 (E1M2, post-RoPE shift)
+
+def e1m2_value(code: int) -> float:
+    return _load().orc_e1m2_value(code)
+
+
+def e1m2_encode(v: float, S: float) -> int:
+    return _load().orc_e1m2_encode(v, S)
+
+
+def kv4_global_scale(amax: float) -> float:
+    return _load().orc_kv4_global_scale(amax)
+
+
+def kv4_scale_byte(amax: float, g: float) -> int:
+    return _load().orc_kv4_scale_byte(amax, g)
+
+
+def _shift_arg(shift, C):
+    if shift is None:
+        return None, None
+    sh = np.ascontiguousarray(shift, np.float32).reshape(C)
+    return sh, _p(sh, ctypes.c_float)
+
+
+def kv4_global(x: np.ndarray, shift=None, g: float | None = None) -> float:
+    """The given g (as FP32), or the computed power of two over the shifted values."""
+    x = _as_u16(x)
+    if g is not None:
+        return float(np.float32(g))
+    sh, shp = _shift_arg(shift, x.shape[1])
+    amax = _load().orc_kv4_amax(_p(x, ctypes.c_uint16), x.shape[0], x.shape[1], x.shape[1], shp)
+    return float(kv4_global_scale(amax))
+
+
+def kv4_quantize(x: np.ndarray, shift=None, g: float | None = None):
+    """KV4 codes [R, C/2], E4M3 scales [R, C/16] and g of the shifted rows x - shift."""
+    x = _as_u16(x)
+    R, C = x.shape
+    if C % 16:
+        raise ValueError("cols must be a multiple of 16")
+    g = kv4_global(x, shift, g)
+    sh, shp = _shift_arg(shift, C)
+    codes = np.zeros((R, C // 2), np.uint8)
+    scales = np.zeros((R, C // 16), np.uint8)
+    rc = _load().orc_kv4_quantize(_p(x, ctypes.c_uint16), R, C, C, shp, g, _p(codes, ctypes.c_uint8),
+                                  _p(scales, ctypes.c_uint8), None, 0)
+    assert rc == 0
+    return codes, scales, g
+
+
+def kv4_fakequant(x: np.ndarray, shift=None, g: float | None = None):
+    """bfloat16 bits of the dequantized shifted rows (shifted domain), and g."""
+    x = _as_u16(x)
+    R, C = x.shape
+    g = kv4_global(x, shift, g)
+    sh, shp = _shift_arg(shift, C)
+    y = np.zeros((R, C), np.uint16)
+    rc = _load().orc_kv4_quantize(_p(x, ctypes.c_uint16), R, C, C, shp, g, None, None,
+                                  _p(y, ctypes.c_uint16), C)
+    assert rc == 0
+    return y, g

@@ -495,3 +495,129 @@ void orc_gemm_w4a16_points(int64_t K, const uint16_t *x, int64_t ldx, const uint
         absy[p] = aacc;
     }
 }
+
+/* ---------- KV4: E1M2 elements with NVFP4-style scaling and the post-RoPE shift ---------- */
+
+/* The KV cache of the NVFP4 W4A4KV4 setting is stored in 4 bits with the E1M2
+ * element format (Sec. 3.3, "Additional implementation details"), and the
+ * keys are shifted channel-wise after RoPE before quantization (Q-FIT,
+ * Sec. 3.3, Eq. for K~: K~ = R(K_pre / s) - m; the pre-RoPE scale s is folded
+ * into the projection weights, so the cache quantizer sees R(...) and m).
+ * Readings:
+ *   - E1M2: sign, 1 exponent bit (bias 0), 2 mantissa bits: magnitudes
+ *     0, 0.5, 1, ..., 3.5 (code magnitude i is i / 2);
+ *   - scaling as NVFP4: blocks of 16 along the channel dimension, an E4M3
+ *     block scale (the smallest positive E4M3 value s with
+ *     block_amax <= 3.5 * s * g) and an FP32 global scale g, computed as the
+ *     smallest power of two 2^k (k >= -126) with tensor_amax <= 3.5 * 448 * 2^k
+ *     (g = 1 for a tensor without non-zero finite values) or given;
+ *   - the shifted value d = x - m[c] is rounded once to FP32 (m is FP32; no
+ *     shift = all zeros), and d is what is quantized; a block with a
+ *     non-finite d gets scale 0x7F and zero codes;
+ *   - elements round to nearest, ties to the even magnitude code, saturating
+ *     at 3.5; the sign is copied.
+ * All comparisons are exact in FP64 (d has 24 significant bits, 3.5 * s * g
+ * and the midpoints times s * g at most 3 + 4 + 24). */
+
+double orc_e1m2_value(uint8_t code)
+{
+    double v = 0.5 * (double)(code & 7);
+    return (code & 8) ? -v : v;
+}
+
+/* E1M2 code of v / S (S > 0): nearest of i / 2, ties to even i, saturating. */
+uint8_t orc_e1m2_encode(double v, double S)
+{
+    double a = fabs(v);
+    int i, m = 7;
+    for (i = 0; i < 7; i++) {
+        double t = (0.5 * i + 0.25) * S;       /* midpoint between i/2 and (i+1)/2 */
+        if (a < t) { m = i; break; }
+        if (a == t) { m = (i % 2 == 0) ? i : i + 1; break; }
+    }
+    return (uint8_t)((signbit(v) ? 8 : 0) | m);
+}
+
+/* Global scale: smallest 2^k, k >= -126, with amax <= 1568 * 2^k
+ * (1568 = 3.5 * 448 = 1.53125 * 2^10), by exact search. */
+float orc_kv4_global_scale(double amax)
+{
+    int k;
+    if (!(amax > 0.0) || isinf(amax)) return 1.0f;
+    for (k = -126; k < 128; k++)
+        if (amax <= 1568.0 * ldexp(1.0, k)) break;
+    return (float)ldexp(1.0, k);
+}
+
+/* Block scale: the smallest positive finite E4M3 value s with amax <= 3.5 s g
+ * (exact product comparison); 448 when none is large enough; 0 for amax 0. */
+uint8_t orc_kv4_scale_byte(double amax, double g)
+{
+    int i;
+    if (isnan(amax) || isinf(amax)) return 0x7F;
+    if (amax == 0.0) return 0x00;
+    e4m3_init();
+    for (i = 0; i < 126; i++)
+        if (amax <= 3.5 * e4m3_pos_val[i] * g) return e4m3_pos_byte[i];
+    return 0x7E;
+}
+
+/* d[r][c] = RN_fp32(x - m[c]) for a rows x cols bfloat16 matrix. */
+static float kv4_shifted(const uint16_t *x, int64_t ldx, const float *shift, int64_t r, int64_t c)
+{
+    float v = (float)orc_bf16_value(x[r * ldx + c]);
+    return shift ? v - shift[c] : v;
+}
+
+double orc_kv4_amax(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx, const float *shift)
+{
+    double m = 0.0;
+    int64_t r, c;
+    for (r = 0; r < rows; r++)
+        for (c = 0; c < cols; c++) {
+            double v = fabs((double)kv4_shifted(x, ldx, shift, r, c));
+            if (!isnan(v) && !isinf(v) && v > m) m = v;
+        }
+    return m;
+}
+
+/* Quantize (codes rows x cols/2, scales rows x cols/16) or, with y != 0,
+ * fake-quantize (y[r][c] = RN_bf16(E1M2(code) * s * g), in the shifted
+ * domain; NaN for a non-finite block) the shifted rows.  g as given. */
+int orc_kv4_quantize(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx, const float *shift,
+                     double g, uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy)
+{
+    int64_t r, b, nb;
+    int j;
+    if (cols % 16) return -1;
+    nb = cols / 16;
+    for (r = 0; r < rows; r++) {
+        for (b = 0; b < nb; b++) {
+            float d[16];
+            double amax = 0.0, S;
+            int bad = 0;
+            uint8_t sb;
+            for (j = 0; j < 16; j++) {
+                d[j] = kv4_shifted(x, ldx, shift, r, b * 16 + j);
+                if (isnan(d[j]) || isinf(d[j])) bad = 1;
+                else if (fabs((double)d[j]) > amax) amax = fabs((double)d[j]);
+            }
+            sb = bad ? 0x7F : orc_kv4_scale_byte(amax, g);
+            S = orc_e4m3_value(sb) * g;
+            if (scales) scales[r * nb + b] = sb;
+            for (j = 0; j < 16; j++) {
+                uint8_t c = (bad || sb == 0) ? (uint8_t)(bad ? 0 : (signbit(d[j]) ? 8 : 0))
+                                            : orc_e1m2_encode((double)d[j], S);
+                int64_t k = b * 16 + j;
+                if (y) {
+                    y[r * ldy + k] = bad ? 0x7FC0 : orc_bf16_from_double(orc_e1m2_value(c) * (sb ? S : 0.0));
+                } else {
+                    uint8_t *p = &codes[r * (cols / 2) + k / 2];
+                    if (k % 2 == 0) *p = (uint8_t)((*p & 0xF0) | c);
+                    else *p = (uint8_t)((*p & 0x0F) | (c << 4));
+                }
+            }
+        }
+    }
+    return 0;
+}
