@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define REQAT_ABI_VERSION 4
+#define REQAT_ABI_VERSION 5
 
 typedef enum {
     REQAT_FMT_NVFP4 = 0, /* B = 16, E4M3 block scale, FP32 global scale */
@@ -168,6 +168,37 @@ reqat_status reqat_fakequant_mxfp4_rht(const void *x, int64_t rows, int64_t cols
 reqat_status reqat_gemm_w4a16(int64_t M, int64_t N, int64_t K, const void *x, int64_t ldx,
                               const uint8_t *w_codes, const uint8_t *w_scales, void *y, reqat_dtype y_dtype,
                               int64_t ldy, void *stream);
+
+/*
+ * KV-cache quantization of the NVFP4 W4A4KV4 setting: E1M2 elements (the KV4
+ * element format, Sec. 3.3 "Additional implementation details") with the
+ * Q-FIT post-RoPE shift applied first (Sec. 3.3, K~ = R(K_pre / s) - m):
+ *     d[r][c] = RN_fp32(x[r][c] - shift[c])            (shift == NULL: d = x)
+ * quantized along c in blocks of 16: an E4M3 block scale, the smallest with
+ * block_amax <= 3.5 * s * g, an FP32 tensor scale g (REQAT_TS_COMPUTE: the
+ * smallest power of two 2^k, k >= -126, with tensor_amax <= 3.5 * 448 * 2^k,
+ * g = 1 for a tensor without non-zero finite values; REQAT_TS_GIVEN: as
+ * given), E1M2 codes (magnitudes 0, 0.5, ..., 3.5; bit 3 sign, bit 2 exponent,
+ * bits 1:0 mantissa) rounded to nearest with ties to the even code.  A block
+ * with a non-finite d gets scale 0x7F and zero codes.  Layouts as
+ * reqat_quantize_fp4 with B = 16.
+ *   shift: NULL or cols FP32 values, 16-byte aligned (keys: the calibrated
+ *          channel means m; values: NULL).
+ *   workspace: reqat_workspace_bytes() bytes, needed for REQAT_TS_COMPUTE.
+ * Requirements and errors as reqat_quantize_fp4 (NVFP4).
+ */
+reqat_status reqat_quantize_kv4(const void *x, int64_t rows, int64_t cols, int64_t ldx, const float *shift,
+                                uint8_t *codes, uint8_t *scales, float *tensor_scale, reqat_tscale_mode ts,
+                                void *workspace, void *stream);
+
+/*
+ * Fake-quant of the KV4 quantization above: y[r][c] = RN_bf16(E1M2(code) * s * g)
+ * in the shifted domain (NaN for a non-finite block).  y [rows][ldy] bfloat16,
+ * 16-byte aligned, ldy % 8 == 0, ldy >= cols.
+ */
+reqat_status reqat_fakequant_kv4(const void *x, int64_t rows, int64_t cols, int64_t ldx, const float *shift,
+                                 void *y, int64_t ldy, float *tensor_scale, reqat_tscale_mode ts, void *workspace,
+                                 void *stream);
 
 /*
  * Block-scaled FP4 x FP4 product (the W4A4 GEMM of Sec. 5.3):

@@ -91,6 +91,39 @@ reqat_status reqat_fakequant_fp4(reqat_format fmt, const void *x, int64_t rows, 
                      workspace, quant_seg_table(workspace), kMaxSegments, stream, true);
 }
 
+static reqat_status run_kv4(const void *x, int64_t rows, int64_t cols, int64_t ldx, const float *shift,
+                            uint8_t *codes, uint8_t *scales, void *y, int64_t ldy, float *tensor_scale,
+                            reqat_tscale_mode ts, void *workspace, void *stream, bool fake) {
+    // same rules as the NVFP4 quantizer (blocks of 16, a tensor scale), plus the shift
+    reqat_status st = check_quant(REQAT_FMT_NVFP4, x, rows, cols, ldx, fake ? y : codes, scales, ldy,
+                                  tensor_scale, ts, workspace, fake);
+    if (st != REQAT_OK) return st;
+    if (shift && (reinterpret_cast<uintptr_t>(shift) & 15u)) return REQAT_E_ALIGN;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const bool compute = ts == REQAT_TS_COMPUTE;
+    if (rows == 0 || cols == 0) {
+        if (compute && launch_unit_scale(tensor_scale, s) != hipSuccess) return REQAT_E_HIP;
+        return REQAT_OK;
+    }
+    hipError_t e = launch_kv4(fake ? kFakeQuant : kCodes, reinterpret_cast<const uint16_t *>(x), rows, cols, ldx,
+                              shift, codes, scales, reinterpret_cast<uint16_t *>(y), ldy, tensor_scale, compute,
+                              reinterpret_cast<uint32_t *>(workspace), s);
+    return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
+}
+
+reqat_status reqat_quantize_kv4(const void *x, int64_t rows, int64_t cols, int64_t ldx, const float *shift,
+                                uint8_t *codes, uint8_t *scales, float *tensor_scale, reqat_tscale_mode ts,
+                                void *workspace, void *stream) {
+    return run_kv4(x, rows, cols, ldx, shift, codes, scales, nullptr, 0, tensor_scale, ts, workspace, stream,
+                   false);
+}
+
+reqat_status reqat_fakequant_kv4(const void *x, int64_t rows, int64_t cols, int64_t ldx, const float *shift,
+                                 void *y, int64_t ldy, float *tensor_scale, reqat_tscale_mode ts, void *workspace,
+                                 void *stream) {
+    return run_kv4(x, rows, cols, ldx, shift, nullptr, nullptr, y, ldy, tensor_scale, ts, workspace, stream, true);
+}
+
 static reqat_status run_rht(const void *x, int64_t rows, int64_t cols, int64_t ldx, uint32_t signs,
                             uint8_t *codes, uint8_t *scales, void *y, int64_t ldy, void *stream, bool fake) {
     reqat_status st = check_quant(REQAT_FMT_MXFP4, x, rows, cols, ldx, fake ? y : codes, scales, ldy,

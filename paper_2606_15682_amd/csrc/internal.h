@@ -48,6 +48,12 @@ hipError_t launch_gemm_w4a16(int64_t M, int64_t N, int64_t K, const uint16_t *x,
                              const uint8_t *w_codes, const uint8_t *w_scales, void *y, bool y_bf16,
                              int64_t ldy, hipStream_t stream);
 
+// KV4 (E1M2 elements, E4M3 block scales of 16, FP32 global scale) of x - shift;
+// `computed` runs the absmax pass into `partials` first (<= kMaxPartials).
+hipError_t launch_kv4(QuantOut out, const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx, const float *shift,
+                      uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy, float *gptr, bool computed,
+                      uint32_t *partials, hipStream_t stream);
+
 bool gemm_tile256_supported(Fmt fmt, int64_t M, int64_t N, int64_t K, int64_t ldy);
 // Skinny product for M <= 64 (K % 64 == 0, K > 0).
 hipError_t launch_gemm_skinny(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *a_codes,

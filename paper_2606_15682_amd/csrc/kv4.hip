@@ -1,0 +1,230 @@
+// KV-cache quantizer for gfx950 (the 4-bit KV cache of the NVFP4 W4A4KV4
+// setting, Sec. 3.3 "Additional implementation details"; Q-FIT's post-RoPE
+// shift, Sec. 3.3, K~ = R(K_pre / s) - m):
+//   d = RN_fp32(x - m[c])                       (m an FP32 vector over channels, optional)
+//   E1M2 elements (magnitudes 0, 0.5, ..., 3.5), an E4M3 scale per 16
+//   channels (the smallest with block_amax <= 3.5 * s * g) and an FP32 global
+//   scale g (given, or the smallest power of two 2^k, k >= -126, with
+//   tensor_amax <= 3.5 * 448 * 2^k), elements rounded to nearest, ties to the
+//   even code; a block with a non-finite d gets scale 0x7F and zero codes.
+// Every decision compares d (FP32, exact in FP64) with products of at most
+// 31 significant bits, so FP64 comparisons decide exactly.
+//
+// One lane per 16-channel block in a grid-stride loop; the shift vector is
+// read with the block (it is small and stays in cache).  A computed g takes
+// two passes: the partial maxima of |d| per workgroup, then the quantizer,
+// whose workgroups fold them.
+#include "fp4_device.h"
+#include "internal.h"
+
+namespace reqat {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kMaxKvGroups = kMaxPartials;
+
+__device__ __forceinline__ uint32_t kv4_wave_max(uint32_t v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint32_t o = __shfl_xor(v, off, 64);
+        v = v > o ? v : o;
+    }
+    return v;
+}
+
+// The 16 shifted values of block `blk` (FP32).
+__device__ __forceinline__ void kv4_load(const uint16_t *__restrict__ x, const float *__restrict__ shift,
+                                         int64_t blk, int64_t nb, int64_t ldx, bool narrow, float (&d)[16]) {
+    const int64_t r = narrow ? (int64_t)((uint32_t)blk / (uint32_t)nb) : blk / nb;
+    const int64_t c0 = (blk - r * nb) * 16;
+    const uint4 *src = reinterpret_cast<const uint4 *>(x + r * ldx + c0);
+    const uint4 a = src[0], b = src[1];
+    const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        d[2 * i] = f32_from_bits(w[i] << 16);
+        d[2 * i + 1] = f32_from_bits(w[i] & 0xFFFF0000u);
+    }
+    if (shift) {
+        const float4 *sp = reinterpret_cast<const float4 *>(shift + c0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float4 m = sp[i];
+            d[4 * i + 0] = d[4 * i + 0] - m.x;
+            d[4 * i + 1] = d[4 * i + 1] - m.y;
+            d[4 * i + 2] = d[4 * i + 2] - m.z;
+            d[4 * i + 3] = d[4 * i + 3] - m.w;
+        }
+    }
+}
+
+// Largest finite |d| over the shifted tensor, one partial per workgroup.
+__global__ __launch_bounds__(kThreads) void kv4_absmax_kernel(const uint16_t *__restrict__ x, int64_t rows,
+                                                              int64_t cols, int64_t ldx,
+                                                              const float *__restrict__ shift,
+                                                              uint32_t *__restrict__ partials) {
+    const int64_t nb = cols / 16, total = rows * nb;
+    const bool narrow = total < (int64_t(1) << 32);
+    uint32_t m = 0;
+    for (int64_t blk = (int64_t)blockIdx.x * kThreads + threadIdx.x; blk < total;
+         blk += (int64_t)gridDim.x * kThreads) {
+        float d[16];
+        kv4_load(x, shift, blk, nb, ldx, narrow, d);
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const uint32_t a = bits_from_f32(d[j]) & 0x7FFFFFFFu;
+            if (a < 0x7F800000u && a > m) m = a;
+        }
+    }
+    __shared__ uint32_t red[kThreads / 64];
+    m = kv4_wave_max(m);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t r = red[0];
+        for (int i = 1; i < kThreads / 64; ++i) r = r > red[i] ? r : red[i];
+        partials[blockIdx.x] = r;
+    }
+}
+
+// Global scale from the FP32 pattern of the tensor amax: smallest 2^k, k >= -126,
+// with amax <= 1568 * 2^k (1568 = 1.53125 * 2^10; 0.53125 = fraction bits 0x440000).
+__device__ __forceinline__ float kv4_global_scale(uint32_t am) {
+    if (am == 0u) return 1.0f;
+    int E;
+    uint32_t frac;
+    if ((am >> 23) != 0u) {
+        E = (int)(am >> 23) - 127;
+        frac = am & 0x7FFFFFu;
+    } else {
+        const int p = 31 - __builtin_clz(am);
+        E = p - 149;
+        frac = (am << (23 - p)) & 0x7FFFFFu;
+    }
+    int k = frac <= 0x440000u ? E - 10 : E - 9;
+    if (k < -126) k = -126;
+    return f32_from_bits((uint32_t)(k + 127) << 23);
+}
+
+// Smallest positive finite E4M3 s with amax <= 3.5 * s * g (0x7E when none).
+__device__ __forceinline__ uint32_t kv4_scale_byte(double a, double g) {
+    uint32_t b = e4m3_ceil_byte(a / (3.5 * g));
+    if (b < 0x7Eu && !(a <= 3.5 * (double)e4m3_value(b) * g)) b += 1u;
+    else if (b > 1u && a <= 3.5 * (double)e4m3_value(b - 1u) * g) b -= 1u;
+    return b;
+}
+
+// E1M2 magnitude code (0..7) of |v| / S, nearest with ties to the even code.
+__device__ __forceinline__ uint32_t e1m2_mag(double a, double S) {
+    uint32_t m = 7u;
+#pragma unroll
+    for (int i = 6; i >= 0; --i) {
+        const double t = (0.5 * i + 0.25) * S;
+        if (a < t || (a == t && (i & 1) == 0)) m = (uint32_t)i;
+    }
+    return m;
+}
+
+template <int OUT>
+__global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
+    const uint16_t *__restrict__ x, int64_t rows, int64_t cols, int64_t ldx, const float *__restrict__ shift,
+    uint8_t *__restrict__ codes, uint8_t *__restrict__ scales, uint16_t *__restrict__ y, int64_t ldy,
+    float *gptr, int computed, const uint32_t *__restrict__ partials, int nparts) {
+    float g;
+    if (computed) {
+        __shared__ uint32_t red[kThreads / 64];
+        uint32_t m = 0;
+        for (int i = threadIdx.x; i < nparts; i += kThreads) {
+            const uint32_t p = partials[i];
+            m = m > p ? m : p;
+        }
+        m = kv4_wave_max(m);
+        if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+        __syncthreads();
+        uint32_t r = red[0];
+#pragma unroll
+        for (int i = 1; i < kThreads / 64; ++i) r = r > red[i] ? r : red[i];
+        g = kv4_global_scale(r);
+        if (blockIdx.x == 0 && threadIdx.x == 0) *gptr = g;
+    } else {
+        g = *gptr;
+    }
+    const double gd = (double)g;
+
+    const int64_t nb = cols / 16, total = rows * nb;
+    const bool narrow = total < (int64_t(1) << 32);
+    for (int64_t blk = (int64_t)blockIdx.x * kThreads + threadIdx.x; blk < total;
+         blk += (int64_t)gridDim.x * kThreads) {
+        float d[16];
+        kv4_load(x, shift, blk, nb, ldx, narrow, d);
+        uint32_t am = 0u;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const uint32_t a = bits_from_f32(d[j]) & 0x7FFFFFFFu;
+            am = am > a ? am : a;
+        }
+        const bool bad = am >= 0x7F800000u;
+        const uint32_t sbyte = bad ? 0x7Fu : (am == 0u ? 0u : kv4_scale_byte((double)f32_from_bits(am), gd));
+        const double S = (double)e4m3_value(sbyte) * gd;
+        uint32_t c[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const uint32_t sign = (bits_from_f32(d[j]) >> 28) & 8u;
+            c[j] = bad ? 0u : (sbyte == 0u ? sign : (e1m2_mag(__builtin_fabs((double)d[j]), S) | sign));
+        }
+        if (OUT == kCodes) {
+            uint32_t lo = 0, hi = 0;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                lo |= c[j] << (4 * j);
+                hi |= c[8 + j] << (4 * j);
+            }
+            *reinterpret_cast<uint2 *>(codes + blk * 8) = make_uint2(lo, hi);
+            scales[blk] = (uint8_t)sbyte;
+        } else {
+            const int64_t r = narrow ? (int64_t)((uint32_t)blk / (uint32_t)nb) : blk / nb;
+            uint32_t o[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                uint32_t h[2];
+#pragma unroll
+                for (int k = 0; k < 2; ++k) {
+                    const uint32_t cc = c[2 * i + k];
+                    const double v = 0.5 * (double)(cc & 7u) * (sbyte == 0u ? 0.0 : S);
+                    h[k] = bad ? 0x7FC0u : (bf16_rne_from_double(v) | ((cc & 8u) << 12));
+                }
+                o[i] = h[0] | (h[1] << 16);
+            }
+            uint4 *dst = reinterpret_cast<uint4 *>(y + r * ldy + (blk - r * nb) * 16);
+            dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
+            dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_kv4(QuantOut out, const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx, const float *shift,
+                      uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy, float *gptr, bool computed,
+                      uint32_t *partials, hipStream_t stream) {
+    const int64_t total = rows * (cols / 16);
+    if (total == 0) return hipSuccess;
+    int64_t grid = (total + kThreads - 1) / kThreads;
+    if (grid > kMaxKvGroups) grid = kMaxKvGroups;
+    if (computed) {
+        hipLaunchKernelGGL(kv4_absmax_kernel, dim3((unsigned)grid), dim3(kThreads), 0, stream, x, rows, cols, ldx,
+                           shift, partials);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (out == kCodes)
+        hipLaunchKernelGGL(kv4_quantize_kernel<kCodes>, dim3((unsigned)grid), dim3(kThreads), 0, stream, x, rows,
+                           cols, ldx, shift, codes, scales, y, ldy, gptr, (int)computed, partials, (int)grid);
+    else
+        hipLaunchKernelGGL(kv4_quantize_kernel<kFakeQuant>, dim3((unsigned)grid), dim3(kThreads), 0, stream, x,
+                           rows, cols, ldx, shift, codes, scales, y, ldy, gptr, (int)computed, partials, (int)grid);
+    return hipGetLastError();
+}
+
+}  // namespace reqat

@@ -43,6 +43,8 @@ SIGNATURES = {
     "reqat_linear_w4a4": (_INT, [_INT, _I64, _I64, _I64, _VP, _I64, _VP, _INT, _VP, _VP, _VP, _VP,
                                  _INT, _I64, _VP, _VP]),
     "reqat_linear_workspace_bytes": (ctypes.c_size_t, [_INT, _I64, _I64]),
+    "reqat_quantize_kv4": (_INT, [_VP, _I64, _I64, _I64, _VP, _VP, _VP, _VP, _INT, _VP, _VP]),
+    "reqat_fakequant_kv4": (_INT, [_VP, _I64, _I64, _I64, _VP, _VP, _I64, _VP, _INT, _VP, _VP]),
     "reqat_gemm_w4a16": (_INT, [_I64, _I64, _I64, _VP, _I64, _VP, _VP, _VP, _INT, _I64, _VP]),
     "reqat_quantize_mxfp4_rht": (_INT, [_VP, _I64, _I64, _I64, ctypes.c_uint32, _VP, _VP, _VP]),
     "reqat_fakequant_mxfp4_rht": (_INT, [_VP, _I64, _I64, _I64, ctypes.c_uint32, _VP, _I64, _VP]),
@@ -99,6 +101,15 @@ def reqat_linear_w4a4(fmt, M, N, K, x, ldx, x_ts, ts, w_codes, w_scales, w_ts, y
                       workspace, stream):
     return load().reqat_linear_w4a4(fmt, M, N, K, x, ldx, x_ts, ts, w_codes, w_scales, w_ts, y,
                                     y_dtype, ldy, workspace, stream)
+
+
+def reqat_quantize_kv4(x, rows, cols, ldx, shift, codes, scales, tensor_scale, ts, workspace, stream):
+    return load().reqat_quantize_kv4(x, rows, cols, ldx, shift, codes, scales, tensor_scale, ts, workspace,
+                                     stream)
+
+
+def reqat_fakequant_kv4(x, rows, cols, ldx, shift, y, ldy, tensor_scale, ts, workspace, stream):
+    return load().reqat_fakequant_kv4(x, rows, cols, ldx, shift, y, ldy, tensor_scale, ts, workspace, stream)
 
 
 def reqat_gemm_w4a16(M, N, K, x, ldx, w_codes, w_scales, y, y_dtype, ldy, stream):
@@ -250,6 +261,44 @@ def gemm(fmt, a_codes, a_scales, a_g, b_codes, b_scales, b_g, out_dtype=torch.fl
                          y.stride(0), _stream(a_codes.device))
     _check(st, "reqat_gemm_w4a4")
     return y
+
+
+def _shift_ptr(shift, cols, device):
+    if shift is None:
+        return None, None
+    if shift.dtype != torch.float32 or shift.numel() != cols or not shift.is_contiguous() \
+            or shift.device != device:
+        raise ValueError("shift must be a contiguous float32 tensor of cols values on the same device")
+    return shift, shift.data_ptr()
+
+
+def quantize_kv4(x: torch.Tensor, shift=None, tensor_scale=None, out=None, g_out=None):
+    """KV4 (E1M2 + E4M3 block scales of 16 + FP32 tensor scale) of x - shift.
+    Returns (codes, scales, g)."""
+    rows, cols, ldx = _x2d(x)
+    if out is not None:
+        codes, scales = out
+    else:
+        codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=x.device)
+        scales = torch.empty((rows, cols // 16), dtype=torch.uint8, device=x.device)
+    g, ts = _gscale(NVFP4, x, tensor_scale, g_out)
+    _, sp = _shift_ptr(shift, cols, x.device)
+    st = reqat_quantize_kv4(x.data_ptr(), rows, cols, ldx, sp, codes.data_ptr(), scales.data_ptr(), _ptr(g), ts,
+                            workspace(x.device).data_ptr(), _stream(x.device))
+    _check(st, "reqat_quantize_kv4")
+    return codes, scales, g
+
+
+def fakequant_kv4(x: torch.Tensor, shift=None, tensor_scale=None, out=None, g_out=None):
+    """bfloat16 quantize-dequantize of x - shift in KV4.  Returns (y, g)."""
+    rows, cols, ldx = _x2d(x)
+    y = out if out is not None else torch.empty((rows, cols), dtype=torch.bfloat16, device=x.device)
+    g, ts = _gscale(NVFP4, x, tensor_scale, g_out)
+    _, sp = _shift_ptr(shift, cols, x.device)
+    st = reqat_fakequant_kv4(x.data_ptr(), rows, cols, ldx, sp, y.data_ptr(), y.stride(0), _ptr(g), ts,
+                             workspace(x.device).data_ptr(), _stream(x.device))
+    _check(st, "reqat_fakequant_kv4")
+    return y, g
 
 
 def gemm_w4a16(x: torch.Tensor, w_codes, w_scales, out_dtype=torch.float32, out=None):

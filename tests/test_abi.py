@@ -34,6 +34,7 @@ def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ("reqat_quantize_fp4", "reqat_fakequant_fp4", "reqat_gemm_w4a4",
               "reqat_quantize_mxfp4_rht", "reqat_fakequant_mxfp4_rht", "reqat_gemm_w4a16",
+              "reqat_quantize_kv4", "reqat_fakequant_kv4",
               "reqat_workspace_bytes", "reqat_status_str", "reqat_abi_version"):
         assert n in names
     assert set(names) == set(reqat.SIGNATURES), "binding and header disagree"
@@ -49,7 +50,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_small_queries(lib):
-    assert reqat.reqat_abi_version() == 4
+    assert reqat.reqat_abi_version() == 5
     assert reqat.reqat_workspace_bytes() == 4 * 4096 + 2 * (1 << 19)   # partials + segment table
     for s in range(7):
         assert reqat.reqat_status_str(s).startswith(reqat.STATUS[s])
@@ -122,6 +123,17 @@ def test_w4a16_validation(lib):
     assert g16(y=None) == E_NULL and g16(x=None) == E_NULL and g16(wc=None) == E_NULL and g16(ws=None) == E_NULL
     assert g16(x=P + 2) == E_ALIGN and g16(ldx=132) == E_ALIGN and g16(wc=P + 8) == E_ALIGN
     assert g16(y=P + 2) == E_ALIGN and g16(y=P + 1, dt=1) == E_ALIGN
+
+
+def test_kv4_validation(lib):
+    kq = lambda x=P, rows=4, cols=64, ldx=64, sh=None, c=P, s=P, ts_ptr=P, ts=0, ws=P: reqat.reqat_quantize_kv4(
+        x, rows, cols, ldx, sh, c, s, ts_ptr, ts, ws, None)
+    kf = lambda y=P, ldy=64, sh=P, ts=1: reqat.reqat_fakequant_kv4(P, 4, 64, 64, sh, y, ldy, P, ts, None, None)
+    assert kq(ts=3) == E_ENUM
+    assert kq(cols=40, ldx=40) == E_SHAPE and kq(ldx=32) == E_SHAPE
+    assert kq(ts_ptr=None) == E_NULL and kq(ws=None) == E_NULL and kq(c=None) == E_NULL
+    assert kq(sh=P + 4) == E_ALIGN and kq(x=P + 2) == E_ALIGN and kq(ldx=68) == E_ALIGN
+    assert kf(ldy=32) == E_SHAPE and kf(y=None) == E_NULL and kf(sh=P + 8) == E_ALIGN
 
 
 def test_gemm_validation(lib):

@@ -163,3 +163,18 @@ def test_fullsize_w4a16_decode(idx):
     ref, aref = oracle.gemm_w4a16_points(xb, wc, ws, ms, ns)
     got = y.cpu().numpy().astype(np.float64)[ms, ns]
     assert float(np.max(np.abs(got - ref) / np.maximum(aref, 1e-300))) <= 1e-3
+
+
+def test_fullsize_kv4_keys():
+    """KV4 of the prefill keys of a 14B-like layer (4096 tokens x 8 KV heads x 128
+    channels, Gaussian with outlier channels) with a calibrated channel shift,
+    bit-exact against the oracle over the whole tensor."""
+    w = wl.WORKLOADS[4]
+    log("full-size kv4 keys 4096 x 1024")
+    kb = wl.bf16_bits(wl.make_x(w))[:, :1024].copy()
+    shift = np.random.default_rng(21).normal(0.0, 0.5, 1024).astype(np.float32)
+    oc, os_, og = oracle.kv4_quantize(kb, shift)
+    c, s, g = reqat.quantize_kv4(wl.from_bits(kb).to(DEV), torch.from_numpy(shift).to(DEV))
+    torch.cuda.synchronize()
+    assert float(g.cpu()[0]) == np.float32(og)
+    assert np.array_equal(s.cpu().numpy(), os_) and np.array_equal(c.cpu().numpy(), oc)

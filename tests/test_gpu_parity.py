@@ -196,6 +196,80 @@ def test_rotated_mxfp4_tiny_and_strided():
     assert_rht_parity(_rand(45, 320, 9, "normal"), 0x2468ACE0, ldx_pad=40)
 
 
+# ------------------------------------------------------------------ KV4
+
+def assert_kv4_parity(xb, shift=None, g=None, ldx_pad=0):
+    R, C = xb.shape
+    oc, os_, og = oracle.kv4_quantize(xb, shift, g)
+    oy, _ = oracle.kv4_fakequant(xb, shift, g)
+    if ldx_pad:
+        big = np.zeros((R, C + ldx_pad), np.uint16)
+        big[:, :C] = xb
+        xt = wl.from_bits(big).to(DEV)[:, :C]
+    else:
+        xt = wl.from_bits(xb).to(DEV)
+    sh = None if shift is None else torch.from_numpy(np.ascontiguousarray(shift, np.float32)).to(DEV)
+    gt = None if g is None else torch.tensor([g], dtype=torch.float32, device=DEV)
+    for poison in (0x00, 0xFF):
+        codes = torch.full((R, C // 2), poison, dtype=torch.uint8, device=DEV)
+        scales = torch.full((R, C // 16), poison, dtype=torch.uint8, device=DEV)
+        _, _, gg = reqat.quantize_kv4(xt, sh, tensor_scale=gt, out=(codes, scales))
+        torch.cuda.synchronize()
+        assert float(gg.cpu()[0]) == np.float32(og)
+        s_, c_ = scales.cpu().numpy(), codes.cpu().numpy()
+        bad = np.argwhere(s_ != os_)
+        assert bad.size == 0, ("kv4 scales differ", bad[:4], s_[tuple(bad[0])], os_[tuple(bad[0])])
+        bad = np.argwhere(c_ != oc)
+        assert bad.size == 0, ("kv4 codes differ", bad[:4], c_[tuple(bad[0])], oc[tuple(bad[0])])
+    y = wl.from_bits(np.full((R, C), 0x7FFF, np.uint16)).to(DEV)
+    reqat.fakequant_kv4(xt, sh, tensor_scale=gt, out=y)
+    torch.cuda.synchronize()
+    yb = wl.bf16_bits(y.cpu())
+    bad = np.argwhere(yb != oy)
+    assert bad.size == 0, ("kv4 fake-quant differs", bad[:4], hex(yb[tuple(bad[0])]), hex(oy[tuple(bad[0])]))
+
+
+@pytest.mark.parametrize("shape", [(16, 1024), (37, 96), (1, 16), (300, 512)])
+@pytest.mark.parametrize("shifted", [False, True])
+def test_kv4_parity_random(shape, shifted):
+    R, C = shape
+    log("kv4 parity shape=%s shifted=%s" % (shape, shifted))
+    xb = _rand(R, C, 500 + R + C, "normal", outliers=max(1, C // 64))
+    shift = np.random.default_rng(R + C).normal(0.0, 1.5, C).astype(np.float32) if shifted else None
+    assert_kv4_parity(xb, shift)
+    assert_kv4_parity(xb, shift, g=0.0123456789)
+    assert_kv4_parity(xb, shift, g=2.0 ** -6)
+
+
+def test_kv4_exhaustive_patterns_and_specials():
+    log("kv4 exhaustive bf16 patterns with a shift, specials, strided rows")
+    pats = np.random.default_rng(13).permutation(np.arange(65536, dtype=np.uint16)).reshape(64, 1024)
+    shift = np.random.default_rng(14).normal(0.0, 3.0, 1024).astype(np.float32)
+    shift[::7] = 0.0
+    assert_kv4_parity(pats, None)
+    assert_kv4_parity(pats, shift)
+    x = np.zeros((5, 32), np.uint16)
+    x[0, 3] = 0x7FC0
+    x[1, :] = 0x8000
+    x[2, :16] = 0x7F7F
+    x[3, 16:] = 0x0001
+    x[4, :] = 0x3F80
+    sh = np.zeros(32, np.float32)
+    sh[:16] = -3.0e38                     # 0x7F7F - (-3e38) overflows FP32: a NaN block
+    assert_kv4_parity(x, sh)
+    assert_kv4_parity(x, None, g=2.0 ** -12)          # caller's g too small: 448 and saturation
+    assert_kv4_parity(_rand(45, 320, 19, "student_t"), np.linspace(-2, 2, 320).astype(np.float32), ldx_pad=24)
+
+
+def test_kv4_empty_writes_unit_scale():
+    log("kv4 empty")
+    x = torch.empty((0, 128), dtype=torch.bfloat16, device=DEV)
+    _, _, g = reqat.quantize_kv4(x, out=(torch.empty((0, 64), dtype=torch.uint8, device=DEV),
+                                         torch.empty((0, 8), dtype=torch.uint8, device=DEV)))
+    torch.cuda.synchronize()
+    assert float(g.cpu()[0]) == 1.0
+
+
 @pytest.mark.parametrize("fmt", [NV, MX])
 def test_strided_rows(fmt):
     log("strided rows fmt=%d" % fmt)
