@@ -381,3 +381,65 @@ def kv4_fakequant(x: np.ndarray, shift=None, g: float | None = None):
                                   _p(y, ctypes.c_uint16), C)
     assert rc == 0
     return y, g
+
+
+# ------------------------------------------------- SEM loss (QAT training side)
+
+def sem_row_stats(logits_bits: np.ndarray, targets: np.ndarray):
+    """Per token t (one row of bfloat16 logits over the vocabulary): the
+    predictive entropy H_t = -sum_j p_j log p_j, the SFT term NLL_t =
+    -log p_{y_t}, and log-sum-exp, with p = softmax(logits) (Sec. 3.2, the
+    token-level entropy of Sec. 2 and the SFT objective), in FP64."""
+    z = _bf16_rows_f64(logits_bits)
+    m = z.max(axis=1, keepdims=True)
+    e = np.exp(z - m)
+    S = e.sum(axis=1, keepdims=True)
+    logp = (z - m) - np.log(S)
+    p = e / S
+    H = -(p * logp).sum(axis=1)
+    t = np.asarray(targets, np.int64)
+    nll = -logp[np.arange(z.shape[0]), t]
+    lse = (m + np.log(S))[:, 0]
+    return H, nll, lse
+
+
+def _bf16_rows_f64(bits: np.ndarray) -> np.ndarray:
+    b = np.ascontiguousarray(bits, np.uint16)
+    return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def sem_weights(H: np.ndarray, eps: float) -> np.ndarray:
+    """Soft weights of SEM (Sec. 3.2): w_t = max(0, 1 - (H_t - H_min) / (tau - H_min + eps)),
+    H_min the minibatch minimum and tau its 75th percentile (linear interpolation
+    between order statistics at position 0.75 (T - 1))."""
+    H = np.asarray(H, np.float64)
+    hs = np.sort(H)
+    q = 0.75 * (len(H) - 1)
+    lo = int(np.floor(q))
+    hi = min(lo + 1, len(H) - 1)
+    tau = hs[lo] + (q - lo) * (hs[hi] - hs[lo])
+    hmin = hs[0]
+    return np.maximum(0.0, 1.0 - (H - hmin) / (tau - hmin + eps)), tau, hmin
+
+
+def sem_loss(H, nll, lam: float, eps: float):
+    """L_SEM = mean_t NLL_t + lam * (1/T) sum_t w_t H_t (Sec. 3.2).  Returns
+    (L, L_SFT, L_ent, w)."""
+    w, _, _ = sem_weights(H, eps)
+    T = len(H)
+    l_sft = float(np.sum(nll)) / T
+    l_ent = float(np.sum(w * np.asarray(H, np.float64))) / T
+    return l_sft + lam * l_ent, l_sft, l_ent, w
+
+
+def sem_grad(logits_bits, targets, H, lse, w, lam: float, scale: float = 1.0):
+    """dL/dlogits with the weights held fixed:
+    (scale / T) * [(p - onehot(y)) - lam * w_t * p * (log p + H_t)]."""
+    z = _bf16_rows_f64(logits_bits)
+    T = z.shape[0]
+    logp = z - np.asarray(lse, np.float64)[:, None]
+    p = np.exp(logp)
+    g = p.copy()
+    g[np.arange(T), np.asarray(targets, np.int64)] -= 1.0
+    g -= lam * np.asarray(w, np.float64)[:, None] * p * (logp + np.asarray(H, np.float64)[:, None])
+    return g * (scale / T)
