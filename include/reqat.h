@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define REQAT_ABI_VERSION 5
+#define REQAT_ABI_VERSION 6
 
 typedef enum {
     REQAT_FMT_NVFP4 = 0, /* B = 16, E4M3 block scale, FP32 global scale */
@@ -199,6 +199,40 @@ reqat_status reqat_quantize_kv4(const void *x, int64_t rows, int64_t cols, int64
 reqat_status reqat_fakequant_kv4(const void *x, int64_t rows, int64_t cols, int64_t ldx, const float *shift,
                                  void *y, int64_t ldy, float *tensor_scale, reqat_tscale_mode ts, void *workspace,
                                  void *stream);
+
+/*
+ * SEM loss, the training objective of ReQAT's TAQ stage (Sec. 3.2):
+ *     L = (1/T) sum_t NLL_t + lambda (1/T) sum_t w_t H_t,
+ *     w_t = max(0, 1 - (H_t - H_min) / (tau - H_min + eps)),
+ * with, per token t (a row of bfloat16 logits over the vocabulary, p its
+ * softmax), the predictive entropy H_t = -sum_j p_j log p_j and
+ * NLL_t = -log p_{y_t}; H_min the minimum of H over the T tokens and tau its
+ * 75th percentile (linear interpolation between order statistics at
+ * position 0.75 (T - 1)).  Computed in FP32 (sums of the weighted terms in
+ * FP64).  The logits are read once.
+ *   logits [T][ld] bfloat16 (finite; 16-byte aligned, ld % 8 == 0, V % 8 == 0);
+ *   targets [T] int32 in [0, V) (outside: NLL_t = NaN, no read);
+ *   stats [T][4] FP32 out: H_t, NLL_t, log-sum-exp_t, 0 (kept for the backward);
+ *   weights [T] FP32 out: w_t;  loss [4] FP32 out: L, mean NLL, mean w H, tau.
+ * T == 0 is a no-op.
+ */
+reqat_status reqat_sem_loss(const void *logits, int64_t T, int64_t V, int64_t ld, const int32_t *targets,
+                            float lambda, float eps, float *stats, float *weights, float *loss, void *stream);
+
+/*
+ * Gradient of the SEM loss with the weights w_t held fixed (they select
+ * tokens, they are not optimized):
+ *     dL/dz_tj = (scale / T) [(p_tj - [j == y_t]) - lambda w_t p_tj (log p_tj + H_t)],
+ * using stats and weights from reqat_sem_loss on the same logits.  With the
+ * quantizers' straight-through estimator (ReQAT's QAT forward quantizes with
+ * fake-quant; every scale rule here is "ceil", so nothing clips and the
+ * estimator passes the gradient through unchanged) this is the whole backward
+ * of the loss head.  grad [T][ldg] of grad_dtype (16-byte aligned; ldg >= V,
+ * a multiple of 8 for bfloat16, 4 for FP32).
+ */
+reqat_status reqat_sem_loss_backward(const void *logits, int64_t T, int64_t V, int64_t ld, const int32_t *targets,
+                                     const float *stats, const float *weights, float lambda, float scale,
+                                     void *grad, reqat_dtype grad_dtype, int64_t ldg, void *stream);
 
 /*
  * Block-scaled FP4 x FP4 product (the W4A4 GEMM of Sec. 5.3):

@@ -12,7 +12,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libreqat.so")
-SOURCES = ["api.hip", "quantize.hip", "gemm.hip", "gemm_skinny.hip", "gemm_tile256.hip", "gemm_w4a16.hip", "kv4.hip"]
+SOURCES = ["api.hip", "quantize.hip", "gemm.hip", "gemm_skinny.hip", "gemm_tile256.hip", "gemm_w4a16.hip", "kv4.hip", "sem.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

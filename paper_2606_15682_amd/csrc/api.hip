@@ -189,6 +189,41 @@ reqat_status reqat_gemm_w4a16(int64_t M, int64_t N, int64_t K, const void *x, in
     return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
 }
 
+reqat_status reqat_sem_loss(const void *logits, int64_t T, int64_t V, int64_t ld, const int32_t *targets,
+                            float lambda, float eps, float *stats, float *weights, float *loss, void *stream) {
+    if (T < 0 || V <= 0 || V % 8 || ld < V) return REQAT_E_SHAPE;
+    if (T > 0x7FFFFFFF) return REQAT_E_SHAPE;
+    if (!loss) return REQAT_E_NULL;
+    if (T > 0 && (!logits || !targets || !stats || !weights)) return REQAT_E_NULL;
+    if (T > 0 && (!aligned16(logits) || ld % 8)) return REQAT_E_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(stats) | reinterpret_cast<uintptr_t>(weights) |
+         reinterpret_cast<uintptr_t>(loss) | reinterpret_cast<uintptr_t>(targets)) & 3u)
+        return REQAT_E_ALIGN;
+    if (T == 0) return REQAT_OK;
+    hipError_t e = launch_sem_forward(reinterpret_cast<const uint16_t *>(logits), T, V, ld, targets, lambda, eps,
+                                      stats, weights, loss, reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
+}
+
+reqat_status reqat_sem_loss_backward(const void *logits, int64_t T, int64_t V, int64_t ld, const int32_t *targets,
+                                     const float *stats, const float *weights, float lambda, float scale,
+                                     void *grad, reqat_dtype grad_dtype, int64_t ldg, void *stream) {
+    if (grad_dtype != REQAT_DT_F32 && grad_dtype != REQAT_DT_BF16) return REQAT_E_ENUM;
+    if (T < 0 || V <= 0 || V % 8 || ld < V || ldg < V) return REQAT_E_SHAPE;
+    if (T > 0x7FFFFFFF) return REQAT_E_SHAPE;
+    if (T == 0) return REQAT_OK;
+    if (!logits || !targets || !stats || !weights || !grad) return REQAT_E_NULL;
+    if (!aligned16(logits) || ld % 8 || !aligned16(grad) || ldg % (grad_dtype == REQAT_DT_BF16 ? 8 : 4))
+        return REQAT_E_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(stats) | reinterpret_cast<uintptr_t>(weights) |
+         reinterpret_cast<uintptr_t>(targets)) & 3u)
+        return REQAT_E_ALIGN;
+    hipError_t e = launch_sem_backward(reinterpret_cast<const uint16_t *>(logits), T, V, ld, targets, stats, weights,
+                                       lambda, scale, grad, grad_dtype == REQAT_DT_BF16, ldg,
+                                       reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
+}
+
 size_t reqat_workspace_bytes(void) {
     return sizeof(uint32_t) * kMaxPartials + sizeof(uint16_t) * kMaxSegments;
 }

@@ -54,6 +54,15 @@ hipError_t launch_kv4(QuantOut out, const uint16_t *x, int64_t rows, int64_t col
                       uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy, float *gptr, bool computed,
                       uint32_t *partials, hipStream_t stream);
 
+// SEM loss: per-row statistics ([T][4]: H, NLL, lse, 0), weights [T], loss[4]
+// (L, L_SFT, L_ent, tau); backward writes dL/dlogits.  V % 8 == 0.
+hipError_t launch_sem_forward(const uint16_t *logits, int64_t T, int64_t V, int64_t ld, const int32_t *targets,
+                              float lambda, float eps, float *stats, float *weights, float *loss,
+                              hipStream_t stream);
+hipError_t launch_sem_backward(const uint16_t *logits, int64_t T, int64_t V, int64_t ld, const int32_t *targets,
+                               const float *stats, const float *weights, float lambda, float scale, void *grad,
+                               bool grad_bf16, int64_t ldg, hipStream_t stream);
+
 bool gemm_tile256_supported(Fmt fmt, int64_t M, int64_t N, int64_t K, int64_t ldy);
 // Skinny product for M <= 64 (K % 64 == 0, K > 0).
 hipError_t launch_gemm_skinny(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *a_codes,

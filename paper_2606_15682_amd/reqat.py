@@ -43,6 +43,9 @@ SIGNATURES = {
     "reqat_linear_w4a4": (_INT, [_INT, _I64, _I64, _I64, _VP, _I64, _VP, _INT, _VP, _VP, _VP, _VP,
                                  _INT, _I64, _VP, _VP]),
     "reqat_linear_workspace_bytes": (ctypes.c_size_t, [_INT, _I64, _I64]),
+    "reqat_sem_loss": (_INT, [_VP, _I64, _I64, _I64, _VP, ctypes.c_float, ctypes.c_float, _VP, _VP, _VP, _VP]),
+    "reqat_sem_loss_backward": (_INT, [_VP, _I64, _I64, _I64, _VP, _VP, _VP, ctypes.c_float, ctypes.c_float,
+                                       _VP, _INT, _I64, _VP]),
     "reqat_quantize_kv4": (_INT, [_VP, _I64, _I64, _I64, _VP, _VP, _VP, _VP, _INT, _VP, _VP]),
     "reqat_fakequant_kv4": (_INT, [_VP, _I64, _I64, _I64, _VP, _VP, _I64, _VP, _INT, _VP, _VP]),
     "reqat_gemm_w4a16": (_INT, [_I64, _I64, _I64, _VP, _I64, _VP, _VP, _VP, _INT, _I64, _VP]),
@@ -101,6 +104,15 @@ def reqat_linear_w4a4(fmt, M, N, K, x, ldx, x_ts, ts, w_codes, w_scales, w_ts, y
                       workspace, stream):
     return load().reqat_linear_w4a4(fmt, M, N, K, x, ldx, x_ts, ts, w_codes, w_scales, w_ts, y,
                                     y_dtype, ldy, workspace, stream)
+
+
+def reqat_sem_loss(logits, T, V, ld, targets, lam, eps, stats, weights, loss, stream):
+    return load().reqat_sem_loss(logits, T, V, ld, targets, lam, eps, stats, weights, loss, stream)
+
+
+def reqat_sem_loss_backward(logits, T, V, ld, targets, stats, weights, lam, scale, grad, grad_dtype, ldg, stream):
+    return load().reqat_sem_loss_backward(logits, T, V, ld, targets, stats, weights, lam, scale, grad, grad_dtype,
+                                          ldg, stream)
 
 
 def reqat_quantize_kv4(x, rows, cols, ldx, shift, codes, scales, tensor_scale, ts, workspace, stream):
@@ -334,3 +346,65 @@ def linear(x: torch.Tensor, fmt, w_codes, w_scales, w_g, x_tensor_scale=None, ou
                            _stream(x.device))
     _check(st, "reqat_linear_w4a4")
     return y, g
+
+
+# ------------------------------------------------------------------ QAT training side
+
+def sem_loss(logits: torch.Tensor, targets: torch.Tensor, lam: float, eps: float = 1e-6):
+    """SEM loss of bfloat16 logits [T, V] and int32 targets [T].  Returns
+    (loss[4] = L, mean NLL, mean w H, tau; stats [T, 4]; weights [T])."""
+    T, V, ld = _x2d(logits)
+    if targets.dtype != torch.int32 or targets.numel() != T or not targets.is_contiguous():
+        raise TypeError("targets must be a contiguous int32 tensor of T entries")
+    stats = torch.empty((T, 4), dtype=torch.float32, device=logits.device)
+    weights = torch.empty(T, dtype=torch.float32, device=logits.device)
+    loss = torch.zeros(4, dtype=torch.float32, device=logits.device)
+    st = reqat_sem_loss(logits.data_ptr(), T, V, ld, targets.data_ptr(), lam, eps, stats.data_ptr(),
+                        weights.data_ptr(), loss.data_ptr(), _stream(logits.device))
+    _check(st, "reqat_sem_loss")
+    return loss, stats, weights
+
+
+def sem_loss_backward(logits, targets, stats, weights, lam: float, scale: float = 1.0, out_dtype=torch.bfloat16,
+                      out=None):
+    """dL/dlogits (weights held fixed) as out_dtype [T, V]."""
+    T, V, ld = _x2d(logits)
+    dt = DT_F32 if out_dtype == torch.float32 else DT_BF16
+    g = out if out is not None else torch.empty((T, V), dtype=out_dtype, device=logits.device)
+    st = reqat_sem_loss_backward(logits.data_ptr(), T, V, ld, targets.data_ptr(), stats.data_ptr(),
+                                 weights.data_ptr(), lam, scale, g.data_ptr(), dt, g.stride(0),
+                                 _stream(logits.device))
+    _check(st, "reqat_sem_loss_backward")
+    return g
+
+
+class FakeQuantSTE(torch.autograd.Function):
+    """QAT forward = fake-quant (bfloat16 in, bfloat16 out); backward = the
+    straight-through estimator.  Under the ceil scale rules no element clips,
+    so the estimator is the identity on the incoming gradient."""
+
+    @staticmethod
+    def forward(ctx, x, fmt=NVFP4):
+        y, _ = fakequant(x.contiguous(), fmt)
+        return y
+
+    @staticmethod
+    def backward(ctx, gy):
+        return gy, None
+
+
+class SemLoss(torch.autograd.Function):
+    """The SEM loss as an autograd function over bfloat16 logits."""
+
+    @staticmethod
+    def forward(ctx, logits, targets, lam, eps=1e-6):
+        loss, stats, weights = sem_loss(logits, targets, lam, eps)
+        ctx.save_for_backward(logits, targets, stats, weights)
+        ctx.lam = lam
+        return loss[0]
+
+    @staticmethod
+    def backward(ctx, g):
+        logits, targets, stats, weights = ctx.saved_tensors
+        grad = sem_loss_backward(logits, targets, stats, weights, ctx.lam, scale=float(g), out_dtype=logits.dtype)
+        return grad, None, None, None

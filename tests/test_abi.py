@@ -34,7 +34,7 @@ def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ("reqat_quantize_fp4", "reqat_fakequant_fp4", "reqat_gemm_w4a4",
               "reqat_quantize_mxfp4_rht", "reqat_fakequant_mxfp4_rht", "reqat_gemm_w4a16",
-              "reqat_quantize_kv4", "reqat_fakequant_kv4",
+              "reqat_quantize_kv4", "reqat_fakequant_kv4", "reqat_sem_loss", "reqat_sem_loss_backward",
               "reqat_workspace_bytes", "reqat_status_str", "reqat_abi_version"):
         assert n in names
     assert set(names) == set(reqat.SIGNATURES), "binding and header disagree"
@@ -50,7 +50,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_small_queries(lib):
-    assert reqat.reqat_abi_version() == 5
+    assert reqat.reqat_abi_version() == 6
     assert reqat.reqat_workspace_bytes() == 4 * 4096 + 2 * (1 << 19)   # partials + segment table
     for s in range(7):
         assert reqat.reqat_status_str(s).startswith(reqat.STATUS[s])
@@ -134,6 +134,19 @@ def test_kv4_validation(lib):
     assert kq(ts_ptr=None) == E_NULL and kq(ws=None) == E_NULL and kq(c=None) == E_NULL
     assert kq(sh=P + 4) == E_ALIGN and kq(x=P + 2) == E_ALIGN and kq(ldx=68) == E_ALIGN
     assert kf(ldy=32) == E_SHAPE and kf(y=None) == E_NULL and kf(sh=P + 8) == E_ALIGN
+
+
+def test_sem_validation(lib):
+    sl = lambda T=4, V=64, ld=64, lg=P, tg=P, st=P, w=P, loss=P: reqat.reqat_sem_loss(
+        lg, T, V, ld, tg, 0.1, 1e-6, st, w, loss, None)
+    sb = lambda T=4, V=64, ld=64, g=P, dt=1, ldg=64: reqat.reqat_sem_loss_backward(
+        P, T, V, ld, P, P, P, 0.1, 1.0, g, dt, ldg, None)
+    assert sl(T=-1) == E_SHAPE and sl(V=60, ld=60) == E_SHAPE and sl(ld=32) == E_SHAPE and sl(V=0) == E_SHAPE
+    assert sl(loss=None) == E_NULL and sl(lg=None) == E_NULL and sl(tg=None) == E_NULL
+    assert sl(lg=P + 2) == E_ALIGN and sl(ld=68) == E_ALIGN and sl(st=P + 2) == E_ALIGN
+    assert sl(T=0, lg=None, tg=None, st=None, w=None) == 0
+    assert sb(dt=7) == E_ENUM and sb(ldg=32) == E_SHAPE and sb(g=None) == E_NULL
+    assert sb(g=P + 4) == E_ALIGN and sb(ldg=68) == E_ALIGN and sb(dt=0, ldg=66) == E_ALIGN
 
 
 def test_gemm_validation(lib):

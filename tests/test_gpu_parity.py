@@ -270,6 +270,77 @@ def test_kv4_empty_writes_unit_scale():
     assert float(g.cpu()[0]) == 1.0
 
 
+# ------------------------------------------------------------------ SEM loss
+
+def run_sem_case(T, V, seed, lam=0.5, eps=1e-6, std=3.0):
+    rng = np.random.default_rng(seed)
+    zb = indep.to_bf16_bits(rng.normal(0.0, std, (T, V)))
+    tg = rng.integers(0, V, T).astype(np.int32)
+    H, nll, lse = oracle.sem_row_stats(zb, tg)
+    L, l_sft, l_ent, w = oracle.sem_loss(H, nll, lam, eps)
+    zt = wl.from_bits(zb).to(DEV)
+    tt = torch.from_numpy(tg).to(DEV)
+    loss, stats, weights = reqat.sem_loss(zt, tt, lam, eps)
+    torch.cuda.synchronize()
+    st = stats.cpu().numpy().astype(np.float64)
+    # FP32 sums of about V / 256 terms per thread and exp2 of arguments rounded
+    # once: errors of order 1e-6; the bounds below leave two orders of margin
+    for got, ref in ((st[:, 0], H), (st[:, 1], nll), (st[:, 2], lse)):
+        assert np.all(np.abs(got - ref) <= 1e-4 * (1 + np.abs(ref))), float(np.max(np.abs(got - ref)))
+    wg = weights.cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(wg - w) <= 1e-3), float(np.max(np.abs(wg - w)))
+    lg = loss.cpu().numpy().astype(np.float64)
+    for got, ref in ((lg[0], L), (lg[1], l_sft), (lg[2], l_ent)):
+        assert abs(got - ref) <= 1e-4 * (1 + abs(ref)), (got, ref)
+    # backward, with the GPU's own weights (the weights are an input of the gradient)
+    gref = oracle.sem_grad(zb, tg, H, lse, wg, lam, scale=1.0)
+    z = indep.bf16_values(zb)
+    p = np.exp(z - lse[:, None])
+    logp = z - lse[:, None]
+    size = (p + lam * wg[:, None] * p * (np.abs(logp) + H[:, None])) / T
+    size[np.arange(T), tg] += 1.0 / T
+    for dt, ulp in ((torch.float32, 0.0), (torch.bfloat16, 2.0 ** -8)):
+        g = reqat.sem_loss_backward(zt, tt, stats, weights, lam, 1.0, out_dtype=dt)
+        torch.cuda.synchronize()
+        gg = g.float().cpu().numpy().astype(np.float64)
+        err = np.abs(gg - gref)
+        assert np.all(err <= 2e-3 * size + ulp * np.abs(gref) + 1e-30), float(np.max(err / (size + 1e-30)))
+
+
+@pytest.mark.parametrize("T,V", [(1, 64), (7, 1000), (64, 4096), (300, 2048), (4, 152064)])
+def test_sem_loss_parity(T, V):
+    log("sem loss T=%d V=%d" % (T, V))
+    run_sem_case(T, V, T + V)
+
+
+def test_sem_loss_low_entropy_rows():
+    log("sem loss with near-deterministic rows")
+    run_sem_case(33, 1024, 7, std=12.0)           # peaked softmax rows: entropies near zero
+
+
+def test_qat_autograd_functions():
+    """The QAT forward (fake-quant) with the straight-through backward, and the
+    SEM loss as an autograd function: gradients reach the inputs unchanged /
+    as the backward kernel computes them."""
+    log("QAT autograd: fake-quant STE and SEM loss")
+    x = wl.from_bits(_rand(8, 64, 71, "normal")).to(DEV).requires_grad_(True)
+    y = reqat.FakeQuantSTE.apply(x, NV)
+    oy, _ = oracle.fakequant(NV, wl.bf16_bits(x.detach().cpu()))
+    assert np.array_equal(wl.bf16_bits(y.detach().cpu()), oy)
+    gy = torch.randn_like(y)
+    y.backward(gy)
+    assert torch.equal(x.grad, gy)
+    rng = np.random.default_rng(72)
+    z = wl.from_bits(indep.to_bf16_bits(rng.normal(0, 2, (16, 512)))).to(DEV).requires_grad_(True)
+    t = torch.from_numpy(rng.integers(0, 512, 16).astype(np.int32)).to(DEV)
+    loss = reqat.SemLoss.apply(z, t, 0.5)
+    loss.backward()
+    _, stats, weights = reqat.sem_loss(z.detach(), t, 0.5)
+    g = reqat.sem_loss_backward(z.detach(), t, stats, weights, 0.5, 1.0, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert torch.equal(z.grad, g)
+
+
 @pytest.mark.parametrize("fmt", [NV, MX])
 def test_strided_rows(fmt):
     log("strided rows fmt=%d" % fmt)
