@@ -68,7 +68,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=4,
-                    help="workload number (4 = 14B gate/up; 6, 7 = MXFP4 W4A16 decode)")
+                    help="workload number (4 = 14B gate/up; 6, 7 = MXFP4 W4A16 decode; 8 = SEM loss head)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes --steps times "
@@ -194,6 +194,88 @@ def bench_w4a16(args, w):
     print(json.dumps(out), flush=True)
 
 
+def bench_sem(args, w):
+    """QAT loss head: SEM loss forward and backward (bfloat16 gradient) over
+    T x V bfloat16 logits.  Bound by HBM: the logits are read twice and the
+    gradient written once."""
+    import numpy as np
+    import torch
+
+    from paper_2606_15682_amd import reqat
+    from paper_2606_15682_amd import workloads as wl
+
+    reqat.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    T, V = w.M, w.N
+    z_cpu, t_cpu = wl.make_logits(w)
+    z, t = z_cpu.to(dev), t_cpu.to(dev)
+    grad = torch.empty_like(z)
+    lam = 0.5
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        loss, stats, weights = reqat.sem_loss(z, t, lam)
+        if ev is not None:
+            ev[1].record()
+        reqat.sem_loss_backward(z, t, stats, weights, lam, 1.0, out_dtype=torch.bfloat16, out=grad)
+        if ev is not None:
+            ev[2].record()
+
+    for _ in range(args.warmup):
+        step()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    fwd = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
+    bwd = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
+    b_fwd, b_bwd = T * V * 2.0, T * V * 4.0
+    gbs_bwd = b_bwd / (bwd * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round((b_fwd + b_bwd) / (ms_step * 1e-3) / 1e9, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded; logits N(0, 3) in bfloat16, uniform targets)",
+        "config": {"workload": w.name, "tokens": T, "vocab": V, "global_batch": T, "parallelism": "single GPU",
+                   "step": "SEM loss forward + backward (bfloat16 gradient)"},
+        "roofline": {"bound": "hbm", "achieved": round(gbs_bwd, 1), "peak": PEAK["hbm"], "unit": "GB/s",
+                     "frac": round(gbs_bwd / PEAK["hbm"], 4), "traffic": None,
+                     "kernel": "sem_backward_kernel (reads T*V*2 B of logits, writes T*V*2 B of gradient)"},
+        "kernels": {"sem_forward": {"ms": round(fwd, 4), "GB/s": round(b_fwd / (fwd * 1e-3) / 1e9, 1)},
+                    "sem_backward": {"ms": round(bwd, 4), "GB/s": round(gbs_bwd, 1)}},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        rows = 64
+        zb = wl.bf16_bits(z_cpu[:rows])
+        t0 = time.perf_counter()
+        n = 0
+        while time.perf_counter() - t0 < 10.0:
+            H, nll, lse = oracle.sem_row_stats(zb, t_cpu[:rows].numpy())
+            _, _, _, wts = oracle.sem_loss(H, nll, lam, 1e-6)
+            oracle.sem_grad(zb, t_cpu[:rows].numpy(), H, lse, wts, lam)
+            n += 1
+        dt = (time.perf_counter() - t0) / n
+        out["cpu_baseline"] = {
+            "value": round(rows * V * 6.0 / dt / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": "FP64 numpy oracle: loss and gradient of %d of the %d token rows, repeated for ~10 s "
+                      "(%d passes), credited with the same bytes per row as the GPU step" % (rows, T, n)}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -217,6 +299,9 @@ def main():
     w = wl.WORKLOADS[args.workload]
     if w.kind == "w4a16":
         bench_w4a16(args, w)
+        return
+    if w.kind == "sem":
+        bench_sem(args, w)
         return
     fmt = reqat.NVFP4 if w.fmt == "nvfp4" else reqat.MXFP4
     B = reqat.BLOCK[fmt]

@@ -63,7 +63,23 @@ WORKLOADS = {
                 "student_t", 0, 0.02, "w4a16"),
     7: Workload(7, "W4A16 decode MXFP4 gate/up 14B-like 16x27648x5120", MXFP4, 16, 27648, 5120,
                 "normal_outliers", 51, 0.02, "w4a16"),
+    # SEM loss head of QAT: M tokens x N vocabulary logits (Qwen-family vocabulary)
+    8: Workload(8, "SEM loss head 4096 tokens x 152064 vocabulary", NVFP4, 4096, 152064, 0,
+                "normal", 0, 3.0, "sem"),
 }
+
+
+def make_logits(w: Workload, rows: int | None = None):
+    """Logits [M, N] (bfloat16, CPU) ~ N(0, w_std) and int32 targets [M], seeded."""
+    M = w.M if rows is None else rows
+    rng = np.random.Generator(np.random.PCG64(_seed(w.index, 0)))
+    z = np.empty((M, w.N), np.float32)
+    for r0 in range(0, M, 256):
+        r1 = min(M, r0 + 256)
+        z[r0:r1] = rng.standard_normal((r1 - r0, w.N), dtype=np.float32) * np.float32(w.w_std)
+    trng = np.random.Generator(np.random.PCG64(_seed(w.index, 1)))
+    t = trng.integers(0, w.N, w.M, dtype=np.int64)[:M].astype(np.int32)
+    return _to_bf16(z), torch.from_numpy(t)
 
 
 def _seed(index: int, stream: int) -> int:
