@@ -28,7 +28,7 @@ if ROOT not in sys.path:
 
 METRIC = "W4A4 GEMM TFLOPS & % FP4 MFMA peak (prefill); quantize/decode HBM GB/s"
 GEMM_SOURCES = ["paper_2606_15682_amd/csrc/gemm_tile256.hip", "paper_2606_15682_amd/csrc/gemm.hip",
-                "paper_2606_15682_amd/csrc/fp4_device.h", "paper_2606_15682_amd/csrc/internal.h"]
+                "paper_2606_15682_amd/csrc/fp4_device.h"]
 
 
 def gemm_source_hash() -> str:
