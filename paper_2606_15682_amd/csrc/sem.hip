@@ -138,7 +138,8 @@ __device__ __forceinline__ uint32_t fkey(float f) {
 constexpr int kBatchThreads = 1024;
 
 // k-th smallest (0-based) of the T entropies, by 4 passes of 8-bit radix selection.
-__device__ uint32_t select_key(const float *__restrict__ stats, int64_t T, int64_t k, uint32_t *hist) {
+__device__ uint32_t select_key(const float *__restrict__ stats, int64_t T, int64_t k, uint32_t *hist,
+                               uint32_t *scan, uint32_t *sel) {
     uint32_t prefix = 0, mask = 0;
     for (int pass = 0; pass < 4; ++pass) {
         const int shift = 24 - 8 * pass;
@@ -149,15 +150,33 @@ __device__ uint32_t select_key(const float *__restrict__ stats, int64_t T, int64
             if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 0xFFu], 1u);
         }
         __syncthreads();
-        // every thread walks the 256 counts (cheap) to find the digit
-        uint32_t digit = 0;
-        int64_t below = 0;
-        for (int d = 0; d < 256; ++d) {
-            const int64_t c = hist[d];
-            if (k < below + c) { digit = (uint32_t)d; break; }
-            below += c;
+        // exclusive prefix sums of the 256 counts (Hillis-Steele in LDS, the
+        // first 256 threads); the bin holding rank k publishes its digit
+        uint32_t c = 0, incl = 0;
+        if (threadIdx.x < 256) {
+            incl = c = hist[threadIdx.x];
+            scan[threadIdx.x] = c;
         }
-        k -= below;
+        for (int off = 1; off < 256; off <<= 1) {
+            __syncthreads();                       // the previous step's sums are written
+            const uint32_t add = (threadIdx.x < 256 && (int)threadIdx.x >= off) ? scan[threadIdx.x - off] : 0u;
+            __syncthreads();                       // every read done before the next writes
+            if (threadIdx.x < 256) {
+                incl += add;
+                scan[threadIdx.x] = incl;
+            }
+        }
+        __syncthreads();
+        if (threadIdx.x < 256) {
+            const int64_t below = (int64_t)(incl - c);
+            if (c != 0 && k >= below && k < below + (int64_t)c) {
+                sel[0] = threadIdx.x;
+                sel[1] = (uint32_t)below;
+            }
+        }
+        __syncthreads();
+        const uint32_t digit = sel[0];
+        k -= (int64_t)sel[1];
         prefix |= digit << shift;
         mask |= 0xFFu << shift;
         __syncthreads();
@@ -173,7 +192,7 @@ __global__ __launch_bounds__(kBatchThreads) void sem_batch_kernel(const float *_
                                                                   float lambda, float eps,
                                                                   float *__restrict__ weights,
                                                                   float *__restrict__ loss) {
-    __shared__ uint32_t hist[256];
+    __shared__ uint32_t hist[256], scan[256], sel[2];
     __shared__ double dred[2][kBatchThreads / 64];
     __shared__ float fred[kBatchThreads / 64];
 
@@ -192,8 +211,8 @@ __global__ __launch_bounds__(kBatchThreads) void sem_batch_kernel(const float *_
     const double q = 0.75 * (double)(T - 1);
     const int64_t lo = (int64_t)q;
     const int64_t hi = lo + 1 < T ? lo + 1 : T - 1;
-    const double hlo = (double)unkey(select_key(stats, T, lo, hist));
-    const double hhi = hi == lo ? hlo : (double)unkey(select_key(stats, T, hi, hist));
+    const double hlo = (double)unkey(select_key(stats, T, lo, hist, scan, sel));
+    const double hhi = hi == lo ? hlo : (double)unkey(select_key(stats, T, hi, hist, scan, sel));
     const double tau = hlo + (q - (double)lo) * (hhi - hlo);
     const double denom = tau - (double)hmin + (double)eps;
 
