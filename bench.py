@@ -140,14 +140,15 @@ def bench_w4a16(args, w):
     x = x_cpu.to(dev)
     wc, ws, _ = reqat.quantize(w_cpu.to(dev), reqat.MXFP4)
     y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    wsp = torch.empty(max(1, reqat.reqat_w4a16_workspace_bytes(M, N, K)), dtype=torch.uint8, device=dev)
     for _ in range(args.warmup):
-        reqat.gemm_w4a16(x, wc, ws, out_dtype=torch.bfloat16, out=y)
+        reqat.gemm_w4a16(x, wc, ws, out_dtype=torch.bfloat16, out=y, ws=wsp)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev[0].record()
     for _ in range(args.steps):
-        reqat.gemm_w4a16(x, wc, ws, out_dtype=torch.bfloat16, out=y)
+        reqat.gemm_w4a16(x, wc, ws, out_dtype=torch.bfloat16, out=y, ws=wsp)
     ev[1].record()
     torch.cuda.synchronize()
     ms_step = (time.perf_counter() - t0) * 1e3 / args.steps

@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define REQAT_ABI_VERSION 6
+#define REQAT_ABI_VERSION 7
 
 typedef enum {
     REQAT_FMT_NVFP4 = 0, /* B = 16, E4M3 block scale, FP32 global scale */
@@ -160,14 +160,22 @@ reqat_status reqat_fakequant_mxfp4_rht(const void *x, int64_t rows, int64_t cols
  * bfloat16 rounding, overflow to Inf included, otherwise; NaN for 0xFF),
  * products exact, FP32 accumulation.
  *   x [M][ldx] bfloat16 (16-byte aligned, ldx % 8 == 0, ldx >= K);
- *   w_codes [N][K/2], w_scales [N][K/32] (as reqat_quantize_fp4, MXFP4);
+ *   w_codes [N][K/2] (16-byte aligned), w_scales [N][K/32] (4-byte aligned),
+ *   as reqat_quantize_fp4 writes them for MXFP4;
  *   y [M][ldy] of y_dtype, ldy >= N.
+ *   workspace: device scratch of reqat_w4a16_workspace_bytes(M, N, K) bytes
+ *              (4-byte aligned; may be NULL when that is 0): FP32 partial sums
+ *              when K is split over several workgroups (few weight rows).
  * Requirements: K % 128 == 0.  M == 0 or N == 0 is a no-op; K == 0 writes zeros.
- * Designed for decode (small M): one pass over the weights.
+ * Designed for decode (small M): one pass over the weights.  The result does
+ * not depend on the split (partial sums are added in a fixed order).
  */
 reqat_status reqat_gemm_w4a16(int64_t M, int64_t N, int64_t K, const void *x, int64_t ldx,
                               const uint8_t *w_codes, const uint8_t *w_scales, void *y, reqat_dtype y_dtype,
-                              int64_t ldy, void *stream);
+                              int64_t ldy, void *workspace, void *stream);
+
+/* Bytes of workspace reqat_gemm_w4a16 needs for an M x N x K product (0: none; 0 on bad arguments). */
+size_t reqat_w4a16_workspace_bytes(int64_t M, int64_t N, int64_t K);
 
 /*
  * KV-cache quantization of the NVFP4 W4A4KV4 setting: E1M2 elements (the KV4

@@ -174,18 +174,27 @@ reqat_status reqat_gemm_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K,
     return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
 }
 
+size_t reqat_w4a16_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+    if (M < 0 || N < 0 || K < 0 || K % 128) return 0;
+    return gemm_w4a16_workspace_bytes(M, N, K);
+}
+
 reqat_status reqat_gemm_w4a16(int64_t M, int64_t N, int64_t K, const void *x, int64_t ldx,
                               const uint8_t *w_codes, const uint8_t *w_scales, void *y, reqat_dtype y_dtype,
-                              int64_t ldy, void *stream) {
+                              int64_t ldy, void *workspace, void *stream) {
     if (y_dtype != REQAT_DT_F32 && y_dtype != REQAT_DT_BF16) return REQAT_E_ENUM;
     if (M < 0 || N < 0 || K < 0) return REQAT_E_SHAPE;
     if (K % 128 || ldx < K || ldy < N) return REQAT_E_SHAPE;
     if (M == 0 || N == 0) return REQAT_OK;
     if (!y || (K > 0 && (!x || !w_codes || !w_scales))) return REQAT_E_NULL;
-    if (K > 0 && (!aligned16(x) || ldx % 8 || !aligned16(w_codes))) return REQAT_E_ALIGN;
+    if (gemm_w4a16_workspace_bytes(M, N, K) > 0 && !workspace) return REQAT_E_NULL;
+    if (K > 0 && (!aligned16(x) || ldx % 8 || !aligned16(w_codes) || (reinterpret_cast<uintptr_t>(w_scales) & 3u)))
+        return REQAT_E_ALIGN;
     if (reinterpret_cast<uintptr_t>(y) & (y_dtype == REQAT_DT_BF16 ? 1u : 3u)) return REQAT_E_ALIGN;
+    if (reinterpret_cast<uintptr_t>(workspace) & 3u) return REQAT_E_ALIGN;
     hipError_t e = launch_gemm_w4a16(M, N, K, reinterpret_cast<const uint16_t *>(x), ldx, w_codes, w_scales, y,
-                                     y_dtype == REQAT_DT_BF16, ldy, reinterpret_cast<hipStream_t>(stream));
+                                     y_dtype == REQAT_DT_BF16, ldy, reinterpret_cast<float *>(workspace),
+                                     reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
 }
 

@@ -8,18 +8,22 @@
 // v_mfma_f32_16x16x32_bf16 multiplies exactly (it keeps subnormal inputs) and
 // sums in FP32.  A NaN scale byte (0xFF) makes its 32 weights NaN.
 //
-// Decode-shaped work streams W once: a workgroup owns 16 rows of W (one
-// 16-wide MFMA tile of the output; N/16 workgroups) and 16*MT rows of x.  Its
-// WAVES waves take contiguous shares of K in 128-element chunks and meet in
-// LDS at the end.  Every workgroup reads all of x (from L2): for M = 16 that is
-// four times the weight bytes, and it, not HBM, bounds the rate (a probe of
-// the same load pattern streams the weights alone at 4.8 TB/s and 0.95 TB/s
-// with the x reads added).  In a chunk, lane l takes the 32-element MX block
-// kg = l / 16 of W row n = l % 16 (16 code bytes + its scale byte) and the
-// same 32 K positions of x row m = l % 16 (64 bytes); MFMA step s uses the
-// lane's elements 8s .. 8s+7, so A and B agree on which K each lane holds and
-// the sum over K is the product's.  Rows past M or N re-read the last real row
-// and are never stored.
+// Decode-shaped work streams W once and is bound by how the activations reach
+// the matrix cores: a workgroup owns 64 weight rows (16 per wave) and loads
+// each 128-element chunk of its activation rows once into LDS, where all four
+// waves read it, so every activation byte read from L2 serves 64 weight rows
+// (reading it per wave, for 16 rows, made the L2 reads four times the weight
+// bytes and capped the rate near 1 TB/s).  With few weight rows the K range
+// is split over more workgroups (>= 512 in total) whose FP32 partial sums a
+// second kernel adds in split order (deterministic).
+//
+// In a chunk, lane l takes the 32-element MX block kg = l / 16 of weight row
+// l % 16 (16 code bytes + its scale byte) and the same 32 K positions of
+// activation row l % 16 from LDS; MFMA step s uses the lane's elements
+// 8s .. 8s+7, so A and B agree on which K each lane holds.  Rows past M or N
+// re-read the last real row and are never stored.
+#include <type_traits>
+
 #include "fp4_device.h"
 #include "internal.h"
 
@@ -30,36 +34,35 @@ namespace {
 typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 
 #ifndef REQAT_W16_DEPTH
 #define REQAT_W16_DEPTH 4
 #endif
-#ifndef REQAT_W16_WAVES
-#define REQAT_W16_WAVES 8
-#endif
 
+constexpr int kThreads = 256;          // four waves
+constexpr int kRows = 64;              // weight rows per workgroup: 16 per wave
+constexpr int kXPitch = 128 + 8;       // LDS row pitch of an x chunk, bfloat16 elements
 
-template <int MT>
-struct W16Chunk {
+struct WFrag {
     uint4 w;             // 32 E2M1 codes of the lane's block
-    uint32_t s;          // its E8M0 scale byte
-    uint4 x[MT][4];      // 32 bfloat16 activations per x row tile
+    uint32_t s;          // the E8M0 scale bytes of the chunk's four blocks (the lane's is byte kg)
 };
 
-template <int MT>
-__device__ __forceinline__ void load_w16(W16Chunk<MT> &q, int64_t c, int r, int kg, int64_t M, int64_t N,
-                                         int64_t m0, int64_t n0, int64_t K, const uint16_t *x, int64_t ldx,
-                                         const uint8_t *w_codes, const uint8_t *w_scales) {
+__device__ __forceinline__ void load_wfrag(WFrag &q, int64_t c, int64_t nrow, int kg, int64_t K,
+                                           const uint8_t *w_codes, const uint8_t *w_scales) {
     const int64_t blk = c * 4 + kg;                             // MX block index along K
-    const int64_t nrow = (n0 + r) < N ? (n0 + r) : N - 1;
     q.w = *reinterpret_cast<const uint4 *>(w_codes + nrow * (K / 2) + blk * 16);
-    q.s = w_scales[nrow * (K / 32) + blk];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int64_t row = (m0 + 16 * mt + r) < M ? (m0 + 16 * mt + r) : M - 1;
-        const uint4 *xp = reinterpret_cast<const uint4 *>(x + row * ldx + blk * 32);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) q.x[mt][i] = xp[i];
+    // one dword for the four blocks of the chunk (K % 128 == 0 keeps it aligned):
+    // a 32-bit value, so the prefetch ring needs no byte extension per turn
+    q.s = *reinterpret_cast<const uint32_t *>(w_scales + nrow * (K / 32) + c * 4);
+}
+
+// Calls f(integral_constant<int, J>) for J = B .. E-1, unrolled at compile time.
+template <int B, int E, typename F> __device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
     }
 }
 
@@ -67,108 +70,189 @@ __device__ __forceinline__ uint32_t pick4(const uint4 &q, int s) {
     return s == 0 ? q.x : s == 1 ? q.y : s == 2 ? q.z : q.w;
 }
 
-template <int MT>
-__device__ __forceinline__ void mul_w16(v4f (&acc)[MT], const W16Chunk<MT> &q) {
-    const float p2 = __builtin_bit_cast(float, q.s << 23);
-    const bool nan = q.s == 0xFFu;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-        const uint32_t word = pick4(q.w, s);
-        const v2bf d0 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, p2, 0);
-        const v2bf d1 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, p2, 1);
-        const v2bf d2 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, p2, 2);
-        const v2bf d3 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, p2, 3);
-        v8bf wb = v8bf{d0[0], d0[1], d1[0], d1[1], d2[0], d2[1], d3[0], d3[1]};
-        if (nan) {
-            const __bf16 qn = __builtin_bit_cast(__bf16, (uint16_t)0x7FC0u);
-            wb = v8bf{qn, qn, qn, qn, qn, qn, qn, qn};
-        }
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, q.x[mt][s]), wb, acc[mt],
-                                                             0, 0, 0);
+// Bfloat16 weights of MFMA step s: the lane's elements 8s .. 8s+7, RN_bf16(code * 2^e).
+__device__ __forceinline__ v8bf decode_step(const WFrag &q, int s, int kg) {
+    const uint32_t sb = (q.s >> (8 * kg)) & 0xFFu;
+    const float p2 = __builtin_bit_cast(float, sb << 23);
+    const uint32_t word = pick4(q.w, s);
+    const v2bf d0 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, p2, 0);
+    const v2bf d1 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, p2, 1);
+    const v2bf d2 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, p2, 2);
+    const v2bf d3 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, p2, 3);
+    v8bf wb = v8bf{d0[0], d0[1], d1[0], d1[1], d2[0], d2[1], d3[0], d3[1]};
+    if (sb == 0xFFu) {                                          // NaN scale: NaN weights
+        const __bf16 qn = __builtin_bit_cast(__bf16, (uint16_t)0x7FC0u);
+        wb = v8bf{qn, qn, qn, qn, qn, qn, qn, qn};
     }
+    return wb;
 }
 
-template <int MT, int DEPTH, int WAVES>
-__global__ __launch_bounds__(64 * WAVES) void gemm_w4a16_kernel(
+// A workgroup owns 64 weight rows (16 per wave) and 16*MT activation rows and
+// walks the K chunks [nch*ks/KS, nch*(ks+1)/KS) of its split ks = blockIdx.y.
+// Each 128-element chunk of the activation rows is loaded once per workgroup
+// (16 bytes per thread per 16-row tile), stored to LDS and read by all four
+// waves; the weights go straight to registers, DEPTH chunks ahead.  With one
+// split the results go to y; otherwise to the FP32 partial sums
+// part[ks][m][n], added in split order by gemm_w4a16_reduce.
+template <int MT, int DEPTH>
+__global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
     int64_t M, int64_t N, int64_t K, const uint16_t *__restrict__ x, int64_t ldx,
     const uint8_t *__restrict__ w_codes, const uint8_t *__restrict__ w_scales, void *__restrict__ y,
-    int y_bf16, int64_t ldy) {
-    __shared__ float part[WAVES][MT][4][64];
+    int y_bf16, int64_t ldy, int KS, float *__restrict__ part) {
+    __shared__ __attribute__((aligned(16))) uint16_t xs[2][MT * 16][kXPitch];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, kg = lane >> 4;
-    const int64_t n0 = (int64_t)blockIdx.x * 16;
-    const int64_t m0 = (int64_t)blockIdx.y * 16 * MT;
+    const int64_t n0 = (int64_t)blockIdx.x * kRows + 16 * wave;
+    const int64_t nrow = (n0 + r) < N ? (n0 + r) : N - 1;
+    const int ks = blockIdx.y;
+    const int64_t m0 = (int64_t)blockIdx.z * 16 * MT;
     const int64_t nch = K / 128;
-    const int64_t c0 = nch * wave / WAVES, my = nch * (wave + 1) / WAVES - c0;   // this wave's chunks
+    const int64_t c0 = nch * ks / KS, nc = nch * (ks + 1) / KS - c0;
+
+    // activation chunk loader: thread t takes row t / 16 of each 16-row tile, elements 8 (t % 16) ..
+    const int xr = tid >> 4, xc = (tid & 15) * 8;
+    auto load_x = [&](int64_t c, v4u (&v)[MT]) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const int64_t row = (m0 + 16 * mt + xr) < M ? (m0 + 16 * mt + xr) : M - 1;
+            v[mt] = *reinterpret_cast<const v4u *>(x + row * ldx + c * 128 + xc);
+        }
+    };
+    auto store_x = [&](int buf, const v4u (&v)[MT]) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) *reinterpret_cast<v4u *>(&xs[buf][16 * mt + xr][xc]) = v[mt];
+    };
 
     v4f acc[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[mt] = v4f{};
 
-    auto chunk = [&](int64_t i) { return c0 + i; };
-    W16Chunk<MT> q[DEPTH];
+    // Chunk c's activations travel global -> registers (ring slot c % DEPTH,
+    // issued DEPTH - 1 iterations before they are needed) -> LDS (buffer
+    // c & 1, one iteration ahead); its weights go to registers DEPTH chunks
+    // ahead.  The ring is unrolled by templates so every slot index is a
+    // constant, and loads past the last chunk re-read it (clamped, never
+    // used) so the main loop has no branches: the compiler then waits on
+    // each load alone instead of draining all of them once per ring turn.
+    if (nc > 0) {
+        v4u xv[DEPTH][MT];
+        WFrag q[DEPTH];
+        auto clamp = [&](int64_t i) { return c0 + (i < nc ? i : nc - 1); };
+        static_for<0, DEPTH>([&](auto J) {
+            constexpr int j = decltype(J)::value;
+            load_x(clamp(j), xv[j]);
+            load_wfrag(q[j], clamp(j), nrow, kg, K, w_codes, w_scales);
+        });
+        store_x(0, xv[0]);
+        auto step = [&](int64_t i, auto J) {
+            constexpr int j = decltype(J)::value;
+            // keep each chunk's decode in its own step: hoisted, it would wait
+            // on weights still in flight and shorten the prefetch
+            __builtin_amdgcn_sched_barrier(0);
+            __syncthreads();                                    // chunk i in LDS; buffer (i+1)&1 free
+            store_x((int)((i + 1) & 1), xv[(j + 1) % DEPTH]);   // chunk i+1 (unused past the end)
+            load_x(clamp(i + DEPTH), xv[j]);
+            const int buf = (int)(i & 1);
 #pragma unroll
-    for (int j = 0; j < DEPTH; ++j)
-        if (j < my) load_w16<MT>(q[j], chunk(j), r, kg, M, N, m0, n0, K, x, ldx, w_codes, w_scales);
-    for (int64_t i0 = 0; i0 < my; i0 += DEPTH) {
+            for (int s = 0; s < 4; ++s) {
+                const v8bf wb = decode_step(q[j], s, kg);
 #pragma unroll
-        for (int j = 0; j < DEPTH; ++j) {
-            const int64_t i = i0 + j;
-            if (i < my) {
-                mul_w16<MT>(acc, q[j]);
-                if (i + DEPTH < my)
-                    load_w16<MT>(q[j], chunk(i + DEPTH), r, kg, M, N, m0, n0, K, x, ldx, w_codes, w_scales);
+                for (int mt = 0; mt < MT; ++mt) {
+                    const v4u xa = *reinterpret_cast<const v4u *>(&xs[buf][16 * mt + r][32 * kg + 8 * s]);
+                    acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, xa), wb, acc[mt],
+                                                                     0, 0, 0);
+                }
             }
-        }
+            load_wfrag(q[j], clamp(i + DEPTH), nrow, kg, K, w_codes, w_scales);
+        };
+        int64_t i0 = 0;
+        for (; i0 + DEPTH <= nc; i0 += DEPTH)
+            static_for<0, DEPTH>([&](auto J) { step(i0 + decltype(J)::value, J); });
+        static_for<0, DEPTH - 1>([&](auto J) {
+            if (i0 + decltype(J)::value < nc) step(i0 + decltype(J)::value, J);   // uniform
+        });
     }
 
-    // the waves' partial sums, added in wave order; D[m][n] of a 16 x 16 tile
-    // is in lane n + 16 * (m / 4), register m % 4.  Thread t < 256 finishes
-    // register t / 64 of every row tile.
+    // D[m][n] of a 16 x 16 tile sits in lane n + 16 * (m / 4), register m % 4
+    const int64_t col = n0 + r;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) part[wave][mt][i][lane] = acc[mt][i];
-    __syncthreads();
-    if (tid >= 256) return;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int i = tid >> 6;                                 // register index 0..3
-        float v = part[0][mt][i][lane];
-#pragma unroll
-        for (int w = 1; w < WAVES; ++w) v += part[w][mt][i][lane];
-        const int64_t row = m0 + 16 * mt + 4 * (lane >> 4) + i;
-        const int64_t col = n0 + (lane & 15);
-        if (row < M && col < N) {
-            if (y_bf16) reinterpret_cast<__bf16 *>(y)[row * ldy + col] = (__bf16)v;
-            else reinterpret_cast<float *>(y)[row * ldy + col] = v;
+        for (int i = 0; i < 4; ++i) {
+            const int64_t row = m0 + 16 * mt + 4 * kg + i;
+            if (row < M && col < N) {
+                const float v = acc[mt][i];
+                if (KS > 1) part[((int64_t)ks * M + row) * N + col] = v;
+                else if (y_bf16) reinterpret_cast<__bf16 *>(y)[row * ldy + col] = (__bf16)v;
+                else reinterpret_cast<float *>(y)[row * ldy + col] = v;
+            }
         }
+}
+
+// y[m][n] = sum over splits, in split order, of part[ks][m][n].
+__global__ __launch_bounds__(kThreads) void gemm_w4a16_reduce(int64_t M, int64_t N, int KS,
+                                                              const float *__restrict__ part, void *__restrict__ y,
+                                                              int y_bf16, int64_t ldy) {
+    const int64_t total = M * N;
+    for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < total; e += (int64_t)gridDim.x * kThreads) {
+        float v = part[e];
+        for (int k = 1; k < KS; ++k) v += part[(int64_t)k * total + e];
+        const int64_t row = e / N, col = e - row * N;
+        if (y_bf16) reinterpret_cast<__bf16 *>(y)[row * ldy + col] = (__bf16)v;
+        else reinterpret_cast<float *>(y)[row * ldy + col] = v;
     }
 }
 
-template <int MT, int DEPTH, int WAVES>
+template <int MT>
 hipError_t launch_mt(int64_t M, int64_t N, int64_t K, const uint16_t *x, int64_t ldx, const uint8_t *w_codes,
-                     const uint8_t *w_scales, void *y, bool y_bf16, int64_t ldy, hipStream_t stream) {
-    const dim3 grid((unsigned)((N + 15) / 16), (unsigned)((M + 16 * MT - 1) / (16 * MT))), block(64 * WAVES);
-    hipLaunchKernelGGL((gemm_w4a16_kernel<MT, DEPTH, WAVES>), grid, block, 0, stream, M, N, K, x, ldx, w_codes,
-                       w_scales, y, (int)y_bf16, ldy);
+                     const uint8_t *w_scales, void *y, bool y_bf16, int64_t ldy, int KS, float *part,
+                     hipStream_t stream) {
+    const dim3 grid((unsigned)((N + kRows - 1) / kRows), (unsigned)KS, (unsigned)((M + 16 * MT - 1) / (16 * MT)));
+    constexpr int kDepth = MT == 1 ? REQAT_W16_DEPTH : 4;
+    hipLaunchKernelGGL((gemm_w4a16_kernel<MT, kDepth>), grid, dim3(kThreads), 0, stream, M, N, K, x, ldx,
+                       w_codes, w_scales, y, (int)y_bf16, ldy, KS, part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || KS == 1) return e;
+    int64_t rgrid = (M * N + kThreads - 1) / kThreads;
+    if (rgrid > 4096) rgrid = 4096;
+    hipLaunchKernelGGL(gemm_w4a16_reduce, dim3((unsigned)rgrid), dim3(kThreads), 0, stream, M, N, KS, part, y,
+                       (int)y_bf16, ldy);
     return hipGetLastError();
 }
 
+int row_tile(int64_t M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
+
 }  // namespace
+
+// K splits: enough workgroups to cover the chip (>= 512) when the weight
+// rows alone give fewer than 256, at most 8 and at most one chunk each.
+int gemm_w4a16_splits(int64_t M, int64_t N, int64_t K) {
+    const int64_t base = ((N + kRows - 1) / kRows) * ((M + 16 * row_tile(M) - 1) / (16 * row_tile(M)));
+    const int64_t nch = K / 128;
+    if (base >= 256 || nch <= 1) return 1;
+    int64_t ks = (512 + base - 1) / base;
+    if (ks > 8) ks = 8;
+    if (ks > nch) ks = nch;
+    return (int)ks;
+}
+
+size_t gemm_w4a16_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+    const int ks = gemm_w4a16_splits(M, N, K);
+    return ks > 1 ? sizeof(float) * (size_t)ks * (size_t)M * (size_t)N : 0;
+}
 
 hipError_t launch_gemm_w4a16(int64_t M, int64_t N, int64_t K, const uint16_t *x, int64_t ldx,
                              const uint8_t *w_codes, const uint8_t *w_scales, void *y, bool y_bf16,
-                             int64_t ldy, hipStream_t stream) {
+                             int64_t ldy, float *workspace, hipStream_t stream) {
     if (M == 0 || N == 0) return hipSuccess;
-    if (M <= 16) return launch_mt<1, REQAT_W16_DEPTH, REQAT_W16_WAVES>(M, N, K, x, ldx, w_codes, w_scales, y, y_bf16,
-                                                                      ldy, stream);
-    if (M <= 32) return launch_mt<2, 3, 8>(M, N, K, x, ldx, w_codes, w_scales, y, y_bf16, ldy, stream);
-    return launch_mt<4, 2, 4>(M, N, K, x, ldx, w_codes, w_scales, y, y_bf16, ldy, stream);
+    const int ks = gemm_w4a16_splits(M, N, K);
+    switch (row_tile(M)) {
+    case 1: return launch_mt<1>(M, N, K, x, ldx, w_codes, w_scales, y, y_bf16, ldy, ks, workspace, stream);
+    case 2: return launch_mt<2>(M, N, K, x, ldx, w_codes, w_scales, y, y_bf16, ldy, ks, workspace, stream);
+    default: return launch_mt<4>(M, N, K, x, ldx, w_codes, w_scales, y, y_bf16, ldy, ks, workspace, stream);
+    }
 }
 
 }  // namespace reqat

@@ -44,9 +44,12 @@ hipError_t launch_quantize_rht(QuantOut out, const uint16_t *x, int64_t rows, in
                                hipStream_t stream);
 
 // W4A16: bfloat16 x [M][ldx] times MXFP4 weights [N][K/2] (+ scales [N][K/32]), K % 128 == 0.
+// `workspace` holds gemm_w4a16_workspace_bytes(M, N, K) bytes of split-K partial sums.
+int gemm_w4a16_splits(int64_t M, int64_t N, int64_t K);
+size_t gemm_w4a16_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_gemm_w4a16(int64_t M, int64_t N, int64_t K, const uint16_t *x, int64_t ldx,
                              const uint8_t *w_codes, const uint8_t *w_scales, void *y, bool y_bf16,
-                             int64_t ldy, hipStream_t stream);
+                             int64_t ldy, float *workspace, hipStream_t stream);
 
 // KV4 (E1M2 elements, E4M3 block scales of 16, FP32 global scale) of x - shift;
 // `computed` runs the absmax pass into `partials` first (<= kMaxPartials).

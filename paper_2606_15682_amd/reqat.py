@@ -48,7 +48,8 @@ SIGNATURES = {
                                        _VP, _INT, _I64, _VP]),
     "reqat_quantize_kv4": (_INT, [_VP, _I64, _I64, _I64, _VP, _VP, _VP, _VP, _INT, _VP, _VP]),
     "reqat_fakequant_kv4": (_INT, [_VP, _I64, _I64, _I64, _VP, _VP, _I64, _VP, _INT, _VP, _VP]),
-    "reqat_gemm_w4a16": (_INT, [_I64, _I64, _I64, _VP, _I64, _VP, _VP, _VP, _INT, _I64, _VP]),
+    "reqat_gemm_w4a16": (_INT, [_I64, _I64, _I64, _VP, _I64, _VP, _VP, _VP, _INT, _I64, _VP, _VP]),
+    "reqat_w4a16_workspace_bytes": (ctypes.c_size_t, [_I64, _I64, _I64]),
     "reqat_quantize_mxfp4_rht": (_INT, [_VP, _I64, _I64, _I64, ctypes.c_uint32, _VP, _VP, _VP]),
     "reqat_fakequant_mxfp4_rht": (_INT, [_VP, _I64, _I64, _I64, ctypes.c_uint32, _VP, _I64, _VP]),
     "reqat_workspace_bytes": (ctypes.c_size_t, []),
@@ -124,8 +125,12 @@ def reqat_fakequant_kv4(x, rows, cols, ldx, shift, y, ldy, tensor_scale, ts, wor
     return load().reqat_fakequant_kv4(x, rows, cols, ldx, shift, y, ldy, tensor_scale, ts, workspace, stream)
 
 
-def reqat_gemm_w4a16(M, N, K, x, ldx, w_codes, w_scales, y, y_dtype, ldy, stream):
-    return load().reqat_gemm_w4a16(M, N, K, x, ldx, w_codes, w_scales, y, y_dtype, ldy, stream)
+def reqat_gemm_w4a16(M, N, K, x, ldx, w_codes, w_scales, y, y_dtype, ldy, workspace, stream):
+    return load().reqat_gemm_w4a16(M, N, K, x, ldx, w_codes, w_scales, y, y_dtype, ldy, workspace, stream)
+
+
+def reqat_w4a16_workspace_bytes(M, N, K) -> int:
+    return load().reqat_w4a16_workspace_bytes(M, N, K)
 
 
 def reqat_quantize_mxfp4_rht(x, rows, cols, ldx, signs, codes, scales, stream):
@@ -313,17 +318,23 @@ def fakequant_kv4(x: torch.Tensor, shift=None, tensor_scale=None, out=None, g_ou
     return y, g
 
 
-def gemm_w4a16(x: torch.Tensor, w_codes, w_scales, out_dtype=torch.float32, out=None):
+def gemm_w4a16(x: torch.Tensor, w_codes, w_scales, out_dtype=torch.float32, out=None, ws=None):
     """Y = x . W^T with x bfloat16 [M, K] and MXFP4 weights (codes [N, K/2],
-    scales [N, K/32]) dequantized to bfloat16; FP32 accumulation."""
+    scales [N, K/32]) dequantized to bfloat16; FP32 accumulation.
+    ws: optional workspace tensor of reqat_w4a16_workspace_bytes(M, N, K) bytes."""
     M, K, ldx = _x2d(x)
     N = w_codes.shape[0]
     if w_codes.shape[1] * 2 != K:
         raise ValueError("K mismatch")
+    if not (w_codes.is_contiguous() and w_scales.is_contiguous()) or tuple(w_scales.shape) != (N, K // 32):
+        raise ValueError("w_codes [N, K/2] and w_scales [N, K/32] must be contiguous")
     dt = DT_F32 if out_dtype == torch.float32 else DT_BF16
     y = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=x.device)
+    nbytes = reqat_w4a16_workspace_bytes(M, N, K)
+    if ws is None and nbytes:
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
     st = reqat_gemm_w4a16(M, N, K, x.data_ptr(), ldx, w_codes.data_ptr(), w_scales.data_ptr(), y.data_ptr(),
-                          dt, y.stride(0), _stream(x.device))
+                          dt, y.stride(0), _ptr(ws), _stream(x.device))
     _check(st, "reqat_gemm_w4a16")
     return y
 

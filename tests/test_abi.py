@@ -50,7 +50,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_small_queries(lib):
-    assert reqat.reqat_abi_version() == 6
+    assert reqat.reqat_abi_version() == 7
     assert reqat.reqat_workspace_bytes() == 4 * 4096 + 2 * (1 << 19)   # partials + segment table
     for s in range(7):
         assert reqat.reqat_status_str(s).startswith(reqat.STATUS[s])
@@ -114,14 +114,21 @@ def test_rotated_quantize_validation(lib):
 
 
 def test_w4a16_validation(lib):
-    g16 = lambda M=4, N=8, K=128, x=P, ldx=128, wc=P, ws=P, y=P, dt=0, ldy=8: reqat.reqat_gemm_w4a16(
-        M, N, K, x, ldx, wc, ws, y, dt, ldy, None)
+    g16 = lambda M=4, N=8, K=128, x=P, ldx=128, wc=P, ws=P, y=P, dt=0, ldy=8, wk=None: reqat.reqat_gemm_w4a16(
+        M, N, K, x, ldx, wc, ws, y, dt, ldy, wk, None)
+    # one 64-row weight tile of a 16 x 5120 x 27648 product: K split 7 ways (FP32 partials)
+    assert reqat.reqat_w4a16_workspace_bytes(16, 5120, 27648) == 4 * 7 * 16 * 5120
+    assert reqat.reqat_w4a16_workspace_bytes(16, 27648, 5120) == 0
+    assert reqat.reqat_w4a16_workspace_bytes(4, 8, 128) == 0          # a single chunk: no split
+    assert reqat.reqat_w4a16_workspace_bytes(4, 8, 100) == 0
+    assert g16(M=16, N=5120, K=27648, ldx=27648, ldy=5120) == E_NULL  # needs the workspace
     assert g16(dt=5) == E_ENUM
     assert g16(M=-1) == E_SHAPE and g16(K=96, ldx=96) == E_SHAPE and g16(ldx=64) == E_SHAPE
     assert g16(ldy=4) == E_SHAPE
     assert g16(M=0, x=None, wc=None, ws=None, y=None) == 0 and g16(N=0, y=None) == 0
     assert g16(y=None) == E_NULL and g16(x=None) == E_NULL and g16(wc=None) == E_NULL and g16(ws=None) == E_NULL
     assert g16(x=P + 2) == E_ALIGN and g16(ldx=132) == E_ALIGN and g16(wc=P + 8) == E_ALIGN
+    assert g16(ws=P + 2) == E_ALIGN and g16(ws=P + 1) == E_ALIGN
     assert g16(y=P + 2) == E_ALIGN and g16(y=P + 1, dt=1) == E_ALIGN
 
 
