@@ -36,27 +36,16 @@ typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 
-#ifndef REQAT_W16_DEPTH
-#define REQAT_W16_DEPTH 4
+#ifndef REQAT_W16_NT
+#define REQAT_W16_NT 1
+#endif
+#ifndef REQAT_W16_KSMAX
+#define REQAT_W16_KSMAX 8
 #endif
 
 constexpr int kThreads = 256;          // four waves
-constexpr int kRows = 64;              // weight rows per workgroup: 16 per wave
+constexpr int kDepth = 4;              // chunks in flight per wave (weights and activations)
 constexpr int kXPitch = 128 + 8;       // LDS row pitch of an x chunk, bfloat16 elements
-
-struct WFrag {
-    uint4 w;             // 32 E2M1 codes of the lane's block
-    uint32_t s;          // the E8M0 scale bytes of the chunk's four blocks (the lane's is byte kg)
-};
-
-__device__ __forceinline__ void load_wfrag(WFrag &q, int64_t c, int64_t nrow, int kg, int64_t K,
-                                           const uint8_t *w_codes, const uint8_t *w_scales) {
-    const int64_t blk = c * 4 + kg;                             // MX block index along K
-    q.w = *reinterpret_cast<const uint4 *>(w_codes + nrow * (K / 2) + blk * 16);
-    // one dword for the four blocks of the chunk (K % 128 == 0 keeps it aligned):
-    // a 32-bit value, so the prefetch ring needs no byte extension per turn
-    q.s = *reinterpret_cast<const uint32_t *>(w_scales + nrow * (K / 32) + c * 4);
-}
 
 // Calls f(integral_constant<int, J>) for J = B .. E-1, unrolled at compile time.
 template <int B, int E, typename F> __device__ __forceinline__ void static_for(F &&f) {
@@ -66,15 +55,15 @@ template <int B, int E, typename F> __device__ __forceinline__ void static_for(F
     }
 }
 
-__device__ __forceinline__ uint32_t pick4(const uint4 &q, int s) {
+__device__ __forceinline__ uint32_t pick4(const v4u &q, int s) {
     return s == 0 ? q.x : s == 1 ? q.y : s == 2 ? q.z : q.w;
 }
 
-// Bfloat16 weights of MFMA step s: the lane's elements 8s .. 8s+7, RN_bf16(code * 2^e).
-__device__ __forceinline__ v8bf decode_step(const WFrag &q, int s, int kg) {
-    const uint32_t sb = (q.s >> (8 * kg)) & 0xFFu;
+// Bfloat16 weights of MFMA step s: the lane's elements 8s .. 8s+7, RN_bf16(code * 2^e)
+// for the block's E8M0 byte sb.
+__device__ __forceinline__ v8bf decode_step(const v4u &w, uint32_t sb, int s) {
     const float p2 = __builtin_bit_cast(float, sb << 23);
-    const uint32_t word = pick4(q.w, s);
+    const uint32_t word = pick4(w, s);
     const v2bf d0 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, p2, 0);
     const v2bf d1 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, p2, 1);
     const v2bf d2 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, p2, 2);
@@ -87,14 +76,14 @@ __device__ __forceinline__ v8bf decode_step(const WFrag &q, int s, int kg) {
     return wb;
 }
 
-// A workgroup owns 64 weight rows (16 per wave) and 16*MT activation rows and
-// walks the K chunks [nch*ks/KS, nch*(ks+1)/KS) of its split ks = blockIdx.y.
-// Each 128-element chunk of the activation rows is loaded once per workgroup
-// (16 bytes per thread per 16-row tile), stored to LDS and read by all four
-// waves; the weights go straight to registers, DEPTH chunks ahead.  With one
-// split the results go to y; otherwise to the FP32 partial sums
-// part[ks][m][n], added in split order by gemm_w4a16_reduce.
-template <int MT, int DEPTH>
+// A workgroup owns 64*NT weight rows (16*NT per wave, NT MFMA column tiles)
+// and 16*MT activation rows and walks the K chunks [nch*ks/KS, nch*(ks+1)/KS)
+// of its split ks = blockIdx.y.  Each 128-element chunk of the activation
+// rows is loaded once per workgroup (16 bytes per thread per 16-row tile),
+// stored to LDS and read by all four waves; each LDS fragment feeds NT
+// MFMAs.  With one split the results go to y; otherwise to the FP32 partial
+// sums part[ks][m][n], added in split order by gemm_w4a16_reduce.
+template <int MT, int NT>
 __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
     int64_t M, int64_t N, int64_t K, const uint16_t *__restrict__ x, int64_t ldx,
     const uint8_t *__restrict__ w_codes, const uint8_t *__restrict__ w_scales, void *__restrict__ y,
@@ -104,8 +93,10 @@ __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, kg = lane >> 4;
-    const int64_t n0 = (int64_t)blockIdx.x * kRows + 16 * wave;
-    const int64_t nrow = (n0 + r) < N ? (n0 + r) : N - 1;
+    const int64_t n0 = (int64_t)blockIdx.x * (64 * NT) + 16 * NT * wave;
+    int64_t nrow[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) nrow[t] = (n0 + 16 * t + r) < N ? (n0 + 16 * t + r) : N - 1;
     const int ks = blockIdx.y;
     const int64_t m0 = (int64_t)blockIdx.z * 16 * MT;
     const int64_t nch = K / 128;
@@ -124,71 +115,104 @@ __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) *reinterpret_cast<v4u *>(&xs[buf][16 * mt + xr][xc]) = v[mt];
     };
-
-    v4f acc[MT];
+    // the lane's 32 codes (MX block kg of the chunk) of each of its weight rows
+    auto load_w = [&](int64_t c, v4u (&v)[NT]) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[mt] = v4f{};
+        for (int t = 0; t < NT; ++t)
+            v[t] = *reinterpret_cast<const v4u *>(w_codes + nrow[t] * (K / 2) + (c * 4 + kg) * 16);
+    };
+    // Scale bytes of four chunks in one load: lane (r, kg) takes the dword of
+    // chunk c + kg (its four blocks' E8M0 bytes; K % 128 == 0 keeps it
+    // aligned); the lanes of chunk c + u read it from lane r + 16u.
+    auto load_s = [&](int64_t c, uint32_t (&v)[NT]) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+            v[t] = *reinterpret_cast<const uint32_t *>(w_scales + nrow[t] * (K / 32) + c * 4);
+    };
 
-    // Chunk c's activations travel global -> registers (ring slot c % DEPTH,
-    // issued DEPTH - 1 iterations before they are needed) -> LDS (buffer
-    // c & 1, one iteration ahead); its weights go to registers DEPTH chunks
-    // ahead.  The ring is unrolled by templates so every slot index is a
-    // constant, and loads past the last chunk re-read it (clamped, never
-    // used) so the main loop has no branches: the compiler then waits on
-    // each load alone instead of draining all of them once per ring turn.
+    v4f acc[MT][NT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[mt][t] = v4f{};
+
+    // Chunk c's activations travel global -> registers (ring slot c % 4,
+    // issued three steps before they are needed) -> LDS (buffer c & 1, one
+    // step ahead); its codes go to registers four chunks ahead and its scale
+    // bytes with those of three neighbours, four to eight chunks ahead.  The
+    // ring is unrolled by templates so every slot index is a constant, and
+    // loads past the last chunk re-read it (clamped, never used), so the main
+    // loop has no branches and the compiler waits on each load alone.
     if (nc > 0) {
-        v4u xv[DEPTH][MT];
-        WFrag q[DEPTH];
+        v4u xv[kDepth][MT];
+        v4u wq[kDepth][NT];
+        uint32_t sq[2][NT];                                     // scale dwords of chunk groups (ring of 2)
         auto clamp = [&](int64_t i) { return c0 + (i < nc ? i : nc - 1); };
-        static_for<0, DEPTH>([&](auto J) {
+        load_s(clamp(kg), sq[0]);                               // first: the oldest load at the loop entry
+        static_for<0, kDepth>([&](auto J) {
             constexpr int j = decltype(J)::value;
             load_x(clamp(j), xv[j]);
-            load_wfrag(q[j], clamp(j), nrow, kg, K, w_codes, w_scales);
+            load_w(clamp(j), wq[j]);
         });
         store_x(0, xv[0]);
+        // step i = i0 + j of a loop turn of 8 chunks (j static)
         auto step = [&](int64_t i, auto J) {
             constexpr int j = decltype(J)::value;
+            constexpr int slot = j % kDepth, grp = (j / 4) & 1;
             // keep each chunk's decode in its own step: hoisted, it would wait
             // on weights still in flight and shorten the prefetch
             __builtin_amdgcn_sched_barrier(0);
             __syncthreads();                                    // chunk i in LDS; buffer (i+1)&1 free
-            store_x((int)((i + 1) & 1), xv[(j + 1) % DEPTH]);   // chunk i+1 (unused past the end)
-            load_x(clamp(i + DEPTH), xv[j]);
+            store_x((int)((i + 1) & 1), xv[(slot + 1) % kDepth]);   // chunk i+1 (unused past the end)
+            load_x(clamp(i + kDepth), xv[slot]);
+            if constexpr (j % 4 == 0) load_s(clamp(i + 4 + kg), sq[grp ^ 1]);   // next group of 4 chunks
+            uint32_t sb[NT];
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+                sb[t] = ((uint32_t)__builtin_amdgcn_ds_bpermute(4 * (r + 16 * (j % 4)), (int)sq[grp][t]) >>
+                         (8 * kg)) & 0xFFu;
             const int buf = (int)(i & 1);
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
-                const v8bf wb = decode_step(q[j], s, kg);
+                v8bf wb[NT];
+#pragma unroll
+                for (int t = 0; t < NT; ++t) wb[t] = decode_step(wq[slot][t], sb[t], s);
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
                     const v4u xa = *reinterpret_cast<const v4u *>(&xs[buf][16 * mt + r][32 * kg + 8 * s]);
-                    acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, xa), wb, acc[mt],
-                                                                     0, 0, 0);
+#pragma unroll
+                    for (int t = 0; t < NT; ++t)
+                        acc[mt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, xa), wb[t],
+                                                                            acc[mt][t], 0, 0, 0);
                 }
             }
-            load_wfrag(q[j], clamp(i + DEPTH), nrow, kg, K, w_codes, w_scales);
+            load_w(clamp(i + kDepth), wq[slot]);
         };
         int64_t i0 = 0;
-        for (; i0 + DEPTH <= nc; i0 += DEPTH)
-            static_for<0, DEPTH>([&](auto J) { step(i0 + decltype(J)::value, J); });
-        static_for<0, DEPTH - 1>([&](auto J) {
+        for (; i0 + 8 <= nc; i0 += 8)
+            static_for<0, 8>([&](auto J) { step(i0 + decltype(J)::value, J); });
+        static_for<0, 7>([&](auto J) {
             if (i0 + decltype(J)::value < nc) step(i0 + decltype(J)::value, J);   // uniform
         });
     }
 
     // D[m][n] of a 16 x 16 tile sits in lane n + 16 * (m / 4), register m % 4
-    const int64_t col = n0 + r;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int t = 0; t < NT; ++t) {
+        const int64_t col = n0 + 16 * t + r;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int64_t row = m0 + 16 * mt + 4 * kg + i;
-            if (row < M && col < N) {
-                const float v = acc[mt][i];
-                if (KS > 1) part[((int64_t)ks * M + row) * N + col] = v;
-                else if (y_bf16) reinterpret_cast<__bf16 *>(y)[row * ldy + col] = (__bf16)v;
-                else reinterpret_cast<float *>(y)[row * ldy + col] = v;
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int64_t row = m0 + 16 * mt + 4 * kg + i;
+                if (row < M && col < N) {
+                    const float v = acc[mt][t][i];
+                    if (KS > 1) part[((int64_t)ks * M + row) * N + col] = v;
+                    else if (y_bf16) reinterpret_cast<__bf16 *>(y)[row * ldy + col] = (__bf16)v;
+                    else reinterpret_cast<float *>(y)[row * ldy + col] = v;
+                }
             }
-        }
+    }
 }
 
 // y[m][n] = sum over splits, in split order, of part[ks][m][n].
@@ -209,10 +233,11 @@ template <int MT>
 hipError_t launch_mt(int64_t M, int64_t N, int64_t K, const uint16_t *x, int64_t ldx, const uint8_t *w_codes,
                      const uint8_t *w_scales, void *y, bool y_bf16, int64_t ldy, int KS, float *part,
                      hipStream_t stream) {
-    const dim3 grid((unsigned)((N + kRows - 1) / kRows), (unsigned)KS, (unsigned)((M + 16 * MT - 1) / (16 * MT)));
-    constexpr int kDepth = MT == 1 ? REQAT_W16_DEPTH : 4;
-    hipLaunchKernelGGL((gemm_w4a16_kernel<MT, kDepth>), grid, dim3(kThreads), 0, stream, M, N, K, x, ldx,
-                       w_codes, w_scales, y, (int)y_bf16, ldy, KS, part);
+    constexpr int NT = REQAT_W16_NT;
+    const dim3 grid((unsigned)((N + 64 * NT - 1) / (64 * NT)), (unsigned)KS,
+                    (unsigned)((M + 16 * MT - 1) / (16 * MT)));
+    hipLaunchKernelGGL((gemm_w4a16_kernel<MT, NT>), grid, dim3(kThreads), 0, stream, M, N, K, x, ldx, w_codes,
+                       w_scales, y, (int)y_bf16, ldy, KS, part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || KS == 1) return e;
     int64_t rgrid = (M * N + kThreads - 1) / kThreads;
@@ -229,11 +254,12 @@ int row_tile(int64_t M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
 // K splits: enough workgroups to cover the chip (>= 512) when the weight
 // rows alone give fewer than 256, at most 8 and at most one chunk each.
 int gemm_w4a16_splits(int64_t M, int64_t N, int64_t K) {
-    const int64_t base = ((N + kRows - 1) / kRows) * ((M + 16 * row_tile(M) - 1) / (16 * row_tile(M)));
+    const int64_t rows = 64 * REQAT_W16_NT;
+    const int64_t base = ((N + rows - 1) / rows) * ((M + 16 * row_tile(M) - 1) / (16 * row_tile(M)));
     const int64_t nch = K / 128;
     if (base >= 256 || nch <= 1) return 1;
     int64_t ks = (512 + base - 1) / base;
-    if (ks > 8) ks = 8;
+    if (ks > REQAT_W16_KSMAX) ks = REQAT_W16_KSMAX;
     if (ks > nch) ks = nch;
     return (int)ks;
 }
