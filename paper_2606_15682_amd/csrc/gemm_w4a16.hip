@@ -43,9 +43,16 @@ typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 #define REQAT_W16_KSMAX 8
 #endif
 
+#ifndef REQAT_W16_DEPTH1
+#define REQAT_W16_DEPTH1 4
+#endif
+#ifndef REQAT_W16_TARGET
+#define REQAT_W16_TARGET 512
+#endif
+
 constexpr int kThreads = 256;          // four waves
-constexpr int kDepth = 4;              // chunks in flight per wave (weights and activations)
 constexpr int kXPitch = 128 + 8;       // LDS row pitch of an x chunk, bfloat16 elements
+constexpr int kMaxSplits = REQAT_W16_KSMAX;
 
 // Calls f(integral_constant<int, J>) for J = B .. E-1, unrolled at compile time.
 template <int B, int E, typename F> __device__ __forceinline__ void static_for(F &&f) {
@@ -60,7 +67,9 @@ __device__ __forceinline__ uint32_t pick4(const v4u &q, int s) {
 }
 
 // Bfloat16 weights of MFMA step s: the lane's elements 8s .. 8s+7, RN_bf16(code * 2^e)
-// for the block's E8M0 byte sb.
+// for the block's E8M0 byte sb.  The NaN byte 0xFF gives the FP32 scale +Inf,
+// which the conversion turns into NaN for every code, zero included (checked
+// on gfx950 for all 256 code pairs and the four byte selects).
 __device__ __forceinline__ v8bf decode_step(const v4u &w, uint32_t sb, int s) {
     const float p2 = __builtin_bit_cast(float, sb << 23);
     const uint32_t word = pick4(w, s);
@@ -68,12 +77,7 @@ __device__ __forceinline__ v8bf decode_step(const v4u &w, uint32_t sb, int s) {
     const v2bf d1 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, p2, 1);
     const v2bf d2 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, p2, 2);
     const v2bf d3 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(word, p2, 3);
-    v8bf wb = v8bf{d0[0], d0[1], d1[0], d1[1], d2[0], d2[1], d3[0], d3[1]};
-    if (sb == 0xFFu) {                                          // NaN scale: NaN weights
-        const __bf16 qn = __builtin_bit_cast(__bf16, (uint16_t)0x7FC0u);
-        wb = v8bf{qn, qn, qn, qn, qn, qn, qn, qn};
-    }
-    return wb;
+    return v8bf{d0[0], d0[1], d1[0], d1[1], d2[0], d2[1], d3[0], d3[1]};
 }
 
 // A workgroup owns 64*NT weight rows (16*NT per wave, NT MFMA column tiles)
@@ -83,7 +87,7 @@ __device__ __forceinline__ v8bf decode_step(const v4u &w, uint32_t sb, int s) {
 // stored to LDS and read by all four waves; each LDS fragment feeds NT
 // MFMAs.  With one split the results go to y; otherwise to the FP32 partial
 // sums part[ks][m][n], added in split order by gemm_w4a16_reduce.
-template <int MT, int NT>
+template <int MT, int NT, int kDepth>
 __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
     int64_t M, int64_t N, int64_t K, const uint16_t *__restrict__ x, int64_t ldx,
     const uint8_t *__restrict__ w_codes, const uint8_t *__restrict__ w_scales, void *__restrict__ y,
@@ -136,36 +140,41 @@ __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
 #pragma unroll
         for (int t = 0; t < NT; ++t) acc[mt][t] = v4f{};
 
-    // Chunk c's activations travel global -> registers (ring slot c % 4,
-    // issued three steps before they are needed) -> LDS (buffer c & 1, one
-    // step ahead); its codes go to registers four chunks ahead and its scale
-    // bytes with those of three neighbours, four to eight chunks ahead.  The
+    // Chunk c's activations travel global -> registers (ring slot c % kDepth,
+    // issued kDepth - 1 steps before they are needed) -> LDS (buffer c & 1,
+    // one step ahead); its codes go to registers kDepth chunks ahead and its
+    // scale bytes with those of three neighbours, kDepth chunks ahead.  The
     // ring is unrolled by templates so every slot index is a constant, and
     // loads past the last chunk re-read it (clamped, never used), so the main
     // loop has no branches and the compiler waits on each load alone.
     if (nc > 0) {
+        constexpr int kTurn = 2 * kDepth;                      // steps per unrolled loop turn
+        constexpr int kGroups = kTurn / 4;                      // scale-group ring slots
         v4u xv[kDepth][MT];
         v4u wq[kDepth][NT];
-        uint32_t sq[2][NT];                                     // scale dwords of chunk groups (ring of 2)
+        uint32_t sq[kGroups][NT];                               // scale dwords of 4-chunk groups
         auto clamp = [&](int64_t i) { return c0 + (i < nc ? i : nc - 1); };
-        load_s(clamp(kg), sq[0]);                               // first: the oldest load at the loop entry
+        static_for<0, kDepth / 4>([&](auto G) {                 // first: the oldest loads at the loop entry
+            load_s(clamp(4 * decltype(G)::value + kg), sq[decltype(G)::value]);
+        });
         static_for<0, kDepth>([&](auto J) {
             constexpr int j = decltype(J)::value;
             load_x(clamp(j), xv[j]);
             load_w(clamp(j), wq[j]);
         });
         store_x(0, xv[0]);
-        // step i = i0 + j of a loop turn of 8 chunks (j static)
+        // step i = i0 + j of a loop turn (j static)
         auto step = [&](int64_t i, auto J) {
             constexpr int j = decltype(J)::value;
-            constexpr int slot = j % kDepth, grp = (j / 4) & 1;
+            constexpr int slot = j % kDepth, grp = (j / 4) % kGroups;
             // keep each chunk's decode in its own step: hoisted, it would wait
             // on weights still in flight and shorten the prefetch
             __builtin_amdgcn_sched_barrier(0);
             __syncthreads();                                    // chunk i in LDS; buffer (i+1)&1 free
             store_x((int)((i + 1) & 1), xv[(slot + 1) % kDepth]);   // chunk i+1 (unused past the end)
             load_x(clamp(i + kDepth), xv[slot]);
-            if constexpr (j % 4 == 0) load_s(clamp(i + 4 + kg), sq[grp ^ 1]);   // next group of 4 chunks
+            if constexpr (j % 4 == 0)                           // the group kDepth chunks ahead
+                load_s(clamp(i + kDepth + kg), sq[((j + kDepth) / 4) % kGroups]);
             uint32_t sb[NT];
 #pragma unroll
             for (int t = 0; t < NT; ++t)
@@ -189,9 +198,9 @@ __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
             load_w(clamp(i + kDepth), wq[slot]);
         };
         int64_t i0 = 0;
-        for (; i0 + 8 <= nc; i0 += 8)
-            static_for<0, 8>([&](auto J) { step(i0 + decltype(J)::value, J); });
-        static_for<0, 7>([&](auto J) {
+        for (; i0 + kTurn <= nc; i0 += kTurn)
+            static_for<0, kTurn>([&](auto J) { step(i0 + decltype(J)::value, J); });
+        static_for<0, kTurn - 1>([&](auto J) {
             if (i0 + decltype(J)::value < nc) step(i0 + decltype(J)::value, J);   // uniform
         });
     }
@@ -221,8 +230,13 @@ __global__ __launch_bounds__(kThreads) void gemm_w4a16_reduce(int64_t M, int64_t
                                                               int y_bf16, int64_t ldy) {
     const int64_t total = M * N;
     for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < total; e += (int64_t)gridDim.x * kThreads) {
-        float v = part[e];
-        for (int k = 1; k < KS; ++k) v += part[(int64_t)k * total + e];
+        float p[kMaxSplits];
+#pragma unroll
+        for (int k = 0; k < kMaxSplits; ++k) p[k] = k < KS ? part[(int64_t)k * total + e] : 0.0f;
+        float v = p[0];
+#pragma unroll
+        for (int k = 1; k < kMaxSplits; ++k)
+            if (k < KS) v += p[k];
         const int64_t row = e / N, col = e - row * N;
         if (y_bf16) reinterpret_cast<__bf16 *>(y)[row * ldy + col] = (__bf16)v;
         else reinterpret_cast<float *>(y)[row * ldy + col] = v;
@@ -236,7 +250,9 @@ hipError_t launch_mt(int64_t M, int64_t N, int64_t K, const uint16_t *x, int64_t
     constexpr int NT = REQAT_W16_NT;
     const dim3 grid((unsigned)((N + 64 * NT - 1) / (64 * NT)), (unsigned)KS,
                     (unsigned)((M + 16 * MT - 1) / (16 * MT)));
-    hipLaunchKernelGGL((gemm_w4a16_kernel<MT, NT>), grid, dim3(kThreads), 0, stream, M, N, K, x, ldx, w_codes,
+    // chunks in flight per wave (8 measured no faster than 4)
+    constexpr int kDepth = MT == 1 ? REQAT_W16_DEPTH1 : 4;
+    hipLaunchKernelGGL((gemm_w4a16_kernel<MT, NT, kDepth>), grid, dim3(kThreads), 0, stream, M, N, K, x, ldx, w_codes,
                        w_scales, y, (int)y_bf16, ldy, KS, part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || KS == 1) return e;
@@ -258,7 +274,7 @@ int gemm_w4a16_splits(int64_t M, int64_t N, int64_t K) {
     const int64_t base = ((N + rows - 1) / rows) * ((M + 16 * row_tile(M) - 1) / (16 * row_tile(M)));
     const int64_t nch = K / 128;
     if (base >= 256 || nch <= 1) return 1;
-    int64_t ks = (512 + base - 1) / base;
+    int64_t ks = (REQAT_W16_TARGET + base - 1) / base;
     if (ks > REQAT_W16_KSMAX) ks = REQAT_W16_KSMAX;
     if (ks > nch) ks = nch;
     return (int)ks;

@@ -548,6 +548,8 @@ def test_w4a16_special_scales():
     wc, ws = _w4a16_weights(24, 512, 91)
     ws[0, :] = 0                               # bfloat16-subnormal weights
     ws[1, 0] = 0xFF                            # a NaN block
+    wc[3, :16] = 0
+    ws[3, 0] = 0xFF                            # a NaN block of zero codes: NaN too
     ws[2, :] = 200                             # large but far from overflow for these x
     run_w4a16(xb, wc, ws)
     # every scale byte 0..250, small activations so that no FP32 sum overflows
