@@ -41,6 +41,8 @@
 // is mapped to the (b % 8)-th contiguous range of tiles, and tiles are walked
 // in groups of 8 tile-rows, keeping the A and B panels a group reuses in the
 // L2 of the XCD that owns it.
+#include <type_traits>
+
 #include "fp4_device.h"
 #include "internal.h"
 
@@ -55,9 +57,6 @@
 #endif
 #ifndef REQAT_NV_NBUF
 #define REQAT_NV_NBUF 2
-#endif
-#ifndef REQAT_MX_PERSISTENT
-#define REQAT_MX_PERSISTENT 1
 #endif
 #ifndef REQAT_NV_LEAD
 #define REQAT_NV_LEAD 3
@@ -75,10 +74,25 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kThreads = 256;
 constexpr int TM = 256, TN = 256;
+
+// Calls f(integral_constant<int, J>) for J = B .. E-1, unrolled at compile time.
+template <int B, int E, typename F> __device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
 constexpr int GROUP_M = 8;
 
-template <int FMT, int KS, int NBUF>
+// GS (MXFP4 with K % 512 == 0 and 16-byte aligned scales): the scale bytes
+// are not part of the stage; they go to LDS four stages at a time, 16 bytes
+// per row (one 1 KB load per 64 rows), into a ring of two group buffers.
+// Loading a stage's 4 bytes per row would touch one cache line per row for
+// every 4 bytes, and the vector memory path of a CU is bound by the number
+// of distinct cache lines its loads touch, not by their bytes.
+template <int FMT, int KS, int NBUF, bool GS = false>
 struct Cfg {
+    static constexpr bool kGS = GS;
     static constexpr int B = FMT == kMX ? 32 : 16;
     static constexpr int ROW = KS / 2;                  // code bytes per row per stage
     static constexpr int CH = ROW / 16;                 // 16-byte chunks per row
@@ -91,14 +105,20 @@ struct Cfg {
     static constexpr int SINS = TM / SRPI;              // scale load instructions per operand
     static constexpr int A_CODES = 0, B_CODES = CODE;
     static constexpr int A_SC = 2 * CODE, B_SC = 2 * CODE + SCALE;
-    static constexpr int STAGE = 2 * CODE + 2 * SCALE;
-    static constexpr int TOTAL = NBUF * STAGE;
+    static constexpr int STAGE = GS ? 2 * CODE : 2 * CODE + 2 * SCALE;
+    static constexpr int GSTAGES = 4;                   // stages per scale group (GS)
+    static constexpr int GROW = GSTAGES * SB;           // scale bytes per row per group (GS)
+    static constexpr int GROUP = 2 * TM * GROW;         // bytes of a scale group buffer: A rows, then B rows
+    static constexpr int SC_RING = NBUF * STAGE;        // offset of the two scale group buffers (GS)
+    static constexpr int TOTAL = NBUF * STAGE + (GS ? 2 * GROUP : 0);
     static constexpr int CODE_LPW = (CODE / 1024) / 4;  // code loads per operand per wave
     static constexpr int SCALE_LPW = SINS / 4;          // scale loads per operand per wave
-    static constexpr int LPS = 2 * CODE_LPW + 2 * SCALE_LPW;   // loads per wave per stage
+    static constexpr int LPS = 2 * CODE_LPW + (GS ? 0 : 2 * SCALE_LPW);   // loads per wave per stage
+    static constexpr int GLPW = GS ? (GROUP / 1024) / 4 : 0;              // scale-group loads per wave
     static_assert(CH == 4 || CH == 8, "row must be 4 or 8 chunks");
     static_assert(SINS % 4 == 0 && (CODE / 1024) % 4 == 0, "loads must split over 4 waves");
     static_assert(TOTAL <= 160 * 1024, "LDS budget");
+    static_assert(!GS || (FMT == kMX && GROW == 16 && GLPW == 2), "scale groups: 16 bytes per row, 2 loads per wave");
 };
 
 // Direct-to-LDS loads: lane i's 16 (4) bytes at base + voff land at LDS
@@ -120,7 +140,6 @@ __device__ __forceinline__ float uniform_load(const float *p) {
 }
 
 __device__ __forceinline__ uint4 lds16(const uint8_t *p) { return *reinterpret_cast<const uint4 *>(p); }
-__device__ __forceinline__ uint32_t lds4(const uint8_t *p) { return *reinterpret_cast<const uint32_t *>(p); }
 
 template <int CH>
 __device__ __forceinline__ int swz(int r) {
@@ -210,17 +229,6 @@ __device__ __forceinline__ v8i as_v8i(uint4 q) {
     return v8i{(int)q.x, (int)q.y, (int)q.z, (int)q.w, 0, 0, 0, 0};
 }
 
-template <int S>
-__device__ __forceinline__ void mx_mfma16(v16f (&acc)[4][4], const uint4 (&a)[4], const uint4 (&b)[4],
-                                          const uint32_t (&sa)[4], const uint32_t (&sb)[4]) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                as_v8i(a[i]), as_v8i(b[j]), acc[i][j], 4, 4, S, (int)sa[i], S, (int)sb[j]);
-}
-
 // Eight codes (one dword) times an NVFP4 block scale (FP16, in both halves) -> FP16 (exact).
 __device__ __forceinline__ v8h nv_decode8(uint32_t c, v2h s) {
     v2h p0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, 1.0f, 0) * s;
@@ -232,61 +240,6 @@ __device__ __forceinline__ v8h nv_decode8(uint32_t c, v2h s) {
 
 __device__ __forceinline__ uint32_t pick(const uint4 &q, int s) {
     return s == 0 ? q.x : s == 1 ? q.y : s == 2 ? q.z : q.w;
-}
-
-// MXFP4: one stage from LDS buffer `buf`, with the loads of a later stage
-// issued in parts between the substeps.
-template <class C, class Issue>
-__device__ __forceinline__ void mx_stage(v16f (&acc)[4][4], const uint8_t *buf, int rA0, int rB0,
-                                         int h, Issue &issue) {
-    constexpr int NSUB = C::CH / 2;                     // K=64 substeps per stage
-    uint32_t sa[4], sb[4];
-    uint4 a0[4], b0[4], a1[4], b1[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int ra = rA0 + 32 * i, rb = rB0 + 32 * i;
-        if constexpr (C::SB == 8) {
-            sa[i] = lds4(buf + C::A_SC + ra * 8 + 4 * h);
-            sb[i] = lds4(buf + C::B_SC + rb * 8 + 4 * h);
-        } else {
-            sa[i] = lds4(buf + C::A_SC + ra * 4) >> (16 * h);
-            sb[i] = lds4(buf + C::B_SC + rb * 4) >> (16 * h);
-        }
-        a0[i] = lds16(buf + C::A_CODES + code_off<C::ROW>(ra, NSUB * h));
-        b0[i] = lds16(buf + C::B_CODES + code_off<C::ROW>(rb, NSUB * h));
-    }
-#define REQAT_MX_READ(A, B, S)                                                           \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                      \
-        A[i] = lds16(buf + C::A_CODES + code_off<C::ROW>(rA0 + 32 * i, NSUB * h + (S))); \
-        B[i] = lds16(buf + C::B_CODES + code_off<C::ROW>(rB0 + 32 * i, NSUB * h + (S))); \
-    }
-    REQAT_MX_READ(a1, b1, 1);
-    issue.template part<0>();
-    __builtin_amdgcn_sched_barrier(0);
-    mx_mfma16<0>(acc, a0, b0, sa, sb);
-    __builtin_amdgcn_sched_barrier(0);
-    if constexpr (NSUB == 4) {
-        REQAT_MX_READ(a0, b0, 2);
-        issue.template part<1>();
-        __builtin_amdgcn_sched_barrier(0);
-        mx_mfma16<1>(acc, a1, b1, sa, sb);
-        __builtin_amdgcn_sched_barrier(0);
-        REQAT_MX_READ(a1, b1, 3);
-        issue.template part<2>();
-        __builtin_amdgcn_sched_barrier(0);
-        mx_mfma16<2>(acc, a0, b0, sa, sb);
-        __builtin_amdgcn_sched_barrier(0);
-        issue.template part<3>();
-        __builtin_amdgcn_sched_barrier(0);
-        mx_mfma16<3>(acc, a1, b1, sa, sb);
-    } else {
-        issue.template part<1>();
-        issue.template part<2>();
-        issue.template part<3>();
-        __builtin_amdgcn_sched_barrier(0);
-        mx_mfma16<1>(acc, a1, b1, sa, sb);
-    }
-#undef REQAT_MX_READ
 }
 
 // NVFP4: one stage from LDS buffer `buf`, software-pipelined by MFMA step.
@@ -604,14 +557,21 @@ struct MxLane {
     static constexpr int NS = C::CH / 2;
     int codeA[NS], codeB[NS];                           // byte offset of this lane's unit in substep s (tile 0)
     int scA, scB;                                       // byte offset of this lane's NS scale bytes (tile 0)
+    // tile i's scale bytes sit SCSTEP * i bytes further (32 rows)
+    static constexpr int SCSTEP = 32 * (C::kGS ? C::GROW : C::SB);
     __device__ __forceinline__ MxLane(int rA0, int rB0, int h) {
 #pragma unroll
         for (int q = 0; q < NS; ++q) {
             codeA[q] = C::A_CODES + code_off<C::ROW>(rA0, NS * h + q);
             codeB[q] = C::B_CODES + code_off<C::ROW>(rB0, NS * h + q);
         }
-        scA = C::A_SC + rA0 * C::SB + NS * h;
-        scB = C::B_SC + rB0 * C::SB + NS * h;
+        if constexpr (C::kGS) {                         // within a group buffer, at the stage's 4-byte column
+            scA = rA0 * C::GROW + NS * h;
+            scB = TM * C::GROW + rB0 * C::GROW + NS * h;
+        } else {
+            scA = C::A_SC + rA0 * C::SB + NS * h;
+            scB = C::B_SC + rB0 * C::SB + NS * h;
+        }
     }
 };
 
@@ -624,7 +584,7 @@ struct MxState {
 
 template <class C>
 __device__ __forceinline__ uint32_t mx_scale_read(const uint8_t *p) {
-    if constexpr (C::CH / 2 == 4) return lds4(p);
+    if constexpr (C::CH / 2 == 4) return *reinterpret_cast<const uint32_t *>(p);
     else return *reinterpret_cast<const uint16_t *>(p);
 }
 
@@ -636,7 +596,8 @@ __device__ __forceinline__ uint32_t mx_scale_read(const uint8_t *p) {
 // second in substep 0 of the following stage.
 template <class C, int S, int NS, int K, class Issue>
 __device__ __forceinline__ void mx_part(v16f (&acc)[4][4], MxState<C> &st, const uint8_t *buf,
-                                        const uint8_t *nbuf, const MxLane<C> &ln, Issue &prev, Issue &next) {
+                                        const uint8_t *nbuf, const uint8_t *nsc, const MxLane<C> &ln, Issue &prev,
+                                        Issue &next) {
     constexpr int E = S & 1, LAST = S == NS - 1;
     constexpr int ND = LAST ? 4 : 2;
     // load parts: 8 per half, two per substep part
@@ -649,8 +610,8 @@ __device__ __forceinline__ void mx_part(v16f (&acc)[4][4], MxState<C> &st, const
     } else {
         st.a[E ^ 1][K] = lds16(nbuf + ln.codeA[0] + 32 * C::ROW * K);
         st.b[E ^ 1][K] = lds16(nbuf + ln.codeB[0] + 32 * C::ROW * K);
-        st.na[K] = mx_scale_read<C>(nbuf + ln.scA + 32 * C::SB * K);
-        st.nb[K] = mx_scale_read<C>(nbuf + ln.scB + 32 * C::SB * K);
+        st.na[K] = mx_scale_read<C>(nsc + ln.scA + MxLane<C>::SCSTEP * K);
+        st.nb[K] = mx_scale_read<C>(nsc + ln.scB + MxLane<C>::SCSTEP * K);
     }
     if constexpr (LAST) {
         next.template region<2 * K, 16>();
@@ -680,12 +641,12 @@ __device__ __forceinline__ void mx_part(v16f (&acc)[4][4], MxState<C> &st, const
 
 template <class C, int S, int NS, class Issue>
 __device__ __forceinline__ void mx_substep(v16f (&acc)[4][4], MxState<C> &st, const uint8_t *buf,
-                                           const uint8_t *nbuf, const MxLane<C> &ln, Issue &prev,
-                                           Issue &next) {
-    mx_part<C, S, NS, 0>(acc, st, buf, nbuf, ln, prev, next);
-    mx_part<C, S, NS, 1>(acc, st, buf, nbuf, ln, prev, next);
-    mx_part<C, S, NS, 2>(acc, st, buf, nbuf, ln, prev, next);
-    mx_part<C, S, NS, 3>(acc, st, buf, nbuf, ln, prev, next);
+                                           const uint8_t *nbuf, const uint8_t *nsc, const MxLane<C> &ln,
+                                           Issue &prev, Issue &next) {
+    mx_part<C, S, NS, 0>(acc, st, buf, nbuf, nsc, ln, prev, next);
+    mx_part<C, S, NS, 1>(acc, st, buf, nbuf, nsc, ln, prev, next);
+    mx_part<C, S, NS, 2>(acc, st, buf, nbuf, nsc, ln, prev, next);
+    mx_part<C, S, NS, 3>(acc, st, buf, nbuf, nsc, ln, prev, next);
 }
 
 template <class C>
@@ -701,31 +662,56 @@ __device__ __forceinline__ void load_first_half(StageIssue<C> &is) {
 // One stage of the MXFP4 stream.  Past the end of the workgroup's stages the
 // loads still go out (re-reading its first stage into a buffer nobody reads
 // again), so every stage issues exactly LPS loads and the wait before the
-// barrier is one constant: the NB - 2 stages issued after stage g + 1 may stay
-// in flight.  FIRST (a tile's first stage, after the previous tile's stores)
-// waits for everything instead.
-template <class C, int NB, bool FIRST>
+// barrier is a constant of the stage's phase: the NB - 2 stages issued after
+// stage g + 1 may stay in flight, and with scale groups (GS) also the group
+// loads issued at the start of this stage or the one before (phases 0 and 1;
+// a group is loaded at the start of phase 0, ahead of that stage's code
+// loads).  A tile's first stage (after the previous tile's stores) waits for
+// everything instead.  PH is the stage's position in its scale group (GS).
+template <class C, int NB, int PH>
 __device__ __forceinline__ void mx_stage_p(v16f (&acc)[4][4], MxState<C> &st, uint8_t *smem, int64_t gs,
-                                           const MxLane<C> &ln, StageIssue<C> &prev, StageIssue<C> &issue) {
+                                           bool first, const MxLane<C> &ln, StageIssue<C> &prev,
+                                           StageIssue<C> &issue) {
     constexpr int NS = C::CH / 2;
     const int bi = (int)(gs % NB);
     uint8_t *buf = smem + bi * C::STAGE;
     const uint8_t *nbuf = smem + (bi + 1 == NB ? 0 : bi + 1) * C::STAGE;
+    // scale bytes of stage gs + 1: its group's buffer, at the stage's column
+    const uint8_t *nsc;
+    if constexpr (C::kGS)
+        nsc = smem + C::SC_RING + (int)(((gs + 1) / C::GSTAGES) & 1) * C::GROUP + ((PH + 1) % C::GSTAGES) * C::SB;
+    else
+        nsc = nbuf;
     issue.buf = buf;                                    // stage gs + NB goes where stage gs was
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         st.sa[i] = st.na[i];
         st.sb[i] = st.nb[i];
     }
-    mx_substep<C, 0, NS>(acc, st, buf, nbuf, ln, prev, issue);
+    mx_substep<C, 0, NS>(acc, st, buf, nbuf, nsc, ln, prev, issue);
     if constexpr (NS == 4) {
-        mx_substep<C, 1, NS>(acc, st, buf, nbuf, ln, prev, issue);
-        mx_substep<C, 2, NS>(acc, st, buf, nbuf, ln, prev, issue);
+        mx_substep<C, 1, NS>(acc, st, buf, nbuf, nsc, ln, prev, issue);
+        mx_substep<C, 2, NS>(acc, st, buf, nbuf, nsc, ln, prev, issue);
     }
-    if constexpr (FIRST) wait_vmcnt<0>();
-    else wait_vmcnt<(NB - 2) * C::LPS>();
+    constexpr int kInFlight = (NB - 2) * C::LPS + (C::kGS && (PH == 0 || PH == 1) ? C::GLPW : 0);
+    if (first) wait_vmcnt<0>();
+    else wait_vmcnt<kInFlight>();
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    mx_substep<C, NS - 1, NS>(acc, st, buf, nbuf, ln, prev, issue);
+    mx_substep<C, NS - 1, NS>(acc, st, buf, nbuf, nsc, ln, prev, issue);
+}
+
+// Scale group loads (GS): wave w takes rows 64w .. 64w+63 of A and of B, 16
+// bytes (four stages) per row, into group buffer `gbuf`; edge tiles clamp rows.
+// The addresses are those of the stage loads that start the group (their
+// scale pointers and row limits).
+template <class C>
+__device__ __forceinline__ void load_scale_group(uint8_t *gbuf, int wave, int lane, const StageIssue<C> &at) {
+    const int row = 64 * wave + lane;
+    const int ra = row < at.rows_a ? row : at.rows_a - 1, rb = row < at.rows_b ? row : at.rows_b - 1;
+    const int64_t spr = at.spr;
+    const uint8_t *a_sc = at.as_, *b_sc = at.bs_;
+    g2l16(a_sc, (uint32_t)(ra * (uint32_t)spr), gbuf + wave * 1024);
+    g2l16(b_sc, (uint32_t)(rb * (uint32_t)spr), gbuf + TM * C::GROW + wave * 1024);
 }
 
 template <class C, int NB>
@@ -734,12 +720,14 @@ __device__ __forceinline__ void mx_persistent(uint8_t *smem, int64_t M, int64_t 
                                               const uint8_t *b_codes, const uint8_t *b_scales, void *y,
                                               int y_bf16, int64_t ldy, int wave, int lane) {
     constexpr int KS = 2 * C::ROW, NS = C::CH / 2;
+    constexpr int U = C::kGS ? C::GSTAGES : 1;          // stages per unrolled loop turn
     static_assert(NS % 2 == 0 && NB >= 2, "even substeps per stage");
-    static_assert((NB - 1) * C::LPS <= 63, "vmcnt range");
+    static_assert((NB - 1) * C::LPS + 2 * C::GLPW <= 63, "vmcnt range");
+    static_assert(!C::kGS || NB == C::GSTAGES, "a group starts at the stage whose loads go out in its first stage");
     const int h = lane >> 5, wm = wave >> 1, wn = wave & 1;
     const int64_t tm_n = (M + TM - 1) / TM, tn_n = (N + TN - 1) / TN, T = tm_n * tn_n;
     const int64_t G = gridDim.x, w = blockIdx.x;
-    const int nst = (int)(K / KS);
+    const int nst = (int)(K / KS);                      // a multiple of U
     const int64_t cpr = K / 2, spr = K / C::B;
     const TileGeo g0 = tile_geo(w, M, N);
 
@@ -752,11 +740,18 @@ __device__ __forceinline__ void mx_persistent(uint8_t *smem, int64_t M, int64_t 
                              a_codes + g.m0 * cpr + k0 / 2, b_codes + g.n0 * cpr + k0 / 2,
                              a_scales + g.m0 * spr + k0 / C::B, b_scales + g.n0 * spr + k0 / C::B};
     };
+    // scale group q (stream stages 4q .. 4q+3) into group buffer q & 1 (GS), from
+    // the loads of its first stage
+    auto group_at = [&](const StageIssue<C> &at, int64_t q) {
+        load_scale_group<C>(smem + C::SC_RING + (int)(q & 1) * C::GROUP, wave, lane, at);
+    };
 
-    // prologue: stages 0 .. NB-1 into buffers 0 .. NB-1 (the second half of
-    // stage NB-1 goes out in substep 0 of stage 0), then wait for stage 0
+    // prologue: scale group 0 (GS), stages 0 .. NB-1 into buffers 0 .. NB-1
+    // (the second half of stage NB-1 goes out in substep 0 of stage 0), then
+    // wait for stage 0
     LoadPos<C> ld{w, 0, g0};
     StageIssue<C> prev = issue_at(ld, smem);
+    if constexpr (C::kGS) group_at(prev, 0);
 #pragma unroll
     for (int p = 0; p < NB; ++p) {
         prev = issue_at(ld, smem + p * C::STAGE);
@@ -769,12 +764,13 @@ __device__ __forceinline__ void mx_persistent(uint8_t *smem, int64_t M, int64_t 
 
     const MxLane<C> ln(wm * 128 + (lane & 31), wn * 128 + (lane & 31), h);
     MxState<C> st;
+    const uint8_t *sc0 = C::kGS ? smem + C::SC_RING : smem;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         st.a[0][i] = lds16(smem + ln.codeA[0] + 32 * C::ROW * i);
         st.b[0][i] = lds16(smem + ln.codeB[0] + 32 * C::ROW * i);
-        st.na[i] = mx_scale_read<C>(smem + ln.scA + 32 * C::SB * i);
-        st.nb[i] = mx_scale_read<C>(smem + ln.scB + 32 * C::SB * i);
+        st.na[i] = mx_scale_read<C>(sc0 + ln.scA + MxLane<C>::SCSTEP * i);
+        st.nb[i] = mx_scale_read<C>(sc0 + ln.scB + MxLane<C>::SCSTEP * i);
     }
 
     int64_t gs = 0;                                     // stream position (buffer gs % NB)
@@ -784,18 +780,18 @@ __device__ __forceinline__ void mx_persistent(uint8_t *smem, int64_t M, int64_t 
         for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j) acc[i][j] = v16f{};
-        {
-            StageIssue<C> issue = issue_at(ld, smem);
-            mx_stage_p<C, NB, true>(acc, st, smem, gs, ln, prev, issue);
-            ld.advance(nst, G, M, N);
-            prev = issue;
-            ++gs;
-        }
-        for (int s = 1; s < nst; ++s, ++gs) {
-            StageIssue<C> issue = issue_at(ld, smem);
-            mx_stage_p<C, NB, false>(acc, st, smem, gs, ln, prev, issue);
-            ld.advance(nst, G, M, N);
-            prev = issue;
+        for (int s = 0; s < nst; s += U) {
+            static_for<0, U>([&](auto P) {
+                constexpr int ph = decltype(P)::value;
+                StageIssue<C> issue = issue_at(ld, smem);   // stage gs + NB
+                // the group after this one starts at stage gs + NB (NB == 4):
+                // loaded ahead of this stage's code loads
+                if constexpr (C::kGS && ph == 0) group_at(issue, gs / U + 1);
+                mx_stage_p<C, NB, ph>(acc, st, smem, gs, s == 0 && ph == 0, ln, prev, issue);
+                ld.advance(nst, G, M, N);
+                prev = issue;
+                ++gs;
+            });
         }
         store_tile(acc, tile_geo(v, M, N), M, N, wm, wn, lane, 1.0f, y, y_bf16, ldy);
     }
@@ -803,92 +799,22 @@ __device__ __forceinline__ void mx_persistent(uint8_t *smem, int64_t M, int64_t 
     wait_vmcnt<0>();
 }
 
-template <int FMT, int KS, int NBUF>
+template <int FMT, int KS, int NBUF, bool GS>
 __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(
     int64_t M, int64_t N, int64_t K, const uint8_t *__restrict__ a_codes,
     const uint8_t *__restrict__ a_scales, const float *__restrict__ ga,
     const uint8_t *__restrict__ b_codes, const uint8_t *__restrict__ b_scales,
     const float *__restrict__ gb, void *__restrict__ y, int y_bf16, int64_t ldy) {
-    using C = Cfg<FMT, KS, NBUF>;
+    using C = Cfg<FMT, KS, NBUF, GS>;
     extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    if constexpr (FMT == kNV) {
+    if constexpr (FMT == kNV)
         nv_persistent<C>(smem, M, N, K, a_codes, a_scales, uniform_load(ga) * uniform_load(gb), b_codes,
                          b_scales, y, y_bf16, ldy, wave, lane);
-        return;
-    } else if constexpr (REQAT_MX_PERSISTENT) {
+    else
         mx_persistent<C, NBUF>(smem, M, N, K, a_codes, a_scales, b_codes, b_scales, y, y_bf16, ldy, wave, lane);
-        return;
-    }
-    const int h = lane >> 5;
-    const int wm = wave >> 1, wn = wave & 1;
-
-    // ---- tile order: XCD-contiguous ranges, then groups of GROUP_M tile-rows
-    const int64_t tm_n = (M + TM - 1) / TM, tn_n = (N + TN - 1) / TN, T = tm_n * tn_n;
-    const int64_t bid = blockIdx.x;
-    const int64_t xcd = bid % 8, local = bid / 8, per = T / 8, rem = T % 8;
-    const int64_t t = xcd * per + (xcd < rem ? xcd : rem) + local;
-    const int64_t width = GROUP_M * tn_n;
-    const int64_t first_m = (t / width) * GROUP_M;
-    const int64_t gsz = (tm_n - first_m) < GROUP_M ? (tm_n - first_m) : GROUP_M;
-    const int64_t tm = first_m + (t % width) % gsz, tn = (t % width) / gsz;
-    const int64_t m0 = tm * TM, n0 = tn * TN;
-    const int64_t cpr = K / 2, spr = K / C::B;
-
-    v16f acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-    const int nst = (int)(K / KS);
-    const int rows_a = (int)(M - m0 < TM ? M - m0 : TM), rows_b = (int)(N - n0 < TN ? N - n0 : TN);
-    const uint8_t *ac = a_codes + m0 * cpr, *bc = b_codes + n0 * cpr;
-    const uint8_t *as_ = a_scales + m0 * spr, *bs_ = b_scales + n0 * spr;
-
-    const int rA0 = wm * 128 + (lane & 31);               // this lane's A row in tile i: rA0 + 32 i
-    const int rB0 = wn * 128 + (lane & 31);
-
-    {
-        // prologue: the first NBUF - 1 stages
-#pragma unroll
-        for (int p = 0; p < NBUF - 1; ++p) {
-            if (p < nst)
-                load_range<C, 0, C::LPS>(smem + p * C::STAGE, wave, lane, rows_a, rows_b, cpr, spr,
-                                         ac + (int64_t)p * KS / 2, bc + (int64_t)p * KS / 2,
-                                         as_ + (int64_t)p * KS / C::B, bs_ + (int64_t)p * KS / C::B);
-        }
-        for (int st = 0; st < nst; ++st) {
-            // stage st has landed once no more than (stages issued after it) x LPS loads remain
-            const int behind = (nst - 1 - st) < (NBUF - 2) ? (nst - 1 - st) : (NBUF - 2);
-            if (NBUF >= 3 && behind == NBUF - 2) wait_vmcnt<(NBUF >= 3 ? NBUF - 2 : 0) * C::LPS>();
-            else if (NBUF >= 4 && behind == 1) wait_vmcnt<C::LPS>();
-            else wait_vmcnt<0>();
-            // A bare barrier: __syncthreads() would also drain every load still in
-            // flight for later stages.  This wave's loads of stage st are done (vmcnt
-            // above) and its LDS reads of the buffer about to be refilled are done
-            // (lgkmcnt), so after the barrier stage st is complete for every wave.
-            asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-
-            const uint8_t *buf = smem + (st % NBUF) * C::STAGE;
-            const int nx = st + NBUF - 1;                      // stage whose loads go out now
-            const int64_t kx = (int64_t)nx * KS;
-            StageIssue<C> issue{smem + (nx % NBUF) * C::STAGE, nx < nst, wave, lane, rows_a, rows_b,
-                                cpr, spr, ac + kx / 2, bc + kx / 2, as_ + kx / C::B, bs_ + kx / C::B};
-            mx_stage<C>(acc, buf, rA0, rB0, h, issue);
-        }
-    }
-
-    TileGeo geo;
-    geo.m0 = m0;
-    geo.n0 = n0;
-    geo.rows_a = rows_a;
-    geo.rows_b = rows_b;
-    store_tile(acc, geo, M, N, wm, wn, lane, 1.0f, y, y_bf16, ldy);
 }
 
 // Compute units of the current device (cached per device).
@@ -903,22 +829,20 @@ int compute_units() {
     return n;
 }
 
-template <int FMT, int KS, int NBUF>
+template <int FMT, int KS, int NBUF, bool GS>
 hipError_t launch_cfg(int64_t M, int64_t N, int64_t K, const uint8_t *a_codes, const uint8_t *a_scales,
                       const float *ga, const uint8_t *b_codes, const uint8_t *b_scales,
                       const float *gb, void *y, bool y_bf16, int64_t ldy, hipStream_t stream) {
     int64_t grid = ((M + TM - 1) / TM) * ((N + TN - 1) / TN);
-    if (FMT == kNV || REQAT_MX_PERSISTENT) {
-        // persistent: one workgroup per CU (a multiple of 8 keeps each one on its XCD)
-        const int cus = compute_units();
-        if (cus <= 0) return hipErrorInvalidDevice;
-        if (grid > cus) grid = cus;
-    }
-    const size_t lds = Cfg<FMT, KS, NBUF>::TOTAL;
-    hipError_t e = hipFuncSetAttribute((const void *)gemm_tile256_kernel<FMT, KS, NBUF>,
+    // persistent: one workgroup per CU (a multiple of 8 keeps each one on its XCD)
+    const int cus = compute_units();
+    if (cus <= 0) return hipErrorInvalidDevice;
+    if (grid > cus) grid = cus;
+    const size_t lds = Cfg<FMT, KS, NBUF, GS>::TOTAL;
+    hipError_t e = hipFuncSetAttribute((const void *)gemm_tile256_kernel<FMT, KS, NBUF, GS>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((gemm_tile256_kernel<FMT, KS, NBUF>), dim3((unsigned)grid), dim3(kThreads), lds,
+    hipLaunchKernelGGL((gemm_tile256_kernel<FMT, KS, NBUF, GS>), dim3((unsigned)grid), dim3(kThreads), lds,
                        stream, M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, (int)y_bf16,
                        ldy);
     return hipGetLastError();
@@ -937,11 +861,18 @@ hipError_t launch_gemm_tile256(Fmt fmt, int64_t M, int64_t N, int64_t K, const u
                                const uint8_t *a_scales, const float *ga, const uint8_t *b_codes,
                                const uint8_t *b_scales, const float *gb, void *y, bool y_bf16,
                                int64_t ldy, hipStream_t stream) {
-    if (fmt == kMX)
-        return launch_cfg<kMX, REQAT_MX_KS, REQAT_MX_NBUF>(M, N, K, a_codes, a_scales, ga, b_codes,
-                                                           b_scales, gb, y, y_bf16, ldy, stream);
-    return launch_cfg<kNV, REQAT_NV_KS, REQAT_NV_NBUF>(M, N, K, a_codes, a_scales, ga, b_codes,
-                                                       b_scales, gb, y, y_bf16, ldy, stream);
+    if (fmt == kMX) {
+        // scale groups need whole groups of four stages per tile and 16-byte aligned group loads
+        const bool gs = K % (4 * REQAT_MX_KS) == 0 && (reinterpret_cast<uintptr_t>(a_scales) & 15u) == 0 &&
+                        (reinterpret_cast<uintptr_t>(b_scales) & 15u) == 0;
+        if (gs)
+            return launch_cfg<kMX, REQAT_MX_KS, REQAT_MX_NBUF, true>(M, N, K, a_codes, a_scales, ga, b_codes,
+                                                                     b_scales, gb, y, y_bf16, ldy, stream);
+        return launch_cfg<kMX, REQAT_MX_KS, REQAT_MX_NBUF, false>(M, N, K, a_codes, a_scales, ga, b_codes,
+                                                                  b_scales, gb, y, y_bf16, ldy, stream);
+    }
+    return launch_cfg<kNV, REQAT_NV_KS, REQAT_NV_NBUF, false>(M, N, K, a_codes, a_scales, ga, b_codes,
+                                                              b_scales, gb, y, y_bf16, ldy, stream);
 }
 
 }  // namespace reqat

@@ -481,6 +481,15 @@ def test_gemm_parity(fmt, M, N, K):
     run_gemm_case(fmt, M, N, K, seed=M * 31 + N * 7 + K, dist="student_t")
 
 
+@pytest.mark.parametrize("fmt,K", [(MX, 1024), (MX, 1152), (NV, 1024)])
+def test_gemm_many_tiles_per_workgroup(fmt, K):
+    """More 256 x 256 tiles than workgroups (17 x 17 = 289), ragged edge tiles
+    (4200 = 16*256 + 104 rows, 4100 = 16*256 + 4 columns); for MXFP4, K = 1024
+    takes the grouped scale loads (K % 512 == 0) and K = 1152 the per-stage ones."""
+    log("gemm many tiles fmt=%d K=%d" % (fmt, K))
+    run_gemm_case(fmt, 4200, 4100, K, seed=K + fmt, dist="student_t", all_points=False)
+
+
 def test_gemm_given_scales_nv():
     log("gemm NV given scales")
     run_gemm_case(NV, 64, 96, 256, seed=5, g=(0.0123, 3.5))
