@@ -9,6 +9,16 @@
 // counts only the loads of the stages still in flight behind it (vmcnt) and is
 // followed by a bare s_barrier (no fence that would drain those loads).
 //
+// The direct-to-LDS loads of a CU are bound by how many distinct cache lines
+// they touch, not by their bytes (measured on gfx950: sixteen 64-byte row
+// pieces per instruction ran at about 60% of the rate of eight whole 128-byte
+// lines).  So MXFP4 with K % 512 == 0 (and 16-byte aligned scales) runs
+// K = 256 per stage in two buffers, each code row a whole line per stage, and
+// keeps its scale bytes out of the stages: 16 bytes per row (two stages) go
+// to LDS in one 1 KB load per 64 rows, into a ring of two group buffers
+// (loaded per stage, 4 bytes per row, they touched one line per 4 bytes).
+// Other MXFP4 shapes run K = 128 per stage in four buffers.
+//
 // LDS code layout: one row = CH chunks of 16 B (32 E2M1 codes each); chunk c of
 // row r is stored at chunk position c ^ f(r).  A wave's 16-byte operand read
 // puts consecutive rows at the same logical chunk on consecutive lanes, and f
@@ -46,11 +56,20 @@
 #include "fp4_device.h"
 #include "internal.h"
 
+// MXFP4 stages: with scale groups (K % 512 == 0), K = 256 per stage in two
+// buffers (each code row a whole 128-byte line per stage); otherwise K = 128
+// in four buffers.
 #ifndef REQAT_MX_KS
 #define REQAT_MX_KS 128
 #endif
 #ifndef REQAT_MX_NBUF
 #define REQAT_MX_NBUF 4
+#endif
+#ifndef REQAT_MX_GS_KS
+#define REQAT_MX_GS_KS 256
+#endif
+#ifndef REQAT_MX_GS_NBUF
+#define REQAT_MX_GS_NBUF 2
 #endif
 #ifndef REQAT_NV_KS
 #define REQAT_NV_KS 256
@@ -106,7 +125,7 @@ struct Cfg {
     static constexpr int A_CODES = 0, B_CODES = CODE;
     static constexpr int A_SC = 2 * CODE, B_SC = 2 * CODE + SCALE;
     static constexpr int STAGE = GS ? 2 * CODE : 2 * CODE + 2 * SCALE;
-    static constexpr int GSTAGES = 4;                   // stages per scale group (GS)
+    static constexpr int GSTAGES = SB <= 16 ? 16 / SB : 1;   // stages per scale group: 16 bytes per row (GS)
     static constexpr int GROW = GSTAGES * SB;           // scale bytes per row per group (GS)
     static constexpr int GROUP = 2 * TM * GROW;         // bytes of a scale group buffer: A rows, then B rows
     static constexpr int SC_RING = NBUF * STAGE;        // offset of the two scale group buffers (GS)
@@ -118,7 +137,8 @@ struct Cfg {
     static_assert(CH == 4 || CH == 8, "row must be 4 or 8 chunks");
     static_assert(SINS % 4 == 0 && (CODE / 1024) % 4 == 0, "loads must split over 4 waves");
     static_assert(TOTAL <= 160 * 1024, "LDS budget");
-    static_assert(!GS || (FMT == kMX && GROW == 16 && GLPW == 2), "scale groups: 16 bytes per row, 2 loads per wave");
+    static_assert(!GS || (FMT == kMX && GROW == 16 && GLPW == 2 && GSTAGES >= 2),
+                  "scale groups: 16 bytes per row, 2 loads per wave");
 };
 
 // Direct-to-LDS loads: lane i's 16 (4) bytes at base + voff land at LDS
@@ -659,15 +679,27 @@ __device__ __forceinline__ void load_first_half(StageIssue<C> &is) {
     is.template region<0, 2>();
 }
 
+// Scale-group loads issued after the last code load of stage g + 1 and before
+// the wait in stage g (phase PH = g % GS_): one at the start of each stage
+// j in [g + 3 - NB, g] with j % GS_ == 0 (stage g + 1's second half goes out
+// in substep 0 of stage g + 2 - NB, after that stage's group loads).
+template <int NB, int GS_, int PH>
+constexpr int groups_after() {
+    int n = 0;
+    for (int d = 0; d <= NB - 3; ++d)
+        if (((PH - d) % GS_ + GS_) % GS_ == 0) ++n;
+    return n;
+}
+
 // One stage of the MXFP4 stream.  Past the end of the workgroup's stages the
 // loads still go out (re-reading its first stage into a buffer nobody reads
 // again), so every stage issues exactly LPS loads and the wait before the
 // barrier is a constant of the stage's phase: the NB - 2 stages issued after
 // stage g + 1 may stay in flight, and with scale groups (GS) also the group
-// loads issued at the start of this stage or the one before (phases 0 and 1;
-// a group is loaded at the start of phase 0, ahead of that stage's code
-// loads).  A tile's first stage (after the previous tile's stores) waits for
-// everything instead.  PH is the stage's position in its scale group (GS).
+// loads issued since (a group is loaded at the start of its phase-0 stage,
+// ahead of that stage's code loads).  A tile's first stage (after the
+// previous tile's stores) waits for everything instead.  PH is the stage's
+// position in its scale group (GS).
 template <class C, int NB, int PH>
 __device__ __forceinline__ void mx_stage_p(v16f (&acc)[4][4], MxState<C> &st, uint8_t *smem, int64_t gs,
                                            bool first, const MxLane<C> &ln, StageIssue<C> &prev,
@@ -693,7 +725,7 @@ __device__ __forceinline__ void mx_stage_p(v16f (&acc)[4][4], MxState<C> &st, ui
         mx_substep<C, 1, NS>(acc, st, buf, nbuf, nsc, ln, prev, issue);
         mx_substep<C, 2, NS>(acc, st, buf, nbuf, nsc, ln, prev, issue);
     }
-    constexpr int kInFlight = (NB - 2) * C::LPS + (C::kGS && (PH == 0 || PH == 1) ? C::GLPW : 0);
+    constexpr int kInFlight = (NB - 2) * C::LPS + C::GLPW * groups_after<NB, C::GSTAGES, PH>();
     if (first) wait_vmcnt<0>();
     else wait_vmcnt<kInFlight>();
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
@@ -863,11 +895,12 @@ hipError_t launch_gemm_tile256(Fmt fmt, int64_t M, int64_t N, int64_t K, const u
                                int64_t ldy, hipStream_t stream) {
     if (fmt == kMX) {
         // scale groups need whole groups of four stages per tile and 16-byte aligned group loads
-        const bool gs = K % (4 * REQAT_MX_KS) == 0 && (reinterpret_cast<uintptr_t>(a_scales) & 15u) == 0 &&
+        constexpr int kGroupK = Cfg<kMX, REQAT_MX_GS_KS, REQAT_MX_GS_NBUF, true>::GSTAGES * REQAT_MX_GS_KS;
+        const bool gs = K % kGroupK == 0 && (reinterpret_cast<uintptr_t>(a_scales) & 15u) == 0 &&
                         (reinterpret_cast<uintptr_t>(b_scales) & 15u) == 0;
         if (gs)
-            return launch_cfg<kMX, REQAT_MX_KS, REQAT_MX_NBUF, true>(M, N, K, a_codes, a_scales, ga, b_codes,
-                                                                     b_scales, gb, y, y_bf16, ldy, stream);
+            return launch_cfg<kMX, REQAT_MX_GS_KS, REQAT_MX_GS_NBUF, true>(M, N, K, a_codes, a_scales, ga, b_codes,
+                                                                           b_scales, gb, y, y_bf16, ldy, stream);
         return launch_cfg<kMX, REQAT_MX_KS, REQAT_MX_NBUF, false>(M, N, K, a_codes, a_scales, ga, b_codes,
                                                                   b_scales, gb, y, y_bf16, ldy, stream);
     }
