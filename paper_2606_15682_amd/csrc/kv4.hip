@@ -8,7 +8,9 @@
 //   tensor_amax <= 3.5 * 448 * 2^k), elements rounded to nearest, ties to the
 //   even code; a block with a non-finite d gets scale 0x7F and zero codes.
 // Every decision compares d (FP32, exact in FP64) with products of at most
-// 31 significant bits, so FP64 comparisons decide exactly.
+// 31 significant bits, so FP64 comparisons decide exactly; with a power-of-two
+// g (every computed g) the element thresholds have at most 8 bits and the
+// comparisons run in FP32, exactly as well.
 //
 // One lane per 16-channel block in a grid-stride loop; the shift vector is
 // read with the block (it is small and stays in cache).  A computed g takes
@@ -126,6 +128,19 @@ __device__ __forceinline__ uint32_t e1m2_mag(double a, double S) {
     return m;
 }
 
+// The same with FP32 thresholds, exact when S = s * g is a power-of-two
+// multiple of an E4M3 value inside the FP32 range: (0.5 i + 0.25) * S has at
+// most 8 significant bits and lies in [2^-137, 2^111].
+__device__ __forceinline__ uint32_t e1m2_mag_f32(float a, float S) {
+    uint32_t m = 7u;
+#pragma unroll
+    for (int i = 6; i >= 0; --i) {
+        const float t = (0.5f * (float)i + 0.25f) * S;
+        if (a < t || (a == t && (i & 1) == 0)) m = (uint32_t)i;
+    }
+    return m;
+}
+
 template <int OUT>
 __global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
     const uint16_t *__restrict__ x, int64_t rows, int64_t cols, int64_t ldx, const float *__restrict__ shift,
@@ -151,6 +166,10 @@ __global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
         g = *gptr;
     }
     const double gd = (double)g;
+    // FP32 element path: g a power of two in [2^-126, 2^100] (a computed g
+    // always is), so every threshold and decoded value is exact in FP32
+    const uint32_t gb = bits_from_f32(g);
+    const bool f32 = (gb & 0x807FFFFFu) == 0u && gb >= 0x00800000u && gb <= ((100u + 127u) << 23);
 
     const int64_t nb = cols / 16, total = rows * nb;
     const bool narrow = total < (int64_t(1) << 32);
@@ -167,11 +186,20 @@ __global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
         const bool bad = am >= 0x7F800000u;
         const uint32_t sbyte = bad ? 0x7Fu : (am == 0u ? 0u : kv4_scale_byte((double)f32_from_bits(am), gd));
         const double S = (double)e4m3_value(sbyte) * gd;
+        const float Sf = e4m3_value(sbyte) * g;             // exact on the FP32 path
         uint32_t c[16];
+        if (f32) {
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const uint32_t sign = (bits_from_f32(d[j]) >> 28) & 8u;
-            c[j] = bad ? 0u : (sbyte == 0u ? sign : (e1m2_mag(__builtin_fabs((double)d[j]), S) | sign));
+            for (int j = 0; j < 16; ++j) {
+                const uint32_t sign = (bits_from_f32(d[j]) >> 28) & 8u;
+                c[j] = bad ? 0u : (sbyte == 0u ? sign : (e1m2_mag_f32(__builtin_fabsf(d[j]), Sf) | sign));
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const uint32_t sign = (bits_from_f32(d[j]) >> 28) & 8u;
+                c[j] = bad ? 0u : (sbyte == 0u ? sign : (e1m2_mag(__builtin_fabs((double)d[j]), S) | sign));
+            }
         }
         if (OUT == kCodes) {
             uint32_t lo = 0, hi = 0;
@@ -191,8 +219,15 @@ __global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
 #pragma unroll
                 for (int k = 0; k < 2; ++k) {
                     const uint32_t cc = c[2 * i + k];
-                    const double v = 0.5 * (double)(cc & 7u) * (sbyte == 0u ? 0.0 : S);
-                    h[k] = bad ? 0x7FC0u : (bf16_rne_from_double(v) | ((cc & 8u) << 12));
+                    uint32_t mag;
+                    if (f32) {
+                        const float v = 0.5f * (float)(cc & 7u) * (sbyte == 0u ? 0.0f : Sf);
+                        mag = bf16_rne_from_float(v);
+                    } else {
+                        const double v = 0.5 * (double)(cc & 7u) * (sbyte == 0u ? 0.0 : S);
+                        mag = bf16_rne_from_double(v);
+                    }
+                    h[k] = bad ? 0x7FC0u : (mag | ((cc & 8u) << 12));
                 }
                 o[i] = h[0] | (h[1] << 16);
             }

@@ -258,6 +258,18 @@ def test_kv4_exhaustive_patterns_and_specials():
     sh[:16] = -3.0e38                     # 0x7F7F - (-3e38) overflows FP32: a NaN block
     assert_kv4_parity(x, sh)
     assert_kv4_parity(x, None, g=2.0 ** -12)          # caller's g too small: 448 and saturation
+    # FP32 element thresholds (power-of-two g up to 2^100): the smallest g (E4M3
+    # subnormal scales times 2^-126 are FP32 subnormals) and the largest; above
+    # 2^100 and for other g the FP64 comparisons run
+    for g in (2.0 ** -126, 2.0 ** 100, 2.0 ** 101, 3.0 * 2.0 ** 90):
+        assert_kv4_parity(pats[:8], shift, g=g)
+    tiny = np.arange(1, 1025, dtype=np.uint16).reshape(32, 32)       # BF16 subnormals and the smallest normals
+    tiny[1] = 1 + np.arange(32) % 3                                  # E4M3 subnormal scale bytes
+    tiny[3] = 1
+    tiny[5] = 1 + np.arange(32) % 6
+    tiny[::2] |= 0x8000
+    assert_kv4_parity(tiny, None)                                   # computed g = 2^-126: subnormal S
+    assert_kv4_parity(tiny, None, g=2.0 ** -126)
     assert_kv4_parity(_rand(45, 320, 19, "student_t"), np.linspace(-2, 2, 320).astype(np.float32), ldx_pad=24)
 
 
