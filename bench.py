@@ -86,6 +86,48 @@ def copy_calibration(nbytes: int, steps: int):
     print(json.dumps({"copy_bytes": src.numel() * 4, "steps": steps}), flush=True)
 
 
+def practical_ceilings(x=None, wt=None, steps=10):
+    """Context, not targets: what a plain device copy and the vendor library's
+    bfloat16 GEMM of the same shape (no quantization; hipBLASLt through torch)
+    reach on this GPU.  Neither is on the product path."""
+    import torch
+    out = {}
+    n = 1 << 28                                         # 1 GiB of float32 per buffer
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(steps):
+        dst.copy_(src)
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / steps
+    out["copy_GBps"] = round(2.0 * n * 4 / (ms * 1e-3) / 1e9, 1)
+    del src, dst
+    if x is not None and wt is not None and x.shape[0] > 64:
+        # W^T made contiguous: a plain (non-batched) NN product
+        b = wt.t().contiguous()
+        y = torch.mm(x, b)
+        torch.cuda.synchronize()
+        ev[0].record()
+        for _ in range(steps):
+            torch.mm(x, b, out=y)
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / steps
+        M, K = x.shape
+        N = b.shape[1]
+        out["bf16_library_gemm_TFLOPs"] = round(2.0 * M * N * K / (ms * 1e-3) / 1e12, 1)
+        out["bf16_library_gemm_ms"] = round(ms, 4)
+        del b, y
+    torch.cuda.empty_cache()
+    out["note"] = ("device copy of 1 GiB (read + write bytes); torch.mm of the same bfloat16 "
+                   "operands, unquantized (vendor GEMM)")
+    return out
+
+
 def cpu_baseline(w, xb, wb):
     """Time the CPU oracle (single thread, as it stands) on a bounded sample of
     the same step and scale its per-element / per-MAC rates to the full step."""
@@ -178,6 +220,7 @@ def bench_w4a16(args, w):
         "kernels": {"gemm_w4a16": {"ms": round(ms_kernel, 4), "GB/s": round(gbs, 1),
                                    "TFLOP/s": round(flops / (ms_kernel * 1e-3) / 1e12, 2)}},
     }
+    out["ceilings"] = practical_ceilings()
     if not args.no_cpu_baseline:
         import oracle
         xb, wb = wl.bf16_bits(x_cpu), wl.bf16_bits(w_cpu)
@@ -258,6 +301,7 @@ def bench_sem(args, w):
         "kernels": {"sem_forward": {"ms": round(fwd, 4), "GB/s": round(b_fwd / (fwd * 1e-3) / 1e9, 1)},
                     "sem_backward": {"ms": round(bwd, 4), "GB/s": round(gbs_bwd, 1)}},
     }
+    out["ceilings"] = practical_ceilings()
     if not args.no_cpu_baseline:
         import oracle
         rows = 64
@@ -445,6 +489,7 @@ def main():
         "roofline": roofline,
         "kernels": kern,
     }
+    out["ceilings"] = practical_ceilings(x, wt)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, wl.bf16_bits(x_cpu), wl.bf16_bits(w_cpu))
     print(json.dumps(out), flush=True)
