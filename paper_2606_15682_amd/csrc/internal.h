@@ -67,7 +67,7 @@ hipError_t launch_sem_backward(const uint16_t *logits, int64_t T, int64_t V, int
                                bool grad_bf16, int64_t ldg, hipStream_t stream);
 
 bool gemm_tile256_supported(Fmt fmt, int64_t M, int64_t N, int64_t K, int64_t ldy);
-// Skinny product for M <= 64 (K % 64 == 0, K > 0).
+// Skinny product for M <= 64 (K % 128 == 0, K > 0).
 hipError_t launch_gemm_skinny(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *a_codes,
                               const uint8_t *a_scales, const float *ga, const uint8_t *b_codes,
                               const uint8_t *b_scales, const float *gb, void *y, bool y_bf16, int64_t ldy,
