@@ -4,10 +4,12 @@
 One step = one pass of the whole hot path over the 14B-like NVFP4 MLP gate/up
 projection (X[4096 x 5120] activations with 1% outlier channels, W[27648 x 5120]
 = gate || up weights, both bfloat16, seeded synthetic):
-  quantize X (dynamic global scale, one pass over X plus a small fix-up kernel),
-  quantize W (dynamic global scale),
-  W4A4 GEMM Y = X^ W^T (FP32 accumulation, bfloat16 output),
-  fake-quant X and W (the QAT forward's quantize-dequantize, bfloat16 out).
+  quantize and fake-quant X in one pass (codes + scales for the product, and
+    the QAT forward's quantize-dequantize in bfloat16; dynamic global scale:
+    one pass over X plus a small fix-up kernel),
+  the same for W,
+  W4A4 GEMM Y = X^ W^T (FP32 accumulation, bfloat16 output).
+The separate quantize and fake-quant entry points are timed apart as well.
 All inputs are resident in HBM before timing starts.  Prints ONE JSON line.
 
 value = 2*M*N*K / step time (TFLOP/s of the layer, whole step).  The roofline
@@ -366,28 +368,26 @@ def main():
     y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
     fx = torch.empty_like(x)
     fw = torch.empty_like(wt)
-    names = ["quantize_x", "quantize_w", "gemm", "fakequant_x", "fakequant_w"]
+    names = ["quantize_fakequant_x", "quantize_fakequant_w", "gemm"]
 
     def step(ev=None):
+        # X and W each quantized (codes for the product) and fake-quantized
+        # (the QAT forward's bfloat16 values) in one pass over the input
         def mark(i):
             if ev is not None:
                 ev[i].record()
         mark(0)
-        reqat.quantize(x, fmt, out=(xc, xs), g_out=gx)
+        reqat.quantize_fakequant(x, fmt, out=(xc, xs, fx), g_out=gx)
         mark(1)
-        reqat.quantize(wt, fmt, out=(wc, wsc), g_out=gw)
+        reqat.quantize_fakequant(wt, fmt, out=(wc, wsc, fw), g_out=gw)
         mark(2)
         reqat.gemm(fmt, xc, xs, gx, wc, wsc, gw, out_dtype=torch.bfloat16, out=y)
         mark(3)
-        reqat.fakequant(x, fmt, out=fx, g_out=gfx)
-        mark(4)
-        reqat.fakequant(wt, fmt, out=fw, g_out=gfw)
-        mark(5)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -397,6 +397,23 @@ def main():
     ms_step = (t1 - t0) * 1e3 / args.steps
     per = {n: float(np.mean([events[i][j].elapsed_time(events[i][j + 1]) for i in range(args.steps)]))
            for j, n in enumerate(names)}
+
+    # the separate entry points (quantize alone, fake-quant alone), timed apart
+    def timed(fn):
+        for _ in range(max(1, args.warmup)):
+            fn()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        e[0].record()
+        for _ in range(args.steps):
+            fn()
+        e[1].record()
+        torch.cuda.synchronize()
+        return e[0].elapsed_time(e[1]) / args.steps
+    per["quantize_x"] = timed(lambda: reqat.quantize(x, fmt, out=(xc, xs), g_out=gx))
+    per["quantize_w"] = timed(lambda: reqat.quantize(wt, fmt, out=(wc, wsc), g_out=gw))
+    per["fakequant_x"] = timed(lambda: reqat.fakequant(x, fmt, out=fx, g_out=gfx))
+    per["fakequant_w"] = timed(lambda: reqat.fakequant(wt, fmt, out=fw, g_out=gfw))
 
     # the same activation quantize + product through the one-call linear entry
     # point (a kernel right before the product on the same stream), timed apart
@@ -432,6 +449,7 @@ def main():
     flops = 2.0 * M * N * K
     q_bytes = lambda rows: rows * K * (2 + 0.5 + 1.0 / B)        # read bf16, write codes + scales
     fq_bytes = lambda rows: rows * K * 4.0                        # read bf16, write bf16
+    qfq_bytes = lambda rows: rows * K * (4 + 0.5 + 1.0 / B)      # read bf16, write codes + scales + bf16
     gemm_tflops = flops / (per["gemm"] * 1e-3) / 1e12
     mfma_dtype = "f16" if fmt == reqat.NVFP4 else "fp4"
     kern = {
@@ -439,13 +457,15 @@ def main():
                  "frac_fp4_peak": round(gemm_tflops / PEAK["fp4"], 4),
                  "frac_own_mfma_peak": round(gemm_tflops / PEAK[mfma_dtype], 4)},
     }
-    for n, rows, fn in (("quantize_x", M, q_bytes), ("quantize_w", N, q_bytes),
+    for n, rows, fn in (("quantize_fakequant_x", M, qfq_bytes), ("quantize_fakequant_w", N, qfq_bytes),
+                        ("quantize_x", M, q_bytes), ("quantize_w", N, q_bytes),
                         ("fakequant_x", M, fq_bytes), ("fakequant_w", N, fq_bytes)):
         gbs = fn(rows) / (per[n] * 1e-3) / 1e9
         kern[n] = {"ms": round(per[n], 4), "GB/s": round(gbs, 1),
                    "frac_hbm_peak": round(gbs / PEAK["hbm"], 4),
                    "note": ("one pass + scale fix-up kernel (computed g); credited bytes = read x + writes"
-                            if fmt == reqat.NVFP4 else "credited bytes = read x + writes")}
+                            if fmt == reqat.NVFP4 else "credited bytes = read x + writes")
+                           + ("" if n.startswith("quantize_fakequant") else "; timed apart, not in the step")}
 
     if M <= 64:
         # decode shape: the product streams the weights once, so it is bounded by HBM
@@ -484,8 +504,8 @@ def main():
         "data": "synthetic (seeded; Gaussian activations with 1% x20 outlier channels, N(0,0.02) weights)",
         "config": {"workload": w.name, "M": M, "N": N, "K": K, "format": w.fmt,
                    "gemm_out": "bf16", "global_batch": M, "parallelism": "single GPU",
-                   "step": "quantize X + quantize W (dynamic global scales) + W4A4 GEMM + "
-                           "fake-quant X and W"},
+                   "step": "quantize + fake-quant X, quantize + fake-quant W (one pass each, "
+                           "dynamic global scales) + W4A4 GEMM"},
         "roofline": roofline,
         "kernels": kern,
     }

@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define REQAT_ABI_VERSION 7
+#define REQAT_ABI_VERSION 8
 
 typedef enum {
     REQAT_FMT_NVFP4 = 0, /* B = 16, E4M3 block scale, FP32 global scale */
@@ -114,11 +114,32 @@ reqat_status reqat_quantize_fp4(reqat_format fmt, const void *x, int64_t rows, i
  * Sec. 4 Stage-2 QAT; every linear layer, App. D.1).  Same rules and
  * tensor-scale handling as reqat_quantize_fp4; y[rows][ldy] bfloat16.
  * Requirements: cols % B == 0; x, y 16-byte aligned; ldx % 8 == 0, ldy % 8 == 0.
- * y may alias x only when ldy == ldx (in-place).
+ * In place (y == x, ldy == ldx) is allowed for MXFP4 and for NVFP4 with a
+ * given tensor scale; any other overlap of y with x, and in place with
+ * NVFP4 and REQAT_TS_COMPUTE (whose second pass re-reads x), returns
+ * REQAT_E_UNSUPPORTED.
  */
 reqat_status reqat_fakequant_fp4(reqat_format fmt, const void *x, int64_t rows, int64_t cols,
                                  int64_t ldx, void *y, int64_t ldy, float *tensor_scale,
                                  reqat_tscale_mode ts, void *workspace, void *stream);
+
+/*
+ * Quantize and fake-quant in one pass over x: codes and scales exactly as
+ * reqat_quantize_fp4 writes them, y exactly as reqat_fakequant_fp4 writes it
+ * (the QAT forward's quantize-dequantize, Sec. 2.2, together with the codes
+ * its 4-bit product consumes, Sec. 5.3), one tensor scale g for both.  Reads
+ * x once instead of twice.
+ *   codes [rows][cols/2], scales [rows][cols/B]: out, as reqat_quantize_fp4;
+ *   y [rows][ldy] bfloat16: out, as reqat_fakequant_fp4 (ldy >= cols);
+ *   tensor_scale, ts, workspace: as reqat_quantize_fp4.
+ * Requirements: cols % B == 0; x, codes, scales, y 16-byte aligned;
+ * ldx % 8 == 0, ldy % 8 == 0; y must not overlap x (REQAT_E_UNSUPPORTED).
+ * rows == 0 or cols == 0 is a no-op (COMPUTE still writes g = 1).
+ */
+reqat_status reqat_quantize_fakequant_fp4(reqat_format fmt, const void *x, int64_t rows, int64_t cols,
+                                          int64_t ldx, uint8_t *codes, uint8_t *scales, void *y, int64_t ldy,
+                                          float *tensor_scale, reqat_tscale_mode ts, void *workspace,
+                                          void *stream);
 
 /*
  * MXFP4 quantization of block-rotated rows (the block rotation ReQAT applies

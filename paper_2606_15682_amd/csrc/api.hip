@@ -35,15 +35,39 @@ reqat_status check_quant(reqat_format fmt, const void *x, int64_t rows, int64_t 
     return REQAT_OK;
 }
 
+// Whether the bytes [a, a + na) and [b, b + nb) overlap.
+bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
+    const uintptr_t pa = reinterpret_cast<uintptr_t>(a), pb = reinterpret_cast<uintptr_t>(b);
+    return na && nb && pa < pb + nb && pb < pa + na;
+}
+
+// Bytes spanned by a rows x cols bfloat16 matrix with leading dimension ld.
+size_t span_bf16(int64_t rows, int64_t cols, int64_t ld) {
+    return rows > 0 && cols > 0 ? (size_t)(((rows - 1) * ld + cols) * 2) : 0;
+}
+
 // `workspace` holds the kMaxPartials partial maxima; `seg_table` (NVFP4 with
 // a computed g) has room for seg_capacity segments, else the quantizer reads x twice.
 reqat_status run_quant(reqat_format fmt, const void *x, int64_t rows, int64_t cols, int64_t ldx,
                        uint8_t *codes, uint8_t *scales, void *y, int64_t ldy, float *tensor_scale,
                        reqat_tscale_mode ts, void *workspace, uint16_t *seg_table, int64_t seg_capacity,
-                       void *stream, bool fake) {
+                       void *stream, QuantOut out) {
+    const bool fake = out == kFakeQuant;
     reqat_status st = check_quant(fmt, x, rows, cols, ldx, fake ? y : codes, scales, ldy,
                                   tensor_scale, ts, workspace, fake);
     if (st != REQAT_OK) return st;
+    if (out == kBoth && rows > 0 && cols > 0) {
+        if (!y) return REQAT_E_NULL;
+        if (ldy < cols) return REQAT_E_SHAPE;
+        if (!aligned16(y) || ldy % 8) return REQAT_E_ALIGN;
+    }
+    if (out != kCodes && overlaps(x, span_bf16(rows, cols, ldx), y, span_bf16(rows, cols, ldy))) {
+        // in place is allowed for fake-quant alone when x is not read again
+        // after y is written: not with a computed NVFP4 scale (the fix-up
+        // pass re-quantizes some blocks from x), and never with codes too
+        const bool reread = fmt == REQAT_FMT_NVFP4 && ts == REQAT_TS_COMPUTE;
+        if (out == kBoth || reread || x != y || ldx != ldy) return REQAT_E_UNSUPPORTED;
+    }
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const bool nv = fmt == REQAT_FMT_NVFP4;
     const bool compute = nv && ts == REQAT_TS_COMPUTE;
@@ -52,7 +76,7 @@ reqat_status run_quant(reqat_format fmt, const void *x, int64_t rows, int64_t co
         return REQAT_OK;
     }
     GSrc gsrc = !nv ? kGNone : (compute ? kGComputed : kGGiven);
-    hipError_t e = launch_quantize(nv ? kNV : kMX, fake ? kFakeQuant : kCodes,
+    hipError_t e = launch_quantize(nv ? kNV : kMX, out,
                                    reinterpret_cast<const uint16_t *>(x), rows, cols, ldx, codes,
                                    scales, reinterpret_cast<uint16_t *>(y), ldy, tensor_scale, gsrc,
                                    reinterpret_cast<uint32_t *>(workspace), compute ? seg_table : nullptr,
@@ -81,14 +105,22 @@ reqat_status reqat_quantize_fp4(reqat_format fmt, const void *x, int64_t rows, i
                                 int64_t ldx, uint8_t *codes, uint8_t *scales, float *tensor_scale,
                                 reqat_tscale_mode ts, void *workspace, void *stream) {
     return run_quant(fmt, x, rows, cols, ldx, codes, scales, nullptr, 0, tensor_scale, ts,
-                     workspace, quant_seg_table(workspace), kMaxSegments, stream, false);
+                     workspace, quant_seg_table(workspace), kMaxSegments, stream, kCodes);
 }
 
 reqat_status reqat_fakequant_fp4(reqat_format fmt, const void *x, int64_t rows, int64_t cols,
                                  int64_t ldx, void *y, int64_t ldy, float *tensor_scale,
                                  reqat_tscale_mode ts, void *workspace, void *stream) {
     return run_quant(fmt, x, rows, cols, ldx, nullptr, nullptr, y, ldy, tensor_scale, ts,
-                     workspace, quant_seg_table(workspace), kMaxSegments, stream, true);
+                     workspace, quant_seg_table(workspace), kMaxSegments, stream, kFakeQuant);
+}
+
+reqat_status reqat_quantize_fakequant_fp4(reqat_format fmt, const void *x, int64_t rows, int64_t cols,
+                                          int64_t ldx, uint8_t *codes, uint8_t *scales, void *y, int64_t ldy,
+                                          float *tensor_scale, reqat_tscale_mode ts, void *workspace,
+                                          void *stream) {
+    return run_quant(fmt, x, rows, cols, ldx, codes, scales, y, ldy, tensor_scale, ts, workspace,
+                     quant_seg_table(workspace), kMaxSegments, stream, kBoth);
 }
 
 static reqat_status run_kv4(const void *x, int64_t rows, int64_t cols, int64_t ldx, const float *shift,
@@ -287,7 +319,7 @@ reqat_status reqat_linear_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K
     const int64_t nseg = nv ? linear_segments(M, K) : 0;
     uint16_t *table = reinterpret_cast<uint16_t *>(a_scales + round256((size_t)M * (size_t)(K / block_of(fmt))));
     reqat_status st = run_quant(fmt, x, M, K, ldx, a_codes, a_scales, nullptr, 0, x_tensor_scale, ts,
-                                workspace, nseg <= kMaxSegments ? table : nullptr, nseg, stream, false);
+                                workspace, nseg <= kMaxSegments ? table : nullptr, nseg, stream, kCodes);
     if (st != REQAT_OK) return st;
     hipError_t e = launch_gemm(nv ? kNV : kMX, M, N, K, a_codes, a_scales, x_tensor_scale, w_codes,
                                w_scales, w_tensor_scale, y, y_dtype == REQAT_DT_BF16, ldy,

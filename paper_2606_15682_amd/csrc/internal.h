@@ -21,7 +21,8 @@ constexpr int64_t kMaxSegments = int64_t(1) << 19;
 enum Fmt : int { kNV = 0, kMX = 1 };
 
 // Output selector for the block quantizer.
-enum QuantOut : int { kCodes = 0, kFakeQuant = 1 };
+// kBoth writes codes, scales and fake-quant values in one pass over x.
+enum QuantOut : int { kCodes = 0, kFakeQuant = 1, kBoth = 2 };
 
 // Global-scale source for NVFP4.
 enum GSrc : int { kGComputed = 0, kGGiven = 1, kGNone = 2 };

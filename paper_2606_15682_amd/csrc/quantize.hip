@@ -32,6 +32,8 @@
 // NVFP4 computed global scale: a first pass writes one partial absmax per
 // workgroup into the workspace; each quantize workgroup folds the partials
 // (<= 1024 words, L2-resident) before its block loop, and workgroup 0 publishes g.
+#include <type_traits>
+
 #include "fp4_device.h"
 #include "internal.h"
 
@@ -43,12 +45,15 @@ constexpr int kThreads = 256;
 #ifndef REQAT_Q_GROUPS
 #define REQAT_Q_GROUPS 4096
 #endif
-// blocks per lane per step: codes output / fake-quant output
+// blocks per lane per step: codes output / fake-quant output / both
 #ifndef REQAT_Q_UCODES
 #define REQAT_Q_UCODES 1
 #endif
 #ifndef REQAT_Q_UFQ
 #define REQAT_Q_UFQ 2
+#endif
+#ifndef REQAT_Q_UBOTH
+#define REQAT_Q_UBOTH 2
 #endif
 #ifndef REQAT_Q_BLOCKED
 #define REQAT_Q_BLOCKED 0
@@ -378,7 +383,7 @@ __device__ __forceinline__ BlockPlan plan_block(uint32_t am, const GScale &G) {
     return pl;
 }
 
-// Fast path: codes (and scale byte) or fake-quant values of one block.
+// Fast path: codes (and scale byte), fake-quant values, or both, of one block.
 template <int FMT, int OUT>
 __device__ __forceinline__ void emit_fast(const uint32_t (&w)[(FMT == kMX ? 32 : 16) / 2], const BlockPlan &pl,
                                           int64_t blk, uint8_t *codes, uint8_t *scales, uint16_t *ydst) {
@@ -386,12 +391,13 @@ __device__ __forceinline__ void emit_fast(const uint32_t (&w)[(FMT == kMX ? 32 :
     uint32_t cw[B / 8];
     if (FMT == kMX) codes_fast_mx<B>(w, pl.p2, cw);
     else codes_fast_nv<B>(w, pl.p2, __builtin_amdgcn_rcpf(pl.mant), cw);
-    if (OUT == kCodes) {
+    if (OUT != kFakeQuant) {
         uint8_t *dst = codes + blk * (B / 2);
         if constexpr (B == 16) *reinterpret_cast<uint2 *>(dst) = make_uint2(cw[0], cw[1]);
         else *reinterpret_cast<uint4 *>(dst) = make_uint4(cw[0], cw[1], cw[2], cw[3]);
         scales[blk] = (uint8_t)pl.sbyte;
-    } else {
+    }
+    if (OUT != kCodes) {
         uint4 *dst = reinterpret_cast<uint4 *>(ydst);
 #pragma unroll
         for (int q = 0; q < B / 8; ++q) {
@@ -428,18 +434,16 @@ __device__ __forceinline__ uint32_t emit_general(const uint16_t *xsrc, const GSc
                                  : (double)e4m3_value(sbyte) * (double)G.g;
     const bool zero = bad || (FMT == kNV && sbyte == 0u);
     uint32_t U[7], P[8];
-    if (OUT == kCodes) {
-        general_plan<false>(Sd, zero, U, P);
+    general_plan<OUT != kCodes>(Sd, zero, U, P);
+    if (OUT != kFakeQuant) {
         uint32_t out[B / 8];
         codes_general<B>(w, U, bad, out);
         uint8_t *dst = codes + blk * (B / 2);
         if constexpr (B == 16) *reinterpret_cast<uint2 *>(dst) = make_uint2(out[0], out[1]);
         else *reinterpret_cast<uint4 *>(dst) = make_uint4(out[0], out[1], out[2], out[3]);
         scales[blk] = (uint8_t)sbyte;
-    } else {
-        general_plan<true>(Sd, zero, U, P);
-        fq_general<B>(w, U, P, bad, ydst);
     }
+    if (OUT != kCodes) fq_general<B>(w, U, P, bad, ydst);
     return sbyte;
 }
 
@@ -585,7 +589,7 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
                 sbyte[u] = pl.sbyte;
                 general[u] = !pl.fast;
                 if (pl.fast) {
-                    uint16_t *ydst = OUT == kFakeQuant ? y + block_offset(blk[u], nb, cols, ldy, B, narrow) : nullptr;
+                    uint16_t *ydst = OUT != kCodes ? y + block_offset(blk[u], nb, cols, ldy, B, narrow) : nullptr;
                     emit_fast<FMT, OUT>(wc[u], pl, blk[u], codes, scales, ydst);
                 }
             }
@@ -593,7 +597,7 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             if (general[u]) {
-                uint16_t *ydst = OUT == kFakeQuant ? y + block_offset(blk[u], nb, cols, ldy, B, narrow) : nullptr;
+                uint16_t *ydst = OUT != kCodes ? y + block_offset(blk[u], nb, cols, ldy, B, narrow) : nullptr;
                 sbyte[u] = emit_general<FMT, OUT>(x + block_offset(blk[u], nb, cols, ldx, B, narrow), Gs[u], blk[u],
                                                   codes, scales, ydst);
             }
@@ -637,10 +641,10 @@ __device__ __forceinline__ uint32_t lower_scale_bytes(uint32_t v, uint32_t sub) 
 // reference scale differs from g by the factor 2^sh.  One lane per segment:
 // when the segment's smallest scale exponent field exceeds sh, every block
 // keeps a normal scale, so codes and fake-quant values stand and only the
-// segment's 64 scale bytes are lowered (codes output).  Otherwise the wave
+// segment's 64 scale bytes are lowered (codes outputs).  Otherwise the wave
 // walks such segments together, one lane per block, lowering the bytes that
-// stay normal and re-quantizing the other blocks from x under g (fake-quant:
-// every block of the segment).  The lane's first table entry and scale bytes
+// stay normal and re-quantizing the other blocks from x under g (fake-quant
+// alone, with no scale bytes to tell them apart: every block of the segment).  The lane's first table entry and scale bytes
 // are requested before the fold, so their latency overlaps it.
 template <int OUT>
 __global__ __launch_bounds__(kThreads) void nv_fixup_kernel(
@@ -660,7 +664,7 @@ __global__ __launch_bounds__(kThreads) void nv_fixup_kernel(
         m = 0u;
         if (seg < nseg) {
             m = seg_table[seg];
-            if (OUT == kCodes && total - seg * kSeg >= kSeg) {
+            if (OUT != kFakeQuant && total - seg * kSeg >= kSeg) {
                 const uint4 *p = reinterpret_cast<const uint4 *>(scales + seg * kSeg);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) v[i] = p[i];
@@ -682,7 +686,7 @@ __global__ __launch_bounds__(kThreads) void nv_fixup_kernel(
         if (m != 0u) sh = G.kg - ((int)(m & 0xFFu) - 127);
         if (sh > 0) {
             redo = (int)(m >> 8) <= sh;
-            if (OUT == kCodes && !redo) {
+            if (OUT != kFakeQuant && !redo) {
                 const uint32_t sub = (uint32_t)sh << 3;
                 const int64_t n = total - seg * kSeg;
                 if (n >= kSeg) {
@@ -708,7 +712,7 @@ __global__ __launch_bounds__(kThreads) void nv_fixup_kernel(
             const int64_t blk = (s0 + l) * kSeg + lane;
             if (blk < total) {
                 bool requant = true;
-                if (OUT == kCodes) {
+                if (OUT != kFakeQuant) {
                     const uint32_t b = scales[blk];
                     if (b == 0u || b == 0x7Fu) {
                         requant = false;
@@ -719,7 +723,7 @@ __global__ __launch_bounds__(kThreads) void nv_fixup_kernel(
                 }
                 if (requant) {
                     const uint16_t *xsrc = x + block_offset(blk, nb, cols, ldx, 16, narrow);
-                    uint16_t *ydst = OUT == kFakeQuant ? y + block_offset(blk, nb, cols, ldy, 16, narrow) : nullptr;
+                    uint16_t *ydst = OUT != kCodes ? y + block_offset(blk, nb, cols, ldy, 16, narrow) : nullptr;
                     uint32_t w[8];
                     load_block<16>(xsrc, w);
                     const BlockPlan pl = plan_block<kNV, OUT, false>(block_mag_max<16>(w), G);
@@ -917,7 +921,7 @@ template <int FMT, int OUT>
 hipError_t launch_fmt_out(GSrc gsrc, bool deferred, int grid, const uint16_t *x, int64_t rows, int64_t cols,
                           int64_t ldx, uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy, float *gptr,
                           uint32_t *partials, int nparts, uint16_t *seg_table, hipStream_t stream) {
-    constexpr int U = OUT == kCodes ? REQAT_Q_UCODES : REQAT_Q_UFQ;
+    constexpr int U = OUT == kCodes ? REQAT_Q_UCODES : OUT == kFakeQuant ? REQAT_Q_UFQ : REQAT_Q_UBOTH;
     if (FMT == kNV && deferred)
         return launch_loop<FMT, OUT, kGDeferred, U>(grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr,
                                                    partials, nparts, seg_table, stream);
@@ -984,26 +988,31 @@ hipError_t launch_quantize(Fmt fmt, QuantOut out, const uint16_t *x, int64_t row
     if (grid < 1) grid = 1;
     if (deferred) nparts = (int)grid;
     hipError_t e;
+    auto run = [&](auto fmt_c, auto out_c) {
+        return launch_fmt_out<decltype(fmt_c)::value, decltype(out_c)::value>(
+            gsrc, deferred, (int)grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr, partials, nparts, seg_table,
+            stream);
+    };
+    using MXc = std::integral_constant<int, kMX>;
+    using NVc = std::integral_constant<int, kNV>;
+    using Cc = std::integral_constant<int, kCodes>;
+    using Fc = std::integral_constant<int, kFakeQuant>;
+    using Bc = std::integral_constant<int, kBoth>;
     if (fmt == kMX)
-        e = out == kCodes ? launch_fmt_out<kMX, kCodes>(gsrc, false, (int)grid, x, rows, cols, ldx, codes, scales,
-                                                         y, ldy, gptr, partials, nparts, seg_table, stream)
-                          : launch_fmt_out<kMX, kFakeQuant>(gsrc, false, (int)grid, x, rows, cols, ldx, codes,
-                                                             scales, y, ldy, gptr, partials, nparts, seg_table,
-                                                             stream);
+        e = out == kCodes ? run(MXc{}, Cc{}) : out == kFakeQuant ? run(MXc{}, Fc{}) : run(MXc{}, Bc{});
     else
-        e = out == kCodes ? launch_fmt_out<kNV, kCodes>(gsrc, deferred, (int)grid, x, rows, cols, ldx, codes,
-                                                         scales, y, ldy, gptr, partials, nparts, seg_table, stream)
-                          : launch_fmt_out<kNV, kFakeQuant>(gsrc, deferred, (int)grid, x, rows, cols, ldx, codes,
-                                                             scales, y, ldy, gptr, partials, nparts, seg_table,
-                                                             stream);
+        e = out == kCodes ? run(NVc{}, Cc{}) : out == kFakeQuant ? run(NVc{}, Fc{}) : run(NVc{}, Bc{});
     if (e != hipSuccess || !deferred) return e;
     int64_t fgrid = (nseg + kThreads - 1) / kThreads;
     if (fgrid > kMaxGroups) fgrid = kMaxGroups;
     if (out == kCodes)
         hipLaunchKernelGGL(nv_fixup_kernel<kCodes>, dim3((unsigned)fgrid), dim3(kThreads), 0, stream, x, rows,
                            cols, ldx, codes, scales, y, ldy, gptr, partials, nparts, seg_table);
-    else
+    else if (out == kFakeQuant)
         hipLaunchKernelGGL(nv_fixup_kernel<kFakeQuant>, dim3((unsigned)fgrid), dim3(kThreads), 0, stream, x, rows,
+                           cols, ldx, codes, scales, y, ldy, gptr, partials, nparts, seg_table);
+    else
+        hipLaunchKernelGGL(nv_fixup_kernel<kBoth>, dim3((unsigned)fgrid), dim3(kThreads), 0, stream, x, rows,
                            cols, ldx, codes, scales, y, ldy, gptr, partials, nparts, seg_table);
     return hipGetLastError();
 }

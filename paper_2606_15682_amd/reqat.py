@@ -38,6 +38,8 @@ _INT = ctypes.c_int
 SIGNATURES = {
     "reqat_quantize_fp4": (_INT, [_INT, _VP, _I64, _I64, _I64, _VP, _VP, _VP, _INT, _VP, _VP]),
     "reqat_fakequant_fp4": (_INT, [_INT, _VP, _I64, _I64, _I64, _VP, _I64, _VP, _INT, _VP, _VP]),
+    "reqat_quantize_fakequant_fp4": (_INT, [_INT, _VP, _I64, _I64, _I64, _VP, _VP, _VP, _I64, _VP, _INT, _VP,
+                                            _VP]),
     "reqat_gemm_w4a4": (_INT, [_INT, _I64, _I64, _I64, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _INT,
                                _I64, _VP]),
     "reqat_linear_w4a4": (_INT, [_INT, _I64, _I64, _I64, _VP, _I64, _VP, _INT, _VP, _VP, _VP, _VP,
@@ -93,6 +95,12 @@ def reqat_quantize_fp4(fmt, x, rows, cols, ldx, codes, scales, tensor_scale, ts,
 def reqat_fakequant_fp4(fmt, x, rows, cols, ldx, y, ldy, tensor_scale, ts, workspace, stream):
     return load().reqat_fakequant_fp4(fmt, x, rows, cols, ldx, y, ldy, tensor_scale, ts, workspace,
                                       stream)
+
+
+def reqat_quantize_fakequant_fp4(fmt, x, rows, cols, ldx, codes, scales, y, ldy, tensor_scale, ts, workspace,
+                                 stream):
+    return load().reqat_quantize_fakequant_fp4(fmt, x, rows, cols, ldx, codes, scales, y, ldy, tensor_scale, ts,
+                                               workspace, stream)
 
 
 def reqat_gemm_w4a4(fmt, M, N, K, a_codes, a_scales, a_ts, b_codes, b_scales, b_ts, y, y_dtype,
@@ -238,6 +246,25 @@ def fakequant(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out=None, g_
                              ts, ws.data_ptr(), _stream(x.device))
     _check(st, "reqat_fakequant_fp4")
     return y, g
+
+
+def quantize_fakequant(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out=None, g_out=None):
+    """Quantize and quantize-dequantize in one pass over x.  Returns
+    (codes, scales, y, g): codes/scales as quantize(), y (bfloat16) as fakequant()."""
+    rows, cols, ldx = _x2d(x)
+    B = BLOCK[fmt]
+    if out is not None:
+        codes, scales, y = out
+    else:
+        codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=x.device)
+        scales = torch.empty((rows, cols // B), dtype=torch.uint8, device=x.device)
+        y = torch.empty((rows, cols), dtype=torch.bfloat16, device=x.device)
+    g, ts = _gscale(fmt, x, tensor_scale, g_out)
+    ws = workspace(x.device)
+    st = reqat_quantize_fakequant_fp4(fmt, x.data_ptr(), rows, cols, ldx, codes.data_ptr(), scales.data_ptr(),
+                                      y.data_ptr(), y.stride(0), _ptr(g), ts, ws.data_ptr(), _stream(x.device))
+    _check(st, "reqat_quantize_fakequant_fp4")
+    return codes, scales, y, g
 
 
 def quantize_rht(x: torch.Tensor, signs: int, out=None):

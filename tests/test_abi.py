@@ -50,7 +50,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_small_queries(lib):
-    assert reqat.reqat_abi_version() == 7
+    assert reqat.reqat_abi_version() == 8
     assert reqat.reqat_workspace_bytes() == 4 * 4096 + 2 * (1 << 19)   # partials + segment table
     for s in range(7):
         assert reqat.reqat_status_str(s).startswith(reqat.STATUS[s])
@@ -63,6 +63,11 @@ def q(fmt=NV, x=P, rows=4, cols=64, ldx=64, codes=P, scales=P, ts_ptr=P, ts=0, w
 
 def fq(fmt=NV, x=P, rows=4, cols=64, ldx=64, y=P, ldy=64, ts_ptr=P, ts=0, ws=P):
     return reqat.reqat_fakequant_fp4(fmt, x, rows, cols, ldx, y, ldy, ts_ptr, ts, ws, None)
+
+
+def qfq(fmt=NV, x=P, rows=4, cols=64, ldx=64, codes=P, scales=P, y=P + 4096, ldy=64, ts_ptr=P, ts=0, ws=P):
+    return reqat.reqat_quantize_fakequant_fp4(fmt, x, rows, cols, ldx, codes, scales, y, ldy, ts_ptr, ts, ws,
+                                              None)
 
 
 def gm(fmt=NV, M=4, N=8, K=128, ac=P, as_=P, ag=P, bc=P, bs=P, bg=P, y=P, dt=0, ldy=8):
@@ -96,6 +101,35 @@ def test_fakequant_validation(lib):
     assert fq(y=P + 4) == E_ALIGN
     assert fq(ldy=68) == E_ALIGN
     assert fq(fmt=MX) == E_UNSUP
+
+
+def test_fakequant_in_place_rules(lib):
+    # computed NVFP4 scale: the second pass re-reads x, so y must not overlap it
+    assert fq(x=P, y=P) == E_UNSUP
+    # partial overlaps are never allowed
+    assert fq(fmt=MX, ts_ptr=None, x=P, y=P + 64) == E_UNSUP
+    assert fq(ts=1, x=P, y=P + 64) == E_UNSUP
+    assert fq(ts=1, x=P, y=P, ldx=64, ldy=72) == E_UNSUP
+
+
+def test_quantize_fakequant_validation(lib):
+    assert qfq(fmt=9) == E_ENUM
+    assert qfq(ts=3) == E_ENUM
+    assert qfq(cols=40, ldx=40, ldy=40) == E_SHAPE
+    assert qfq(ldx=32) == E_SHAPE
+    assert qfq(ldy=32) == E_SHAPE
+    assert qfq(fmt=MX) == E_UNSUP                # MXFP4 has no global scale
+    assert qfq(ws=None) == E_NULL
+    assert qfq(codes=None) == E_NULL
+    assert qfq(scales=None) == E_NULL
+    assert qfq(y=None) == E_NULL
+    assert qfq(x=P + 8) == E_ALIGN
+    assert qfq(y=P + 4096 + 8) == E_ALIGN
+    assert qfq(ldy=68) == E_ALIGN
+    # y must not overlap x, in place included
+    assert qfq(y=P) == E_UNSUP
+    assert qfq(fmt=MX, ts_ptr=None, y=P + 256) == E_UNSUP
+    assert qfq(ts=1, y=P + 496) == E_UNSUP       # x spans 4 rows * 64 * 2 = 512 bytes
 
 
 def test_rotated_quantize_validation(lib):

@@ -91,6 +91,14 @@ def test_fullsize_14b_fakequant():
         assert float(g.cpu()[0]) == og
         assert np.array_equal(wl.bf16_bits(y.cpu()), oy), "%s fake-quant differs" % name
         log("  %s fake-quant bit-exact" % name)
+        # the one-pass quantize + fake-quant the benchmark step runs
+        c, sc, y2, g2 = reqat.quantize_fakequant(t.to(DEV), reqat.NVFP4)
+        torch.cuda.synchronize()
+        oc, os_, og2 = oracle.quantize(oracle.FMT_NVFP4, wl.bf16_bits(t))
+        assert float(g2.cpu()[0]) == og2 == og
+        assert np.array_equal(sc.cpu().numpy(), os_) and np.array_equal(c.cpu().numpy(), oc)
+        assert np.array_equal(wl.bf16_bits(y2.cpu()), oy), "%s fused fake-quant differs" % name
+        log("  %s fused quantize + fake-quant bit-exact" % name)
 
 
 def test_fullsize_32b_down_mxfp4():

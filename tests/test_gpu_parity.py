@@ -72,6 +72,32 @@ def assert_fq_parity(fmt, xb, g=None):
         y, gg = gpu_fakequant(fmt, xb, g, poison)
         bad = np.argwhere(y != oy)
         assert bad.size == 0, ("fake-quant differs", bad[:4], hex(y[tuple(bad[0])]), hex(oy[tuple(bad[0])]))
+    assert_both_parity(fmt, xb, g, oy=oy)
+
+
+def assert_both_parity(fmt, xb, g=None, oy=None):
+    """The one-pass quantize + fake-quant entry point: codes, scales, g and y all
+    equal the oracle's quantize and fake-quant outputs."""
+    R, C = xb.shape
+    B = reqat.BLOCK[fmt]
+    oc, os_, og = oracle.quantize(fmt, xb, g)
+    if oy is None:
+        oy, _ = oracle.fakequant(fmt, xb, g)
+    xt = wl.from_bits(xb).to(DEV)
+    gt = None if (g is None or fmt == MX) else torch.tensor([g], dtype=torch.float32, device=DEV)
+    for pc, py in ((0x00, 0x7FFF), (0xFF, 0x0000)):
+        codes = torch.full((R, C // 2), pc, dtype=torch.uint8, device=DEV)
+        scales = torch.full((R, C // B), pc, dtype=torch.uint8, device=DEV)
+        y = wl.from_bits(np.full((R, C), py, np.uint16)).to(DEV)
+        _, _, _, gg = reqat.quantize_fakequant(xt, fmt, tensor_scale=gt, out=(codes, scales, y))
+        torch.cuda.synchronize()
+        if fmt == NV:
+            assert float(gg.cpu()[0]) == np.float32(og)
+        assert np.array_equal(scales.cpu().numpy(), os_), "fused: scales differ"
+        assert np.array_equal(codes.cpu().numpy(), oc), "fused: codes differ"
+        yb = wl.bf16_bits(y.cpu())
+        bad = np.argwhere(yb != oy)
+        assert bad.size == 0, ("fused fake-quant differs", bad[:4], hex(yb[tuple(bad[0])]), hex(oy[tuple(bad[0])]))
 
 
 def _rand(R, C, seed, dist="normal", std=1.0, outliers=0):
@@ -427,6 +453,30 @@ def test_special_values(fmt):
     assert_quant_parity(fmt, x)
     assert_fq_parity(fmt, x)
     assert_quant_parity(fmt, x[[0, 4]])           # tensor of only zeros / subnormals
+
+
+@pytest.mark.parametrize("fmt,g", [(MX, None), (NV, 2.0 ** -5), (NV, 0.0123456789)])
+def test_fakequant_in_place(fmt, g):
+    """In place (y is x) is allowed when x is not read again after y is written:
+    MXFP4, and NVFP4 with a given tensor scale."""
+    log("fake-quant in place fmt=%d g=%r" % (fmt, g))
+    xb = _rand(37, 512, 77, "student_t", outliers=5)
+    g = None if g is None else float(np.float32(g))
+    oy, _ = oracle.fakequant(fmt, xb, g)
+    xt = wl.from_bits(xb).to(DEV)
+    gt = None if g is None else torch.tensor([g], dtype=torch.float32, device=DEV)
+    reqat.fakequant(xt, fmt, tensor_scale=gt, out=xt)
+    torch.cuda.synchronize()
+    assert np.array_equal(wl.bf16_bits(xt.cpu()), oy)
+
+
+def test_fused_rejects_overlap():
+    x = torch.zeros((4, 64), dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(RuntimeError):
+        reqat.quantize_fakequant(x, NV, out=(torch.empty((4, 32), dtype=torch.uint8, device=DEV),
+                                             torch.empty((4, 4), dtype=torch.uint8, device=DEV), x))
+    with pytest.raises(RuntimeError):
+        reqat.fakequant(x, NV, out=x)             # computed g re-reads x in its second pass
 
 
 def test_empty_tensor_writes_unit_global_scale():
