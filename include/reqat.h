@@ -133,7 +133,8 @@ reqat_status reqat_fakequant_fp4(reqat_format fmt, const void *x, int64_t rows, 
  *   y [rows][ldy] bfloat16: out, as reqat_fakequant_fp4 (ldy >= cols);
  *   tensor_scale, ts, workspace: as reqat_quantize_fp4.
  * Requirements: cols % B == 0; x, codes, scales, y 16-byte aligned;
- * ldx % 8 == 0, ldy % 8 == 0; y must not overlap x (REQAT_E_UNSUPPORTED).
+ * ldx % 8 == 0, ldy % 8 == 0; y must not overlap x (REQAT_E_UNSUPPORTED);
+ * codes and scales must not overlap x or y.
  * rows == 0 or cols == 0 is a no-op (COMPUTE still writes g = 1).
  */
 reqat_status reqat_quantize_fakequant_fp4(reqat_format fmt, const void *x, int64_t rows, int64_t cols,

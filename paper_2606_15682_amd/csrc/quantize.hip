@@ -644,8 +644,9 @@ __device__ __forceinline__ uint32_t lower_scale_bytes(uint32_t v, uint32_t sub) 
 // segment's 64 scale bytes are lowered (codes outputs).  Otherwise the wave
 // walks such segments together, one lane per block, lowering the bytes that
 // stay normal and re-quantizing the other blocks from x under g (fake-quant
-// alone, with no scale bytes to tell them apart: every block of the segment).  The lane's first table entry and scale bytes
-// are requested before the fold, so their latency overlaps it.
+// alone, with no scale bytes to tell them apart: every block of the segment).
+// The lane's first table entry and scale bytes are requested before the fold,
+// so their latency overlaps it.
 template <int OUT>
 __global__ __launch_bounds__(kThreads) void nv_fixup_kernel(
     const uint16_t *__restrict__ x, int64_t rows, int64_t cols, int64_t ldx,
