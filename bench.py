@@ -62,6 +62,9 @@ def profiled_traffic(fmt_name: str, workload: int):
     except (KeyError, ValueError):
         return None
 PEAK = {"fp4": 10100.0, "f16": 2500.0, "hbm": 8000.0}   # TFLOP/s, TFLOP/s, GB/s (MI355X published)
+# workloads timed as a decode step (quantize X + product, weights quantized once,
+# untimed); the others run the whole step (quantize and fake-quant both operands)
+DECODE_WORKLOADS = {2}
 
 
 def parse():
@@ -70,7 +73,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=4,
-                    help="workload number (4 = 14B gate/up; 6, 7 = MXFP4 W4A16 decode; 8 = SEM loss head)")
+                    help="workload number (4 = 14B gate/up; 2 = NVFP4 W4A4 decode; 6, 7 = MXFP4 W4A16 "
+                         "decode; 8 = SEM loss head)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes --steps times "
@@ -202,8 +206,8 @@ def bench_w4a16(args, w):
     gbs = nbytes / (ms_kernel * 1e-3) / 1e9
     out = {
         "metric": METRIC,
-        "value": round(flops / (ms_step * 1e-3) / 1e12, 3),
-        "unit": "TFLOP/s",
+        "value": round(nbytes / (ms_step * 1e-3) / 1e9, 1),
+        "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -233,10 +237,121 @@ def bench_w4a16(args, w):
         oracle.gemm_w4a16_points(xb, owc, ows, ms_, ns_)
         dt = time.perf_counter() - t0
         per_mac = dt / (npts * K)
+        full = per_mac * M * N * K
         out["cpu_baseline"] = {
-            "value": round(2.0 / per_mac / 1e12, 9), "unit": "TFLOP/s", "cores": 1, "kind": "oracle",
+            "value": round(nbytes / full / 1e9, 6), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": ("FP64 W4A16 oracle on %d output points (each a %d-term dot product), per-MAC "
-                       "rate scaled to the full product (%.2f s of CPU work)" % (npts, K, dt))}
+                       "rate scaled to the full product and credited with its bytes (%.2f s of CPU work)"
+                       % (npts, K, dt))}
+    print(json.dumps(out), flush=True)
+
+
+def bench_decode(args, w):
+    """Decode step of the W4A4 layer (M <= 64 activation rows): quantize X and
+    multiply by weights that were quantized once, untimed (served weights are
+    stored quantized), in one reqat_linear_w4a4 call.  Bound by HBM: the
+    weights stream once per step."""
+    import numpy as np
+    import torch
+
+    from paper_2606_15682_amd import reqat
+    from paper_2606_15682_amd import workloads as wl
+
+    reqat.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    fmt = reqat.NVFP4 if w.fmt == "nvfp4" else reqat.MXFP4
+    B = reqat.BLOCK[fmt]
+    M, N, K = w.M, w.N, w.K
+    x_cpu, w_cpu = wl.make_x(w), wl.make_w(w)
+    x = x_cpu.to(dev)
+    wc, wsc, gw = reqat.quantize(w_cpu.to(dev), fmt)
+    y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    gl = torch.empty(1, dtype=torch.float32, device=dev) if fmt == reqat.NVFP4 else None
+    lws = torch.empty(reqat.reqat_linear_workspace_bytes(fmt, M, K), dtype=torch.uint8, device=dev)
+
+    def step():
+        reqat.linear(x, fmt, wc, wsc, gw, out_dtype=torch.bfloat16, out=y, g_out=gl, ws=lws)
+
+    for _ in range(args.warmup):
+        step()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record()
+    for _ in range(args.steps):
+        step()
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms_dev = ev[0].elapsed_time(ev[1]) / args.steps
+
+    # the product alone (activation codes from one quantize), timed apart
+    xc, xs, gx = reqat.quantize(x, fmt)
+    ms_gemm = None
+    for _ in range(max(1, args.warmup)):
+        reqat.gemm(fmt, xc, xs, gx, wc, wsc, gw, out_dtype=torch.bfloat16, out=y)
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(args.steps):
+        reqat.gemm(fmt, xc, xs, gx, wc, wsc, gw, out_dtype=torch.bfloat16, out=y)
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms_gemm = ev[0].elapsed_time(ev[1]) / args.steps
+
+    w_bytes = N * K * (0.5 + 1.0 / B)
+    step_bytes = w_bytes + M * K * 2.0 + M * N * 2.0              # weights once, x read, Y (bf16)
+    gemm_bytes = w_bytes + M * K * (0.5 + 1.0 / B) + M * N * 2.0  # weights once, x codes, Y (bf16)
+    gbs_gemm = gemm_bytes / (ms_gemm * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16" if fmt == reqat.NVFP4 else "fp4",
+        "data": "synthetic (seeded; Gaussian activations with outlier channels, N(0,0.02) weights)",
+        "config": {"workload": w.name, "M": M, "N": N, "K": K, "format": w.fmt, "gemm_out": "bf16",
+                   "global_batch": M, "parallelism": "single GPU",
+                   "step": "quantize X + W4A4 GEMM in one reqat_linear_w4a4 call (weights quantized once, "
+                           "untimed)"},
+        "roofline": {"bound": "hbm", "achieved": round(gbs_gemm, 1), "peak": PEAK["hbm"], "unit": "GB/s",
+                     "frac": round(gbs_gemm / PEAK["hbm"], 4), "traffic": None,
+                     "kernel": "gemm_skinny_kernel (%s W4A4 GEMM, M <= 64; algorithmic bytes %d)"
+                               % (w.fmt, int(gemm_bytes))},
+        "kernels": {"linear_step": {"ms": round(ms_dev, 4),
+                                    "GB/s": round(step_bytes / (ms_dev * 1e-3) / 1e9, 1),
+                                    "note": "device time of the step (quantize X kernels + product)"},
+                    "gemm": {"ms": round(ms_gemm, 4), "GB/s": round(gbs_gemm, 1),
+                             "TFLOP/s": round(2.0 * M * N * K / (ms_gemm * 1e-3) / 1e12, 2),
+                             "note": "product alone, timed apart"}},
+        "note": ("the same weights are re-read every step, so they sit in the 256 MB Infinity Cache: "
+                 "a cache-resident rate, an upper bound for weights streamed from HBM"),
+    }
+    out["ceilings"] = practical_ceilings()
+    if not args.no_cpu_baseline:
+        import oracle
+        ofmt = oracle.FMT_NVFP4 if fmt == reqat.NVFP4 else oracle.FMT_MXFP4
+        xb, wb = wl.bf16_bits(x_cpu), wl.bf16_bits(w_cpu)
+        t0 = time.perf_counter()
+        owc, ows, owg = oracle.quantize(ofmt, wb[:256])
+        oxc, oxs, oxg = oracle.quantize(ofmt, xb)
+        n = 0
+        while time.perf_counter() - t0 < 10.0:
+            oracle.gemm(ofmt, oxc, oxs, oxg, owc, ows, owg)
+            n += 1
+        dt = time.perf_counter() - t0
+        per_row = dt / (n * 256)                      # seconds per weight row of the product (+ quantize share)
+        full = per_row * N
+        out["cpu_baseline"] = {
+            "value": round(step_bytes / full / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": ("oracle quantize of X and of 256 weight rows, then the FP64 product against those "
+                       "rows repeated for ~10 s (%d passes); per-row rate scaled to all %d rows" % (n, N))}
     print(json.dumps(out), flush=True)
 
 
@@ -349,6 +464,9 @@ def main():
         return
     if w.kind == "sem":
         bench_sem(args, w)
+        return
+    if args.workload in DECODE_WORKLOADS:
+        bench_decode(args, w)
         return
     fmt = reqat.NVFP4 if w.fmt == "nvfp4" else reqat.MXFP4
     B = reqat.BLOCK[fmt]
@@ -468,14 +586,14 @@ def main():
                            + ("" if n.startswith("quantize_fakequant") else "; timed apart, not in the step")}
 
     if M <= 64:
-        # decode shape: the product streams the weights once, so it is bounded by HBM
+        # few activation rows (the tiny workload): the product streams the weights once
         gemm_bytes = (N + M) * K * (0.5 + 1.0 / B) + M * N * 2.0
         gbs = gemm_bytes / (per["gemm"] * 1e-3) / 1e9
         kern["gemm"]["GB/s"] = round(gbs, 1)
-        kern["gemm"]["algorithmic_bytes"] = int(gemm_bytes)
         roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK["hbm"], "unit": "GB/s",
                     "frac": round(gbs / PEAK["hbm"], 4), "traffic": None,
-                    "kernel": "gemm_skinny_kernel (%s W4A4 GEMM, M <= 64)" % w.fmt}
+                    "kernel": "gemm_skinny_kernel (%s W4A4 GEMM, M <= 64; algorithmic bytes %d)"
+                              % (w.fmt, int(gemm_bytes))}
     else:
         roofline = {"bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": PEAK[mfma_dtype],
                     "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK[mfma_dtype], 4),
