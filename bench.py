@@ -74,7 +74,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=4,
                     help="workload number (4 = 14B gate/up; 2 = NVFP4 W4A4 decode; 6, 7 = MXFP4 W4A16 "
-                         "decode; 8 = SEM loss head)")
+                         "decode; 8 = SEM loss head; 9 = KV4 keys)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes --steps times "
@@ -355,6 +355,89 @@ def bench_decode(args, w):
     print(json.dumps(out), flush=True)
 
 
+def bench_kv4(args, w):
+    """KV4 cache quantization of post-RoPE keys with the calibrated channel
+    shift subtracted first (E1M2 codes, E4M3 block scales of 16, computed FP32
+    tensor scale).  Bound by HBM: the keys are read once, codes and scales written."""
+    import numpy as np
+    import torch
+
+    from paper_2606_15682_amd import reqat
+    from paper_2606_15682_amd import workloads as wl
+
+    reqat.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    T, C = w.M, w.K
+    k_cpu, mu_cpu = wl.make_keys(w)
+    k, mu = k_cpu.to(dev), mu_cpu.to(dev)
+    codes = torch.empty((T, C // 2), dtype=torch.uint8, device=dev)
+    scales = torch.empty((T, C // 16), dtype=torch.uint8, device=dev)
+    g = torch.empty(1, dtype=torch.float32, device=dev)
+    fq = torch.empty_like(k)
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e[0].record()
+        for _ in range(args.steps):
+            fn()
+        e[1].record()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / args.steps, e[0].elapsed_time(e[1]) / args.steps
+
+    ms_step, ms_q = timed(lambda: reqat.quantize_kv4(k, mu, out=(codes, scales), g_out=g))
+    gq = g.clone()
+    _, ms_given = timed(lambda: reqat.quantize_kv4(k, mu, tensor_scale=gq, out=(codes, scales)))
+    _, ms_fq = timed(lambda: reqat.fakequant_kv4(k, mu, out=fq, g_out=g))
+    q_bytes = T * C * (2 + 0.5 + 1.0 / 16)                        # read keys, write codes + scales
+    fq_bytes = T * C * 4.0
+    gbs = lambda b, ms: b / (ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(gbs(q_bytes, ms_step), 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded; N(0,1) keys plus per-channel offsets N(0,2), the offsets given as the shift)",
+        "config": {"workload": w.name, "tokens": T, "channels": C, "global_batch": T,
+                   "parallelism": "single GPU",
+                   "step": "KV4 quantize of keys - shift (computed tensor scale: absmax pass + quantize)"},
+        "roofline": {"bound": "hbm", "achieved": round(gbs(q_bytes, ms_q), 1), "peak": PEAK["hbm"],
+                     "unit": "GB/s", "frac": round(gbs(q_bytes, ms_q) / PEAK["hbm"], 4), "traffic": None,
+                     "kernel": "kv4_absmax_kernel + kv4_quantize_kernel (algorithmic bytes %d)" % int(q_bytes)},
+        "kernels": {"quantize_kv4_computed_g": {"ms": round(ms_q, 4), "GB/s": round(gbs(q_bytes, ms_q), 1)},
+                    "quantize_kv4_given_g": {"ms": round(ms_given, 4), "GB/s": round(gbs(q_bytes, ms_given), 1)},
+                    "fakequant_kv4_computed_g": {"ms": round(ms_fq, 4), "GB/s": round(gbs(fq_bytes, ms_fq), 1)}},
+    }
+    out["ceilings"] = practical_ceilings()
+    if not args.no_cpu_baseline:
+        import oracle
+        rows = 2048
+        kb = wl.bf16_bits(k_cpu[:rows])
+        t0 = time.perf_counter()
+        n = 0
+        while time.perf_counter() - t0 < 10.0:
+            oracle.kv4_quantize(kb, mu_cpu.numpy())
+            n += 1
+        dt = (time.perf_counter() - t0) / n
+        out["cpu_baseline"] = {
+            "value": round(rows * C * (2 + 0.5 + 1.0 / 16) / dt / 1e9, 4), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": "oracle KV4 quantize (computed g) of %d of the %d token rows, repeated for ~10 s (%d passes), "
+                      "credited with the same bytes per row as the GPU step" % (rows, T, n)}
+    print(json.dumps(out), flush=True)
+
+
 def bench_sem(args, w):
     """QAT loss head: SEM loss forward and backward (bfloat16 gradient) over
     T x V bfloat16 logits.  Bound by HBM: the logits are read twice and the
@@ -464,6 +547,9 @@ def main():
         return
     if w.kind == "sem":
         bench_sem(args, w)
+        return
+    if w.kind == "kv4":
+        bench_kv4(args, w)
         return
     if args.workload in DECODE_WORKLOADS:
         bench_decode(args, w)

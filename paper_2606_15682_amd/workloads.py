@@ -42,6 +42,7 @@ class Workload:
     n_outliers: int     # outlier channels in X (multiplied by 20)
     w_std: float        # weight standard deviation
     kind: str = "w4a4"  # "w4a4" (both operands FP4) | "w4a16" (FP4 weights, bfloat16 activations)
+    #                     | "sem" (loss head) | "kv4" (KV-cache keys)
 
     @property
     def flops(self) -> int:
@@ -66,6 +67,10 @@ WORKLOADS = {
     # SEM loss head of QAT: M tokens x N vocabulary logits (Qwen-family vocabulary)
     8: Workload(8, "SEM loss head 4096 tokens x 152064 vocabulary", NVFP4, 4096, 152064, 0,
                 "normal", 0, 3.0, "sem"),
+    # KV4 cache: post-RoPE keys of one 14B-like layer (8 KV heads x 128 channels) over a
+    # 32768-token prefill, M tokens x K channels
+    9: Workload(9, "KV4 keys 14B-like 32768 tokens x 1024 channels", NVFP4, 32768, 0, 1024,
+                "normal_offsets", 0, 0.0, "kv4"),
 }
 
 
@@ -80,6 +85,20 @@ def make_logits(w: Workload, rows: int | None = None):
     trng = np.random.Generator(np.random.PCG64(_seed(w.index, 1)))
     t = trng.integers(0, w.N, w.M, dtype=np.int64)[:M].astype(np.int32)
     return _to_bf16(z), torch.from_numpy(t)
+
+
+def make_keys(w: Workload, rows: int | None = None):
+    """Keys [M, K] (bfloat16, CPU) and the channel shift [K] (float32) that a
+    calibration would supply: per-channel offsets mu_c ~ N(0, 2) added to a
+    N(0, 1) bulk, and mu itself as the shift.  Seeded; stream 0 = bulk,
+    stream 1 = offsets."""
+    M = w.M if rows is None else rows
+    rng = np.random.Generator(np.random.PCG64(_seed(w.index, 0)))
+    a = rng.standard_normal((M, w.K), dtype=np.float32)
+    orng = np.random.Generator(np.random.PCG64(_seed(w.index, 1)))
+    mu = (orng.standard_normal(w.K, dtype=np.float32) * np.float32(2.0)).astype(np.float32)
+    a += mu[None, :]
+    return _to_bf16(a), torch.from_numpy(mu)
 
 
 def _seed(index: int, stream: int) -> int:

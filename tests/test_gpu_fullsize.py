@@ -186,3 +186,31 @@ def test_fullsize_kv4_keys():
     torch.cuda.synchronize()
     assert float(g.cpu()[0]) == np.float32(og)
     assert np.array_equal(s.cpu().numpy(), os_) and np.array_equal(c.cpu().numpy(), oc)
+
+
+def test_fullsize_kv4_keys():
+    """KV4 quantization of the full 32768 x 1024 key workload (shift = the
+    channel offsets), computed and given tensor scales, bit-exact; fake-quant
+    on a 4096-row slice."""
+    w = wl.WORKLOADS[9]
+    log("full-size KV4 keys: %s" % w.name)
+    k, mu = wl.make_keys(w)
+    kb = wl.bf16_bits(k)
+    kd, mud = k.to(DEV), mu.to(DEV)
+    c, s, g = reqat.quantize_kv4(kd, mud)
+    torch.cuda.synchronize()
+    oc, os_, og = oracle.kv4_quantize(kb, mu.numpy())
+    assert float(g.cpu()[0]) == og
+    assert np.array_equal(s.cpu().numpy(), os_) and np.array_equal(c.cpu().numpy(), oc)
+    log("  computed g bit-exact")
+    gg = torch.tensor([og * 0.75], dtype=torch.float32, device=DEV)
+    c2, s2, _ = reqat.quantize_kv4(kd, mud, tensor_scale=gg)
+    torch.cuda.synchronize()
+    oc2, os2, _ = oracle.kv4_quantize(kb, mu.numpy(), float(np.float32(og * 0.75)))
+    assert np.array_equal(s2.cpu().numpy(), os2) and np.array_equal(c2.cpu().numpy(), oc2)
+    log("  given g bit-exact")
+    y, _ = reqat.fakequant_kv4(kd[:4096].contiguous(), mud)
+    torch.cuda.synchronize()
+    oy, _ = oracle.kv4_fakequant(kb[:4096], mu.numpy())
+    assert np.array_equal(wl.bf16_bits(y.cpu()), oy)
+    log("  fake-quant bit-exact")
