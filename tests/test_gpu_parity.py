@@ -538,8 +538,11 @@ def run_gemm_case(fmt, M, N, K, seed, dist="normal", wstd=0.02, g=(None, None), 
 @pytest.mark.parametrize("M,N,K", [(16, 256, 256), (37, 200, 384), (1, 1, 128), (130, 129, 512),
                                    (256, 384, 1024), (5, 300, 128), (300, 520, 768),
                                    (257, 256, 2048), (512, 1000, 1280), (48, 100, 1152),
-                                   (64, 40, 640), (33, 17, 128), (2, 8960, 1536)])
+                                   (64, 40, 640), (33, 17, 128), (2, 8960, 1536),
+                                   (100, 96, 384), (200, 130, 1152), (65, 300, 128)])
 def test_gemm_parity(fmt, M, N, K):
+    """(100, 96, 384), (200, 130, 1152) and (65, 300, 128): K % 256 == 128 with
+    M > 64, which NVFP4 runs on the 128 x 128 register-staged kernel."""
     log("gemm parity fmt=%d M=%d N=%d K=%d" % (fmt, M, N, K))
     run_gemm_case(fmt, M, N, K, seed=M * 31 + N * 7 + K, dist="student_t")
 
