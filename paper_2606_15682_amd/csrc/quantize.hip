@@ -29,9 +29,15 @@
 // Fake-quant decodes the codes again with v_cvt_scalef32_pk_{bf16,f32}_fp4
 // (code * 2^e, exact) and, for NVFP4, multiplies by m (exact, <= 6 bits).
 //
-// NVFP4 computed global scale: a first pass writes one partial absmax per
-// workgroup into the workspace; each quantize workgroup folds the partials
-// (<= 1024 words, L2-resident) before its block loop, and workgroup 0 publishes g.
+// NVFP4 computed global scale, by tensor size:
+//   up to 2^16 elements: one launch; each workgroup reads the whole tensor for
+//     its amax before its block loop (kGLocal);
+//   up to 2^19 segments of 64 blocks: one pass over x under per-segment
+//     reference scales, then a fix-up kernel (kGDeferred, nv_fixup_kernel);
+//   beyond: a first pass writes one partial absmax per workgroup into the
+//     workspace; each quantize workgroup folds the partials (<= 4096 words,
+//     L2-resident) before its block loop (kGFold).
+// Workgroup 0 publishes g in every case.
 #include <type_traits>
 
 #include "fp4_device.h"
@@ -454,7 +460,42 @@ enum GMode : int {
     kGFixed = 0,      // read from *gptr (NVFP4 given g), or none (MXFP4)
     kGFold = 1,       // folded from the partial maxima of a preceding absmax pass
     kGDeferred = 2,   // per-segment reference, corrected by nv_fixup_kernel
+    kGLocal = 3,      // small tensor: every workgroup reads all of x for the amax first
 };
+
+// Tensors of at most this many elements take kGLocal: one launch, each of its
+// (at most 8) workgroups reading the whole tensor (<= 128 KB) for the amax.
+constexpr int64_t kLocalMaxElems = int64_t(1) << 16;
+
+// Global scale of the whole tensor, computed by one workgroup (kGLocal):
+// the finite maximum over every element, eight 16-byte loads in flight per
+// thread.  Loads past the end re-read the last vector (a maximum does not
+// change), so they need no branch and all go out before the first wait.
+__device__ __forceinline__ float local_global_scale(const uint16_t *__restrict__ x, int64_t rows, int64_t cols,
+                                                    int64_t ldx) {
+    __shared__ uint32_t red[kThreads / 64];
+    const uint32_t vpr = (uint32_t)(cols / 8), nvec = (uint32_t)rows * vpr;
+    auto vec = [&](uint32_t i) {
+        i = i < nvec ? i : nvec - 1;
+        const uint32_t r = i / vpr;
+        return *reinterpret_cast<const uint4 *>(x + (int64_t)r * ldx + (int64_t)(i - r * vpr) * 8);
+    };
+    uint32_t m = 0;
+    for (uint32_t i = threadIdx.x; i < nvec; i += 8 * kThreads) {
+        uint4 d[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) d[u] = vec(i + u * kThreads);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) m = finite_max8(d[u], m);
+    }
+    m = wave_max_u32(m);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    uint32_t r = red[0];
+#pragma unroll
+    for (int k = 1; k < kThreads / 64; ++k) r = r > red[k] ? r : red[k];
+    return nv_global_scale(r);
+}
 
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
 #pragma unroll
@@ -517,6 +558,9 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
     GScale G = make_gscale(1.0f);
     if (FMT == kNV && GM == kGFold) {
         G = make_gscale(fold_partials(partials, nparts));
+        if (blockIdx.x == 0 && threadIdx.x == 0) *gptr = G.g;
+    } else if (FMT == kNV && GM == kGLocal) {
+        G = make_gscale(local_global_scale(x, rows, cols, ldx));
         if (blockIdx.x == 0 && threadIdx.x == 0) *gptr = G.g;
     } else if (FMT == kNV && GM == kGFixed) {
         G = make_gscale(*gptr);
@@ -919,10 +963,13 @@ hipError_t launch_loop(int grid, const uint16_t *x, int64_t rows, int64_t cols, 
 }
 
 template <int FMT, int OUT>
-hipError_t launch_fmt_out(GSrc gsrc, bool deferred, int grid, const uint16_t *x, int64_t rows, int64_t cols,
-                          int64_t ldx, uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy, float *gptr,
-                          uint32_t *partials, int nparts, uint16_t *seg_table, hipStream_t stream) {
+hipError_t launch_fmt_out(GSrc gsrc, bool local, bool deferred, int grid, const uint16_t *x, int64_t rows,
+                          int64_t cols, int64_t ldx, uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy,
+                          float *gptr, uint32_t *partials, int nparts, uint16_t *seg_table, hipStream_t stream) {
     constexpr int U = OUT == kCodes ? REQAT_Q_UCODES : OUT == kFakeQuant ? REQAT_Q_UFQ : REQAT_Q_UBOTH;
+    if (FMT == kNV && local)
+        return launch_loop<FMT, OUT, kGLocal, U>(grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr, partials,
+                                                nparts, seg_table, stream);
     if (FMT == kNV && deferred)
         return launch_loop<FMT, OUT, kGDeferred, U>(grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr,
                                                    partials, nparts, seg_table, stream);
@@ -977,9 +1024,10 @@ hipError_t launch_quantize(Fmt fmt, QuantOut out, const uint16_t *x, int64_t row
     if (total == 0) return hipSuccess;
     const int64_t nseg = (total + kSeg - 1) / kSeg;
     const bool nv = fmt == kNV;
-    const bool deferred = nv && gsrc == kGComputed && seg_table != nullptr && nseg <= seg_capacity;
+    const bool local = nv && gsrc == kGComputed && total * B <= kLocalMaxElems;
+    const bool deferred = !local && nv && gsrc == kGComputed && seg_table != nullptr && nseg <= seg_capacity;
     int nparts = 0;
-    if (nv && gsrc == kGComputed && !deferred) {
+    if (nv && gsrc == kGComputed && !deferred && !local) {
         hipError_t e = launch_absmax(x, rows, cols, ldx, partials, &nparts, stream);
         if (e != hipSuccess) return e;
     }
@@ -991,8 +1039,8 @@ hipError_t launch_quantize(Fmt fmt, QuantOut out, const uint16_t *x, int64_t row
     hipError_t e;
     auto run = [&](auto fmt_c, auto out_c) {
         return launch_fmt_out<decltype(fmt_c)::value, decltype(out_c)::value>(
-            gsrc, deferred, (int)grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr, partials, nparts, seg_table,
-            stream);
+            gsrc, local, deferred, (int)grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr, partials, nparts,
+            seg_table, stream);
     };
     using MXc = std::integral_constant<int, kMX>;
     using NVc = std::integral_constant<int, kNV>;

@@ -142,11 +142,14 @@ def _ramp(R, C, seed, step):
 
 
 @pytest.mark.parametrize("shape,step", [((40, 1040), 1.5), ((48, 1024), 1.0), ((7, 4096), 9.0),
-                                        ((300, 96), 0.25)])
+                                        ((300, 96), 0.25), ((80, 1040), 1.5), ((96, 1024), 1.0),
+                                        ((20, 4096), 9.0), ((1000, 96), 0.1)])
 def test_nvfp4_computed_scale_wide_range(shape, step):
-    """NVFP4 with a computed g over tensors whose rows span many binades: the
-    one-pass quantizer must lower the scale exponents of rows quantized under a
-    smaller reference and re-quantize blocks whose scale leaves the normal range."""
+    """NVFP4 with a computed g over tensors whose rows span many binades.  Up to
+    2^16 elements (the first four shapes) the single-launch path computes g
+    first; beyond (the last four), the one-pass quantizer must lower the scale
+    exponents of rows quantized under a smaller reference and re-quantize
+    blocks whose scale leaves the normal range."""
     R, C = shape
     log("nvfp4 computed scale, wide range shape=%s step=%g" % (shape, step))
     xb = _ramp(R, C, 31 + R, step)
