@@ -13,9 +13,13 @@
 // comparisons run in FP32, exactly as well.
 //
 // One lane per 16-channel block in a grid-stride loop; the shift vector is
-// read with the block (it is small and stays in cache).  A computed g takes
+// staged in LDS once per workgroup (up to kShiftLds channels; from global
+// memory beyond).  With a power-of-two g the scale byte is computed in FP32
+// as well, with an exact correction step.  A computed g takes
 // two passes: the partial maxima of |d| per workgroup, then the quantizer,
 // whose workgroups fold them.
+#include <type_traits>
+
 #include "fp4_device.h"
 #include "internal.h"
 
@@ -25,6 +29,20 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kMaxKvGroups = kMaxPartials;
+// Shift vectors of up to this many channels are staged in LDS once per
+// workgroup: read per block from global memory, the 64 shift bytes of a
+// 16-channel block would double the bytes the vector memory path moves.
+constexpr int kShiftLds = 4096;
+
+// Where a kernel reads the shift from.
+enum ShiftSrc : int { kNoShift = 0, kShiftGlobal = 1, kShiftLdsSrc = 2 };
+
+// Copies shift[0 .. cols) into LDS (cols % 4 == 0, cols <= kShiftLds).
+__device__ __forceinline__ void kv4_stage_shift(const float *__restrict__ shift, int64_t cols, float4 *lds) {
+    const float4 *src = reinterpret_cast<const float4 *>(shift);
+    for (int i = threadIdx.x; i < (int)(cols / 4); i += kThreads) lds[i] = src[i];
+    __syncthreads();
+}
 
 __device__ __forceinline__ uint32_t kv4_wave_max(uint32_t v) {
 #pragma unroll
@@ -35,9 +53,12 @@ __device__ __forceinline__ uint32_t kv4_wave_max(uint32_t v) {
     return v;
 }
 
-// The 16 shifted values of block `blk` (FP32).
+// The 16 shifted values of block `blk` (FP32); the shift comes from global
+// memory (SRC = kShiftGlobal), from its LDS copy (kShiftLdsSrc) or is absent.
+template <int SRC>
 __device__ __forceinline__ void kv4_load(const uint16_t *__restrict__ x, const float *__restrict__ shift,
-                                         int64_t blk, int64_t nb, int64_t ldx, bool narrow, float (&d)[16]) {
+                                         const float4 *lds_shift, int64_t blk, int64_t nb, int64_t ldx, bool narrow,
+                                         float (&d)[16]) {
     const int64_t r = narrow ? (int64_t)((uint32_t)blk / (uint32_t)nb) : blk / nb;
     const int64_t c0 = (blk - r * nb) * 16;
     const uint4 *src = reinterpret_cast<const uint4 *>(x + r * ldx + c0);
@@ -48,8 +69,8 @@ __device__ __forceinline__ void kv4_load(const uint16_t *__restrict__ x, const f
         d[2 * i] = f32_from_bits(w[i] << 16);
         d[2 * i + 1] = f32_from_bits(w[i] & 0xFFFF0000u);
     }
-    if (shift) {
-        const float4 *sp = reinterpret_cast<const float4 *>(shift + c0);
+    if (SRC != kNoShift) {
+        const float4 *sp = SRC == kShiftLdsSrc ? lds_shift + c0 / 4 : reinterpret_cast<const float4 *>(shift + c0);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const float4 m = sp[i];
@@ -62,17 +83,20 @@ __device__ __forceinline__ void kv4_load(const uint16_t *__restrict__ x, const f
 }
 
 // Largest finite |d| over the shifted tensor, one partial per workgroup.
+template <int SRC>
 __global__ __launch_bounds__(kThreads) void kv4_absmax_kernel(const uint16_t *__restrict__ x, int64_t rows,
                                                               int64_t cols, int64_t ldx,
                                                               const float *__restrict__ shift,
                                                               uint32_t *__restrict__ partials) {
+    __shared__ float4 lds_shift[SRC == kShiftLdsSrc ? kShiftLds / 4 : 1];
+    if (SRC == kShiftLdsSrc) kv4_stage_shift(shift, cols, lds_shift);
     const int64_t nb = cols / 16, total = rows * nb;
     const bool narrow = total < (int64_t(1) << 32);
     uint32_t m = 0;
     for (int64_t blk = (int64_t)blockIdx.x * kThreads + threadIdx.x; blk < total;
          blk += (int64_t)gridDim.x * kThreads) {
         float d[16];
-        kv4_load(x, shift, blk, nb, ldx, narrow, d);
+        kv4_load<SRC>(x, shift, lds_shift, blk, nb, ldx, narrow, d);
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             const uint32_t a = bits_from_f32(d[j]) & 0x7FFFFFFFu;
@@ -117,6 +141,37 @@ __device__ __forceinline__ uint32_t kv4_scale_byte(double a, double g) {
     return b;
 }
 
+// FP32 counterpart for a power-of-two g = 2^kg in [2^-126, 2^100]: q = a / (3.5 g)
+// to within a few ulp, its E4M3 ceiling, then one exact correction.  Every
+// bound 3.5 * s * g has at most 7 significant bits and lies in
+// [7 * 2^-136, 1568 * 2^100], so it is exact in FP32 (subnormals included).
+__device__ __forceinline__ uint32_t kv4_scale_byte_f32(float a, float g, int kg) {
+    const float q = __builtin_ldexpf(a * (2.0f / 7.0f), -kg);
+    uint32_t b;
+    if (!(q <= 448.0f)) {
+        b = 0x7Eu;
+    } else if (q <= 0x1p-9f) {
+        b = 0x01u;
+    } else {
+        const uint32_t qb = bits_from_f32(q);           // normal: q > 2^-9
+        int E = (int)(qb >> 23) - 127;
+        if (E < -6) {
+            b = (uint32_t)__builtin_ceilf(q * 0x1p9f);  // E4M3 subnormals: multiples of 2^-9 (1..8)
+        } else {
+            uint32_t m = ((qb & 0x7FFFFFu) + 0xFFFFFu) >> 20;   // ceil of the top three mantissa bits
+            if (m == 8u) {
+                m = 0u;
+                E += 1;
+            }
+            b = ((uint32_t)(E + 7) << 3) | m;
+            b = b > 0x7Eu ? 0x7Eu : b;
+        }
+    }
+    if (b < 0x7Eu && !(a <= 3.5f * e4m3_value(b) * g)) b += 1u;
+    else if (b > 1u && a <= 3.5f * e4m3_value(b - 1u) * g) b -= 1u;
+    return b;
+}
+
 // E1M2 magnitude code (0..7) of |v| / S, nearest with ties to the even code.
 __device__ __forceinline__ uint32_t e1m2_mag(double a, double S) {
     uint32_t m = 7u;
@@ -141,11 +196,13 @@ __device__ __forceinline__ uint32_t e1m2_mag_f32(float a, float S) {
     return m;
 }
 
-template <int OUT>
+template <int OUT, int SRC>
 __global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
     const uint16_t *__restrict__ x, int64_t rows, int64_t cols, int64_t ldx, const float *__restrict__ shift,
     uint8_t *__restrict__ codes, uint8_t *__restrict__ scales, uint16_t *__restrict__ y, int64_t ldy,
     float *gptr, int computed, const uint32_t *__restrict__ partials, int nparts) {
+    __shared__ float4 lds_shift[SRC == kShiftLdsSrc ? kShiftLds / 4 : 1];
+    if (SRC == kShiftLdsSrc) kv4_stage_shift(shift, cols, lds_shift);
     float g;
     if (computed) {
         __shared__ uint32_t red[kThreads / 64];
@@ -170,13 +227,14 @@ __global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
     // always is), so every threshold and decoded value is exact in FP32
     const uint32_t gb = bits_from_f32(g);
     const bool f32 = (gb & 0x807FFFFFu) == 0u && gb >= 0x00800000u && gb <= ((100u + 127u) << 23);
+    const int kg = (int)(gb >> 23) - 127;
 
     const int64_t nb = cols / 16, total = rows * nb;
     const bool narrow = total < (int64_t(1) << 32);
     for (int64_t blk = (int64_t)blockIdx.x * kThreads + threadIdx.x; blk < total;
          blk += (int64_t)gridDim.x * kThreads) {
         float d[16];
-        kv4_load(x, shift, blk, nb, ldx, narrow, d);
+        kv4_load<SRC>(x, shift, lds_shift, blk, nb, ldx, narrow, d);
         uint32_t am = 0u;
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
@@ -184,7 +242,10 @@ __global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
             am = am > a ? am : a;
         }
         const bool bad = am >= 0x7F800000u;
-        const uint32_t sbyte = bad ? 0x7Fu : (am == 0u ? 0u : kv4_scale_byte((double)f32_from_bits(am), gd));
+        const uint32_t sbyte = bad ? 0x7Fu
+                               : am == 0u ? 0u
+                               : f32 ? kv4_scale_byte_f32(f32_from_bits(am), g, kg)
+                                     : kv4_scale_byte((double)f32_from_bits(am), gd);
         const double S = (double)e4m3_value(sbyte) * gd;
         const float Sf = e4m3_value(sbyte) * g;             // exact on the FP32 path
         uint32_t c[16];
@@ -247,19 +308,27 @@ hipError_t launch_kv4(QuantOut out, const uint16_t *x, int64_t rows, int64_t col
     if (total == 0) return hipSuccess;
     int64_t grid = (total + kThreads - 1) / kThreads;
     if (grid > kMaxKvGroups) grid = kMaxKvGroups;
-    if (computed) {
-        hipLaunchKernelGGL(kv4_absmax_kernel, dim3((unsigned)grid), dim3(kThreads), 0, stream, x, rows, cols, ldx,
-                           shift, partials);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    if (out == kCodes)
-        hipLaunchKernelGGL(kv4_quantize_kernel<kCodes>, dim3((unsigned)grid), dim3(kThreads), 0, stream, x, rows,
-                           cols, ldx, shift, codes, scales, y, ldy, gptr, (int)computed, partials, (int)grid);
-    else
-        hipLaunchKernelGGL(kv4_quantize_kernel<kFakeQuant>, dim3((unsigned)grid), dim3(kThreads), 0, stream, x,
-                           rows, cols, ldx, shift, codes, scales, y, ldy, gptr, (int)computed, partials, (int)grid);
-    return hipGetLastError();
+    auto run = [&](auto src_c) {
+        constexpr int SRC = decltype(src_c)::value;
+        if (computed) {
+            hipLaunchKernelGGL(kv4_absmax_kernel<SRC>, dim3((unsigned)grid), dim3(kThreads), 0, stream, x, rows, cols,
+                               ldx, shift, partials);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+        if (out == kCodes)
+            hipLaunchKernelGGL((kv4_quantize_kernel<kCodes, SRC>), dim3((unsigned)grid), dim3(kThreads), 0, stream, x,
+                               rows, cols, ldx, shift, codes, scales, y, ldy, gptr, (int)computed, partials,
+                               (int)grid);
+        else
+            hipLaunchKernelGGL((kv4_quantize_kernel<kFakeQuant, SRC>), dim3((unsigned)grid), dim3(kThreads), 0,
+                               stream, x, rows, cols, ldx, shift, codes, scales, y, ldy, gptr, (int)computed,
+                               partials, (int)grid);
+        return hipGetLastError();
+    };
+    if (!shift) return run(std::integral_constant<int, kNoShift>{});
+    if (cols <= kShiftLds) return run(std::integral_constant<int, kShiftLdsSrc>{});
+    return run(std::integral_constant<int, kShiftGlobal>{});
 }
 
 }  // namespace reqat
