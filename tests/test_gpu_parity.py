@@ -701,3 +701,69 @@ def test_linear_parity(fmt, M, N, K, given):
     assert np.array_equal(outs[0], outs[1], equal_nan=True), "poison visible or nondeterministic"
     ms, ns = np.arange(M).repeat(N), np.tile(np.arange(N), M)
     check_gemm_points(fmt, ac, as_, ga, bc, bs, gb, outs[0], outs[2], ms, ns)
+
+
+# ------------------------------------------------------- strided operands
+
+@pytest.mark.parametrize("fmt", [NV, MX])
+@pytest.mark.parametrize("M,N,K", [(16, 200, 512), (300, 520, 1024), (130, 96, 384)])
+def test_products_into_strided_output(fmt, M, N, K):
+    """Products written into a wider row-major buffer (ldy > N, e.g. one slice
+    of a fused QKV output) and, for the linear layer, read from a wider
+    activation buffer (ldx > K): the slice matches the oracle and the padding
+    columns keep their poison.  Covers the skinny (M <= 64), tiled and
+    register-staged (NVFP4 with K % 256 == 128) kernels."""
+    log("strided products fmt=%d M=%d N=%d K=%d" % (fmt, M, N, K))
+    seed = 3 * M + N + K
+    xa = _rand(M, K, seed, "student_t", outliers=max(1, K // 100))
+    xb = _rand(N, K, seed + 1, "normal", std=0.02)
+    ac, as_, ga = oracle.quantize(fmt, xa)
+    bc, bs, gb = oracle.quantize(fmt, xb)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    gat = None if fmt == MX else torch.tensor([ga], dtype=torch.float32, device=DEV)
+    gbt = None if fmt == MX else torch.tensor([gb], dtype=torch.float32, device=DEV)
+    pad = 40
+    ms, ns = np.arange(M).repeat(N), np.tile(np.arange(N), M)
+    ref, aref = oracle.gemm_points(fmt, ac, as_, ga, bc, bs, gb, ms, ns)
+    ref, aref = ref.reshape(M, N), aref.reshape(M, N)
+    for dt in (torch.float32, torch.bfloat16):
+        big = torch.full((M, N + pad), float("nan"), dtype=dt, device=DEV)
+        reqat.gemm(fmt, t(ac), t(as_), gat, t(bc), t(bs), gbt, out_dtype=dt, out=big[:, :N])
+        # the linear layer, activations read with ldx = K + 64
+        xbig = np.zeros((M, K + 64), np.uint16)
+        xbig[:, :K] = xa
+        xv = wl.from_bits(xbig).to(DEV)[:, :K]
+        big2 = torch.full((M, N + pad), float("nan"), dtype=dt, device=DEV)
+        reqat.linear(xv, fmt, t(bc), t(bs), gbt, out_dtype=dt, out=big2[:, :N])
+        torch.cuda.synchronize()
+        for b in (big, big2):
+            got = b.float().cpu().numpy().astype(np.float64)
+            assert np.all(np.isnan(got[:, N:])), "padding columns written"
+            y = got[:, :N]
+            if dt == torch.float32:
+                assert np.all(np.abs(y - ref) <= GEMM_TOL * aref)
+            else:
+                rb = indep.bf16_values(oracle.bf16_from_double_array(ref.reshape(-1))).reshape(M, N)
+                ulp = np.maximum(np.abs(rb), 2.0 ** -133) * 2.0 ** -7
+                assert np.all(np.abs(y - rb) <= ulp + GEMM_TOL * aref)
+
+
+@pytest.mark.parametrize("M,N,K", [(16, 200, 512), (40, 130, 1024)])
+def test_w4a16_strided(M, N, K):
+    """W4A16 with activations read at ldx > K and the output written at ldy > N."""
+    log("w4a16 strided M=%d N=%d K=%d" % (M, N, K))
+    xb = _rand(M, K, 71 + M, "student_t", outliers=3)
+    wc, ws = _w4a16_weights(N, K, 72 + N)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    xbig = np.zeros((M, K + 128), np.uint16)
+    xbig[:, :K] = xb
+    xv = wl.from_bits(xbig).to(DEV)[:, :K]
+    big = torch.full((M, N + 24), float("nan"), dtype=torch.float32, device=DEV)
+    reqat.gemm_w4a16(xv, t(wc), t(ws), out_dtype=torch.float32, out=big[:, :N])
+    torch.cuda.synchronize()
+    got = big.cpu().numpy().astype(np.float64)
+    assert np.all(np.isnan(got[:, N:])), "padding columns written"
+    ms, ns = np.arange(M).repeat(N), np.tile(np.arange(N), M)
+    ref, aref = oracle.gemm_w4a16_points(xb, wc, ws, ms, ns)
+    err = np.abs(got[:, :N].reshape(-1) - ref)
+    assert np.all(err <= GEMM_TOL * aref)
