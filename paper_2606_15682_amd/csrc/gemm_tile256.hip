@@ -610,19 +610,16 @@ __device__ __forceinline__ uint32_t mx_scale_read(const uint8_t *p) {
 
 // Part K of substep S of a stage: the 4 MFMAs of A tile K, the reads of A
 // tile K's and B tile K's operands for the next substep (and, in the last
-// substep, the next stage's scale bytes for them), and a share of the loads.
-// The loads of a stage go out in two halves: the first in the last substep of
-// the stage NB before it (right after the barrier that frees its buffer), the
-// second in substep 0 of the following stage.
+// substep, the next stage's scale bytes for them), and, in the last substep,
+// a quarter of the loads of the stage NB later: they go out right after the
+// barrier that frees its buffer, one per MFMA, which leaves them the most time.
 template <class C, int S, int NS, int K, class Issue>
 __device__ __forceinline__ void mx_part(v16f (&acc)[4][4], MxState<C> &st, const uint8_t *buf,
-                                        const uint8_t *nbuf, const uint8_t *nsc, const MxLane<C> &ln, Issue &prev,
+                                        const uint8_t *nbuf, const uint8_t *nsc, const MxLane<C> &ln,
                                         Issue &next) {
     constexpr int E = S & 1, LAST = S == NS - 1;
     constexpr int ND = LAST ? 4 : 2;
-    // load parts: 8 per half, two per substep part
-    constexpr int NGN = LAST ? Issue::template count<2 * K, 8>() + Issue::template count<2 * K + 1, 8>() : 0;
-    constexpr int HALF2 = S == 0 ? 1 : 0;
+    constexpr int NG = LAST ? Issue::template count<K, 4>() : 0;
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (!LAST) {
         st.a[E ^ 1][K] = lds16(buf + ln.codeA[S + 1] + 32 * C::ROW * K);
@@ -633,19 +630,11 @@ __device__ __forceinline__ void mx_part(v16f (&acc)[4][4], MxState<C> &st, const
         st.na[K] = mx_scale_read<C>(nsc + ln.scA + MxLane<C>::SCSTEP * K);
         st.nb[K] = mx_scale_read<C>(nsc + ln.scB + MxLane<C>::SCSTEP * K);
     }
-    if constexpr (LAST) {
-        next.template region<2 * K, 16>();
-        next.template region<2 * K + 1, 16>();
-    }
-    if constexpr (HALF2) {
-        prev.template region<8 + 2 * K, 16>();
-        prev.template region<9 + 2 * K, 16>();
-    }
+    if constexpr (LAST) next.template region<K, 4>();
 #pragma unroll
     for (int j = 0; j < 4; ++j)
         acc[K][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
             as_v8i(st.a[E][K]), as_v8i(st.b[E][j]), acc[K][j], 4, 4, S, (int)st.sa[K], S, (int)st.sb[j]);
-    constexpr int NG = NGN + (HALF2 ? Issue::template count<8 + 2 * K, 16>() + Issue::template count<9 + 2 * K, 16>() : 0);
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // one MFMA
@@ -662,48 +651,37 @@ __device__ __forceinline__ void mx_part(v16f (&acc)[4][4], MxState<C> &st, const
 template <class C, int S, int NS, class Issue>
 __device__ __forceinline__ void mx_substep(v16f (&acc)[4][4], MxState<C> &st, const uint8_t *buf,
                                            const uint8_t *nbuf, const uint8_t *nsc, const MxLane<C> &ln,
-                                           Issue &prev, Issue &next) {
-    mx_part<C, S, NS, 0>(acc, st, buf, nbuf, nsc, ln, prev, next);
-    mx_part<C, S, NS, 1>(acc, st, buf, nbuf, nsc, ln, prev, next);
-    mx_part<C, S, NS, 2>(acc, st, buf, nbuf, nsc, ln, prev, next);
-    mx_part<C, S, NS, 3>(acc, st, buf, nbuf, nsc, ln, prev, next);
-}
-
-template <class C>
-constexpr int half_count() {
-    return StageIssue<C>::template count<0, 2>();       // loads in parts 0..7 of 16
-}
-
-template <class C>
-__device__ __forceinline__ void load_first_half(StageIssue<C> &is) {
-    is.template region<0, 2>();
+                                           Issue &next) {
+    mx_part<C, S, NS, 0>(acc, st, buf, nbuf, nsc, ln, next);
+    mx_part<C, S, NS, 1>(acc, st, buf, nbuf, nsc, ln, next);
+    mx_part<C, S, NS, 2>(acc, st, buf, nbuf, nsc, ln, next);
+    mx_part<C, S, NS, 3>(acc, st, buf, nbuf, nsc, ln, next);
 }
 
 // Scale-group loads issued after the last code load of stage g + 1 and before
-// the wait in stage g (phase PH = g % GS_): one at the start of each stage
-// j in [g + 3 - NB, g] with j % GS_ == 0 (stage g + 1's second half goes out
-// in substep 0 of stage g + 2 - NB, after that stage's group loads).
+// the wait in stage g (phase PH = g % GS_): stage g + 1's loads go out in the
+// last substep of stage g + 1 - NB, and a group at the start of each stage j
+// with j % GS_ == 0, so the groups of stages j in [g + 2 - NB, g] count.
 template <int NB, int GS_, int PH>
 constexpr int groups_after() {
     int n = 0;
-    for (int d = 0; d <= NB - 3; ++d)
+    for (int d = 0; d <= NB - 2; ++d)
         if (((PH - d) % GS_ + GS_) % GS_ == 0) ++n;
     return n;
 }
 
 // One stage of the MXFP4 stream.  Past the end of the workgroup's stages the
-// loads still go out (re-reading its first stage into a buffer nobody reads
-// again), so every stage issues exactly LPS loads and the wait before the
-// barrier is a constant of the stage's phase: the NB - 2 stages issued after
-// stage g + 1 may stay in flight, and with scale groups (GS) also the group
-// loads issued since (a group is loaded at the start of its phase-0 stage,
-// ahead of that stage's code loads).  A tile's first stage (after the
-// previous tile's stores) waits for everything instead.  PH is the stage's
-// position in its scale group (GS).
+// loads still go out (re-reading a stage of its first tile into a buffer
+// nobody reads again), so every stage issues exactly LPS loads and the wait
+// before the barrier is a constant of the stage's phase: the NB - 2 stages
+// issued after stage g + 1 may stay in flight, and with scale groups (GS)
+// also the group loads issued since (a group is loaded at the start of the
+// stage whose loads, issued at its end, are the group's first stage).  A
+// tile's first stage (after the previous tile's stores) waits for everything
+// instead.  PH is the stage's position in its scale group (GS).
 template <class C, int NB, int PH>
 __device__ __forceinline__ void mx_stage_p(v16f (&acc)[4][4], MxState<C> &st, uint8_t *smem, int64_t gs,
-                                           bool first, const MxLane<C> &ln, StageIssue<C> &prev,
-                                           StageIssue<C> &issue) {
+                                           bool first, const MxLane<C> &ln, StageIssue<C> &issue) {
     constexpr int NS = C::CH / 2;
     const int bi = (int)(gs % NB);
     uint8_t *buf = smem + bi * C::STAGE;
@@ -720,20 +698,20 @@ __device__ __forceinline__ void mx_stage_p(v16f (&acc)[4][4], MxState<C> &st, ui
         st.sa[i] = st.na[i];
         st.sb[i] = st.nb[i];
     }
-    mx_substep<C, 0, NS>(acc, st, buf, nbuf, nsc, ln, prev, issue);
+    mx_substep<C, 0, NS>(acc, st, buf, nbuf, nsc, ln, issue);
     if constexpr (NS == 4) {
-        mx_substep<C, 1, NS>(acc, st, buf, nbuf, nsc, ln, prev, issue);
-        mx_substep<C, 2, NS>(acc, st, buf, nbuf, nsc, ln, prev, issue);
+        mx_substep<C, 1, NS>(acc, st, buf, nbuf, nsc, ln, issue);
+        mx_substep<C, 2, NS>(acc, st, buf, nbuf, nsc, ln, issue);
     }
     constexpr int kInFlight = (NB - 2) * C::LPS + C::GLPW * groups_after<NB, C::GSTAGES, PH>();
     if (first) wait_vmcnt<0>();
     else wait_vmcnt<kInFlight>();
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    mx_substep<C, NS - 1, NS>(acc, st, buf, nbuf, nsc, ln, prev, issue);
+    mx_substep<C, NS - 1, NS>(acc, st, buf, nbuf, nsc, ln, issue);
 }
 
 // Scale group loads (GS): wave w takes rows 64w .. 64w+63 of A and of B, 16
-// bytes (four stages) per row, into group buffer `gbuf`; edge tiles clamp rows.
+// bytes (GSTAGES stages) per row, into group buffer `gbuf`; edge tiles clamp rows.
 // The addresses are those of the stage loads that start the group (their
 // scale pointers and row limits).
 template <class C>
@@ -763,35 +741,45 @@ __device__ __forceinline__ void mx_persistent(uint8_t *smem, int64_t M, int64_t 
     const int64_t cpr = K / 2, spr = K / C::B;
     const TileGeo g0 = tile_geo(w, M, N);
 
-    // loads of the stream position p (the workgroup's first stage once past its end)
-    auto issue_at = [&](const LoadPos<C> &p, uint8_t *buf) {
-        const bool live = p.v < T;
-        const TileGeo &g = live ? p.g : g0;
-        const int64_t k0 = live ? (int64_t)p.s * KS : 0;
-        return StageIssue<C>{buf, true, wave, lane, g.rows_a, g.rows_b, cpr, spr,
-                             a_codes + g.m0 * cpr + k0 / 2, b_codes + g.n0 * cpr + k0 / 2,
-                             a_scales + g.m0 * spr + k0 / C::B, b_scales + g.n0 * spr + k0 / C::B};
+    // The load stream's position: the stage s within tile v, with the row
+    // bases of that tile's operands (of the workgroup's first tile once past
+    // the end: those loads land in a buffer nobody reads, and any stage of
+    // that tile is in range).  The bases change only with the tile, so a
+    // stage adds just its K offset.
+    struct Pos {
+        int64_t v;
+        int s, rows_a, rows_b;
+        const uint8_t *ac, *bc, *as_, *bs_;
     };
-    // scale group q (stream stages 4q .. 4q+3) into group buffer q & 1 (GS), from
-    // the loads of its first stage
+    auto pos_at = [&](int64_t v) {
+        const TileGeo g = v < T ? tile_geo(v, M, N) : g0;
+        return Pos{v, 0, g.rows_a, g.rows_b, a_codes + g.m0 * cpr, b_codes + g.n0 * cpr,
+                   a_scales + g.m0 * spr, b_scales + g.n0 * spr};
+    };
+    auto advance = [&](Pos &p) {
+        if (++p.s == nst) p = pos_at(p.v + G);
+    };
+    auto issue_at = [&](const Pos &p, uint8_t *buf) {
+        const int64_t k0 = (int64_t)p.s * KS;
+        return StageIssue<C>{buf, true, wave, lane, p.rows_a, p.rows_b, cpr, spr,
+                             p.ac + k0 / 2, p.bc + k0 / 2, p.as_ + k0 / C::B, p.bs_ + k0 / C::B};
+    };
+    // scale group q (stream stages GSTAGES*q ..) into group buffer q & 1 (GS),
+    // from the loads of its first stage
     auto group_at = [&](const StageIssue<C> &at, int64_t q) {
         load_scale_group<C>(smem + C::SC_RING + (int)(q & 1) * C::GROUP, wave, lane, at);
     };
 
-    // prologue: scale group 0 (GS), stages 0 .. NB-1 into buffers 0 .. NB-1
-    // (the second half of stage NB-1 goes out in substep 0 of stage 0), then
-    // wait for stage 0
-    LoadPos<C> ld{w, 0, g0};
-    StageIssue<C> prev = issue_at(ld, smem);
-    if constexpr (C::kGS) group_at(prev, 0);
+    // prologue: scale group 0 (GS), stages 0 .. NB-1 into buffers 0 .. NB-1,
+    // then wait for stage 0
+    Pos ld = pos_at(w);
+    if constexpr (C::kGS) group_at(issue_at(ld, smem), 0);
 #pragma unroll
     for (int p = 0; p < NB; ++p) {
-        prev = issue_at(ld, smem + p * C::STAGE);
-        if (p < NB - 1) prev.template region<0, 1>();
-        else load_first_half(prev);
-        ld.advance(nst, G, M, N);
+        issue_at(ld, smem + p * C::STAGE).template region<0, 1>();
+        advance(ld);
     }
-    wait_vmcnt<(NB - 2) * C::LPS + half_count<C>()>();
+    wait_vmcnt<(NB - 1) * C::LPS>();
     asm volatile("s_barrier" ::: "memory");
 
     const MxLane<C> ln(wm * 128 + (lane & 31), wn * 128 + (lane & 31), h);
@@ -816,12 +804,11 @@ __device__ __forceinline__ void mx_persistent(uint8_t *smem, int64_t M, int64_t 
             static_for<0, U>([&](auto P) {
                 constexpr int ph = decltype(P)::value;
                 StageIssue<C> issue = issue_at(ld, smem);   // stage gs + NB
-                // the group after this one starts at stage gs + NB (NB == 4):
-                // loaded ahead of this stage's code loads
+                // the group after this one starts at stage gs + NB (NB == GSTAGES):
+                // loaded ahead of the code loads of that stage
                 if constexpr (C::kGS && ph == 0) group_at(issue, gs / U + 1);
-                mx_stage_p<C, NB, ph>(acc, st, smem, gs, s == 0 && ph == 0, ln, prev, issue);
-                ld.advance(nst, G, M, N);
-                prev = issue;
+                mx_stage_p<C, NB, ph>(acc, st, smem, gs, s == 0 && ph == 0, ln, issue);
+                advance(ld);
                 ++gs;
             });
         }
