@@ -76,6 +76,7 @@ def parse():
                     help="workload number (4 = 14B gate/up; 2 = NVFP4 W4A4 decode; 6, 7 = MXFP4 W4A16 "
                          "decode; 8 = SEM loss head; 9 = KV4 keys)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="skip timing the step as a HIP graph replay")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes --steps times "
                          "(calibrates rocprof FETCH_SIZE/WRITE_SIZE against a known size)")
@@ -634,6 +635,31 @@ def main():
     torch.cuda.synchronize()
     linear_ms = lev[0].elapsed_time(lev[1]) / args.steps
 
+    # the same step captured once in a HIP graph and replayed: the library
+    # allocates, clears and synchronises nothing, so the step captures as is
+    graph_ms = None
+    if not args.no_graph:
+        gstream = torch.cuda.Stream()
+        gstream.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(gstream):
+            step()
+        torch.cuda.current_stream().wait_stream(gstream)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        for _ in range(max(1, args.warmup)):
+            graph.replay()
+        gev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        gev[0].record()
+        for _ in range(args.steps):
+            graph.replay()
+        gev[1].record()
+        torch.cuda.synchronize()
+        graph_ms = gev[0].elapsed_time(gev[1]) / args.steps
+        del graph
+
     # MXFP4: the block-rotated activation quantizer (randomized Hadamard of 32
     # fused into the quantizer), timed apart from the step
     rht_ms = None
@@ -693,6 +719,10 @@ def main():
     kern["linear"] = {"ms": round(linear_ms, 4),
                       "vs_quantize_x_plus_gemm": round(linear_ms / (per["quantize_x"] + per["gemm"]), 4),
                       "note": "reqat_linear_w4a4: quantize X + GEMM in one call, timed separately"}
+    if graph_ms is not None:
+        kern["graph_step"] = {"ms": round(graph_ms, 4), "vs_eager_step": round(graph_ms / ms_step, 4),
+                              "note": "the same step captured once in a HIP graph and replayed (no launch gaps "
+                                      "between its kernels); value and ms_per_step use the eager launches"}
     out = {
         "metric": METRIC,
         "value": round(flops / (ms_step * 1e-3) / 1e12, 2),

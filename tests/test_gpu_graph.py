@@ -1,0 +1,112 @@
+"""The QAT layer step captured in a HIP graph (torch.cuda.CUDAGraph).
+
+The library allocates nothing, records no memset and never synchronises, so
+a caller may capture its calls.  A captured step (fused quantize + fake-quant
+of X and W with computed global scales, the product, the one-call linear)
+is replayed several times, with other eager library work and host
+synchronisation between replays and its outputs overwritten before each
+replay; every replay must reproduce the eager outputs bit for bit.  Eager
+parity with the oracle is covered by the other GPU tests.
+"""
+import pytest
+import torch
+
+from paper_2606_15682_amd import reqat
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def _inputs(M, N, K, seed):
+    gen = torch.Generator().manual_seed(seed)
+    x = (torch.randn(M, K, generator=gen) * 2.0).to(torch.bfloat16).to(DEV)
+    w = (torch.randn(N, K, generator=gen) * 0.02).to(torch.bfloat16).to(DEV)
+    return x, w
+
+
+def _buffers(fmt, M, N, K):
+    B = reqat.BLOCK[fmt]
+    def q(R):
+        return (torch.empty((R, K // 2), dtype=torch.uint8, device=DEV),
+                torch.empty((R, K // B), dtype=torch.uint8, device=DEV),
+                torch.empty((R, K), dtype=torch.bfloat16, device=DEV),
+                torch.empty(1, dtype=torch.float32, device=DEV))
+    return {"x": q(M), "w": q(N),
+            "y": torch.empty((M, N), dtype=torch.bfloat16, device=DEV),
+            "yl": torch.empty((M, N), dtype=torch.bfloat16, device=DEV),
+            "gl": torch.empty(1, dtype=torch.float32, device=DEV),
+            "lws": torch.empty(max(reqat.reqat_linear_workspace_bytes(fmt, M, K), 16), dtype=torch.uint8,
+                               device=DEV)}
+
+
+def _step(fmt, x, w, b):
+    """One pass of the layer's hot path into the preallocated buffers."""
+    xc, xs, xy, xg = b["x"]
+    wc, ws, wy, wg = b["w"]
+    reqat.quantize_fakequant(x, fmt, out=(xc, xs, xy), g_out=xg if fmt == reqat.NVFP4 else None)
+    reqat.quantize_fakequant(w, fmt, out=(wc, ws, wy), g_out=wg if fmt == reqat.NVFP4 else None)
+    nv = fmt == reqat.NVFP4
+    reqat.gemm(fmt, xc, xs, xg if nv else None, wc, ws, wg if nv else None, out_dtype=torch.bfloat16, out=b["y"])
+    reqat.linear(x, fmt, wc, ws, wg if nv else None, out_dtype=torch.bfloat16, out=b["yl"],
+                 g_out=b["gl"] if nv else None, ws=b["lws"])
+
+
+def _flat(fmt, b):
+    """Every output of the step (the global scales only for NVFP4, which has them)."""
+    nv = fmt == reqat.NVFP4
+    out = []
+    for k in ("x", "w"):
+        out += list(b[k][:3]) + ([b[k][3]] if nv else [])
+    out += [b["y"], b["yl"]] + ([b["gl"]] if nv else [])
+    return out
+
+
+def _scramble(fmt, b):
+    for t in _flat(fmt, b):
+        if t.dtype == torch.uint8:
+            t.fill_(0xA5)
+        else:
+            t.fill_(float("nan"))
+
+
+@pytest.mark.parametrize("fmt", [reqat.NVFP4, reqat.MXFP4], ids=["nvfp4", "mxfp4"])
+@pytest.mark.parametrize("M,N,K", [(300, 520, 1024), (16, 768, 512)])
+def test_step_graph_replays_match_eager(fmt, M, N, K):
+    log(f"graph step fmt={fmt} M={M} N={N} K={K}")
+    x, w = _inputs(M, N, K, seed=1000 + 7 * M + fmt)
+    b = _buffers(fmt, M, N, K)
+    reqat.workspace(torch.device(DEV))                  # library workspace exists before capture
+    _step(fmt, x, w, b)
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in _flat(fmt, b)]
+
+    # unrelated eager work between replays: the same step on other inputs into other buffers
+    x2, w2 = _inputs(M, N, K, seed=2000 + M)
+    b2 = _buffers(fmt, M, N, K)
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):                          # warm-up on the capture stream
+        _step(fmt, x, w, b)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        _step(fmt, x, w, b)
+    torch.cuda.synchronize()
+
+    for rep in range(3):
+        _scramble(fmt, b)
+        _step(fmt, x2, w2, b2)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (got, want) in enumerate(zip(_flat(fmt, b), ref)):
+            assert torch.equal(got.view(torch.uint8), want.view(torch.uint8)), \
+                f"replay {rep}: output {i} differs from the eager step"
+    log("graph replays match")
