@@ -83,6 +83,32 @@ def parse():
     return ap.parse_args()
 
 
+def graph_step_ms(step, args) -> float:
+    """Mean time of `step` captured once in a HIP graph and replayed args.steps
+    times (events around the replays).  The library allocates, clears and
+    synchronises nothing, so a step of its calls captures as is."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):                       # warm-up on the capture stream
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for _ in range(max(1, args.warmup)):
+        graph.replay()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(args.steps):
+        graph.replay()
+    ev[1].record()
+    torch.cuda.synchronize()
+    return ev[0].elapsed_time(ev[1]) / args.steps
+
+
 def copy_calibration(nbytes: int, steps: int):
     import torch
     src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
@@ -286,6 +312,7 @@ def bench_decode(args, w):
     torch.cuda.synchronize()
     ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
     ms_dev = ev[0].elapsed_time(ev[1]) / args.steps
+    graph_ms = None if args.no_graph else graph_step_ms(step, args)
 
     # the product alone (activation codes from one quantize), timed apart
     xc, xs, gx = reqat.quantize(x, fmt)
@@ -334,6 +361,12 @@ def bench_decode(args, w):
         "note": ("the same weights are re-read every step, so they sit in the 256 MB Infinity Cache: "
                  "a cache-resident rate, an upper bound for weights streamed from HBM"),
     }
+    if graph_ms is not None:
+        out["kernels"]["graph_step"] = {
+            "ms": round(graph_ms, 4), "GB/s": round(step_bytes / (graph_ms * 1e-3) / 1e9, 1),
+            "note": "the same step captured once in a HIP graph and replayed (events around the replays); "
+                    "at this size the graph launch costs more than the eager launches it replaces; value "
+                    "and ms_per_step use the eager launches"}
     out["ceilings"] = practical_ceilings()
     if not args.no_cpu_baseline:
         import oracle
@@ -635,30 +668,7 @@ def main():
     torch.cuda.synchronize()
     linear_ms = lev[0].elapsed_time(lev[1]) / args.steps
 
-    # the same step captured once in a HIP graph and replayed: the library
-    # allocates, clears and synchronises nothing, so the step captures as is
-    graph_ms = None
-    if not args.no_graph:
-        gstream = torch.cuda.Stream()
-        gstream.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(gstream):
-            step()
-        torch.cuda.current_stream().wait_stream(gstream)
-        torch.cuda.synchronize()
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            step()
-        for _ in range(max(1, args.warmup)):
-            graph.replay()
-        gev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-        torch.cuda.synchronize()
-        gev[0].record()
-        for _ in range(args.steps):
-            graph.replay()
-        gev[1].record()
-        torch.cuda.synchronize()
-        graph_ms = gev[0].elapsed_time(gev[1]) / args.steps
-        del graph
+    graph_ms = None if args.no_graph else graph_step_ms(step, args)
 
     # MXFP4: the block-rotated activation quantizer (randomized Hadamard of 32
     # fused into the quantizer), timed apart from the step
