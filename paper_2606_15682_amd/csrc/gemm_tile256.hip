@@ -104,11 +104,11 @@ template <int B, int E, typename F> __device__ __forceinline__ void static_for(F
 constexpr int GROUP_M = 8;
 
 // GS (MXFP4 with K % 512 == 0 and 16-byte aligned scales): the scale bytes
-// are not part of the stage; they go to LDS four stages at a time, 16 bytes
-// per row (one 1 KB load per 64 rows), into a ring of two group buffers.
-// Loading a stage's 4 bytes per row would touch one cache line per row for
-// every 4 bytes, and the vector memory path of a CU is bound by the number
-// of distinct cache lines its loads touch, not by their bytes.
+// are not part of the stage; they go to LDS 16 bytes per row at a time (two
+// stages of K = 256: one 1 KB load per 64 rows), into a ring of two group
+// buffers.  Loading a stage's 8 bytes per row would touch one cache line per
+// row for every 8 bytes, and the vector memory path of a CU is bound by the
+// number of distinct cache lines its loads touch, not by their bytes.
 template <int FMT, int KS, int NBUF, bool GS = false>
 struct Cfg {
     static constexpr bool kGS = GS;
@@ -881,7 +881,7 @@ hipError_t launch_gemm_tile256(Fmt fmt, int64_t M, int64_t N, int64_t K, const u
                                const uint8_t *b_scales, const float *gb, void *y, bool y_bf16,
                                int64_t ldy, hipStream_t stream) {
     if (fmt == kMX) {
-        // scale groups need whole groups of four stages per tile and 16-byte aligned group loads
+        // scale groups need whole groups (GSTAGES stages) per tile and 16-byte aligned group loads
         constexpr int kGroupK = Cfg<kMX, REQAT_MX_GS_KS, REQAT_MX_GS_NBUF, true>::GSTAGES * REQAT_MX_GS_KS;
         const bool gs = K % kGroupK == 0 && (reinterpret_cast<uintptr_t>(a_scales) & 15u) == 0 &&
                         (reinterpret_cast<uintptr_t>(b_scales) & 15u) == 0;
