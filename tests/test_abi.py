@@ -49,6 +49,21 @@ def test_library_exports_every_declared_symbol(lib):
         assert hasattr(lib, n)
 
 
+def test_library_imports_no_allocation_copy_or_sync(lib):
+    """The library launches kernels and queries the device, nothing else: it
+    allocates no memory, clears and copies none, and never synchronises (so
+    callers may capture its calls in a graph and own every buffer)."""
+    out = subprocess.run(["nm", "-D", "--undefined-only", reqat.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    imported = {s.split("@")[0] for s in re.findall(r"\sU\s(\S+)", out)}
+    hip = {s for s in imported if s.lower().startswith(("hip", "__hip", "hsa"))}
+    allowed = {"hipLaunchKernel", "hipFuncSetAttribute", "hipGetDevice", "hipDeviceGetAttribute",
+               "hipGetLastError", "__hipPushCallConfiguration", "__hipPopCallConfiguration",
+               "__hipRegisterFatBinary", "__hipRegisterFunction", "__hipUnregisterFatBinary"}
+    assert hip <= allowed, sorted(hip - allowed)
+    assert "hipLaunchKernel" in hip
+
+
 def test_small_queries(lib):
     assert reqat.reqat_abi_version() == 8
     assert reqat.reqat_workspace_bytes() == 4 * 4096 + 2 * (1 << 19)   # partials + segment table
