@@ -480,13 +480,15 @@ __device__ __forceinline__ float local_global_scale(const uint16_t *__restrict__
         const uint32_t r = i / vpr;
         return *reinterpret_cast<const uint4 *>(x + (int64_t)r * ldx + (int64_t)(i - r * vpr) * 8);
     };
+    // 16 loads in flight per thread: a tensor of up to 16 * kThreads vectors
+    // (32K elements, a decode step's activations) costs one memory round trip
     uint32_t m = 0;
-    for (uint32_t i = threadIdx.x; i < nvec; i += 8 * kThreads) {
-        uint4 d[8];
+    for (uint32_t i = threadIdx.x; i < nvec; i += 16 * kThreads) {
+        uint4 d[16];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) d[u] = vec(i + u * kThreads);
+        for (int u = 0; u < 16; ++u) d[u] = vec(i + u * kThreads);
 #pragma unroll
-        for (int u = 0; u < 8; ++u) m = finite_max8(d[u], m);
+        for (int u = 0; u < 16; ++u) m = finite_max8(d[u], m);
     }
     m = wave_max_u32(m);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
