@@ -144,7 +144,7 @@ reqat_status reqat_quantize_fakequant_fp4(reqat_format fmt, const void *x, int64
 
 /*
  * MXFP4 quantization of block-rotated rows (the block rotation ReQAT applies
- * to MXFP4 activations before quantizing them, Sec. 3.3 "Additional
+ * to MXFP4 activations before quantizing them, Sec. 4.3 "Additional
  * implementation details" and App. C.2): each 32-element block x of a row
  * becomes
  *     y = H_32 * D * x / sqrt(32),   D = diag(d), d_j = -1 where bit j of signs is set,
@@ -201,8 +201,8 @@ size_t reqat_w4a16_workspace_bytes(int64_t M, int64_t N, int64_t K);
 
 /*
  * KV-cache quantization of the NVFP4 W4A4KV4 setting: E1M2 elements (the KV4
- * element format, Sec. 3.3 "Additional implementation details") with the
- * Q-FIT post-RoPE shift applied first (Sec. 3.3, K~ = R(K_pre / s) - m):
+ * element format, Sec. 4.3 "Additional implementation details") with the
+ * Q-FIT post-RoPE shift applied first (Sec. 4.3, K~ = R(K_pre / s) - m):
  *     d[r][c] = RN_fp32(x[r][c] - shift[c])            (shift == NULL: d = x)
  * quantized along c in blocks of 16: an E4M3 block scale, the smallest with
  * block_amax <= 3.5 * s * g, an FP32 tensor scale g (REQAT_TS_COMPUTE: the
@@ -231,7 +231,7 @@ reqat_status reqat_fakequant_kv4(const void *x, int64_t rows, int64_t cols, int6
                                  void *stream);
 
 /*
- * SEM loss, the training objective of ReQAT's TAQ stage (Sec. 3.2):
+ * SEM loss, the training objective of ReQAT's TAQ stage (Sec. 4.2):
  *     L = (1/T) sum_t NLL_t + lambda (1/T) sum_t w_t H_t,
  *     w_t = max(0, 1 - (H_t - H_min) / (tau - H_min + eps)),
  * with, per token t (a row of bfloat16 logits over the vocabulary, p its

@@ -388,7 +388,7 @@ def kv4_fakequant(x: np.ndarray, shift=None, g: float | None = None):
 def sem_row_stats(logits_bits: np.ndarray, targets: np.ndarray):
     """Per token t (one row of bfloat16 logits over the vocabulary): the
     predictive entropy H_t = -sum_j p_j log p_j, the SFT term NLL_t =
-    -log p_{y_t}, and log-sum-exp, with p = softmax(logits) (Sec. 3.2, the
+    -log p_{y_t}, and log-sum-exp, with p = softmax(logits) (Sec. 4.2, the
     token-level entropy of Sec. 2 and the SFT objective), in FP64."""
     z = _bf16_rows_f64(logits_bits)
     m = z.max(axis=1, keepdims=True)
@@ -409,7 +409,7 @@ def _bf16_rows_f64(bits: np.ndarray) -> np.ndarray:
 
 
 def sem_weights(H: np.ndarray, eps: float) -> np.ndarray:
-    """Soft weights of SEM (Sec. 3.2): w_t = max(0, 1 - (H_t - H_min) / (tau - H_min + eps)),
+    """Soft weights of SEM (Sec. 4.2): w_t = max(0, 1 - (H_t - H_min) / (tau - H_min + eps)),
     H_min the minibatch minimum and tau its 75th percentile (linear interpolation
     between order statistics at position 0.75 (T - 1))."""
     H = np.asarray(H, np.float64)
@@ -423,7 +423,7 @@ def sem_weights(H: np.ndarray, eps: float) -> np.ndarray:
 
 
 def sem_loss(H, nll, lam: float, eps: float):
-    """L_SEM = mean_t NLL_t + lam * (1/T) sum_t w_t H_t (Sec. 3.2).  Returns
+    """L_SEM = mean_t NLL_t + lam * (1/T) sum_t w_t H_t (Sec. 4.2).  Returns
     (L, L_SFT, L_ent, w)."""
     w, _, _ = sem_weights(H, eps)
     T = len(H)

@@ -24,9 +24,14 @@
  *     k >= -126, with tensor_absmax <= 6 * 448 * 2^k;
  *   - a block holding NaN or Inf gets a NaN scale and zero codes;
  *   - codes are packed two per byte, element 2i in bits 3:0.
- * Arithmetic is FP64 throughout, and every product formed is exact in FP64
- * (at most 30 significant bits), so every decision below is the decision of
- * exact real arithmetic.
+ * Arithmetic is FP64 throughout.  Every rounding decision compares |x| with
+ * a product of at most 31 significant bits, exact in FP64, so each decision is
+ * that of exact real arithmetic.  The product reference is not exact in
+ * general: a dequantized value code * s * g carries up to 30 significant bits
+ * under a caller-given g (6 under a power-of-two g), so a product of two of
+ * them may need 60 bits and is rounded once in FP64, and the sums over K are
+ * rounded in FP64 too; both are many orders of magnitude below the 1e-3
+ * tolerance the product is checked against.
  *
  * Parity status: every function here is pinned by a CPU test against an
  * independent statement (brute-force nearest search, torch's float8 and
@@ -355,7 +360,7 @@ void orc_bf16_from_double_array(const double *v, int64_t n, uint16_t *out)
 /* ---------- block rotation before MXFP4 quantization ---------- */
 
 /* MXFP4 activations in ReQAT are rotated block by block before quantization
- * (Sec. 3.3, "Additional implementation details"; App. C.2, "Challenges in
+ * (Sec. 4.3, "Additional implementation details"; App. C.2, "Challenges in
  * MXFP4 activation quantization"): a randomized Hadamard transform over each
  * 32-element block.  The paper fixes neither the normalization, the sign
  * vector nor the arithmetic; the readings used here:
@@ -499,9 +504,9 @@ void orc_gemm_w4a16_points(int64_t K, const uint16_t *x, int64_t ldx, const uint
 /* ---------- KV4: E1M2 elements with NVFP4-style scaling and the post-RoPE shift ---------- */
 
 /* The KV cache of the NVFP4 W4A4KV4 setting is stored in 4 bits with the E1M2
- * element format (Sec. 3.3, "Additional implementation details"), and the
+ * element format (Sec. 4.3, "Additional implementation details"), and the
  * keys are shifted channel-wise after RoPE before quantization (Q-FIT,
- * Sec. 3.3, Eq. for K~: K~ = R(K_pre / s) - m; the pre-RoPE scale s is folded
+ * Sec. 4.3, Eq. for K~: K~ = R(K_pre / s) - m; the pre-RoPE scale s is folded
  * into the projection weights, so the cache quantizer sees R(...) and m).
  * Readings:
  *   - E1M2: sign, 1 exponent bit (bias 0), 2 mantissa bits: magnitudes

@@ -1,6 +1,6 @@
 // KV-cache quantizer for gfx950 (the 4-bit KV cache of the NVFP4 W4A4KV4
-// setting, Sec. 3.3 "Additional implementation details"; Q-FIT's post-RoPE
-// shift, Sec. 3.3, K~ = R(K_pre / s) - m):
+// setting, Sec. 4.3 "Additional implementation details"; Q-FIT's post-RoPE
+// shift, Sec. 4.3, K~ = R(K_pre / s) - m):
 //   d = RN_fp32(x - m[c])                       (m an FP32 vector over channels, optional)
 //   E1M2 elements (magnitudes 0, 0.5, ..., 3.5), an E4M3 scale per 16
 //   channels (the smallest with block_amax <= 3.5 * s * g) and an FP32 global

@@ -785,7 +785,7 @@ __global__ __launch_bounds__(kThreads) void nv_fixup_kernel(
 // ---------------------------------------------------------------- block rotation
 
 // MXFP4 activations may be rotated block by block before quantization (a
-// randomized Hadamard transform per 32-element block, Sec. 3.3 and App. C.2):
+// randomized Hadamard transform per 32-element block, Sec. 4.3 and App. C.2):
 // y = H_32 D x / sqrt(32), D = diag(d), d_j = -1 where bit j of `signs` is set,
 // H_32 the Sylvester Hadamard matrix.  Arithmetic is FP32 in a fixed order:
 // the fast Walsh-Hadamard transform in stages h = 1, 2, 4, 8, 16 (each

@@ -1,4 +1,4 @@
-// SEM loss for gfx950 (selective entropy minimization, Sec. 3.2):
+// SEM loss for gfx950 (selective entropy minimization, Sec. 4.2):
 //   per token t (a row of bfloat16 logits over the vocabulary, p = softmax):
 //     H_t = -sum_j p_j log p_j,  NLL_t = -log p_{y_t},  lse_t = log sum_j exp(z_j)
 //   over the minibatch: H_min = min_t H_t, tau = 75th percentile of H (linear

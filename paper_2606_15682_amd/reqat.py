@@ -181,11 +181,73 @@ def _ptr(t):
 
 
 def _x2d(x: torch.Tensor):
-    if x.dtype != torch.bfloat16 or x.dim() != 2 or not x.is_cuda:
-        raise TypeError("expected a 2-D bfloat16 CUDA tensor")
+    if not isinstance(x, torch.Tensor) or x.dtype != torch.bfloat16 or x.dim() != 2:
+        raise TypeError("expected a 2-D bfloat16 tensor")
     if x.stride(1) != 1:
         raise ValueError("rows must be contiguous")
     return x.shape[0], x.shape[1], x.stride(0)
+
+
+def _same_device(t, device, name):
+    if t.device != device:
+        raise ValueError("%s must be on %s" % (name, device))
+
+
+def _require_cuda(t, name="x"):
+    """Checked after every shape, dtype and size check, right before the C call."""
+    if not t.is_cuda:
+        raise TypeError("%s must be a CUDA (HIP) tensor" % name)
+
+
+def _packed_u8(t, rows, cols, device, name):
+    """A uint8 [rows, cols] tensor with dense rows (the C ABI takes no row stride for codes and scales)."""
+    if not isinstance(t, torch.Tensor) or t.dtype != torch.uint8:
+        raise TypeError("%s must be a uint8 tensor" % name)
+    if tuple(t.shape) != (rows, cols):
+        raise ValueError("%s must have shape (%d, %d), got %s" % (name, rows, cols, tuple(t.shape)))
+    if rows > 1 and cols > 0 and t.stride(0) != cols or cols > 1 and t.stride(1) != 1:
+        raise ValueError("%s must be contiguous" % name)
+    _same_device(t, device, name)
+    return t
+
+
+def _out2d(t, rows, cols, dtype, device, name):
+    """An output [rows, cols] of `dtype` with unit column stride; returns its row stride."""
+    if not isinstance(t, torch.Tensor) or t.dtype != dtype:
+        raise TypeError("%s must be a %s tensor" % (name, dtype))
+    if t.dim() != 2 or tuple(t.shape) != (rows, cols):
+        raise ValueError("%s must have shape (%d, %d), got %s" % (name, rows, cols, tuple(t.shape)))
+    if cols > 1 and t.stride(1) != 1:
+        raise ValueError("%s rows must be contiguous" % name)
+    _same_device(t, device, name)
+    return t.stride(0) if rows > 1 else max(cols, 1)
+
+
+def _workspace_arg(ws, nbytes, device, name="ws"):
+    if not isinstance(ws, torch.Tensor) or ws.dtype != torch.uint8 or not ws.is_contiguous():
+        raise TypeError("%s must be a contiguous uint8 tensor" % name)
+    if ws.numel() < nbytes:
+        raise ValueError("%s holds %d bytes, %d needed" % (name, ws.numel(), nbytes))
+    _same_device(ws, device, name)
+    return ws
+
+
+def _scale_arg(g, fmt, device, name):
+    """The 1-element float32 device tensor of an NVFP4 global scale (MXFP4: None)."""
+    if fmt == MXFP4:
+        if g is not None:
+            raise ValueError("MXFP4 has no global scale (%s must be None)" % name)
+        return None
+    if not isinstance(g, torch.Tensor) or g.dtype != torch.float32 or g.numel() < 1:
+        raise TypeError("%s must be a float32 tensor holding the NVFP4 global scale" % name)
+    _same_device(g, device, name)
+    return g
+
+
+def _fmt_arg(fmt):
+    if fmt not in (NVFP4, MXFP4):
+        raise ValueError("unknown format %r" % (fmt,))
+    return fmt
 
 
 _workspaces: dict = {}
@@ -211,10 +273,10 @@ def _gscale(fmt, x, tensor_scale, g_out=None):
         return None, TS_COMPUTE
     if tensor_scale is None:
         if g_out is not None:
-            return g_out, TS_COMPUTE
+            return _scale_arg(g_out, fmt, x.device, "g_out"), TS_COMPUTE
         return torch.empty(1, dtype=torch.float32, device=x.device), TS_COMPUTE
     if isinstance(tensor_scale, torch.Tensor):
-        return tensor_scale, TS_GIVEN
+        return _scale_arg(tensor_scale, fmt, x.device, "tensor_scale"), TS_GIVEN
     return torch.tensor([float(tensor_scale)], dtype=torch.float32, device=x.device), TS_GIVEN
 
 
@@ -222,13 +284,18 @@ def quantize(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out=None, g_o
     """Quantize a 2-D bfloat16 CUDA tensor.  Returns (codes, scales, g) with g a
     1-element float32 tensor (NVFP4: computed unless given) or None (MXFP4)."""
     rows, cols, ldx = _x2d(x)
-    B = BLOCK[fmt]
+    B = BLOCK[_fmt_arg(fmt)]
+    if cols % B:
+        raise ValueError("cols must be a multiple of %d" % B)
     if out is not None:
         codes, scales = out
+        _packed_u8(codes, rows, cols // 2, x.device, "codes")
+        _packed_u8(scales, rows, cols // B, x.device, "scales")
     else:
         codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=x.device)
         scales = torch.empty((rows, cols // B), dtype=torch.uint8, device=x.device)
     g, ts = _gscale(fmt, x, tensor_scale, g_out)
+    _require_cuda(x, 'x')
     ws = workspace(x.device)
     st = reqat_quantize_fp4(fmt, x.data_ptr(), rows, cols, ldx, codes.data_ptr(), scales.data_ptr(),
                             _ptr(g), ts, ws.data_ptr(), _stream(x.device))
@@ -239,10 +306,13 @@ def quantize(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out=None, g_o
 def fakequant(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out=None, g_out=None):
     """Quantize-dequantize to bfloat16.  Returns (y, g)."""
     rows, cols, ldx = _x2d(x)
+    _fmt_arg(fmt)
     y = out if out is not None else torch.empty((rows, cols), dtype=torch.bfloat16, device=x.device)
+    ldy = _out2d(y, rows, cols, torch.bfloat16, x.device, "out")
     g, ts = _gscale(fmt, x, tensor_scale, g_out)
+    _require_cuda(x, 'x')
     ws = workspace(x.device)
-    st = reqat_fakequant_fp4(fmt, x.data_ptr(), rows, cols, ldx, y.data_ptr(), y.stride(0), _ptr(g),
+    st = reqat_fakequant_fp4(fmt, x.data_ptr(), rows, cols, ldx, y.data_ptr(), ldy, _ptr(g),
                              ts, ws.data_ptr(), _stream(x.device))
     _check(st, "reqat_fakequant_fp4")
     return y, g
@@ -252,17 +322,23 @@ def quantize_fakequant(x: torch.Tensor, fmt: int = NVFP4, tensor_scale=None, out
     """Quantize and quantize-dequantize in one pass over x.  Returns
     (codes, scales, y, g): codes/scales as quantize(), y (bfloat16) as fakequant()."""
     rows, cols, ldx = _x2d(x)
-    B = BLOCK[fmt]
+    B = BLOCK[_fmt_arg(fmt)]
+    if cols % B:
+        raise ValueError("cols must be a multiple of %d" % B)
     if out is not None:
         codes, scales, y = out
+        _packed_u8(codes, rows, cols // 2, x.device, "codes")
+        _packed_u8(scales, rows, cols // B, x.device, "scales")
     else:
         codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=x.device)
         scales = torch.empty((rows, cols // B), dtype=torch.uint8, device=x.device)
         y = torch.empty((rows, cols), dtype=torch.bfloat16, device=x.device)
+    ldy = _out2d(y, rows, cols, torch.bfloat16, x.device, "y")
     g, ts = _gscale(fmt, x, tensor_scale, g_out)
+    _require_cuda(x, 'x')
     ws = workspace(x.device)
     st = reqat_quantize_fakequant_fp4(fmt, x.data_ptr(), rows, cols, ldx, codes.data_ptr(), scales.data_ptr(),
-                                      y.data_ptr(), y.stride(0), _ptr(g), ts, ws.data_ptr(), _stream(x.device))
+                                      y.data_ptr(), ldy, _ptr(g), ts, ws.data_ptr(), _stream(x.device))
     _check(st, "reqat_quantize_fakequant_fp4")
     return codes, scales, y, g
 
@@ -271,11 +347,16 @@ def quantize_rht(x: torch.Tensor, signs: int, out=None):
     """MXFP4 codes and scales of the block-rotated rows of x (randomized Hadamard
     of 32 with the given 32-bit sign draw).  Returns (codes, scales)."""
     rows, cols, ldx = _x2d(x)
+    if cols % 32:
+        raise ValueError("cols must be a multiple of 32")
     if out is not None:
         codes, scales = out
+        _packed_u8(codes, rows, cols // 2, x.device, "codes")
+        _packed_u8(scales, rows, cols // 32, x.device, "scales")
     else:
         codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=x.device)
         scales = torch.empty((rows, cols // 32), dtype=torch.uint8, device=x.device)
+    _require_cuda(x, 'x')
     st = reqat_quantize_mxfp4_rht(x.data_ptr(), rows, cols, ldx, signs & 0xFFFFFFFF, codes.data_ptr(),
                                   scales.data_ptr(), _stream(x.device))
     _check(st, "reqat_quantize_mxfp4_rht")
@@ -286,25 +367,49 @@ def fakequant_rht(x: torch.Tensor, signs: int, out=None):
     """bfloat16 quantize-dequantize of the block-rotated rows (rotated basis)."""
     rows, cols, ldx = _x2d(x)
     y = out if out is not None else torch.empty((rows, cols), dtype=torch.bfloat16, device=x.device)
+    ldy = _out2d(y, rows, cols, torch.bfloat16, x.device, "out")
+    _require_cuda(x, 'x')
     st = reqat_fakequant_mxfp4_rht(x.data_ptr(), rows, cols, ldx, signs & 0xFFFFFFFF, y.data_ptr(),
-                                   y.stride(0), _stream(x.device))
+                                   ldy, _stream(x.device))
     _check(st, "reqat_fakequant_mxfp4_rht")
     return y
 
 
 def gemm(fmt, a_codes, a_scales, a_g, b_codes, b_scales, b_g, out_dtype=torch.float32, out=None):
     """Y[M, N] = A^ B^T with FP32 accumulation; Y float32 or bfloat16."""
+    B = BLOCK[_fmt_arg(fmt)]
+    dev = a_codes.device
+    if a_codes.dim() != 2 or b_codes.dim() != 2:
+        raise ValueError("codes must be 2-D")
     M, K = a_codes.shape[0], a_codes.shape[1] * 2
     N = b_codes.shape[0]
     if b_codes.shape[1] * 2 != K:
         raise ValueError("K mismatch")
-    dt = DT_F32 if out_dtype == torch.float32 else DT_BF16
-    y = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=a_codes.device)
+    if K % 128:
+        raise ValueError("K must be a multiple of 128")
+    _packed_u8(a_codes, M, K // 2, dev, "a_codes")
+    _packed_u8(a_scales, M, K // B, dev, "a_scales")
+    _packed_u8(b_codes, N, K // 2, dev, "b_codes")
+    _packed_u8(b_scales, N, K // B, dev, "b_scales")
+    _scale_arg(a_g, fmt, dev, "a_g")
+    _scale_arg(b_g, fmt, dev, "b_g")
+    dt = _dtype_arg(out_dtype)
+    y = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=dev)
+    ldy = _out2d(y, M, N, out_dtype, dev, "out")
+    _require_cuda(a_codes, 'a_codes')
     st = reqat_gemm_w4a4(fmt, M, N, K, a_codes.data_ptr(), a_scales.data_ptr(), _ptr(a_g),
                          b_codes.data_ptr(), b_scales.data_ptr(), _ptr(b_g), y.data_ptr(), dt,
-                         y.stride(0), _stream(a_codes.device))
+                         ldy, _stream(dev))
     _check(st, "reqat_gemm_w4a4")
     return y
+
+
+def _dtype_arg(out_dtype):
+    if out_dtype == torch.float32:
+        return DT_F32
+    if out_dtype == torch.bfloat16:
+        return DT_BF16
+    raise TypeError("out_dtype must be torch.float32 or torch.bfloat16")
 
 
 def _shift_ptr(shift, cols, device):
@@ -320,13 +425,18 @@ def quantize_kv4(x: torch.Tensor, shift=None, tensor_scale=None, out=None, g_out
     """KV4 (E1M2 + E4M3 block scales of 16 + FP32 tensor scale) of x - shift.
     Returns (codes, scales, g)."""
     rows, cols, ldx = _x2d(x)
+    if cols % 16:
+        raise ValueError("cols must be a multiple of 16")
     if out is not None:
         codes, scales = out
+        _packed_u8(codes, rows, cols // 2, x.device, "codes")
+        _packed_u8(scales, rows, cols // 16, x.device, "scales")
     else:
         codes = torch.empty((rows, cols // 2), dtype=torch.uint8, device=x.device)
         scales = torch.empty((rows, cols // 16), dtype=torch.uint8, device=x.device)
     g, ts = _gscale(NVFP4, x, tensor_scale, g_out)
     _, sp = _shift_ptr(shift, cols, x.device)
+    _require_cuda(x, 'x')
     st = reqat_quantize_kv4(x.data_ptr(), rows, cols, ldx, sp, codes.data_ptr(), scales.data_ptr(), _ptr(g), ts,
                             workspace(x.device).data_ptr(), _stream(x.device))
     _check(st, "reqat_quantize_kv4")
@@ -337,9 +447,11 @@ def fakequant_kv4(x: torch.Tensor, shift=None, tensor_scale=None, out=None, g_ou
     """bfloat16 quantize-dequantize of x - shift in KV4.  Returns (y, g)."""
     rows, cols, ldx = _x2d(x)
     y = out if out is not None else torch.empty((rows, cols), dtype=torch.bfloat16, device=x.device)
+    ldy = _out2d(y, rows, cols, torch.bfloat16, x.device, "out")
     g, ts = _gscale(NVFP4, x, tensor_scale, g_out)
     _, sp = _shift_ptr(shift, cols, x.device)
-    st = reqat_fakequant_kv4(x.data_ptr(), rows, cols, ldx, sp, y.data_ptr(), y.stride(0), _ptr(g), ts,
+    _require_cuda(x, 'x')
+    st = reqat_fakequant_kv4(x.data_ptr(), rows, cols, ldx, sp, y.data_ptr(), ldy, _ptr(g), ts,
                              workspace(x.device).data_ptr(), _stream(x.device))
     _check(st, "reqat_fakequant_kv4")
     return y, g
@@ -350,18 +462,26 @@ def gemm_w4a16(x: torch.Tensor, w_codes, w_scales, out_dtype=torch.float32, out=
     scales [N, K/32]) dequantized to bfloat16; FP32 accumulation.
     ws: optional workspace tensor of reqat_w4a16_workspace_bytes(M, N, K) bytes."""
     M, K, ldx = _x2d(x)
+    if w_codes.dim() != 2:
+        raise ValueError("w_codes must be 2-D")
     N = w_codes.shape[0]
     if w_codes.shape[1] * 2 != K:
         raise ValueError("K mismatch")
-    if not (w_codes.is_contiguous() and w_scales.is_contiguous()) or tuple(w_scales.shape) != (N, K // 32):
-        raise ValueError("w_codes [N, K/2] and w_scales [N, K/32] must be contiguous")
-    dt = DT_F32 if out_dtype == torch.float32 else DT_BF16
+    if K % 128:
+        raise ValueError("K must be a multiple of 128")
+    _packed_u8(w_codes, N, K // 2, x.device, "w_codes")
+    _packed_u8(w_scales, N, K // 32, x.device, "w_scales")
+    dt = _dtype_arg(out_dtype)
     y = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=x.device)
+    ldy = _out2d(y, M, N, out_dtype, x.device, "out")
     nbytes = reqat_w4a16_workspace_bytes(M, N, K)
     if ws is None and nbytes:
         ws = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
+    if ws is not None:
+        _workspace_arg(ws, nbytes, x.device)
+    _require_cuda(x, 'x')
     st = reqat_gemm_w4a16(M, N, K, x.data_ptr(), ldx, w_codes.data_ptr(), w_scales.data_ptr(), y.data_ptr(),
-                          dt, y.stride(0), _ptr(ws), _stream(x.device))
+                          dt, ldy, _ptr(ws), _stream(x.device))
     _check(st, "reqat_gemm_w4a16")
     return y
 
@@ -371,19 +491,44 @@ def linear(x: torch.Tensor, fmt, w_codes, w_scales, w_g, x_tensor_scale=None, ou
     """Y = quantize(x) . W^T for already-quantized weights.  Returns (Y, g_x).
     ws: optional workspace tensor of reqat_linear_workspace_bytes(fmt, M, K) bytes."""
     M, K, ldx = _x2d(x)
+    B = BLOCK[_fmt_arg(fmt)]
+    if w_codes.dim() != 2:
+        raise ValueError("w_codes must be 2-D")
     N = w_codes.shape[0]
     if w_codes.shape[1] * 2 != K:
         raise ValueError("K mismatch")
-    dt = DT_F32 if out_dtype == torch.float32 else DT_BF16
+    if K % 128:
+        raise ValueError("K must be a multiple of 128")
+    _packed_u8(w_codes, N, K // 2, x.device, "w_codes")
+    _packed_u8(w_scales, N, K // B, x.device, "w_scales")
+    _scale_arg(w_g, fmt, x.device, "w_g")
+    dt = _dtype_arg(out_dtype)
     y = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=x.device)
+    ldy = _out2d(y, M, N, out_dtype, x.device, "out")
     g, ts = _gscale(fmt, x, x_tensor_scale, g_out)
+    nbytes = reqat_linear_workspace_bytes(fmt, M, K)
     if ws is None:
-        ws = torch.empty(reqat_linear_workspace_bytes(fmt, M, K), dtype=torch.uint8, device=x.device)
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
+    _workspace_arg(ws, nbytes, x.device)
+    _require_cuda(x, 'x')
     st = reqat_linear_w4a4(fmt, M, N, K, x.data_ptr(), ldx, _ptr(g), ts, w_codes.data_ptr(),
-                           w_scales.data_ptr(), _ptr(w_g), y.data_ptr(), dt, y.stride(0), ws.data_ptr(),
+                           w_scales.data_ptr(), _ptr(w_g), y.data_ptr(), dt, ldy, ws.data_ptr(),
                            _stream(x.device))
     _check(st, "reqat_linear_w4a4")
     return y, g
+
+
+def linear_workspace_views(ws: torch.Tensor, fmt, M: int, K: int):
+    """(codes [M, K/2], scales [M, K/B]) views of the activation codes and scales
+    that linear() leaves in its workspace: [4096 partial maxima | codes | scales | ...],
+    each part on a 256-byte boundary."""
+    B = BLOCK[_fmt_arg(fmt)]
+    r256 = lambda n: (n + 255) // 256 * 256
+    off = r256(4 * 4096)
+    off2 = off + r256(M * (K // 2))
+    codes = ws[off:off + M * (K // 2)].view(M, K // 2)
+    scales = ws[off2:off2 + M * (K // B)].view(M, K // B)
+    return codes, scales
 
 
 # ------------------------------------------------------------------ QAT training side
@@ -397,6 +542,7 @@ def sem_loss(logits: torch.Tensor, targets: torch.Tensor, lam: float, eps: float
     stats = torch.empty((T, 4), dtype=torch.float32, device=logits.device)
     weights = torch.empty(T, dtype=torch.float32, device=logits.device)
     loss = torch.zeros(4, dtype=torch.float32, device=logits.device)
+    _require_cuda(logits, 'logits')
     st = reqat_sem_loss(logits.data_ptr(), T, V, ld, targets.data_ptr(), lam, eps, stats.data_ptr(),
                         weights.data_ptr(), loss.data_ptr(), _stream(logits.device))
     _check(st, "reqat_sem_loss")
@@ -407,10 +553,18 @@ def sem_loss_backward(logits, targets, stats, weights, lam: float, scale: float 
                       out=None):
     """dL/dlogits (weights held fixed) as out_dtype [T, V]."""
     T, V, ld = _x2d(logits)
-    dt = DT_F32 if out_dtype == torch.float32 else DT_BF16
+    dt = _dtype_arg(out_dtype)
+    if targets.dtype != torch.int32 or targets.numel() != T or not targets.is_contiguous():
+        raise TypeError("targets must be a contiguous int32 tensor of T entries")
+    for name, t, n in (("stats", stats, 4 * T), ("weights", weights, T)):
+        if t.dtype != torch.float32 or t.numel() != n or not t.is_contiguous():
+            raise TypeError("%s must be a contiguous float32 tensor of %d entries" % (name, n))
+        _same_device(t, logits.device, name)
     g = out if out is not None else torch.empty((T, V), dtype=out_dtype, device=logits.device)
+    ldg = _out2d(g, T, V, out_dtype, logits.device, "out")
+    _require_cuda(logits, 'logits')
     st = reqat_sem_loss_backward(logits.data_ptr(), T, V, ld, targets.data_ptr(), stats.data_ptr(),
-                                 weights.data_ptr(), lam, scale, g.data_ptr(), dt, g.stride(0),
+                                 weights.data_ptr(), lam, scale, g.data_ptr(), dt, ldg,
                                  _stream(logits.device))
     _check(st, "reqat_sem_loss_backward")
     return g

@@ -98,3 +98,28 @@ def dequant_indep(fmt: int, codes: np.ndarray, scales: np.ndarray, g: float) -> 
     if fmt == 0:
         S = S * g
     return v * S
+
+
+def gemm_error_metrics(got: np.ndarray, ref: np.ndarray, aref: np.ndarray) -> dict:
+    """Error of a product against its FP64 reference, three ways: the largest
+    |Y - Yref| / sum_k |A^ B^| (the scale FP32 accumulation error grows with),
+    the largest elementwise relative error over entries with |Yref| >= 1e-2 of
+    the rms of Yref, and the Frobenius relative error.  NaN references are left out."""
+    ok = ~np.isnan(ref)
+    got, ref, aref = got[ok].astype(np.float64), ref[ok], aref[ok]
+    err = np.abs(got - ref)
+    out = {"n": int(ok.sum()), "max_rel_sum": 0.0, "max_rel_elem": 0.0, "frob_rel": 0.0}
+    if not ref.size:
+        return out
+    out["max_rel_sum"] = float(np.max(err / np.maximum(aref, 1e-300)))
+    rms = float(np.sqrt(np.mean(ref * ref)))
+    big = np.abs(ref) >= 1e-2 * rms
+    if big.any():
+        out["max_rel_elem"] = float(np.max(err[big] / np.abs(ref[big])))
+    out["frob_rel"] = float(np.linalg.norm(got - ref) / max(float(np.linalg.norm(ref)), 1e-300))
+    return out
+
+
+def format_metrics(m: dict) -> str:
+    return "n=%d max|err|/sum|ab|=%.3g max rel(|Yref|>=1e-2 rms)=%.3g frobenius rel=%.3g" % (
+        m["n"], m["max_rel_sum"], m["max_rel_elem"], m["frob_rel"])

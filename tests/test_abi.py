@@ -268,3 +268,105 @@ def test_binding_raises_when_library_missing(tmp_path):
             reqat.load(str(tmp_path / "missing.so"))
     finally:
         reqat._lib = saved
+
+
+# ------------------------------------------------- binding-side buffer checks
+# The C ABI takes no buffer sizes, so the torch binding is where an output,
+# operand or workspace of the wrong shape, dtype or size is caught.  Every C
+# entry point is replaced by a trap here: each bad call must raise before any
+# of them is reached, and a well-formed call on CPU tensors gets as far as the
+# final device check.
+
+import torch  # noqa: E402
+
+
+@pytest.fixture
+def trapped(lib, monkeypatch):
+    def trap(*a, **k):
+        raise AssertionError("a C entry point was reached")
+    for name in reqat.SIGNATURES:
+        if name.endswith("_bytes") or name in ("reqat_status_str", "reqat_abi_version"):
+            continue
+        monkeypatch.setattr(reqat, name, trap)
+    return reqat
+
+
+def _u8(*shape):
+    return torch.zeros(shape, dtype=torch.uint8)
+
+
+def _gemm_args(fmt, M=8, N=16, K=256):
+    B = reqat.BLOCK[fmt]
+    g = torch.ones(1, dtype=torch.float32) if fmt == NV else None
+    return [fmt, _u8(M, K // 2), _u8(M, K // B), g, _u8(N, K // 2), _u8(N, K // B),
+            None if g is None else g.clone()]
+
+
+def _raises_before_device(fn, exc=(ValueError, TypeError), match=None):
+    with pytest.raises(exc) as ei:
+        fn()
+    assert "CUDA" not in str(ei.value), "the bad argument was not caught: %s" % ei.value
+    if match:
+        assert match in str(ei.value), str(ei.value)
+
+
+@pytest.mark.parametrize("fmt", [NV, MX])
+def test_binding_gemm_checks_operands_and_output(trapped, fmt):
+    a = _gemm_args(fmt)
+    with pytest.raises(TypeError, match="CUDA"):                    # well formed: only the device is wrong
+        reqat.gemm(*a, out_dtype=torch.float32)
+    # bfloat16 buffer for a float32 product (would be written 4 bytes per element)
+    _raises_before_device(lambda: reqat.gemm(*a, out_dtype=torch.float32,
+                                             out=torch.zeros(8, 16, dtype=torch.bfloat16)), match="out")
+    _raises_before_device(lambda: reqat.gemm(*a, out=torch.zeros(8, 15)), match="out")
+    _raises_before_device(lambda: reqat.gemm(*a, out_dtype=torch.float16))
+    # the other format's scale layout (NVFP4 reads K/16 bytes per row)
+    b = list(a)
+    other = reqat.BLOCK[MX if fmt == NV else NV]
+    b[2] = _u8(8, 256 // other)
+    _raises_before_device(lambda: reqat.gemm(*b), match="a_scales")
+    c = list(a)
+    c[4] = _u8(16, 256)[:, ::2]                                        # strided codes rows
+    _raises_before_device(lambda: reqat.gemm(*c), match="b_codes")
+    d = list(a)
+    d[3] = torch.ones(1, dtype=torch.float32) if fmt == MX else None   # a global scale where none is (not) allowed
+    _raises_before_device(lambda: reqat.gemm(*d), match="a_g")
+    e = list(a)
+    e[1] = _u8(8, 64)                                                   # K = 128 against b's 256
+    _raises_before_device(lambda: reqat.gemm(*e), match="K")
+
+
+def test_binding_quantize_and_fakequant_check_outputs(trapped):
+    x = torch.zeros(4, 64, dtype=torch.bfloat16)
+    with pytest.raises(TypeError, match="CUDA"):
+        reqat.quantize(x, NV, out=(_u8(4, 32), _u8(4, 4)))
+    _raises_before_device(lambda: reqat.quantize(x, NV, out=(_u8(4, 32), _u8(4, 2))), match="scales")
+    _raises_before_device(lambda: reqat.quantize(x, MX, out=(_u8(4, 16), _u8(4, 2))), match="codes")
+    _raises_before_device(lambda: reqat.quantize(torch.zeros(4, 40, dtype=torch.bfloat16), MX))
+    _raises_before_device(lambda: reqat.fakequant(x, NV, out=torch.zeros(4, 64)), match="out")
+    _raises_before_device(lambda: reqat.fakequant(x, NV, out=torch.zeros(4, 32, dtype=torch.bfloat16)))
+    _raises_before_device(lambda: reqat.quantize_fakequant(
+        x, NV, out=(_u8(4, 32), _u8(4, 4), torch.zeros(4, 64, dtype=torch.float16))), match="y")
+    _raises_before_device(lambda: reqat.quantize_rht(x, 1, out=(_u8(4, 32), _u8(4, 4))), match="scales")
+    _raises_before_device(lambda: reqat.quantize(x, NV, g_out=torch.zeros(1, dtype=torch.float64)),
+                          match="g_out")
+    _raises_before_device(lambda: reqat.quantize(x, MX, tensor_scale=torch.ones(1)), match="MXFP4")
+
+
+def test_binding_checks_workspace_sizes(trapped):
+    x = torch.zeros(16, 256, dtype=torch.bfloat16)
+    wc, ws_ = _u8(32, 128), _u8(32, 16)
+    g = torch.ones(1, dtype=torch.float32)
+    need = reqat.reqat_linear_workspace_bytes(NV, 16, 256)
+    with pytest.raises(TypeError, match="CUDA"):
+        reqat.linear(x, NV, wc, ws_, g, ws=_u8(need))
+    _raises_before_device(lambda: reqat.linear(x, NV, wc, ws_, g, ws=_u8(need - 1)), match="ws")
+    _raises_before_device(lambda: reqat.linear(x, NV, wc, ws_, g, ws=torch.zeros(need)), match="ws")
+    _raises_before_device(lambda: reqat.linear(x, NV, wc, _u8(32, 8), g), match="w_scales")
+    mc, ms = _u8(5120, 128), _u8(5120, 8)
+    need16 = reqat.reqat_w4a16_workspace_bytes(16, 5120, 256)
+    assert need16 > 0
+    _raises_before_device(lambda: reqat.gemm_w4a16(x, mc, ms, ws=_u8(need16 - 4)), match="ws")
+    _raises_before_device(lambda: reqat.gemm_w4a16(x, mc, _u8(5120, 16)), match="w_scales")
+    _raises_before_device(lambda: reqat.gemm_w4a16(x, mc, ms, out=torch.zeros(16, 5120, dtype=torch.bfloat16)),
+                          match="out")

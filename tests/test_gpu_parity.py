@@ -511,6 +511,8 @@ def check_gemm_points(fmt, ac, as_, ga, bc, bs, gb, y32, ybf, ms, ns):
     assert np.array_equal(np.isnan(got), nanref)
     ok = ~nanref
     err = np.abs(got[ok] - ref[ok])
+    m = indep.gemm_error_metrics(got, ref, aref)
+    log("  gemm fp32 K=%d %s" % (ac.shape[1] * 2, indep.format_metrics(m)))
     assert np.all(err <= GEMM_TOL * aref[ok]), float(np.max(err / np.maximum(aref[ok], 1e-300)))
     if ybf is not None:
         gb_ = ybf[ms, ns][ok]

@@ -1,6 +1,6 @@
 """Pins for the oracle's block rotation before MXFP4 quantization (CPU only).
 
-The rotation is y = H_32 D x / sqrt(32) per 32-element block (Sec. 3.3,
+The rotation is y = H_32 D x / sqrt(32) per 32-element block (Sec. 4.3,
 App. C.2), evaluated in FP32 by the fast Walsh-Hadamard transform.  Pinned
 here against statements that do not reuse the oracle's arithmetic: scipy's
 Sylvester Hadamard matrix on inputs where FP32 is exact, the involution

@@ -1,4 +1,4 @@
-"""Pins for the oracle's SEM loss (selective entropy minimization, Sec. 3.2)
+"""Pins for the oracle's SEM loss (selective entropy minimization, Sec. 4.2)
 and its gradient (CPU only): closed forms (uniform and one-hot distributions),
 scipy's log-softmax and entropy, numpy's percentile, and central finite
 differences of an independently written FP64 loss."""
