@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define REQAT_ABI_VERSION 8
+#define REQAT_ABI_VERSION 9
 
 typedef enum {
     REQAT_FMT_NVFP4 = 0, /* B = 16, E4M3 block scale, FP32 global scale */
@@ -148,15 +148,15 @@ reqat_status reqat_quantize_fakequant_fp4(reqat_format fmt, const void *x, int64
  * implementation details" and App. C.2): each 32-element block x of a row
  * becomes
  *     y = H_32 * D * x / sqrt(32),   D = diag(d), d_j = -1 where bit j of signs is set,
- * H_32 the Sylvester Hadamard matrix (H[i][j] = (-1)^popcount(i & j)), and y
- * is quantized as an MXFP4 block (same rules as reqat_quantize_fp4).  The map
- * is orthonormal: rotating the weights' rows with the same signs leaves the
- * product X W^T unchanged.  y is evaluated in FP32 in a fixed order: the fast
- * Walsh-Hadamard transform in stages h = 1, 2, 4, 8, 16, each pair
- * (t[j], t[j+h]) -> (t[j] + t[j+h], t[j] - t[j+h]) rounded to nearest even,
- * then each value times 1/sqrt(32) rounded to FP32 (0x3E3504F3).  A block
- * with a non-finite y (NaN/Inf input or FP32 overflow) gets scale 0xFF and
- * zero codes.
+ * H_32 the Sylvester Hadamard matrix (H[i][j] = (-1)^popcount(i & j)), and the
+ * exact real y is quantized as an MXFP4 block by the rules of
+ * reqat_quantize_fp4: scale 2^e with e the smallest integer in [-127, 127]
+ * with max|y_i| <= 6 * 2^e (byte 0 for y == 0; 127 when none fits, elements
+ * then saturate), each code the E2M1 value nearest to |y_i| / 2^e with the
+ * sign of y_i (a zero y_i gives code 0).  No tie can occur (y_i is an
+ * irrational multiple of 2^e unless it is zero).  The map is orthonormal:
+ * rotating the weights' rows with the same signs leaves the product X W^T
+ * unchanged.  A block with a NaN or Inf input gets scale 0xFF and zero codes.
  *   x [rows][ldx] bfloat16 (cols % 32 == 0, 16-byte aligned, ldx % 8 == 0);
  *   signs: the random sign draw, bit j for position j of every block;
  *   codes [rows][cols/2], scales [rows][cols/32] as reqat_quantize_fp4 (MXFP4).
@@ -166,9 +166,10 @@ reqat_status reqat_quantize_mxfp4_rht(const void *x, int64_t rows, int64_t cols,
                                       uint32_t signs, uint8_t *codes, uint8_t *scales, void *stream);
 
 /*
- * Fake-quant of block-rotated rows: y_out = bfloat16(dequantize(quantize(y)))
- * with y the rotated blocks of reqat_quantize_mxfp4_rht (values stay in the
- * rotated basis; NaN for a non-finite block).  y_out [rows][ldy] bfloat16,
+ * Fake-quant of block-rotated rows: y_out = dequantize(quantize(y)), i.e.
+ * code * 2^e (exact in bfloat16), with y the rotated blocks of
+ * reqat_quantize_mxfp4_rht (values stay in the rotated basis; NaN 0x7FC0 for a
+ * block with a NaN or Inf input).  y_out [rows][ldy] bfloat16,
  * 16-byte aligned, ldy % 8 == 0, ldy >= cols.
  */
 reqat_status reqat_fakequant_mxfp4_rht(const void *x, int64_t rows, int64_t cols, int64_t ldx,

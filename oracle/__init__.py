@@ -79,9 +79,6 @@ def _load():
             "orc_kv4_amax": (ctypes.c_double, [u16p, i64, i64, i64, ctypes.POINTER(ctypes.c_float)]),
             "orc_kv4_quantize": (ctypes.c_int, [u16p, i64, i64, i64, ctypes.POINTER(ctypes.c_float),
                                                 ctypes.c_double, u8p, u8p, u16p, i64]),
-            "orc_rht_norm": (ctypes.c_float, []),
-            "orc_fwht32_f32": (None, [ctypes.POINTER(ctypes.c_float)]),
-            "orc_rht32": (None, [u16p, ctypes.c_uint32, ctypes.POINTER(ctypes.c_float)]),
             "orc_quantize_mx_rht": (ctypes.c_int, [u16p, i64, i64, i64, ctypes.c_uint32, u8p, u8p]),
             "orc_fakequant_mx_rht": (ctypes.c_int, [u16p, i64, i64, i64, ctypes.c_uint32, u16p, i64]),
         }
@@ -251,26 +248,6 @@ def gemm_points(fmt, a_codes, a_scales, ga, b_codes, b_scales, gb, ms, ns):
 
 
 # ------------------------------------------------- block rotation (MXFP4)
-
-def rht_norm() -> float:
-    """The FP32 constant 1/sqrt(32) the rotation multiplies by."""
-    return float(np.float32(_load().orc_rht_norm()))
-
-
-def fwht32_f32(v: np.ndarray) -> np.ndarray:
-    """Unnormalized FP32 fast Walsh-Hadamard transform of 32 float32 values."""
-    t = np.array(v, np.float32).reshape(32).copy()
-    _load().orc_fwht32_f32(_p(t, ctypes.c_float))
-    return t
-
-
-def rht32(x: np.ndarray, signs: int) -> np.ndarray:
-    """FP32 rotated block y = H_32 D x / sqrt(32) of 32 bfloat16 bit patterns."""
-    x = np.ascontiguousarray(x, np.uint16).reshape(32)
-    y = np.empty(32, np.float32)
-    _load().orc_rht32(_p(x, ctypes.c_uint16), ctypes.c_uint32(signs), _p(y, ctypes.c_float))
-    return y
-
 
 def quantize_mx_rht(x: np.ndarray, signs: int):
     """MXFP4 codes and scales of the block-rotated rows: (codes [R, C/2], scales [R, C/32])."""

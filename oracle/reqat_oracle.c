@@ -362,58 +362,180 @@ void orc_bf16_from_double_array(const double *v, int64_t n, uint16_t *out)
 /* MXFP4 activations in ReQAT are rotated block by block before quantization
  * (Sec. 4.3, "Additional implementation details"; App. C.2, "Challenges in
  * MXFP4 activation quantization"): a randomized Hadamard transform over each
- * 32-element block.  The paper fixes neither the normalization, the sign
- * vector nor the arithmetic; the readings used here:
+ * 32-element block.  The paper fixes neither the normalization nor the sign
+ * vector; the readings used here:
  *   - y = (1/sqrt(32)) * H_32 * D * x per block, H_32 the Sylvester Hadamard
  *     matrix (H[i][j] = (-1)^popcount(i & j)), D = diag(d) with d_j = -1 where
  *     bit j of the 32-bit `signs` word is set (the random draw is an input);
  *     the map is orthonormal, so rotating both operands of a product leaves
  *     the product unchanged;
- *   - arithmetic is FP32: the fast Walsh-Hadamard transform in stages
- *     h = 1, 2, 4, 8, 16, each replacing (t[j], t[j+h]) by (t[j] + t[j+h],
- *     t[j] - t[j+h]) for every j with bit h clear, every sum rounded to
- *     nearest-even FP32; then each entry times 1/sqrt(32) rounded once to FP32
- *     (one more rounding);
- *   - the FP32 results are quantized exactly as a block of MXFP4 values
- *     (ceil E8M0 scale, RNE codes); a block with a non-finite result (a NaN or
- *     Inf input, or an FP32 overflow) gets scale 0xFF and zero codes.
- * FP32 here is the C `float` type with SSE arithmetic (no excess precision),
- * compiled without contraction of multiply-add. */
+ *   - y is the exact real value, and it is quantized exactly as a block of
+ *     MXFP4 values: e the smallest integer in [-127, 127] with
+ *     max_i |y_i| <= 6 * 2^e (127 if none; byte 0x00 for an all-zero y),
+ *     then each code the nearest E2M1 value to |y_i| / 2^e (saturating at 6)
+ *     with the sign of y_i (y_i == 0 gives code 0);
+ *   - a block with a NaN or Inf input gets scale 0xFF and zero codes.
+ * No rounding tie can occur: with s_i = sqrt(32) * y_i a dyadic rational,
+ * |y_i| = t * 2^e would make sqrt(32) = |s_i| / (t * 2^e) rational.
+ *
+ * Every decision is made in exact integer arithmetic.  A bfloat16 value is
+ * m * 2^u with an integer m < 256 and u >= -133, so S_i = s_i * 2^133 is an
+ * integer below 2^266, accumulated here as a multi-word unsigned integer
+ * (separate sums of the positive and the negative terms).  Then
+ *     |y_i| <= 6 * 2^e          <=>  S_i^2 <= 1152 * 2^(2e + 266)
+ *     |y_i| >  (k/4) * 2^e      <=>  S_i^2 >  2 k^2 * 2^(2e + 266)
+ * (y_i = S_i * 2^-133 / sqrt(32), sqrt(32) = 4 sqrt(2)), and the E2M1
+ * midpoints 0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5 are k/4 for
+ * k = 1, 3, 5, 7, 10, 14, 20. */
 
-/* The FP32 constant 1/sqrt(32): sqrt and the division are correctly rounded
- * in FP64 and the value is far from an FP32 rounding boundary (pinned). */
-float orc_rht_norm(void) { return (float)(1.0 / sqrt(32.0)); }
+#define BIG_WORDS 20            /* 640 bits: S < 2^266, S^2 and the bounds < 2^532 */
 
-/* In-place FP32 fast Walsh-Hadamard transform of 32 values (unnormalized). */
-void orc_fwht32_f32(float *t)
+typedef struct { uint32_t w[BIG_WORDS]; } big_t;
+
+static void big_zero(big_t *a) { memset(a->w, 0, sizeof(a->w)); }
+
+/* a += m * 2^sh (m < 2^32) */
+static void big_add_shifted(big_t *a, uint32_t m, int sh)
 {
-    int h, i, j;
-    for (h = 1; h < 32; h *= 2)
-        for (i = 0; i < 32; i += 2 * h)
-            for (j = i; j < i + h; j++) {
-                float a = t[j], b = t[j + h];
-                t[j] = a + b;
-                t[j + h] = a - b;
-            }
+    uint64_t carry = 0, add;
+    int i, q = sh / 32, r = sh % 32;
+    uint64_t t = (uint64_t)m << r;                     /* < 2^63 */
+    for (i = q; i < BIG_WORDS; i++) {
+        add = (i == q) ? (t & 0xFFFFFFFFu) : (i == q + 1) ? (t >> 32) : 0;
+        carry += (uint64_t)a->w[i] + add;
+        a->w[i] = (uint32_t)carry;
+        carry >>= 32;
+    }
 }
 
-/* y = rotated block of the 32 bfloat16 values x. */
-void orc_rht32(const uint16_t *x, uint32_t signs, float *y)
+static int big_cmp(const big_t *a, const big_t *b)
 {
-    int j;
-    float c = orc_rht_norm();
-    for (j = 0; j < 32; j++) {
-        float v = (float)orc_bf16_value(x[j]);          /* exact */
-        y[j] = ((signs >> j) & 1u) ? -v : v;
+    int i;
+    for (i = BIG_WORDS - 1; i >= 0; i--)
+        if (a->w[i] != b->w[i]) return a->w[i] < b->w[i] ? -1 : 1;
+    return 0;
+}
+
+/* out = a - b, a >= b */
+static void big_sub(const big_t *a, const big_t *b, big_t *out)
+{
+    int64_t borrow = 0, d;
+    int i;
+    for (i = 0; i < BIG_WORDS; i++) {
+        d = (int64_t)a->w[i] - (int64_t)b->w[i] - borrow;
+        borrow = d < 0;
+        out->w[i] = (uint32_t)(d + (borrow ? ((int64_t)1 << 32) : 0));
     }
-    orc_fwht32_f32(y);
-    for (j = 0; j < 32; j++) y[j] = y[j] * c;
+}
+
+/* out = a * a (a < 2^320) */
+static void big_square(const big_t *a, big_t *out)
+{
+    int i, j;
+    big_zero(out);
+    for (i = 0; i < BIG_WORDS / 2; i++) {
+        uint64_t carry = 0;
+        for (j = 0; j < BIG_WORDS / 2; j++) {
+            uint64_t cur = (uint64_t)a->w[i] * a->w[j] + out->w[i + j] + carry;
+            out->w[i + j] = (uint32_t)cur;
+            carry = cur >> 32;
+        }
+        for (j = i + BIG_WORDS / 2; carry && j < BIG_WORDS; j++) {
+            uint64_t cur = (uint64_t)out->w[j] + carry;
+            out->w[j] = (uint32_t)cur;
+            carry = cur >> 32;
+        }
+    }
+}
+
+/* c * 2^sh for a small constant c */
+static big_t big_const(uint32_t c, int sh)
+{
+    big_t b;
+    big_zero(&b);
+    big_add_shifted(&b, c, sh);
+    return b;
+}
+
+/* bfloat16 h (finite) as sign and m * 2^(u + 133): returns the shift u + 133. */
+static int bf16_int_parts(uint16_t h, int *neg, uint32_t *m)
+{
+    int e = (h >> 7) & 0xFF;
+    *neg = (h >> 15) & 1;
+    if (e == 0) {                                     /* subnormal: frac * 2^-133 */
+        *m = h & 0x7F;
+        return 0;
+    }
+    *m = 0x80 | (h & 0x7F);                           /* (128 + frac) * 2^(e - 134) */
+    return e - 1;
+}
+
+/* E8M0 byte and the 32 codes of the rotated block of x (exact).  Returns 0, or
+ * 1 for a block with a NaN or Inf input (byte 0xFF, codes 0). */
+static int rht_block_exact(const uint16_t *x, uint32_t signs, uint8_t *sbyte, uint8_t *codes)
+{
+    static const uint32_t mid_k[7] = {1, 3, 5, 7, 10, 14, 20};
+    big_t pos[32], neg[32], mag[32], sq, amax2, bound, zero;
+    int negative[32];
+    int i, j, e;
+    for (j = 0; j < 32; j++)
+        if (((x[j] >> 7) & 0xFF) == 0xFF) {
+            *sbyte = 0xFF;
+            memset(codes, 0, 32);
+            return 1;
+        }
+    for (i = 0; i < 32; i++) {
+        big_zero(&pos[i]);
+        big_zero(&neg[i]);
+    }
+    for (j = 0; j < 32; j++) {
+        int xneg, sh;
+        uint32_t m;
+        sh = bf16_int_parts(x[j], &xneg, &m);
+        if (m == 0) continue;
+        if ((signs >> j) & 1u) xneg = !xneg;             /* d_j = -1 */
+        for (i = 0; i < 32; i++) {
+            int hneg = __builtin_popcount((unsigned)(i & j)) & 1;   /* H[i][j] = -1 */
+            if (hneg ^ xneg) big_add_shifted(&neg[i], m, sh);
+            else big_add_shifted(&pos[i], m, sh);
+        }
+    }
+    big_zero(&amax2);
+    big_zero(&zero);
+    for (i = 0; i < 32; i++) {
+        int c = big_cmp(&pos[i], &neg[i]);
+        negative[i] = c < 0;
+        if (c >= 0) big_sub(&pos[i], &neg[i], &mag[i]);
+        else big_sub(&neg[i], &pos[i], &mag[i]);
+        big_square(&mag[i], &sq);
+        if (big_cmp(&sq, &amax2) > 0) amax2 = sq;
+    }
+    memset(codes, 0, 32);
+    if (big_cmp(&amax2, &zero) == 0) {                 /* y == 0 */
+        *sbyte = 0;
+        return 0;
+    }
+    for (e = -127; e < 127; e++) {                      /* smallest e with max|y| <= 6 * 2^e */
+        bound = big_const(1152, 2 * e + 266);
+        if (big_cmp(&amax2, &bound) <= 0) break;
+    }
+    *sbyte = (uint8_t)(e + 127);
+    for (i = 0; i < 32; i++) {
+        int k, m3 = 0;
+        big_square(&mag[i], &sq);
+        for (k = 0; k < 7; k++) {
+            bound = big_const(2 * mid_k[k] * mid_k[k], 2 * e + 266);
+            if (big_cmp(&sq, &bound) > 0) m3 = k + 1;
+        }
+        codes[i] = (uint8_t)(m3 | (negative[i] ? 8 : 0));     /* negative: S_i < 0, so y_i != 0 */
+    }
+    return 0;
 }
 
 /* MXFP4 quantization of the rotated blocks of a rows x cols bfloat16 matrix
  * (cols % 32 == 0): codes rows x cols/2, scales rows x cols/32.  With fake != 0
  * it writes instead y_out (row stride ldy): each dequantized rotated value
- * rounded once to bfloat16 (NaN for a non-finite block). */
+ * code * 2^e in bfloat16, exact (NaN for a non-finite block). */
 static int quantize_mx_rht(const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx,
                            uint32_t signs, uint8_t *codes, uint8_t *scales,
                            uint16_t *y_out, int64_t ldy, int fake)
@@ -424,27 +546,18 @@ static int quantize_mx_rht(const uint16_t *x, int64_t rows, int64_t cols, int64_
     nb = cols / 32;
     for (r = 0; r < rows; r++) {
         for (b = 0; b < nb; b++) {
-            float y[32];
-            double amax = 0.0, S;
-            int bad = 0;
-            uint8_t sb;
-            orc_rht32(x + r * ldx + b * 32, signs, y);
-            for (j = 0; j < 32; j++) {
-                if (isnan(y[j]) || isinf(y[j])) bad = 1;
-                else if (fabs((double)y[j]) > amax) amax = fabs((double)y[j]);
-            }
-            sb = bad ? 0xFF : orc_mx_scale_byte(amax);
-            S = orc_e8m0_value(sb);
+            uint8_t sb, cs[32];
+            int bad = rht_block_exact(x + r * ldx + b * 32, signs, &sb, cs);
+            double S = orc_e8m0_value(sb);
             if (!fake) scales[r * nb + b] = sb;
             for (j = 0; j < 32; j++) {
-                uint8_t c = bad ? 0 : orc_e2m1_encode((double)y[j], S);
                 int64_t k = b * 32 + j;
                 if (fake) {
-                    y_out[r * ldy + k] = bad ? 0x7FC0 : orc_bf16_from_double(orc_e2m1_value(c) * S);
+                    y_out[r * ldy + k] = bad ? 0x7FC0 : orc_bf16_from_double(orc_e2m1_value(cs[j]) * S);
                 } else {
                     uint8_t *p = &codes[r * (cols / 2) + k / 2];
-                    if (k % 2 == 0) *p = (uint8_t)((*p & 0xF0) | c);
-                    else *p = (uint8_t)((*p & 0x0F) | (c << 4));
+                    if (k % 2 == 0) *p = (uint8_t)((*p & 0xF0) | cs[j]);
+                    else *p = (uint8_t)((*p & 0x0F) | (cs[j] << 4));
                 }
             }
         }

@@ -34,23 +34,40 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libreqat)")
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every HIP source into LIB; always recompiles."""
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc(), *HIPCC_FLAGS, "-o", tmp, *srcs]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError("hipcc failed building libreqat.so")
+        raise RuntimeError("hipcc failed: %s" % " ".join(cmd[-3:]))
     # keep warnings visible, minus hipcc's host-pass note about the device-only feature flag
     noise = ("packed-fp32-ops", "is not a recognized feature")
     for line in (res.stdout + res.stderr).splitlines():
         if line.strip() and not any(n in line for n in noise):
             sys.stderr.write(line + "\n")
-    os.replace(tmp, LIB)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every HIP source (in parallel, one object each) and link LIB; always recompiles."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    cc = hipcc()
+    tag = "%d" % os.getpid()
+    objs = [os.path.join(CSRC, s[:-4] + ".%s.o" % tag) for s in SOURCES]
+    flags = [f for f in HIPCC_FLAGS if f != "-shared"]
+    jobs = [[cc, *flags, "-c", os.path.join(CSRC, s), "-o", o] for s, o in zip(SOURCES, objs)]
+    workers = max(1, min(len(jobs), len(os.sched_getaffinity(0)), 8))
+    tmp = LIB + ".tmp" + tag
+    try:
+        with ThreadPoolExecutor(workers) as ex:
+            list(ex.map(lambda c: _run(c, verbose), jobs))
+        _run([cc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
+        os.replace(tmp, LIB)
+    finally:
+        for o in objs + [tmp]:
+            if os.path.exists(o):
+                os.remove(o)
     return LIB
 
 

@@ -42,6 +42,7 @@
 
 #include "fp4_device.h"
 #include "internal.h"
+#include "rht_exact.h"
 
 namespace reqat {
 
@@ -787,22 +788,39 @@ __global__ __launch_bounds__(kThreads) void nv_fixup_kernel(
 // MXFP4 activations may be rotated block by block before quantization (a
 // randomized Hadamard transform per 32-element block, Sec. 4.3 and App. C.2):
 // y = H_32 D x / sqrt(32), D = diag(d), d_j = -1 where bit j of `signs` is set,
-// H_32 the Sylvester Hadamard matrix.  Arithmetic is FP32 in a fixed order:
-// the fast Walsh-Hadamard transform in stages h = 1, 2, 4, 8, 16 (each
-// (t[j], t[j+h]) -> (t[j] + t[j+h], t[j] - t[j+h]), rounded to nearest even),
-// then each value times the FP32 constant nearest 1/sqrt(32).  Only adds,
-// subtracts and one multiply per value, none contracted, so the values are
-// fixed bit for bit.  The FP32 values are then quantized as an MXFP4 block.
+// H_32 the Sylvester Hadamard matrix.  The codes and the scale are those of
+// the exact real y (see rht_exact.h).
+//
+// Fast path: y^ in FP32 (the fast Walsh-Hadamard transform in five stages of
+// sums and differences, then a product with RN(1/sqrt(32))).  Its error is at
+// most (7u + O(u^2)) / sqrt(32) * sum|x| + 2^-150 (u = 2^-24: one rounding per
+// stage on each input's path, one in the constant, one in the product; the
+// sums of bfloat16 inputs are exact where they are subnormal).  With
+//     err = 2.5 u sum|x| + 2^-149
+// (about 1.8 times that, which also covers the rounding of y^ +- err and of
+// the FP32 sum|x|), the exact y_i lies strictly between y^_i - err and
+// y^_i + err on the side of y^_i's sign whenever |y^_i| > err.  A decision is
+// kept when it comes out the same at both ends: the scale byte of
+// max|y^| - err and of max|y^| + err, and the code (sign included) of
+// y^_i - copysign(err, y^_i) and of y^_i + copysign(err, y^_i); at a lower
+// end of -0 or the wrong sign the codes differ.  A block where any of them
+// differs, or whose FP32 values overflowed, is decided exactly instead
+// (rht::block_exact).  About one block in a thousand of Gaussian or
+// Student-t activations takes that path.
 
 constexpr uint32_t kInvSqrt32 = 0x3E3504F3u;   // 1/sqrt(32) rounded to nearest FP32
+constexpr float kRotErr = 2.5f * 0x1p-24f;      // err = kRotErr * sum|x| + 2^-149
 
-__device__ __forceinline__ void rotate32(const uint32_t (&w)[16], uint32_t signs, float (&t)[32]) {
+// y^ of one block; returns the FP32 sum of |x|.
+__device__ __forceinline__ float rotate32(const uint32_t (&w)[16], uint32_t signs, float (&t)[32]) {
+    float sabs = 0.0f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
         const uint32_t lo = (w[i] << 16) ^ (((signs >> (2 * i)) & 1u) << 31);
         const uint32_t hi = (w[i] & 0xFFFF0000u) ^ (((signs >> (2 * i + 1)) & 1u) << 31);
         t[2 * i] = f32_from_bits(lo);
         t[2 * i + 1] = f32_from_bits(hi);
+        sabs += f32_from_bits(lo & 0x7FFFFFFFu) + f32_from_bits(hi & 0x7FFFFFFFu);
     }
 #pragma unroll
     for (int h = 1; h < 32; h *= 2)
@@ -817,6 +835,7 @@ __device__ __forceinline__ void rotate32(const uint32_t (&w)[16], uint32_t signs
     const float c = f32_from_bits(kInvSqrt32);
 #pragma unroll
     for (int j = 0; j < 32; ++j) t[j] = t[j] * c;
+    return sabs;
 }
 
 // E8M0 byte of the smallest e in [-127, 127] with amax <= 6 * 2^e, for an FP32
@@ -838,99 +857,190 @@ __device__ __forceinline__ uint32_t mx_scale_byte_f32(uint32_t am) {
     return (uint32_t)(e + 127);
 }
 
-// E2M1 code of v / S (S = 2^e), nearest with ties to the even code, saturating
-// at 6, sign copied; decided by exact FP64 comparisons (v is FP32).
-__device__ __forceinline__ uint32_t e2m1_code_exact(float v, double S) {
-    const double a = __builtin_fabs((double)v);
-    const double mids[7] = {0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0};
-    uint32_t m = 7u;
-#pragma unroll
-    for (int i = 6; i >= 0; --i) {
-        const double t = mids[i] * S;
-        if (a < t || (a == t && (i & 1) == 0)) m = (uint32_t)i;
-    }
-    return m | ((bits_from_f32(v) >> 28) & 8u);
+// Codes of 8 FP32 values at scale p2 (one packed word).
+__device__ __forceinline__ uint32_t cvt8(const float *v, float p2) {
+    uint32_t word = 0;
+    word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, v[0], v[1], p2, 0);
+    word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, v[2], v[3], p2, 1);
+    word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, v[4], v[5], p2, 2);
+    word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, v[6], v[7], p2, 3);
+    return word;
 }
 
-// Quantizes (codes) or fake-quantizes one rotated block.  v_cvt_scalef32_pk_fp4_f32
-// rounds FP32 inputs to nearest-even E2M1 exactly for every power-of-two scale
-// 2^-126..2^127 (checked on gfx950 at every midpoint and its neighbouring FP32
-// values); scale byte 0, the fake-quant outputs below 2^-124 and non-finite
-// blocks take the FP64 comparisons instead.
-template <int OUT>
-__device__ __forceinline__ void emit_rotated(const float (&t)[32], int64_t blk, uint8_t *codes,
-                                             uint8_t *scales, uint16_t *ydst) {
+// The fast path's decisions: true (and sbyte, cw) when every one is proven.
+// v_cvt_scalef32_pk_fp4_f32 rounds an FP32 value v to the nearest E2M1 value
+// of v / 2^e with ties to the even code (checked on gfx950 for every scale
+// 2^-126..2^127 at each midpoint and its neighbouring FP32 values).
+__device__ __forceinline__ bool rotated_certified(const float (&t)[32], float sabs, uint32_t &sbyte,
+                                                  uint32_t (&cw)[4]) {
     uint32_t am = 0u;
 #pragma unroll
     for (int j = 0; j < 32; ++j) {
         const uint32_t m = bits_from_f32(t[j]) & 0x7FFFFFFFu;
         am = am > m ? am : m;
     }
-    const bool bad = am >= 0x7F800000u;
-    const uint32_t sbyte = bad ? 0xFFu : mx_scale_byte_f32(am);
+    const float err = __builtin_fmaf(sabs, kRotErr, 0x1p-149f);
+    const float amf = f32_from_bits(am);
+    const float alo = amf - err, ahi = amf + err;
+    // finite y^ (no FP32 overflow) and a finite upper end
+    bool ok = am < 0x7F800000u && bits_from_f32(ahi) < 0x7F800000u;
+    const uint32_t slo = alo > 0.0f ? mx_scale_byte_f32(bits_from_f32(alo)) : 0u;
+    sbyte = mx_scale_byte_f32(bits_from_f32(ahi));
+    ok = ok && slo == sbyte && sbyte >= 1u;         // scale byte 0 has no FP32 scale operand
     const float p2 = f32_from_bits(sbyte << 23);
-    const bool fast = !bad && sbyte >= (OUT == kCodes ? 1u : 3u);
-    uint32_t cw[4];
-    if (fast) {
+    uint32_t diff = 0u;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            uint32_t word = 0;
-            word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, t[8 * q + 0], t[8 * q + 1], p2, 0);
-            word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, t[8 * q + 2], t[8 * q + 3], p2, 1);
-            word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, t[8 * q + 4], t[8 * q + 5], p2, 2);
-            word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, t[8 * q + 6], t[8 * q + 7], p2, 3);
-            cw[q] = word;
+    for (int q = 0; q < 4; ++q) {
+        float lo[8], hi[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const float v = t[8 * q + k];
+            const float se = f32_from_bits(bits_from_f32(err) | (bits_from_f32(v) & 0x80000000u));
+            lo[k] = v - se;
+            hi[k] = v + se;
         }
-    } else {
-        const double S = __builtin_ldexp(1.0, (int)sbyte - 127);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            uint32_t word = 0;
-#pragma unroll
-            for (int k = 0; k < 8; ++k) word |= (bad ? 0u : e2m1_code_exact(t[8 * q + k], S)) << (4 * k);
-            cw[q] = word;
-        }
+        const uint32_t wl = cvt8(lo, p2), wh = cvt8(hi, p2);
+        diff |= wl ^ wh;
+        cw[q] = wh;
     }
+    return ok && diff == 0u;
+}
+
+// Stores one rotated block: codes and scale byte, or the fake-quant values
+// code * 2^e (exact in bfloat16; a NaN block is 0x7FC0).
+template <int OUT>
+__device__ __forceinline__ void store_rotated(uint32_t sbyte, const uint32_t (&cw)[4], bool bad, int64_t blk,
+                                              uint8_t *codes, uint8_t *scales, uint16_t *ydst) {
     if (OUT == kCodes) {
         *reinterpret_cast<uint4 *>(codes + blk * 16) = make_uint4(cw[0], cw[1], cw[2], cw[3]);
         scales[blk] = (uint8_t)sbyte;
         return;
     }
     uint4 *dst = reinterpret_cast<uint4 *>(ydst);
-    if (fast) {
+    if (!bad && sbyte >= 3u) {
+        const float p2 = f32_from_bits(sbyte << 23);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             uint32_t o[4];
             fq_fast_mx(cw[q], p2, o);
             dst[q] = make_uint4(o[0], o[1], o[2], o[3]);
         }
-    } else {
-        const double S = __builtin_ldexp(1.0, (int)sbyte - 127);
+        return;
+    }
+    const double S = __builtin_ldexp(1.0, (int)sbyte - 127);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            uint32_t o[4];
+    for (int q = 0; q < 4; ++q) {
+        uint32_t o[4];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                uint32_t h2[2];
+        for (int k = 0; k < 4; ++k) {
+            uint32_t h2[2];
 #pragma unroll
-                for (int hf = 0; hf < 2; ++hf) {
-                    const uint32_t c = (cw[q] >> (8 * k + 4 * hf)) & 0xFu;
-                    const double v = (double)e2m1_mag_value((int)(c & 7u)) * S;
-                    h2[hf] = bad ? 0x7FC0u : (bf16_rne_from_double(v) | ((c & 8u) << 12));
-                }
-                o[k] = h2[0] | (h2[1] << 16);
+            for (int hf = 0; hf < 2; ++hf) {
+                const uint32_t c = (cw[q] >> (8 * k + 4 * hf)) & 0xFu;
+                const double v = (double)e2m1_mag_value((int)(c & 7u)) * S;
+                h2[hf] = bad ? 0x7FC0u : (bf16_rne_from_double(v) | ((c & 8u) << 12));
             }
-            dst[q] = make_uint4(o[0], o[1], o[2], o[3]);
+            o[k] = h2[0] | (h2[1] << 16);
         }
+        dst[q] = make_uint4(o[0], o[1], o[2], o[3]);
     }
 }
 
+// Exact decisions for the block at `bsrc` (32 finite bfloat16 values), with
+// the whole wave taking part (every lane must be active): lane j (and j + 32)
+// holds input j; in units of 2^(min sh) the inputs are integers, and with an
+// exponent spread of at most 40 the five butterfly stages across lanes compute
+// the sums S_i exactly in FP64, lane i ending with S_i.  The scale and the
+// codes then follow from signs of fused multiply-adds (rht_exact.h).  Wider
+// spreads go to the wide-integer path on lane 0, its words in `wide` (LDS).
+// Returns the scale byte; cw (the same in every lane) gets the packed codes.
+__device__ __forceinline__ uint32_t rotated_exact_wave(const uint16_t *bsrc, uint32_t signs, int lane,
+                                                       uint32_t (&cw)[4], uint32_t *wide) {
+    const int j = lane & 31;
+    const uint32_t h = bsrc[j];
+    bool neg;
+    uint32_t m;
+    int sh;
+    rht::int_parts(h, ((signs >> j) & 1u) != 0u, neg, m, sh);
+    int lo = m ? sh : 1 << 20, hi = m ? sh : -1;
+#pragma unroll
+    for (int off = 16; off > 0; off >>= 1) {            // lanes 32..63 mirror 0..31
+        const int lo2 = __shfl_xor(lo, off, 64), hi2 = __shfl_xor(hi, off, 64);
+        lo = lo < lo2 ? lo : lo2;
+        hi = hi > hi2 ? hi : hi2;
+    }
+    const int shmin = __builtin_amdgcn_readfirstlane(lo), shmax = __builtin_amdgcn_readfirstlane(hi);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) cw[q] = 0u;
+    if (shmax < 0) return 0u;                           // every input is +-0: y == 0
+    if (shmax - shmin > 40) {
+        uint32_t sb = 0u;
+        if (lane == 0) {
+#pragma unroll 1
+            for (int k = 0; k < 16; ++k) wide[k] = (uint32_t)bsrc[2 * k] | ((uint32_t)bsrc[2 * k + 1] << 16);
+            uint32_t c4[4];
+            rht::block_wide(signs, sb, c4, wide);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) wide[q] = c4[q];
+        }
+        sb = (uint32_t)__builtin_amdgcn_readfirstlane((int)sb);
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+#pragma unroll
+        for (int q = 0; q < 4; ++q) cw[q] = (uint32_t)__builtin_amdgcn_readfirstlane((int)wide[q]);
+        __builtin_amdgcn_wave_barrier();
+        return sb;
+    }
+    const double v0 = m ? __builtin_ldexp((double)m, sh - shmin) : 0.0;   // <= 255 * 2^40: exact
+    double v = neg ? -v0 : v0;
+#pragma unroll
+    for (int off = 1; off < 32; off <<= 1) {            // integers below 2^53: exact
+        const double o = __shfl_xor(v, off, 64);
+        v = (j & off) ? o - v : v + o;
+    }
+    double amax = __builtin_fabs(v);
+#pragma unroll
+    for (int off = 16; off > 0; off >>= 1) amax = __builtin_fmax(amax, __shfl_xor(amax, off, 64));
+    {
+        const uint64_t ab = __builtin_bit_cast(uint64_t, amax);
+        const uint32_t alo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)ab);
+        const uint32_t ahi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(ab >> 32));
+        amax = __builtin_bit_cast(double, (uint64_t)alo | ((uint64_t)ahi << 32));
+    }
+    if (amax == 0.0) return 0u;
+    // smallest e with S_max^2 <= 1152 * 2^P, P = 2e + 266 - 2 shmin: with S_max in
+    // [2^L, 2^(L+1)) it is L + shmin - 138 or one above
+    const int L = (int)((__builtin_bit_cast(uint64_t, amax) >> 52) & 0x7FFu) - 1023;
+    int e = L + shmin - 138;
+    e = e < -127 ? -127 : (e > 127 ? 127 : e);
+    while (e > -127 && __builtin_fma(amax, amax, -__builtin_ldexp(1152.0, 2 * e - 2 + 266 - 2 * shmin)) < 0.0) --e;
+    while (e < 127 && !(__builtin_fma(amax, amax, -__builtin_ldexp(1152.0, 2 * e + 266 - 2 * shmin)) < 0.0)) ++e;
+    const int P = 2 * e + 266 - 2 * shmin;
+    uint32_t m3 = 0u;
+#pragma unroll
+    for (int k = 0; k < 7; ++k) {
+        const double bound = __builtin_ldexp((double)(2u * rht::mid_k(k) * rht::mid_k(k)), P);
+        m3 += __builtin_fma(v, v, -bound) > 0.0 ? 1u : 0u;
+    }
+    // code of output j in nibble j % 8 of word j / 8: OR over groups of 8 lanes
+    uint32_t word = (m3 | (v < 0.0 ? 8u : 0u)) << (4 * (j & 7));
+#pragma unroll
+    for (int off = 1; off < 8; off <<= 1) word |= __shfl_xor(word, off, 64);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) cw[q] = (uint32_t)__builtin_amdgcn_readlane((int)word, 8 * q);
+    return (uint32_t)(e + 127);
+}
+
 // One lane per 32-element block, blocks in segments of 64 (one per lane of a
-// wave), wave w of workgroup b taking segments b*4 + w + k*(4*grid).
+// wave), wave w of workgroup b taking segments b*4 + w + k*(4*grid).  After
+// the wave's fast stores, the blocks the fast path could not decide are
+// decided exactly one at a time by the whole wave (about one wave in ten
+// has one, for Gaussian or Student-t activations).
 template <int OUT>
 __global__ __launch_bounds__(kThreads) void quantize_rht_kernel(
     const uint16_t *__restrict__ x, int64_t rows, int64_t cols, int64_t ldx, uint32_t signs,
     uint8_t *__restrict__ codes, uint8_t *__restrict__ scales, uint16_t *__restrict__ y, int64_t ldy) {
+    __shared__ uint32_t wide_buf[4][rht::kWideWords];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t nb = cols / 32;
@@ -941,13 +1051,34 @@ __global__ __launch_bounds__(kThreads) void quantize_rht_kernel(
     for (int64_t s = (int64_t)blockIdx.x * 4 + wave; s < nseg; s += step) {
         const int64_t blk = s * kSeg + lane;
         const int64_t b = blk < total ? blk : total - 1;       // branch-free load, result unused
+        const uint16_t *src = x + block_offset(b, nb, cols, ldx, 32, narrow);
         uint32_t w[16];
-        load_block<32>(x + block_offset(b, nb, cols, ldx, 32, narrow), w);
+        load_block<32>(src, w);
+        const bool bad = block_mag_max<32>(w) >= 0x7F80u;       // a NaN or Inf input
         float t[32];
-        rotate32(w, signs, t);
-        if (blk < total) {
-            uint16_t *ydst = OUT == kFakeQuant ? y + block_offset(blk, nb, cols, ldy, 32, narrow) : nullptr;
-            emit_rotated<OUT>(t, blk, codes, scales, ydst);
+        const float sabs = rotate32(w, signs, t);
+        uint32_t sbyte, cw[4];
+        bool done = rotated_certified(t, sabs, sbyte, cw);
+        if (bad || sabs == 0.0f) {                             // NaN block, or every input +-0 (y == 0)
+            sbyte = bad ? 0xFFu : 0u;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) cw[q] = 0u;
+            done = true;
+        }
+        uint16_t *ydst = nullptr;
+        if (OUT == kFakeQuant && blk < total) ydst = y + block_offset(blk, nb, cols, ldy, 32, narrow);
+        if (blk < total && done) store_rotated<OUT>(sbyte, cw, bad, blk, codes, scales, ydst);
+        uint64_t pend = __ballot(blk < total && !done);
+        while (pend) {                                         // wave-uniform
+            const int L = __builtin_ctzll(pend);
+            pend &= pend - 1;
+            const uint64_t pa = (uint64_t)(uintptr_t)src;
+            const uint16_t *bsrc = (const uint16_t *)(uintptr_t)(
+                (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)pa, L) |
+                ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(pa >> 32), L) << 32));
+            uint32_t ecw[4];
+            const uint32_t esb = rotated_exact_wave(bsrc, signs, lane, ecw, wide_buf[wave]);
+            if (lane == L) store_rotated<OUT>(esb, ecw, false, blk, codes, scales, ydst);
         }
     }
 }

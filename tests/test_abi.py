@@ -65,7 +65,7 @@ def test_library_imports_no_allocation_copy_or_sync(lib):
 
 
 def test_small_queries(lib):
-    assert reqat.reqat_abi_version() == 8
+    assert reqat.reqat_abi_version() == 9
     assert reqat.reqat_workspace_bytes() == 4 * 4096 + 2 * (1 << 19)   # partials + segment table
     for s in range(7):
         assert reqat.reqat_status_str(s).startswith(reqat.STATUS[s])

@@ -7,6 +7,8 @@ output must additionally be within one bf16 ulp of round(Yref).  Outputs are
 pre-filled with two different poison patterns, so an element the kernel does
 not write, or a run-to-run difference, fails the comparison.
 """
+from fractions import Fraction
+
 import numpy as np
 import pytest
 import torch
@@ -223,6 +225,42 @@ def test_rotated_mxfp4_tiny_and_strided():
     xb = _ramp(24, 320, 77, 6.0)                 # rows down to 2^-138: E8M0 byte 0 and FP32 subnormals
     assert_rht_parity(xb, 0x13579BDF)
     assert_rht_parity(_rand(45, 320, 9, "normal"), 0x2468ACE0, ldx_pad=40)
+
+
+def _near_threshold_rows(signs):
+    """Blocks whose scale or first code hinges on bits up to ~2^-128 below the leading
+    one (each threshold from both sides): neither FP32 nor FP64 evaluation decides them,
+    and with 12 or 16 slices the inputs span more than 40 binades (the wide-integer path)."""
+    rows = []
+    cases = [(Fraction(6), 0, None), (Fraction(6), 50, None), (Fraction(5), -3, None),
+             (Fraction(7, 2), 10, None), (Fraction(1, 4), 2, 9), (Fraction(3, 4), -20, 9),
+             (Fraction(5, 4), 0, 9), (Fraction(7, 4), 5, 9), (Fraction(5, 2), -7, 9)]
+    for t, e, big in cases:
+        for chunks in (3, 4, 6, 12, 16):
+            for above in (False, True):
+                bigv = None if big is None else Fraction(big) * Fraction(2) ** e
+                rows.append(indep.rht_near_threshold_block(t, e, above, chunks, signs, bigv))
+    return np.concatenate(rows).reshape(-1, 64) if len(rows) % 2 == 0 else np.concatenate(rows[:-1]).reshape(-1, 64)
+
+
+@pytest.mark.parametrize("signs", [0, 0x13579BDF])
+def test_rotated_mxfp4_decisions_below_fp32_and_fp64_precision(signs):
+    """The exact rotation on blocks the FP32 fast path cannot decide: near-threshold
+    blocks (FP64 and wide-integer paths), small-integer and constant blocks (exact zero
+    outputs), and a mix of them with ordinary blocks in the same waves."""
+    log("rotated mxfp4 near-threshold signs=%08x" % signs)
+    near = _near_threshold_rows(signs)
+    assert_rht_parity(near, signs)
+    rng = np.random.default_rng(signs & 0xFFFF)
+    ints = indep.to_bf16_bits(rng.integers(-40, 41, (96, 256)).astype(np.float64))
+    const = np.repeat(indep.to_bf16_bits(rng.normal(0, 1, 96)), 256).reshape(96, 256)
+    mixed = _rand(96, 256, 4, "student_t", outliers=2)
+    mixed[::3] = ints[::3]
+    mixed[1::7] = const[1::7]
+    assert_rht_parity(np.concatenate([ints, const, mixed]), signs)
+    spread = mixed.copy()
+    spread[:, ::5] = indep.to_bf16_bits(indep.bf16_values(spread[:, ::5]) * 2.0 ** -90)   # wide spreads
+    assert_rht_parity(spread, signs)
 
 
 # ------------------------------------------------------------------ KV4
@@ -512,8 +550,10 @@ def check_gemm_points(fmt, ac, as_, ga, bc, bs, gb, y32, ybf, ms, ns):
     ok = ~nanref
     err = np.abs(got[ok] - ref[ok])
     m = indep.gemm_error_metrics(got, ref, aref)
-    log("  gemm fp32 K=%d %s" % (ac.shape[1] * 2, indep.format_metrics(m)))
+    K = ac.shape[1] * 2
+    log("  gemm fp32 K=%d %s" % (K, indep.format_metrics(m)))
     assert np.all(err <= GEMM_TOL * aref[ok]), float(np.max(err / np.maximum(aref[ok], 1e-300)))
+    assert m["max_rel_sum"] <= indep.fp32_accumulation_bound(K), m
     if ybf is not None:
         gb_ = ybf[ms, ns][ok]
         rb = indep.bf16_values(oracle.bf16_from_double_array(ref[ok]))

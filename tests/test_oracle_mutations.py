@@ -72,12 +72,17 @@ MUTATIONS = [
     (C, "            acc += t;\n            aacc += fabs(t);\n        }\n        y[p] = acc;\n        absy[p] = aacc;\n    }\n}\n\n/* ---------- array",
      "            acc += fabs(t);\n            aacc += fabs(t);\n        }\n        y[p] = acc;\n        absy[p] = aacc;\n    }\n}\n\n/* ---------- array",
      TEN, "GEMM sums magnitudes"),
-    (C, "                t[j + h] = a - b;", "                t[j + h] = b - a;", ["test_oracle_rht.py"],
-     "Hadamard butterfly sign"),
-    (C, "y[j] = ((signs >> j) & 1u) ? -v : v;", "y[j] = ((signs >> (31 - j)) & 1u) ? -v : v;",
+    (C, "int hneg = __builtin_popcount((unsigned)(i & j)) & 1;",
+     "int hneg = __builtin_popcount((unsigned)(i | j)) & 1;", ["test_oracle_rht.py"], "Hadamard sign pattern"),
+    (C, "if ((signs >> j) & 1u) xneg = !xneg;", "if ((signs >> (31 - j)) & 1u) xneg = !xneg;",
      ["test_oracle_rht.py"], "sign word bit order"),
-    (C, "for (j = 0; j < 32; j++) y[j] = y[j] * c;", "for (j = 0; j < 32; j++) y[j] = y[j];",
-     ["test_oracle_rht.py"], "rotation normalisation dropped"),
+    (C, "bound = big_const(1152, 2 * e + 266);", "bound = big_const(36, 2 * e + 266);",
+     ["test_oracle_rht.py"], "rotation normalisation dropped from the scale bound"),
+    (C, "static const uint32_t mid_k[7] = {1, 3, 5, 7, 10, 14, 20};",
+     "static const uint32_t mid_k[7] = {1, 3, 5, 7, 10, 14, 21};", ["test_oracle_rht.py"],
+     "rotated E2M1 midpoint 5 moved"),
+    (C, "    return e - 1;\n}", "    return e;\n}", ["test_oracle_rht.py"], "bfloat16 exponent offset in the exact sums"),
+    (C, "negative[i] = c < 0;", "negative[i] = c <= 0;", ["test_oracle_rht.py"], "sign of a zero rotated value"),
     (C, "    return orc_bf16_value(orc_bf16_from_double(v));", "    return v;", ["test_oracle_w4a16.py"],
      "W4A16 weight not rounded to bfloat16"),
     (C, "if (a == t) { m = (i % 2 == 0) ? i : i + 1; break; }", "if (a == t) { m = i; break; }",
