@@ -791,27 +791,27 @@ __global__ __launch_bounds__(kThreads) void nv_fixup_kernel(
 // H_32 the Sylvester Hadamard matrix.  The codes and the scale are those of
 // the exact real y (see rht_exact.h).
 //
-// Fast path: y^ in FP32 (the fast Walsh-Hadamard transform in five stages of
-// sums and differences, then a product with RN(1/sqrt(32))).  Its error is at
-// most (7u + O(u^2)) / sqrt(32) * sum|x| + 2^-150 (u = 2^-24: one rounding per
-// stage on each input's path, one in the constant, one in the product; the
-// sums of bfloat16 inputs are exact where they are subnormal).  With
+// Fast path: y^ = s^ * RN(1/sqrt(32)) with s^ = H D x in FP32 (the fast
+// Walsh-Hadamard transform in five stages of sums and differences).  Its error
+// is at most (7u + O(u^2)) / sqrt(32) * sum|x| + 2^-150 (u = 2^-24: one
+// rounding per stage on each input's path, one in the constant, one in the
+// product; sums of bfloat16 inputs are exact where they are subnormal).  With
 //     err = 2.5 u sum|x| + 2^-149
-// (about 1.8 times that, which also covers the rounding of y^ +- err and of
-// the FP32 sum|x|), the exact y_i lies strictly between y^_i - err and
-// y^_i + err on the side of y^_i's sign whenever |y^_i| > err.  A decision is
-// kept when it comes out the same at both ends: the scale byte of
-// max|y^| - err and of max|y^| + err, and the code (sign included) of
-// y^_i - copysign(err, y^_i) and of y^_i + copysign(err, y^_i); at a lower
-// end of -0 or the wrong sign the codes differ.  A block where any of them
-// differs, or whose FP32 values overflowed, is decided exactly instead
-// (rht::block_exact).  About one block in a thousand of Gaussian or
-// Student-t activations takes that path.
+// (about 1.8 times that, which also covers the FP32 sum|x|), the exact y_i lies
+// strictly between the two ends y^_i -+ copysign(err, y^_i) (each one FP32
+// rounding of an exact product-sum, within the margin).  A decision is kept
+// when it comes out the same at both ends: the scale byte of max|y^| -+ err,
+// and the code (sign included) of each element's ends; an end of -0 or of the
+// wrong sign gives a different code.  A block where any of them differs, or
+// with sum|x| >= 2^127 (where the FP32 sums could overflow), is decided
+// exactly instead, by the whole wave (rotated_exact_wave).  About one block in
+// a thousand of Gaussian or Student-t activations takes that path.
 
 constexpr uint32_t kInvSqrt32 = 0x3E3504F3u;   // 1/sqrt(32) rounded to nearest FP32
 constexpr float kRotErr = 2.5f * 0x1p-24f;      // err = kRotErr * sum|x| + 2^-149
 
-// y^ of one block; returns the FP32 sum of |x|.
+// The unnormalized FP32 transform s^ = H D x of one block (y^ = s^ / sqrt(32));
+// returns the FP32 sum of |x|.
 __device__ __forceinline__ float rotate32(const uint32_t (&w)[16], uint32_t signs, float (&t)[32]) {
     float sabs = 0.0f;
 #pragma unroll
@@ -820,7 +820,7 @@ __device__ __forceinline__ float rotate32(const uint32_t (&w)[16], uint32_t sign
         const uint32_t hi = (w[i] & 0xFFFF0000u) ^ (((signs >> (2 * i + 1)) & 1u) << 31);
         t[2 * i] = f32_from_bits(lo);
         t[2 * i + 1] = f32_from_bits(hi);
-        sabs += f32_from_bits(lo & 0x7FFFFFFFu) + f32_from_bits(hi & 0x7FFFFFFFu);
+        sabs += __builtin_fabsf(t[2 * i]) + __builtin_fabsf(t[2 * i + 1]);
     }
 #pragma unroll
     for (int h = 1; h < 32; h *= 2)
@@ -832,9 +832,6 @@ __device__ __forceinline__ float rotate32(const uint32_t (&w)[16], uint32_t sign
                 t[j] = a + b;
                 t[j + h] = a - b;
             }
-    const float c = f32_from_bits(kInvSqrt32);
-#pragma unroll
-    for (int j = 0; j < 32; ++j) t[j] = t[j] * c;
     return sabs;
 }
 
@@ -868,22 +865,24 @@ __device__ __forceinline__ uint32_t cvt8(const float *v, float p2) {
 }
 
 // The fast path's decisions: true (and sbyte, cw) when every one is proven.
+// t holds s^ (unnormalized); the ends y^ -+ copysign(err, y^) are formed as
+// single fused products with the FP32 constant RN(1/sqrt(32)), so y^ itself is
+// never rounded (the bound above covers this form too).
 // v_cvt_scalef32_pk_fp4_f32 rounds an FP32 value v to the nearest E2M1 value
 // of v / 2^e with ties to the even code (checked on gfx950 for every scale
 // 2^-126..2^127 at each midpoint and its neighbouring FP32 values).
 __device__ __forceinline__ bool rotated_certified(const float (&t)[32], float sabs, uint32_t &sbyte,
                                                   uint32_t (&cw)[4]) {
-    uint32_t am = 0u;
+    const float c = f32_from_bits(kInvSqrt32);
+    float ams = 0.0f;
 #pragma unroll
-    for (int j = 0; j < 32; ++j) {
-        const uint32_t m = bits_from_f32(t[j]) & 0x7FFFFFFFu;
-        am = am > m ? am : m;
-    }
+    for (int j = 0; j < 32; j += 2)
+        ams = __builtin_fmaxf(ams, __builtin_fmaxf(__builtin_fabsf(t[j]), __builtin_fabsf(t[j + 1])));
     const float err = __builtin_fmaf(sabs, kRotErr, 0x1p-149f);
-    const float amf = f32_from_bits(am);
+    const float amf = ams * c;
     const float alo = amf - err, ahi = amf + err;
-    // finite y^ (no FP32 overflow) and a finite upper end
-    bool ok = am < 0x7F800000u && bits_from_f32(ahi) < 0x7F800000u;
+    // no partial sum can overflow while sum|x| < 2^127 (and then y^, err and ahi are finite)
+    bool ok = sabs < 0x1p127f;
     const uint32_t slo = alo > 0.0f ? mx_scale_byte_f32(bits_from_f32(alo)) : 0u;
     sbyte = mx_scale_byte_f32(bits_from_f32(ahi));
     ok = ok && slo == sbyte && sbyte >= 1u;         // scale byte 0 has no FP32 scale operand
@@ -896,8 +895,8 @@ __device__ __forceinline__ bool rotated_certified(const float (&t)[32], float sa
         for (int k = 0; k < 8; ++k) {
             const float v = t[8 * q + k];
             const float se = f32_from_bits(bits_from_f32(err) | (bits_from_f32(v) & 0x80000000u));
-            lo[k] = v - se;
-            hi[k] = v + se;
+            lo[k] = __builtin_fmaf(v, c, -se);
+            hi[k] = __builtin_fmaf(v, c, se);
         }
         const uint32_t wl = cvt8(lo, p2), wh = cvt8(hi, p2);
         diff |= wl ^ wh;
@@ -1054,9 +1053,10 @@ __global__ __launch_bounds__(kThreads) void quantize_rht_kernel(
         const uint16_t *src = x + block_offset(b, nb, cols, ldx, 32, narrow);
         uint32_t w[16];
         load_block<32>(src, w);
-        const bool bad = block_mag_max<32>(w) >= 0x7F80u;       // a NaN or Inf input
         float t[32];
         const float sabs = rotate32(w, signs, t);
+        // a NaN or Inf input makes sum|x| NaN or Inf
+        const bool bad = !(sabs < 0x1p127f) && block_mag_max<32>(w) >= 0x7F80u;
         uint32_t sbyte, cw[4];
         bool done = rotated_certified(t, sabs, sbyte, cw);
         if (bad || sabs == 0.0f) {                             // NaN block, or every input +-0 (y == 0)
