@@ -43,10 +43,13 @@
  *   y (product): [M][ldy] float32 or bfloat16 (round to nearest even).
  *
  * Ownership and concurrency: the caller allocates and frees every buffer;
- * the library allocates nothing and keeps no mutable global state.  Every
- * call only enqueues work on `stream` (a hipStream_t passed as void*; NULL
- * means the null stream) and returns without waiting.  Calls on different
- * streams that share a workspace race.
+ * the library allocates nothing.  Its only global state is set up once per
+ * device and read afterwards: a cache of the device's compute-unit count, and
+ * the device address of the fixed scratch array of reqat_linear_w4a4_noalloc
+ * (whose contents every such call on that device shares).  Every call only
+ * enqueues work on `stream` (a hipStream_t passed as void*; NULL means the
+ * null stream; it must belong to the current device) and returns without
+ * waiting.  Calls on different streams that share a workspace race.
  *
  * Errors: arguments are validated on the host before any HIP call; a bad
  * argument returns a status != REQAT_OK and enqueues nothing.  A failed
@@ -87,7 +90,8 @@ typedef enum {
     REQAT_E_ALIGN = 3,       /* a pointer or leading dimension breaks the alignment rule */
     REQAT_E_ENUM = 4,        /* unknown format, dtype or tensor-scale mode */
     REQAT_E_UNSUPPORTED = 5, /* valid but not implemented (e.g. MXFP4 with a tensor scale) */
-    REQAT_E_HIP = 6          /* a HIP launch failed */
+    REQAT_E_HIP = 6,         /* a HIP launch failed */
+    REQAT_E_TOO_LARGE = 7    /* beyond the fixed scratch of reqat_linear_w4a4_noalloc */
 } reqat_status;
 
 /*
@@ -312,6 +316,26 @@ reqat_status reqat_linear_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K
 
 /* Bytes of workspace reqat_linear_w4a4 needs for M x K activations (0 on bad arguments). */
 size_t reqat_linear_workspace_bytes(reqat_format fmt, int64_t M, int64_t K);
+
+/*
+ * reqat_linear_w4a4 for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same operation, kernels and results, with the workspace replaced by a
+ * fixed scratch array the library holds on each device (REQAT_NOALLOC_SCRATCH_BYTES
+ * bytes, from the first call on a device until the process ends).  It calls
+ * no allocating routine.  Arguments as reqat_linear_w4a4 without `workspace`;
+ * returns REQAT_E_TOO_LARGE, enqueueing nothing, when
+ * reqat_linear_workspace_bytes(fmt, M, K) exceeds the scratch (NVFP4: about
+ * 14.8 million activation elements, MXFP4: 15.3 million).  Every call on a
+ * device uses the same scratch, so calls that overlap in time on one device
+ * (different streams, or host threads) race; calls in order on one stream do not.
+ */
+#define REQAT_NOALLOC_SCRATCH_BYTES (8u << 20)
+reqat_status reqat_linear_w4a4_noalloc(reqat_format fmt, int64_t M, int64_t N, int64_t K,
+                                       const void *x, int64_t ldx, float *x_tensor_scale,
+                                       reqat_tscale_mode ts, const uint8_t *w_codes,
+                                       const uint8_t *w_scales, const float *w_tensor_scale,
+                                       void *y, reqat_dtype y_dtype, int64_t ldy, void *stream);
 
 /* Bytes of device workspace that a quantize / fake-quant call may use. */
 size_t reqat_workspace_bytes(void);

@@ -1,6 +1,8 @@
 // C ABI of libreqat: host-side argument validation and dispatch to the kernels.
 // Validation happens before any HIP call, so a bad argument is reported without
 // touching the device (and can be tested on a host without a GPU).
+#include <mutex>
+
 #include "../../include/reqat.h"
 #include "internal.h"
 
@@ -281,11 +283,15 @@ size_t reqat_linear_workspace_bytes(reqat_format fmt, int64_t M, int64_t K) {
     return round256(sizeof(uint32_t) * kMaxPartials) + round256(codes) + round256(scales) + round256(table);
 }
 
-reqat_status reqat_linear_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K, const void *x,
-                               int64_t ldx, float *x_tensor_scale, reqat_tscale_mode ts,
-                               const uint8_t *w_codes, const uint8_t *w_scales,
-                               const float *w_tensor_scale, void *y, reqat_dtype y_dtype,
-                               int64_t ldy, void *workspace, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Validation of the linear layer's arguments, workspace excluded.
+reqat_status check_linear(reqat_format fmt, int64_t M, int64_t N, int64_t K, const void *x, int64_t ldx,
+                          const float *x_tensor_scale, reqat_tscale_mode ts, const uint8_t *w_codes,
+                          const uint8_t *w_scales, const float *w_tensor_scale, const void *y,
+                          reqat_dtype y_dtype, int64_t ldy) {
     if (!fmt_ok(fmt)) return REQAT_E_ENUM;
     if (y_dtype != REQAT_DT_F32 && y_dtype != REQAT_DT_BF16) return REQAT_E_ENUM;
     const bool nv = fmt == REQAT_FMT_NVFP4;
@@ -294,8 +300,6 @@ reqat_status reqat_linear_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K
     if (K % 128 || ldx < K || ldy < N) return REQAT_E_SHAPE;
     if (!nv && (x_tensor_scale || w_tensor_scale)) return REQAT_E_UNSUPPORTED;
     if (nv && (!x_tensor_scale || !w_tensor_scale)) return REQAT_E_NULL;
-    if (!workspace) return REQAT_E_NULL;
-    if (reinterpret_cast<uintptr_t>(workspace) & 255u) return REQAT_E_ALIGN;
     if (M > 0 && N > 0) {
         if (!x || !y) return REQAT_E_NULL;
         if (K > 0 && (!w_codes || !w_scales)) return REQAT_E_NULL;
@@ -306,6 +310,16 @@ reqat_status reqat_linear_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K
                    (reinterpret_cast<uintptr_t>(w_tensor_scale) & 3u)))
             return REQAT_E_ALIGN;
     }
+    return REQAT_OK;
+}
+
+// Quantize x into `workspace` (laid out as reqat_linear_workspace_bytes describes)
+// and run the product; arguments already validated.
+reqat_status run_linear(reqat_format fmt, int64_t M, int64_t N, int64_t K, const void *x, int64_t ldx,
+                        float *x_tensor_scale, reqat_tscale_mode ts, const uint8_t *w_codes,
+                        const uint8_t *w_scales, const float *w_tensor_scale, void *y, reqat_dtype y_dtype,
+                        int64_t ldy, void *workspace, void *stream) {
+    const bool nv = fmt == REQAT_FMT_NVFP4;
     uint8_t *ws = reinterpret_cast<uint8_t *>(workspace);
     uint8_t *a_codes = ws + round256(sizeof(uint32_t) * kMaxPartials);
     uint8_t *a_scales = a_codes + round256((size_t)M * (size_t)(K / 2));
@@ -327,6 +341,74 @@ reqat_status reqat_linear_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K
     return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
 }
 
+}  // namespace
+
+extern "C" {
+
+reqat_status reqat_linear_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K, const void *x,
+                               int64_t ldx, float *x_tensor_scale, reqat_tscale_mode ts,
+                               const uint8_t *w_codes, const uint8_t *w_scales,
+                               const float *w_tensor_scale, void *y, reqat_dtype y_dtype,
+                               int64_t ldy, void *workspace, void *stream) {
+    reqat_status st = check_linear(fmt, M, N, K, x, ldx, x_tensor_scale, ts, w_codes, w_scales, w_tensor_scale,
+                                   y, y_dtype, ldy);
+    if (st != REQAT_OK) return st;
+    if (!workspace) return REQAT_E_NULL;
+    if (reinterpret_cast<uintptr_t>(workspace) & 255u) return REQAT_E_ALIGN;
+    return run_linear(fmt, M, N, K, x, ldx, x_tensor_scale, ts, w_codes, w_scales, w_tensor_scale, y, y_dtype,
+                      ldy, workspace, stream);
+}
+
+
+}  // extern "C"
+
+// ------------------------------------------------------ linear layer without allocation
+// For callers that cannot allocate: the linear layer's workspace is this
+// file-scope array, one copy on each GPU the library runs on, held until the
+// process ends.  In host code its name is only a stand-in; the kernels get the
+// device address hipGetSymbolAddress returns, taken once per device with that
+// device current.  Nothing in it needs clearing: every part (partial maxima,
+// activation codes and scales, segment table) is written before it is read.
+namespace {
+
+__device__ __align__(256) uint8_t scratch[REQAT_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device (nullptr on failure).
+void *scratch_on_current_device() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+        g_scratch[dev] = p;
+    }
+    return g_scratch[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+reqat_status reqat_linear_w4a4_noalloc(reqat_format fmt, int64_t M, int64_t N, int64_t K, const void *x,
+                                       int64_t ldx, float *x_tensor_scale, reqat_tscale_mode ts,
+                                       const uint8_t *w_codes, const uint8_t *w_scales,
+                                       const float *w_tensor_scale, void *y, reqat_dtype y_dtype, int64_t ldy,
+                                       void *stream) {
+    reqat_status st = check_linear(fmt, M, N, K, x, ldx, x_tensor_scale, ts, w_codes, w_scales, w_tensor_scale,
+                                   y, y_dtype, ldy);
+    if (st != REQAT_OK) return st;
+    if (reqat_linear_workspace_bytes(fmt, M, K) > (size_t)REQAT_NOALLOC_SCRATCH_BYTES) return REQAT_E_TOO_LARGE;
+    void *ws = scratch_on_current_device();
+    if (!ws) return REQAT_E_HIP;
+    return run_linear(fmt, M, N, K, x, ldx, x_tensor_scale, ts, w_codes, w_scales, w_tensor_scale, y, y_dtype,
+                      ldy, ws, stream);
+}
+
 const char *reqat_status_str(reqat_status s) {
     switch (s) {
     case REQAT_OK: return "REQAT_OK";
@@ -336,6 +418,7 @@ const char *reqat_status_str(reqat_status s) {
     case REQAT_E_ENUM: return "REQAT_E_ENUM: unknown format, dtype or tensor-scale mode";
     case REQAT_E_UNSUPPORTED: return "REQAT_E_UNSUPPORTED: combination not supported";
     case REQAT_E_HIP: return "REQAT_E_HIP: HIP launch failed";
+    case REQAT_E_TOO_LARGE: return "REQAT_E_TOO_LARGE: input exceeds the fixed scratch of the no-allocation entry point";
     }
     return "unknown reqat_status";
 }

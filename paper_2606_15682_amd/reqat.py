@@ -27,7 +27,8 @@ TS_COMPUTE = 0
 TS_GIVEN = 1
 
 STATUS = {0: "REQAT_OK", 1: "REQAT_E_NULL", 2: "REQAT_E_SHAPE", 3: "REQAT_E_ALIGN",
-          4: "REQAT_E_ENUM", 5: "REQAT_E_UNSUPPORTED", 6: "REQAT_E_HIP"}
+          4: "REQAT_E_ENUM", 5: "REQAT_E_UNSUPPORTED", 6: "REQAT_E_HIP", 7: "REQAT_E_TOO_LARGE"}
+NOALLOC_SCRATCH_BYTES = 8 << 20          # REQAT_NOALLOC_SCRATCH_BYTES
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libreqat.so")
 
@@ -45,6 +46,8 @@ SIGNATURES = {
     "reqat_linear_w4a4": (_INT, [_INT, _I64, _I64, _I64, _VP, _I64, _VP, _INT, _VP, _VP, _VP, _VP,
                                  _INT, _I64, _VP, _VP]),
     "reqat_linear_workspace_bytes": (ctypes.c_size_t, [_INT, _I64, _I64]),
+    "reqat_linear_w4a4_noalloc": (_INT, [_INT, _I64, _I64, _I64, _VP, _I64, _VP, _INT, _VP, _VP, _VP, _VP,
+                                         _INT, _I64, _VP]),
     "reqat_sem_loss": (_INT, [_VP, _I64, _I64, _I64, _VP, ctypes.c_float, ctypes.c_float, _VP, _VP, _VP, _VP]),
     "reqat_sem_loss_backward": (_INT, [_VP, _I64, _I64, _I64, _VP, _VP, _VP, ctypes.c_float, ctypes.c_float,
                                        _VP, _INT, _I64, _VP]),
@@ -151,6 +154,11 @@ def reqat_fakequant_mxfp4_rht(x, rows, cols, ldx, signs, y, ldy, stream):
 
 def reqat_linear_workspace_bytes(fmt, M, K) -> int:
     return load().reqat_linear_workspace_bytes(fmt, M, K)
+
+
+def reqat_linear_w4a4_noalloc(fmt, M, N, K, x, ldx, x_ts, ts, w_codes, w_scales, w_ts, y, y_dtype, ldy, stream):
+    return load().reqat_linear_w4a4_noalloc(fmt, M, N, K, x, ldx, x_ts, ts, w_codes, w_scales, w_ts, y,
+                                            y_dtype, ldy, stream)
 
 
 def reqat_workspace_bytes() -> int:

@@ -57,9 +57,9 @@ def test_library_imports_no_allocation_copy_or_sync(lib):
                          text=True, check=True).stdout
     imported = {s.split("@")[0] for s in re.findall(r"\sU\s(\S+)", out)}
     hip = {s for s in imported if s.lower().startswith(("hip", "__hip", "hsa"))}
-    allowed = {"hipLaunchKernel", "hipFuncSetAttribute", "hipGetDevice", "hipDeviceGetAttribute",
+    allowed = {"hipLaunchKernel", "hipFuncSetAttribute", "hipGetDevice", "hipDeviceGetAttribute", "hipGetSymbolAddress",
                "hipGetLastError", "__hipPushCallConfiguration", "__hipPopCallConfiguration",
-               "__hipRegisterFatBinary", "__hipRegisterFunction", "__hipUnregisterFatBinary"}
+               "__hipRegisterFatBinary", "__hipRegisterFunction", "__hipRegisterVar", "__hipUnregisterFatBinary"}
     assert hip <= allowed, sorted(hip - allowed)
     assert "hipLaunchKernel" in hip
 
@@ -67,7 +67,7 @@ def test_library_imports_no_allocation_copy_or_sync(lib):
 def test_small_queries(lib):
     assert reqat.reqat_abi_version() == 9
     assert reqat.reqat_workspace_bytes() == 4 * 4096 + 2 * (1 << 19)   # partials + segment table
-    for s in range(7):
+    for s in range(8):
         assert reqat.reqat_status_str(s).startswith(reqat.STATUS[s])
     assert "unknown" in reqat.reqat_status_str(99)
 
@@ -370,3 +370,30 @@ def test_binding_checks_workspace_sizes(trapped):
     _raises_before_device(lambda: reqat.gemm_w4a16(x, mc, _u8(5120, 16)), match="w_scales")
     _raises_before_device(lambda: reqat.gemm_w4a16(x, mc, ms, out=torch.zeros(16, 5120, dtype=torch.bfloat16)),
                           match="out")
+
+
+def lnn(fmt=NV, M=4, N=8, K=128, x=P, ldx=128, xg=P, ts=0, wc=P, ws_=P, wg=P, y=P, dt=0, ldy=8):
+    return reqat.reqat_linear_w4a4_noalloc(fmt, M, N, K, x, ldx, xg, ts, wc, ws_, wg, y, dt, ldy, None)
+
+
+def test_linear_noalloc_validation(lib):
+    """The no-allocation linear call validates like reqat_linear_w4a4 and refuses
+    inputs whose workspace would exceed its fixed scratch, before any HIP call."""
+    assert lnn(fmt=2) == E_ENUM
+    assert lnn(dt=9) == E_ENUM
+    assert lnn(M=-1) == E_SHAPE
+    assert lnn(K=64, ldx=64) == E_SHAPE
+    assert lnn(fmt=MX) == E_UNSUP
+    assert lnn(xg=None) == E_NULL
+    assert lnn(x=None) == E_NULL
+    assert lnn(x=P + 2) == E_ALIGN
+    cap = reqat.NOALLOC_SCRATCH_BYTES
+    for fmt, g in ((NV, P), (MX, None)):
+        K = 5120
+        M = 1
+        while reqat.reqat_linear_workspace_bytes(fmt, M + 1, K) <= cap:
+            M += 1
+        assert reqat.reqat_linear_workspace_bytes(fmt, M, K) <= cap
+        assert lnn(fmt=fmt, M=M + 1, K=K, ldx=K, xg=g, wg=g) == 7           # REQAT_E_TOO_LARGE
+        assert lnn(fmt=fmt, M=1 << 20, K=K, ldx=K, xg=g, wg=g) == 7
+    assert "no-allocation" in reqat.reqat_status_str(7)
