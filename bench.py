@@ -73,8 +73,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=4,
-                    help="workload number (4 = 14B gate/up; 2 = NVFP4 W4A4 decode; 6, 7 = MXFP4 W4A16 "
-                         "decode; 8 = SEM loss head; 9 = KV4 keys)")
+                    help="workload number (4 = 14B gate/up; 10 = the same shape in MXFP4; 5 = 32B down-proj "
+                         "MXFP4; 2 = NVFP4 W4A4 decode; 6, 7 = MXFP4 W4A16 decode; 8 = SEM loss head; "
+                         "9 = KV4 keys)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="skip timing the step as a HIP graph replay")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -107,6 +108,62 @@ def graph_step_ms(step, args) -> float:
     ev[1].record()
     torch.cuda.synchronize()
     return ev[0].elapsed_time(ev[1]) / args.steps
+
+
+MALL_DEFEAT_BYTES = 512 << 20       # twice the 256 MB Infinity Cache
+
+
+def n_copies(nbytes_one: int, args) -> int:
+    """Copies of a per-step operand to rotate through so that every timed step
+    reads bytes that are not in the Infinity Cache: more than 512 MB in all, and
+    enough that the timed steps never come back to a copy the warm-up touched."""
+    return max(-(-MALL_DEFEAT_BYTES // max(1, int(nbytes_one))), args.steps + args.warmup + 1)
+
+
+def timed_rotation(step, n, args):
+    """Eager steps over rotating copies (step(i) uses copy i % n): warm-up on
+    copies 0 .. W-1, then args.steps timed steps on copies W, W+1, ...; returns
+    (wall-clock ms per step, device ms per step from HIP events on the stream)."""
+    import torch
+    for i in range(args.warmup):
+        step(i % n)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record()
+    for i in range(args.steps):
+        step((args.warmup + i) % n)
+    ev[1].record()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / args.steps, ev[0].elapsed_time(ev[1]) / args.steps
+
+
+def graph_rotation_ms(step, n, args, replays: int = 3) -> float:
+    """Amortized device time per step: n consecutive steps (one per copy, so the
+    graph's working set exceeds the Infinity Cache) captured in one HIP graph,
+    replayed `replays` times after one untimed replay."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step(0)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(n):
+            step(i)
+    graph.replay()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(replays):
+        graph.replay()
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / (replays * n)
+    del graph
+    return ms
 
 
 def copy_calibration(nbytes: int, steps: int):
@@ -213,23 +270,26 @@ def bench_w4a16(args, w):
     M, N, K = w.M, w.N, w.K
     x_cpu, w_cpu = wl.make_x(w), wl.make_w(w)
     x = x_cpu.to(dev)
-    wc, ws, _ = reqat.quantize(w_cpu.to(dev), reqat.MXFP4)
+    wc0, ws0, _ = reqat.quantize(w_cpu.to(dev), reqat.MXFP4)
     y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
     wsp = torch.empty(max(1, reqat.reqat_w4a16_workspace_bytes(M, N, K)), dtype=torch.uint8, device=dev)
-    for _ in range(args.warmup):
-        reqat.gemm_w4a16(x, wc, ws, out_dtype=torch.bfloat16, out=y, ws=wsp)
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev[0].record()
-    for _ in range(args.steps):
-        reqat.gemm_w4a16(x, wc, ws, out_dtype=torch.bfloat16, out=y, ws=wsp)
-    ev[1].record()
-    torch.cuda.synchronize()
-    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
-    ms_kernel = ev[0].elapsed_time(ev[1]) / args.steps
     flops = 2.0 * M * N * K
     nbytes = N * K * (0.5 + 1.0 / 32) + M * K * 2.0 + M * N * 2.0       # W codes + scales, x, Y (bf16)
+    # rotate through copies of the weights (> 512 MB in all): every step streams them from HBM
+    ncp = n_copies(N * K * (0.5 + 1.0 / 32), args)
+    copies = [(wc0.clone(), ws0.clone()) for _ in range(ncp)]
+
+    def step(i):
+        wc, ws = copies[i]
+        reqat.gemm_w4a16(x, wc, ws, out_dtype=torch.bfloat16, out=y, ws=wsp)
+
+    # value: the product over the weight copies, ncp launches captured in one HIP
+    # graph (back to back, as a serving loop runs them), per launch
+    ms_eager, ms_eager_dev = timed_rotation(step, ncp, args)
+    ms_step = graph_rotation_ms(step, ncp, args)
+    ms_kernel = ms_step
+    # context: the same weights every step (they then sit in the Infinity Cache)
+    _, ms_resident = timed_rotation(lambda i: step(0), ncp, args)
     gbs = nbytes / (ms_kernel * 1e-3) / 1e9
     out = {
         "metric": METRIC,
@@ -246,12 +306,21 @@ def bench_w4a16(args, w):
         "data": "synthetic (seeded; Student-t or Gaussian-with-outlier activations, N(0,0.02) weights)",
         "config": {"workload": w.name, "M": M, "N": N, "K": K, "format": "mxfp4 weights, bf16 activations",
                    "gemm_out": "bf16", "global_batch": M, "parallelism": "single GPU",
-                   "step": "W4A16 GEMM (weights pre-quantized, untimed)"},
+                   "step": "W4A16 GEMM (weights pre-quantized, untimed), each step on another of %d weight "
+                           "copies (%.0f MB in all, twice the Infinity Cache), the %d steps captured in one "
+                           "HIP graph, time per step" % (ncp, ncp * N * K * (0.5 + 1.0 / 32) / 1e6, ncp)},
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK["hbm"], "unit": "GB/s",
                      "frac": round(gbs / PEAK["hbm"], 4), "traffic": None,
                      "kernel": "gemm_w4a16_kernel (MXFP4 W4A16, algorithmic bytes %d)" % int(nbytes)},
         "kernels": {"gemm_w4a16": {"ms": round(ms_kernel, 4), "GB/s": round(gbs, 1),
-                                   "TFLOP/s": round(flops / (ms_kernel * 1e-3) / 1e12, 2)}},
+                                   "TFLOP/s": round(flops / (ms_kernel * 1e-3) / 1e12, 2),
+                                   "note": "per launch in the graph, weights from HBM (rotating copies)"},
+                    "eager": {"ms": round(ms_eager, 4), "device_ms": round(ms_eager_dev, 4),
+                              "note": "context: eager launches from Python, wall clock and HIP-event time"},
+                    "cache_resident": {"ms": round(ms_resident, 4),
+                                       "GB/s": round(nbytes / (ms_resident * 1e-3) / 1e9, 1),
+                                       "note": "context only: the same weights every step (Infinity-Cache "
+                                               "resident after the first)"}},
     }
     out["ceilings"] = practical_ceilings()
     if not args.no_cpu_baseline:
@@ -292,44 +361,38 @@ def bench_decode(args, w):
     M, N, K = w.M, w.N, w.K
     x_cpu, w_cpu = wl.make_x(w), wl.make_w(w)
     x = x_cpu.to(dev)
-    wc, wsc, gw = reqat.quantize(w_cpu.to(dev), fmt)
+    wc0, wsc0, gw = reqat.quantize(w_cpu.to(dev), fmt)
     y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
     gl = torch.empty(1, dtype=torch.float32, device=dev) if fmt == reqat.NVFP4 else None
     lws = torch.empty(reqat.reqat_linear_workspace_bytes(fmt, M, K), dtype=torch.uint8, device=dev)
-
-    def step():
-        reqat.linear(x, fmt, wc, wsc, gw, out_dtype=torch.bfloat16, out=y, g_out=gl, ws=lws)
-
-    for _ in range(args.warmup):
-        step()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev[0].record()
-    for _ in range(args.steps):
-        step()
-    ev[1].record()
-    torch.cuda.synchronize()
-    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
-    ms_dev = ev[0].elapsed_time(ev[1]) / args.steps
-    graph_ms = None if args.no_graph else graph_step_ms(step, args)
-
-    # the product alone (activation codes from one quantize), timed apart
-    xc, xs, gx = reqat.quantize(x, fmt)
-    ms_gemm = None
-    for _ in range(max(1, args.warmup)):
-        reqat.gemm(fmt, xc, xs, gx, wc, wsc, gw, out_dtype=torch.bfloat16, out=y)
-    torch.cuda.synchronize()
-    ev[0].record()
-    for _ in range(args.steps):
-        reqat.gemm(fmt, xc, xs, gx, wc, wsc, gw, out_dtype=torch.bfloat16, out=y)
-    ev[1].record()
-    torch.cuda.synchronize()
-    ms_gemm = ev[0].elapsed_time(ev[1]) / args.steps
-
     w_bytes = N * K * (0.5 + 1.0 / B)
     step_bytes = w_bytes + M * K * 2.0 + M * N * 2.0              # weights once, x read, Y (bf16)
     gemm_bytes = w_bytes + M * K * (0.5 + 1.0 / B) + M * N * 2.0  # weights once, x codes, Y (bf16)
+    # rotate through copies of the quantized weights (> 512 MB in all): every
+    # step streams its weights from HBM, as a model's layers do
+    ncp = n_copies(w_bytes, args)
+    copies = [(wc0.clone(), wsc0.clone()) for _ in range(ncp)]
+
+    def step(i):
+        wc, wsc = copies[i]
+        reqat.linear(x, fmt, wc, wsc, gw, out_dtype=torch.bfloat16, out=y, g_out=gl, ws=lws)
+
+    # A decode step is a few microseconds of device work, less than one eager
+    # launch from Python costs: steps run back to back only when captured, as a
+    # serving loop captures them.  value = the step captured ncp times in one HIP
+    # graph (each on its own weight copy), per step; eager launches are context.
+    ms_eager, ms_dev = timed_rotation(step, ncp, args)
+    ms_step = graph_rotation_ms(step, ncp, args)
+    _, ms_resident = timed_rotation(lambda i: step(0), ncp, args)
+
+    # the product alone (activation codes from one quantize), timed apart, also over the copies
+    xc, xs, gx = reqat.quantize(x, fmt)
+
+    def gemm_step(i):
+        wc, wsc = copies[i]
+        reqat.gemm(fmt, xc, xs, gx, wc, wsc, gw, out_dtype=torch.bfloat16, out=y)
+
+    ms_gemm = graph_rotation_ms(gemm_step, ncp, args)
     gbs_gemm = gemm_bytes / (ms_gemm * 1e-3) / 1e9
     out = {
         "metric": METRIC,
@@ -347,26 +410,26 @@ def bench_decode(args, w):
         "config": {"workload": w.name, "M": M, "N": N, "K": K, "format": w.fmt, "gemm_out": "bf16",
                    "global_batch": M, "parallelism": "single GPU",
                    "step": "quantize X + W4A4 GEMM in one reqat_linear_w4a4 call (weights quantized once, "
-                           "untimed)"},
+                           "untimed), each step on another of %d weight copies (%.0f MB in all, twice the "
+                           "Infinity Cache); the %d steps captured in one HIP graph, time per step"
+                           % (ncp, ncp * w_bytes / 1e6, ncp)},
         "roofline": {"bound": "hbm", "achieved": round(gbs_gemm, 1), "peak": PEAK["hbm"], "unit": "GB/s",
                      "frac": round(gbs_gemm / PEAK["hbm"], 4), "traffic": None,
                      "kernel": "gemm_skinny_kernel (%s W4A4 GEMM, M <= 64; algorithmic bytes %d)"
                                % (w.fmt, int(gemm_bytes))},
-        "kernels": {"linear_step": {"ms": round(ms_dev, 4),
-                                    "GB/s": round(step_bytes / (ms_dev * 1e-3) / 1e9, 1),
-                                    "note": "device time of the step (quantize X kernels + product)"},
+        "kernels": {"linear_step_eager": {"ms": round(ms_eager, 4), "device_ms": round(ms_dev, 4),
+                                          "GB/s": round(step_bytes / (ms_eager * 1e-3) / 1e9, 1),
+                                          "note": "context: eager launches from Python (bound by the launch "
+                                                  "rate); wall clock and HIP-event time per step"},
                     "gemm": {"ms": round(ms_gemm, 4), "GB/s": round(gbs_gemm, 1),
                              "TFLOP/s": round(2.0 * M * N * K / (ms_gemm * 1e-3) / 1e12, 2),
-                             "note": "product alone, timed apart"}},
-        "note": ("the same weights are re-read every step, so they sit in the 256 MB Infinity Cache: "
-                 "a cache-resident rate, an upper bound for weights streamed from HBM"),
+                             "note": "product alone over the weight copies, %d launches in one HIP graph, "
+                                     "per launch (HIP events around the replays)" % ncp},
+                    "cache_resident_step": {"ms": round(ms_resident, 4),
+                                            "GB/s": round(step_bytes / (ms_resident * 1e-3) / 1e9, 1),
+                                            "note": "context only: the same weights every step (Infinity-Cache "
+                                                    "resident after the first)"}},
     }
-    if graph_ms is not None:
-        out["kernels"]["graph_step"] = {
-            "ms": round(graph_ms, 4), "GB/s": round(step_bytes / (graph_ms * 1e-3) / 1e9, 1),
-            "note": "the same step captured once in a HIP graph and replayed (events around the replays); "
-                    "at this size the graph launch costs more than the eager launches it replaces; value "
-                    "and ms_per_step use the eager launches"}
     out["ceilings"] = practical_ceilings()
     if not args.no_cpu_baseline:
         import oracle
@@ -404,7 +467,11 @@ def bench_kv4(args, w):
     torch.cuda.set_device(dev)
     T, C = w.M, w.K
     k_cpu, mu_cpu = wl.make_keys(w)
-    k, mu = k_cpu.to(dev), mu_cpu.to(dev)
+    k0, mu = k_cpu.to(dev), mu_cpu.to(dev)
+    # rotate through copies of the keys (> 512 MB in all): every step reads them from HBM
+    ncp = n_copies(T * C * 2, args)
+    keys = [k0.clone() for _ in range(ncp)]
+    k = k0
     codes = torch.empty((T, C // 2), dtype=torch.uint8, device=dev)
     scales = torch.empty((T, C // 16), dtype=torch.uint8, device=dev)
     g = torch.empty(1, dtype=torch.float32, device=dev)
@@ -423,10 +490,13 @@ def bench_kv4(args, w):
         torch.cuda.synchronize()
         return (time.perf_counter() - t0) * 1e3 / args.steps, e[0].elapsed_time(e[1]) / args.steps
 
-    ms_step, ms_q = timed(lambda: reqat.quantize_kv4(k, mu, out=(codes, scales), g_out=g))
+    ms_step, ms_q = timed_rotation(lambda i: reqat.quantize_kv4(keys[i], mu, out=(codes, scales), g_out=g),
+                                   ncp, args)
     gq = g.clone()
-    _, ms_given = timed(lambda: reqat.quantize_kv4(k, mu, tensor_scale=gq, out=(codes, scales)))
-    _, ms_fq = timed(lambda: reqat.fakequant_kv4(k, mu, out=fq, g_out=g))
+    _, ms_given = timed_rotation(lambda i: reqat.quantize_kv4(keys[i], mu, tensor_scale=gq, out=(codes, scales)),
+                                 ncp, args)
+    _, ms_fq = timed_rotation(lambda i: reqat.fakequant_kv4(keys[i], mu, out=fq, g_out=g), ncp, args)
+    _, ms_resident = timed(lambda: reqat.quantize_kv4(k, mu, out=(codes, scales), g_out=g))
     q_bytes = T * C * (2 + 0.5 + 1.0 / 16)                        # read keys, write codes + scales
     fq_bytes = T * C * 4.0
     gbs = lambda b, ms: b / (ms * 1e-3) / 1e9
@@ -445,13 +515,18 @@ def bench_kv4(args, w):
         "data": "synthetic (seeded; N(0,1) keys plus per-channel offsets N(0,2), the offsets given as the shift)",
         "config": {"workload": w.name, "tokens": T, "channels": C, "global_batch": T,
                    "parallelism": "single GPU",
-                   "step": "KV4 quantize of keys - shift (computed tensor scale: absmax pass + quantize)"},
+                   "step": "KV4 quantize of keys - shift (computed tensor scale: absmax pass + quantize), each "
+                           "step on another of %d key copies (%.0f MB in all, twice the Infinity Cache)"
+                           % (ncp, ncp * T * C * 2 / 1e6)},
         "roofline": {"bound": "hbm", "achieved": round(gbs(q_bytes, ms_q), 1), "peak": PEAK["hbm"],
                      "unit": "GB/s", "frac": round(gbs(q_bytes, ms_q) / PEAK["hbm"], 4), "traffic": None,
                      "kernel": "kv4_absmax_kernel + kv4_quantize_kernel (algorithmic bytes %d)" % int(q_bytes)},
         "kernels": {"quantize_kv4_computed_g": {"ms": round(ms_q, 4), "GB/s": round(gbs(q_bytes, ms_q), 1)},
                     "quantize_kv4_given_g": {"ms": round(ms_given, 4), "GB/s": round(gbs(q_bytes, ms_given), 1)},
-                    "fakequant_kv4_computed_g": {"ms": round(ms_fq, 4), "GB/s": round(gbs(fq_bytes, ms_fq), 1)}},
+                    "fakequant_kv4_computed_g": {"ms": round(ms_fq, 4), "GB/s": round(gbs(fq_bytes, ms_fq), 1)},
+                    "cache_resident_computed_g": {"ms": round(ms_resident, 4),
+                                                  "GB/s": round(gbs(q_bytes, ms_resident), 1),
+                                                  "note": "context only: the same keys every step"}},
     }
     out["ceilings"] = practical_ceilings()
     if not args.no_cpu_baseline:

@@ -67,6 +67,9 @@ WORKLOADS = {
     # SEM loss head of QAT: M tokens x N vocabulary logits (Qwen-family vocabulary)
     8: Workload(8, "SEM loss head 4096 tokens x 152064 vocabulary", NVFP4, 4096, 152064, 0,
                 "normal", 0, 3.0, "sem"),
+    # the 14B-like gate/up shape of workload 4 in MXFP4 (E8M0 scales feed the FP4 matrix cores directly)
+    10: Workload(10, "MXFP4 gate/up 14B-like 4096x27648x5120", MXFP4, 4096, 27648, 5120,
+                 "normal_outliers", 51, 0.02),
     # KV4 cache: post-RoPE keys of one 14B-like layer (8 KV heads x 128 channels) over a
     # 32768-token prefill, M tokens x K channels
     9: Workload(9, "KV4 keys 14B-like 32768 tokens x 1024 channels", NVFP4, 32768, 0, 1024,

@@ -149,6 +149,16 @@ def test_fullsize_7b_qkv_linear():
         log("  linear %s: workspace codes bit-exact, sampled product ok" % dt)
 
 
+def test_fullsize_14b_gate_up_mxfp4():
+    """The 14B-like gate/up shape (4096 x 27648 x 5120) in MXFP4: full quantize
+    of X and W bit-exact, the product on sampled outputs (both output types)."""
+    w = wl.WORKLOADS[10]
+    log("full-size workload 10: %s" % w.name)
+    fmt, ofmt, q = _quant_both(w)
+    _check_gemm(w, fmt, ofmt, q, torch.bfloat16, seed=40)
+    _check_gemm(w, fmt, ofmt, q, torch.float32, seed=41, npts=1000)
+
+
 def test_fullsize_32b_down_mxfp4():
     w = wl.WORKLOADS[5]
     log("full-size workload 5: %s" % w.name)
