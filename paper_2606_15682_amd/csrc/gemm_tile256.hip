@@ -608,39 +608,53 @@ __device__ __forceinline__ uint32_t mx_scale_read(const uint8_t *p) {
     else return *reinterpret_cast<const uint16_t *>(p);
 }
 
-// Part K of substep S of a stage: the 4 MFMAs of A tile K, the reads of A
-// tile K's and B tile K's operands for the next substep (and, in the last
-// substep, the next stage's scale bytes for them), and, in the last substep,
-// a quarter of the loads of the stage NB later: they go out right after the
-// barrier that frees its buffer, one per MFMA, which leaves them the most time.
+// Part K of substep S of a stage: the 4 MFMAs of A tile K, reads of operands
+// for the next substep (in the last substep, of the next stage's first one,
+// with its scale bytes), and, in the last substep, a quarter of the loads of
+// the stage NB later: they go out right after the barrier that frees its
+// buffer, one per MFMA, which leaves them the most time.
+// The next substep's first part multiplies A tile 0 by all four B tiles, so
+// the B tiles are read first (parts 0 and 1, two each, with A tiles 0 and 1)
+// and A tiles 2 and 3 after them: every operand is read at least 15 MFMAs
+// (about 480 cycles) before its use.  Reading B tile K in part K left B tile
+// 3 only 4 MFMAs ahead of its first use, under the LDS latency.
 template <class C, int S, int NS, int K, class Issue>
 __device__ __forceinline__ void mx_part(v16f (&acc)[4][4], MxState<C> &st, const uint8_t *buf,
                                         const uint8_t *nbuf, const uint8_t *nsc, const MxLane<C> &ln,
                                         Issue &next) {
     constexpr int E = S & 1, LAST = S == NS - 1;
-    constexpr int ND = LAST ? 4 : 2;
+    constexpr int NB_ = K < 2 ? 2 : 0;                  // B tiles read in this part: 2K, 2K + 1
+    constexpr int ND = (1 + NB_) * (LAST ? 2 : 1);      // LDS reads in this part (operands, scale words)
     constexpr int NG = LAST ? Issue::template count<K, 4>() : 0;
+    const uint8_t *src = LAST ? nbuf : buf;
+    const int q = LAST ? 0 : (S + 1 < NS ? S + 1 : 0);
     __builtin_amdgcn_sched_barrier(0);
-    if constexpr (!LAST) {
-        st.a[E ^ 1][K] = lds16(buf + ln.codeA[S + 1] + 32 * C::ROW * K);
-        st.b[E ^ 1][K] = lds16(buf + ln.codeB[S + 1] + 32 * C::ROW * K);
-    } else {
-        st.a[E ^ 1][K] = lds16(nbuf + ln.codeA[0] + 32 * C::ROW * K);
-        st.b[E ^ 1][K] = lds16(nbuf + ln.codeB[0] + 32 * C::ROW * K);
+    st.a[E ^ 1][K] = lds16(src + ln.codeA[q] + 32 * C::ROW * K);
+    if constexpr (NB_) {
+        st.b[E ^ 1][2 * K] = lds16(src + ln.codeB[q] + 32 * C::ROW * (2 * K));
+        st.b[E ^ 1][2 * K + 1] = lds16(src + ln.codeB[q] + 32 * C::ROW * (2 * K + 1));
+    }
+    if constexpr (LAST) {
         st.na[K] = mx_scale_read<C>(nsc + ln.scA + MxLane<C>::SCSTEP * K);
-        st.nb[K] = mx_scale_read<C>(nsc + ln.scB + MxLane<C>::SCSTEP * K);
+        if constexpr (NB_) {
+            st.nb[2 * K] = mx_scale_read<C>(nsc + ln.scB + MxLane<C>::SCSTEP * (2 * K));
+            st.nb[2 * K + 1] = mx_scale_read<C>(nsc + ln.scB + MxLane<C>::SCSTEP * (2 * K + 1));
+        }
     }
     if constexpr (LAST) next.template region<K, 4>();
 #pragma unroll
     for (int j = 0; j < 4; ++j)
         acc[K][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
             as_v8i(st.a[E][K]), as_v8i(st.b[E][j]), acc[K][j], 4, 4, S, (int)st.sa[K], S, (int)st.sb[j]);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
+    static_for<0, 4>([&](auto KK) {
+        constexpr int k = decltype(KK)::value;
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // one MFMA
-        if (k < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);       // one LDS read
-        if (k < NG) __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);       // one load
-    }
+        // the part's LDS reads spread over its four MFMAs, the earliest first
+        constexpr int per = (ND + 3) / 4;
+        constexpr int nr = (k + 1) * per <= ND ? per : (k * per < ND ? ND - k * per : 0);
+        if constexpr (nr > 0) __builtin_amdgcn_sched_group_barrier(0x100, nr, 0);
+        if constexpr (k < NG) __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);       // one load
+    });
     // keep the part's MFMAs in it (they would otherwise be sunk past the
     // stage's barrier and branches)
 #pragma unroll
