@@ -218,9 +218,32 @@ def practical_ceilings(x=None, wt=None, steps=10):
     return out
 
 
+class pinned_to_one_core:
+    """Runs the enclosed oracle timing on one host core (the affinity of
+    taskset -c <core>), restoring the process's affinity afterwards."""
+
+    def __enter__(self):
+        self.saved = os.sched_getaffinity(0)
+        self.core = min(self.saved)
+        os.sched_setaffinity(0, {self.core})
+        return self
+
+    def __exit__(self, *exc):
+        os.sched_setaffinity(0, self.saved)
+        return False
+
+
 def cpu_baseline(w, xb, wb):
-    """Time the CPU oracle (single thread, as it stands) on a bounded sample of
-    the same step and scale its per-element / per-MAC rates to the full step."""
+    """Time the CPU oracle (single thread, as it stands, pinned to one core) on
+    a bounded sample of the same step and scale its per-element / per-MAC rates
+    to the full step."""
+    with pinned_to_one_core() as pin:
+        out = _cpu_baseline(w, xb, wb)
+    out["pinned_core"] = pin.core
+    return out
+
+
+def _cpu_baseline(w, xb, wb):
     import numpy as np
     import oracle
     fmt = oracle.FMT_NVFP4 if w.fmt == "nvfp4" else oracle.FMT_MXFP4
@@ -324,21 +347,22 @@ def bench_w4a16(args, w):
     }
     out["ceilings"] = practical_ceilings()
     if not args.no_cpu_baseline:
-        import oracle
-        xb, wb = wl.bf16_bits(x_cpu), wl.bf16_bits(w_cpu)
-        owc, ows, _ = oracle.quantize(oracle.FMT_MXFP4, wb[:64])
-        npts = int(5e8 // K)                        # about 10 s of single-thread CPU work
-        ms_, ns_ = np.arange(npts) % M, np.arange(npts) % 64
-        t0 = time.perf_counter()
-        oracle.gemm_w4a16_points(xb, owc, ows, ms_, ns_)
-        dt = time.perf_counter() - t0
-        per_mac = dt / (npts * K)
-        full = per_mac * M * N * K
-        out["cpu_baseline"] = {
-            "value": round(nbytes / full / 1e9, 6), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": ("FP64 W4A16 oracle on %d output points (each a %d-term dot product), per-MAC "
-                       "rate scaled to the full product and credited with its bytes (%.2f s of CPU work)"
-                       % (npts, K, dt))}
+        with pinned_to_one_core():
+            import oracle
+            xb, wb = wl.bf16_bits(x_cpu), wl.bf16_bits(w_cpu)
+            owc, ows, _ = oracle.quantize(oracle.FMT_MXFP4, wb[:64])
+            npts = int(5e8 // K)                        # about 10 s of single-thread CPU work
+            ms_, ns_ = np.arange(npts) % M, np.arange(npts) % 64
+            t0 = time.perf_counter()
+            oracle.gemm_w4a16_points(xb, owc, ows, ms_, ns_)
+            dt = time.perf_counter() - t0
+            per_mac = dt / (npts * K)
+            full = per_mac * M * N * K
+            out["cpu_baseline"] = {
+                "value": round(nbytes / full / 1e9, 6), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                "sample": ("FP64 W4A16 oracle on %d output points (each a %d-term dot product), per-MAC "
+                           "rate scaled to the full product and credited with its bytes (%.2f s of CPU work)"
+                           % (npts, K, dt))}
     print(json.dumps(out), flush=True)
 
 
@@ -432,23 +456,24 @@ def bench_decode(args, w):
     }
     out["ceilings"] = practical_ceilings()
     if not args.no_cpu_baseline:
-        import oracle
-        ofmt = oracle.FMT_NVFP4 if fmt == reqat.NVFP4 else oracle.FMT_MXFP4
-        xb, wb = wl.bf16_bits(x_cpu), wl.bf16_bits(w_cpu)
-        t0 = time.perf_counter()
-        owc, ows, owg = oracle.quantize(ofmt, wb[:256])
-        oxc, oxs, oxg = oracle.quantize(ofmt, xb)
-        n = 0
-        while time.perf_counter() - t0 < 10.0:
-            oracle.gemm(ofmt, oxc, oxs, oxg, owc, ows, owg)
-            n += 1
-        dt = time.perf_counter() - t0
-        per_row = dt / (n * 256)                      # seconds per weight row of the product (+ quantize share)
-        full = per_row * N
-        out["cpu_baseline"] = {
-            "value": round(step_bytes / full / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": ("oracle quantize of X and of 256 weight rows, then the FP64 product against those "
-                       "rows repeated for ~10 s (%d passes); per-row rate scaled to all %d rows" % (n, N))}
+        with pinned_to_one_core():
+            import oracle
+            ofmt = oracle.FMT_NVFP4 if fmt == reqat.NVFP4 else oracle.FMT_MXFP4
+            xb, wb = wl.bf16_bits(x_cpu), wl.bf16_bits(w_cpu)
+            t0 = time.perf_counter()
+            owc, ows, owg = oracle.quantize(ofmt, wb[:256])
+            oxc, oxs, oxg = oracle.quantize(ofmt, xb)
+            n = 0
+            while time.perf_counter() - t0 < 10.0:
+                oracle.gemm(ofmt, oxc, oxs, oxg, owc, ows, owg)
+                n += 1
+            dt = time.perf_counter() - t0
+            per_row = dt / (n * 256)                      # seconds per weight row of the product (+ quantize share)
+            full = per_row * N
+            out["cpu_baseline"] = {
+                "value": round(step_bytes / full / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                "sample": ("oracle quantize of X and of 256 weight rows, then the FP64 product against those "
+                           "rows repeated for ~10 s (%d passes); per-row rate scaled to all %d rows" % (n, N))}
     print(json.dumps(out), flush=True)
 
 
@@ -530,20 +555,21 @@ def bench_kv4(args, w):
     }
     out["ceilings"] = practical_ceilings()
     if not args.no_cpu_baseline:
-        import oracle
-        rows = 2048
-        kb = wl.bf16_bits(k_cpu[:rows])
-        t0 = time.perf_counter()
-        n = 0
-        while time.perf_counter() - t0 < 10.0:
-            oracle.kv4_quantize(kb, mu_cpu.numpy())
-            n += 1
-        dt = (time.perf_counter() - t0) / n
-        out["cpu_baseline"] = {
-            "value": round(rows * C * (2 + 0.5 + 1.0 / 16) / dt / 1e9, 4), "unit": "GB/s", "cores": 1,
-            "kind": "oracle",
-            "sample": "oracle KV4 quantize (computed g) of %d of the %d token rows, repeated for ~10 s (%d passes), "
-                      "credited with the same bytes per row as the GPU step" % (rows, T, n)}
+        with pinned_to_one_core():
+            import oracle
+            rows = 2048
+            kb = wl.bf16_bits(k_cpu[:rows])
+            t0 = time.perf_counter()
+            n = 0
+            while time.perf_counter() - t0 < 10.0:
+                oracle.kv4_quantize(kb, mu_cpu.numpy())
+                n += 1
+            dt = (time.perf_counter() - t0) / n
+            out["cpu_baseline"] = {
+                "value": round(rows * C * (2 + 0.5 + 1.0 / 16) / dt / 1e9, 4), "unit": "GB/s", "cores": 1,
+                "kind": "oracle",
+                "sample": "oracle KV4 quantize (computed g) of %d of the %d token rows, repeated for ~10 s (%d passes), "
+                          "credited with the same bytes per row as the GPU step" % (rows, T, n)}
     print(json.dumps(out), flush=True)
 
 
@@ -612,21 +638,22 @@ def bench_sem(args, w):
     }
     out["ceilings"] = practical_ceilings()
     if not args.no_cpu_baseline:
-        import oracle
-        rows = 64
-        zb = wl.bf16_bits(z_cpu[:rows])
-        t0 = time.perf_counter()
-        n = 0
-        while time.perf_counter() - t0 < 10.0:
-            H, nll, lse = oracle.sem_row_stats(zb, t_cpu[:rows].numpy())
-            _, _, _, wts = oracle.sem_loss(H, nll, lam, 1e-6)
-            oracle.sem_grad(zb, t_cpu[:rows].numpy(), H, lse, wts, lam)
-            n += 1
-        dt = (time.perf_counter() - t0) / n
-        out["cpu_baseline"] = {
-            "value": round(rows * V * 6.0 / dt / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": "FP64 numpy oracle: loss and gradient of %d of the %d token rows, repeated for ~10 s "
-                      "(%d passes), credited with the same bytes per row as the GPU step" % (rows, T, n)}
+        with pinned_to_one_core():
+            import oracle
+            rows = 64
+            zb = wl.bf16_bits(z_cpu[:rows])
+            t0 = time.perf_counter()
+            n = 0
+            while time.perf_counter() - t0 < 10.0:
+                H, nll, lse = oracle.sem_row_stats(zb, t_cpu[:rows].numpy())
+                _, _, _, wts = oracle.sem_loss(H, nll, lam, 1e-6)
+                oracle.sem_grad(zb, t_cpu[:rows].numpy(), H, lse, wts, lam)
+                n += 1
+            dt = (time.perf_counter() - t0) / n
+            out["cpu_baseline"] = {
+                "value": round(rows * V * 6.0 / dt / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                "sample": "FP64 numpy oracle: loss and gradient of %d of the %d token rows, repeated for ~10 s "
+                          "(%d passes), credited with the same bytes per row as the GPU step" % (rows, T, n)}
     print(json.dumps(out), flush=True)
 
 

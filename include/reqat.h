@@ -68,22 +68,31 @@ extern "C" {
 
 #define REQAT_ABI_VERSION 9
 
-typedef enum {
+/* The enums travel as C ints.  Compiled as C++ they get int as their fixed
+ * underlying type, so any int a caller passes is a value the library may
+ * read and reject (REQAT_E_ENUM) without undefined behaviour. */
+#ifdef __cplusplus
+#define REQAT_ENUM(tag) enum tag : int
+#else
+#define REQAT_ENUM(tag) enum tag
+#endif
+
+typedef REQAT_ENUM(reqat_format_e) {
     REQAT_FMT_NVFP4 = 0, /* B = 16, E4M3 block scale, FP32 global scale */
     REQAT_FMT_MXFP4 = 1  /* B = 32, E8M0 block scale */
 } reqat_format;
 
-typedef enum {
+typedef REQAT_ENUM(reqat_dtype_e) {
     REQAT_DT_F32 = 0,
     REQAT_DT_BF16 = 1
 } reqat_dtype;
 
-typedef enum {
+typedef REQAT_ENUM(reqat_tscale_mode_e) {
     REQAT_TS_COMPUTE = 0, /* library computes g from the tensor and writes *tensor_scale */
     REQAT_TS_GIVEN = 1    /* *tensor_scale holds the caller's g (finite, > 0) */
 } reqat_tscale_mode;
 
-typedef enum {
+typedef REQAT_ENUM(reqat_status_e) {
     REQAT_OK = 0,
     REQAT_E_NULL = 1,        /* a required pointer is NULL */
     REQAT_E_SHAPE = 2,       /* negative size, cols/K not a multiple of the block, ld too small */
