@@ -17,6 +17,11 @@ constexpr int kMaxPartials = REQAT_MAX_PARTIALS;
 // Segment-table capacity of the quantize workspace (segments of 64 blocks).
 constexpr int64_t kMaxSegments = int64_t(1) << 19;
 
+// Tensors of at most this many elements are small enough for every workgroup
+// to read whole (<= 128 KB): their NVFP4 global scale is computed in one launch
+// (kGLocal).
+constexpr int64_t kLocalMaxElems = int64_t(1) << 16;
+
 // Format selector shared by the launchers (same values as the C ABI enum).
 enum Fmt : int { kNV = 0, kMX = 1 };
 

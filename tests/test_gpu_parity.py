@@ -709,7 +709,10 @@ def test_gemm_k_zero_writes_zeros():
 
 @pytest.mark.parametrize("fmt", [NV, MX])
 @pytest.mark.parametrize("M,N,K,given", [(16, 256, 256, False), (5, 300, 128, False),
-                                         (300, 520, 768, False), (257, 256, 2048, True)])
+                                         (300, 520, 768, False), (257, 256, 2048, True),
+                                         (16, 8960, 1536, False), (16, 1000, 1536, True),
+                                         (64, 300, 1024, False), (33, 130, 1920, False),
+                                         (1, 17, 128, False), (48, 64, 1280, True), (64, 96, 1152, False)])
 def test_linear_parity(fmt, M, N, K, given):
     """reqat_linear_w4a4 = quantize X (same codes, scales and g as reqat_quantize_fp4,
     checked against the oracle) followed by the product, to the GEMM bar."""
@@ -743,6 +746,42 @@ def test_linear_parity(fmt, M, N, K, given):
     assert np.array_equal(outs[0], outs[1], equal_nan=True), "poison visible or nondeterministic"
     ms, ns = np.arange(M).repeat(N), np.tile(np.arange(N), M)
     check_gemm_points(fmt, ac, as_, ga, bc, bs, gb, outs[0], outs[2], ms, ns)
+
+
+@pytest.mark.parametrize("fmt", [NV, MX])
+@pytest.mark.parametrize("M,K,given", [(16, 1536, False), (16, 1536, True), (64, 1024, False), (7, 2944, False)])
+def test_decode_linear_equals_two_launch_path(fmt, M, K, given):
+    """The linear call on decode-sized activations: its outputs, the activation
+    codes and scales it leaves in its workspace, and g are bitwise those of
+    quantize() then gemm(), also with NaN blocks, an all-zero row, subnormal and
+    huge values."""
+    log("decode linear vs two launches fmt=%d M=%d K=%d given=%s" % (fmt, M, K, given))
+    N = 700
+    xa = _rand(M, K, 91 + M, "student_t", outliers=max(1, K // 100))
+    xa[M // 2, 5] = 0x7FC0
+    xa[M - 1, :] = 0x8000
+    xa[0, 40:48] = 0x0003
+    xa[0, 64] = 0x7F7F
+    xb = _rand(N, K, 92, "normal", std=0.02)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    bc, bs, gb = oracle.quantize(fmt, xb)
+    wg = None if fmt == MX else torch.tensor([gb], dtype=torch.float32, device=DEV)
+    gx = None if not (given and fmt == NV) else torch.tensor([0.03125], dtype=torch.float32, device=DEV)
+    x = wl.from_bits(xa).to(DEV)
+    for dt in (torch.float32, torch.bfloat16):
+        ws = torch.full((reqat.reqat_linear_workspace_bytes(fmt, M, K),), 0xCD, dtype=torch.uint8, device=DEV)
+        y1 = torch.full((M, N), float("nan"), dtype=dt, device=DEV)
+        _, g1 = reqat.linear(x, fmt, t(bc), t(bs), wg, x_tensor_scale=gx, out_dtype=dt, out=y1, ws=ws)
+        xc, xs, g2 = reqat.quantize(x, fmt, tensor_scale=gx)
+        y2 = torch.full((M, N), float("nan"), dtype=dt, device=DEV)
+        reqat.gemm(fmt, xc, xs, g2, t(bc), t(bs), wg, out_dtype=dt, out=y2)
+        torch.cuda.synchronize()
+        c1, s1 = reqat.linear_workspace_views(ws, fmt, M, K)
+        assert torch.equal(c1, xc) and torch.equal(s1, xs)
+        if fmt == NV:
+            assert float(g1.cpu()[0]) == float(g2.cpu()[0])
+        iv = torch.int32 if dt == torch.float32 else torch.int16
+        assert torch.equal(y1.view(iv), y2.view(iv)), "outputs differ"
 
 
 # ------------------------------------------------------- strided operands
