@@ -203,8 +203,9 @@ reqat_status reqat_fakequant_mxfp4_rht(const void *x, int64_t rows, int64_t cols
  *              (4-byte aligned; may be NULL when that is 0): FP32 partial sums
  *              when K is split over several workgroups (few weight rows).
  * Requirements: K % 128 == 0.  M == 0 or N == 0 is a no-op; K == 0 writes zeros.
- * Designed for decode (small M): one pass over the weights.  The result does
- * not depend on the split (partial sums are added in a fixed order).
+ * Designed for decode (small M): one pass over the weights.  The result is
+ * deterministic: the split is a function of (M, N, K) alone and the partial
+ * sums are added in a fixed order.
  */
 reqat_status reqat_gemm_w4a16(int64_t M, int64_t N, int64_t K, const void *x, int64_t ldx,
                               const uint8_t *w_codes, const uint8_t *w_scales, void *y, reqat_dtype y_dtype,

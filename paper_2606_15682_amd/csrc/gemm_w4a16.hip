@@ -47,11 +47,13 @@ typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 #define REQAT_W16_DEPTH1 4
 #endif
 #ifndef REQAT_W16_TARGET
-#define REQAT_W16_TARGET 512
+#define REQAT_W16_TARGET 1024
+#endif
+#ifndef REQAT_W16_XG
+#define REQAT_W16_XG 4
 #endif
 
 constexpr int kThreads = 256;          // four waves
-constexpr int kXPitch = 128 + 8;       // LDS row pitch of an x chunk, bfloat16 elements
 constexpr int kMaxSplits = REQAT_W16_KSMAX;
 
 // Calls f(integral_constant<int, J>) for J = B .. E-1, unrolled at compile time.
@@ -81,18 +83,19 @@ __device__ __forceinline__ v8bf decode_step(const v4u &w, uint32_t sb, int s) {
 }
 
 // A workgroup owns 64*NT weight rows (16*NT per wave, NT MFMA column tiles)
-// and 16*MT activation rows and walks the K chunks [nch*ks/KS, nch*(ks+1)/KS)
-// of its split ks = blockIdx.y.  Each 128-element chunk of the activation
-// rows is loaded once per workgroup (16 bytes per thread per 16-row tile),
-// stored to LDS and read by all four waves; each LDS fragment feeds NT
-// MFMAs.  With one split the results go to y; otherwise to the FP32 partial
+// and 16*MT activation rows and walks the K chunks of its split ks =
+// blockIdx.y (whole chunk pairs, balanced over the splits).  Each 128-element
+// chunk of the activation rows is loaded once per workgroup (16 bytes per
+// thread per 16-row tile), stored to LDS and read by all four waves; each LDS
+// fragment feeds NT MFMAs.  With one split the results go to y; otherwise to the FP32 partial
 // sums part[ks][m][n], added in split order by gemm_w4a16_reduce.
-template <int MT, int NT, int kDepth>
+template <int MT, int NT, int kDepth, int XG>
 __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
     int64_t M, int64_t N, int64_t K, const uint16_t *__restrict__ x, int64_t ldx,
     const uint8_t *__restrict__ w_codes, const uint8_t *__restrict__ w_scales, void *__restrict__ y,
     int y_bf16, int64_t ldy, int KS, float *__restrict__ part) {
-    __shared__ __attribute__((aligned(16))) uint16_t xs[2][MT * 16][kXPitch];
+    constexpr int XP = XG * 128 + 8;                    // LDS row pitch of an x group (bfloat16 elements)
+    __shared__ __attribute__((aligned(16))) uint16_t xs[2][MT * 16][XP];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -104,7 +107,11 @@ __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
     const int ks = blockIdx.y;
     const int64_t m0 = (int64_t)blockIdx.z * 16 * MT;
     const int64_t nch = K / 128;
-    const int64_t c0 = nch * ks / KS, nc = nch * (ks + 1) / KS - c0;
+    // splits start at even chunks: a pair of chunks is a whole 128-byte line
+    // of each weight row (when K % 256 == 0)
+    const int64_t npair = nch / 2;
+    const int64_t c0 = 2 * (npair * ks / KS);
+    const int64_t nc = (ks + 1 == KS ? nch : 2 * (npair * (ks + 1) / KS)) - c0;
 
     // activation chunk loader: thread t takes row t / 16 of each 16-row tile, elements 8 (t % 16) ..
     const int xr = tid >> 4, xc = (tid & 15) * 8;
@@ -115,9 +122,9 @@ __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
             v[mt] = *reinterpret_cast<const v4u *>(x + row * ldx + c * 128 + xc);
         }
     };
-    auto store_x = [&](int buf, const v4u (&v)[MT]) {
+    auto store_x = [&](int buf, int u, const v4u (&v)[MT]) {
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) *reinterpret_cast<v4u *>(&xs[buf][16 * mt + xr][xc]) = v[mt];
+        for (int mt = 0; mt < MT; ++mt) *reinterpret_cast<v4u *>(&xs[buf][16 * mt + xr][128 * u + xc]) = v[mt];
     };
     // the lane's 32 codes (MX block kg of the chunk) of each of its weight rows
     auto load_w = [&](int64_t c, v4u (&v)[NT]) {
@@ -140,39 +147,47 @@ __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
 #pragma unroll
         for (int t = 0; t < NT; ++t) acc[mt][t] = v4f{};
 
-    // Chunk c's activations travel global -> registers (ring slot c % kDepth,
-    // issued kDepth - 1 steps before they are needed) -> LDS (buffer c & 1,
-    // one step ahead); its codes go to registers kDepth chunks ahead and its
-    // scale bytes with those of three neighbours, kDepth chunks ahead.  The
-    // ring is unrolled by templates so every slot index is a constant, and
-    // loads past the last chunk re-read it (clamped, never used), so the main
-    // loop has no branches and the compiler waits on each load alone.
+    // Activations move in groups of XG chunks: group q travels global ->
+    // registers (issued at the start of group q - 2) -> LDS (buffer q & 1,
+    // stored at the start of group q - 1), so the workgroup meets at one
+    // barrier per group, not per chunk.  A chunk's codes go to registers
+    // kDepth chunks ahead (in pairs, below) and its scale bytes with those of
+    // three neighbours, kDepth chunks ahead.  The loop is unrolled by
+    // templates so every ring slot is a constant, and loads past the last
+    // chunk re-read it (clamped, never used), so the main loop has no
+    // branches and the compiler waits on each load alone.
     if (nc > 0) {
         constexpr int kTurn = 2 * kDepth;                      // steps per unrolled loop turn
         constexpr int kGroups = kTurn / 4;                      // scale-group ring slots
-        v4u xv[kDepth][MT];
+        static_assert(kTurn % XG == 0 && kDepth % 2 == 0, "loop turn of whole x groups and code pairs");
+        v4u xv[XG][MT];                                         // the next x group in flight
         v4u wq[kDepth][NT];
         uint32_t sq[kGroups][NT];                               // scale dwords of 4-chunk groups
         auto clamp = [&](int64_t i) { return c0 + (i < nc ? i : nc - 1); };
         static_for<0, kDepth / 4>([&](auto G) {                 // first: the oldest loads at the loop entry
             load_s(clamp(4 * decltype(G)::value + kg), sq[decltype(G)::value]);
         });
-        static_for<0, kDepth>([&](auto J) {
-            constexpr int j = decltype(J)::value;
-            load_x(clamp(j), xv[j]);
-            load_w(clamp(j), wq[j]);
-        });
-        store_x(0, xv[0]);
+        static_for<0, XG>([&](auto U) { load_x(clamp(decltype(U)::value), xv[decltype(U)::value]); });
+        static_for<0, kDepth>([&](auto J) { load_w(clamp(decltype(J)::value), wq[decltype(J)::value]); });
+        static_for<0, XG>([&](auto U) { store_x(0, decltype(U)::value, xv[decltype(U)::value]); });
+        static_for<0, XG>([&](auto U) { load_x(clamp(XG + decltype(U)::value), xv[decltype(U)::value]); });
         // step i = i0 + j of a loop turn (j static)
         auto step = [&](int64_t i, auto J) {
             constexpr int j = decltype(J)::value;
-            constexpr int slot = j % kDepth, grp = (j / 4) % kGroups;
+            constexpr int slot = j % kDepth, grp = (j / 4) % kGroups, u = j % XG;
             // keep each chunk's decode in its own step: hoisted, it would wait
             // on weights still in flight and shorten the prefetch
             __builtin_amdgcn_sched_barrier(0);
-            __syncthreads();                                    // chunk i in LDS; buffer (i+1)&1 free
-            store_x((int)((i + 1) & 1), xv[(slot + 1) % kDepth]);   // chunk i+1 (unused past the end)
-            load_x(clamp(i + kDepth), xv[slot]);
+            const int64_t xgrp = i / XG;
+            if constexpr (u == 0) {
+                __syncthreads();                                // group xgrp in LDS; the other buffer free
+                static_for<0, XG>([&](auto U) {                 // group xgrp + 1 (unused past the end)
+                    store_x((int)((xgrp + 1) & 1), decltype(U)::value, xv[decltype(U)::value]);
+                });
+                static_for<0, XG>([&](auto U) {
+                    load_x(clamp((xgrp + 2) * XG + decltype(U)::value), xv[decltype(U)::value]);
+                });
+            }
             if constexpr (j % 4 == 0)                           // the group kDepth chunks ahead
                 load_s(clamp(i + kDepth + kg), sq[((j + kDepth) / 4) % kGroups]);
             uint32_t sb[NT];
@@ -180,7 +195,7 @@ __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
             for (int t = 0; t < NT; ++t)
                 sb[t] = ((uint32_t)__builtin_amdgcn_ds_bpermute(4 * (r + 16 * (j % 4)), (int)sq[grp][t]) >>
                          (8 * kg)) & 0xFFu;
-            const int buf = (int)(i & 1);
+            const int buf = (int)(xgrp & 1);
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
                 v8bf wb[NT];
@@ -188,14 +203,21 @@ __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
                 for (int t = 0; t < NT; ++t) wb[t] = decode_step(wq[slot][t], sb[t], s);
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
-                    const v4u xa = *reinterpret_cast<const v4u *>(&xs[buf][16 * mt + r][32 * kg + 8 * s]);
+                    const v4u xa = *reinterpret_cast<const v4u *>(&xs[buf][16 * mt + r][128 * u + 32 * kg + 8 * s]);
 #pragma unroll
                     for (int t = 0; t < NT; ++t)
                         acc[mt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, xa), wb[t],
                                                                             acc[mt][t], 0, 0, 0);
                 }
             }
-            load_w(clamp(i + kDepth), wq[slot]);
+            // codes go out in pairs of chunks once the odd chunk of a pair is
+            // consumed: chunks 2p and 2p+1 are the two 64-byte halves of each
+            // row's 128-byte line, requested back to back (one chunk at a time,
+            // the halves went out a step apart: 12% slower from HBM)
+            if constexpr (j % 2 == 1) {
+                load_w(clamp(i - 1 + kDepth), wq[(slot + kDepth - 1) % kDepth]);
+                load_w(clamp(i + kDepth), wq[slot]);
+            }
         };
         int64_t i0 = 0;
         for (; i0 + kTurn <= nc; i0 += kTurn)
@@ -252,7 +274,8 @@ hipError_t launch_mt(int64_t M, int64_t N, int64_t K, const uint16_t *x, int64_t
                     (unsigned)((M + 16 * MT - 1) / (16 * MT)));
     // chunks in flight per wave (8 measured no faster than 4)
     constexpr int kDepth = MT == 1 ? REQAT_W16_DEPTH1 : 4;
-    hipLaunchKernelGGL((gemm_w4a16_kernel<MT, NT, kDepth>), grid, dim3(kThreads), 0, stream, M, N, K, x, ldx, w_codes,
+    constexpr int XG = MT == 1 ? REQAT_W16_XG : 1;
+    hipLaunchKernelGGL((gemm_w4a16_kernel<MT, NT, kDepth, XG>), grid, dim3(kThreads), 0, stream, M, N, K, x, ldx, w_codes,
                        w_scales, y, (int)y_bf16, ldy, KS, part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || KS == 1) return e;
