@@ -218,6 +218,57 @@ def practical_ceilings(x=None, wt=None, steps=10):
     return out
 
 
+def mfma_probe_tflops(kind: int, ops, warmup: int = 10, reps: int = 20, iters: int = 1500) -> float:
+    """Context, not a target: the rate of the register-only MFMA loop of
+    libreqat_probe.so (one wave per SIMD, 256 workgroups) on 8 KB of operand
+    words `ops` (uint8 device tensor: A words, then B words) -- what the
+    matrix cores sustain on that data with no memory traffic.  kind 0: scaled
+    FP4 32x32x64, kind 1: FP16 32x32x16."""
+    import ctypes
+
+    import torch
+
+    from paper_2606_15682_amd import build as pbuild
+    lib = ctypes.CDLL(pbuild.PROBE_LIB)
+    lib.reqat_probe_mfma.restype = ctypes.c_int
+    lib.reqat_probe_mfma.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                                     ctypes.c_void_p]
+    assert ops.dtype == torch.uint8 and ops.numel() == 8192 and ops.is_contiguous()
+    blocks = 256
+    out = torch.empty(blocks * 256, dtype=torch.float32, device=ops.device)
+    st = torch.cuda.current_stream(ops.device).cuda_stream
+
+    def launch():
+        rc = lib.reqat_probe_mfma(kind, ops.data_ptr(), out.data_ptr(), blocks, iters, st)
+        if rc != 0:
+            raise RuntimeError("reqat_probe_mfma failed (%d)" % rc)
+
+    for _ in range(warmup):
+        launch()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(reps):
+        launch()
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / reps
+    flops = blocks * 4 * iters * 16 * (131072 if kind == 0 else 32768)
+    return flops / (ms * 1e-3) / 1e12
+
+
+def operand_words(a, b):
+    """8 KB of probe operand words: the first 4 KB of a's and of b's bytes (repeated if shorter)."""
+    import torch
+
+    def first(t):
+        v = t.contiguous().view(torch.uint8).flatten()
+        if v.numel() < 4096:
+            v = v.repeat(-(-4096 // v.numel()))
+        return v[:4096]
+    return torch.cat([first(a), first(b)])
+
+
 class pinned_to_one_core:
     """Runs the enclosed oracle timing on one host core (the affinity of
     taskset -c <core>), restoring the process's affinity afterwards."""
@@ -737,6 +788,15 @@ def main():
     ms_step = (t1 - t0) * 1e3 / args.steps
     per = {n: float(np.mean([events[i][j].elapsed_time(events[i][j + 1]) for i in range(args.steps)]))
            for j, n in enumerate(names)}
+    # the product's operand data for the matrix-core probe (context, below):
+    # MXFP4 feeds its packed codes; NVFP4 feeds FP16 code * scale, which is the
+    # fake-quant value over the power-of-two g
+    if M > 64:
+        if fmt == reqat.MXFP4:
+            probe_ops, probe_kind = operand_words(xc, wc), 0
+        else:
+            probe_ops = operand_words((fx.float() / gx).to(torch.float16), (fw.float() / gw).to(torch.float16))
+            probe_kind = 1
 
     # the separate entry points (quantize alone, fake-quant alone), timed apart
     def timed(fn):
@@ -856,6 +916,15 @@ def main():
         "kernels": kern,
     }
     out["ceilings"] = practical_ceilings(x, wt)
+    if M > 64:
+        kind = probe_kind
+        probe = mfma_probe_tflops(kind, probe_ops)
+        out["ceilings"]["mfma_probe"] = {
+            "TFLOP/s": round(probe, 1), "frac_of_nominal_peak": round(probe / PEAK[mfma_dtype], 4),
+            "gemm_frac_of_probe": round(gemm_tflops / probe, 4),
+            "note": "register-only %s MFMA loop at one wave per SIMD on the first 4 KB of each operand "
+                    "(libreqat_probe.so): what the matrix cores sustain on this data with no memory traffic"
+                    % ("scaled FP4 32x32x64" if kind == 0 else "FP16 32x32x16")}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, wl.bf16_bits(x_cpu), wl.bf16_bits(w_cpu))
     print(json.dumps(out), flush=True)

@@ -1,4 +1,5 @@
-"""Build libreqat.so (HIP, gfx950) in-tree with hipcc.
+"""Build libreqat.so (HIP, gfx950) in-tree with hipcc, and libreqat_probe.so,
+the matrix-core rate probe that bench.py reports as context (not the product).
 
     python -m paper_2606_15682_amd.build          # or: python paper_2606_15682_amd/build.py
 """
@@ -13,6 +14,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libreqat.so")
 SOURCES = ["api.hip", "quantize.hip", "gemm.hip", "gemm_skinny.hip", "gemm_tile256.hip", "gemm_w4a16.hip", "kv4.hip", "sem.hip"]
+PROBE_LIB = os.path.join(HERE, "libreqat_probe.so")
+PROBE_SOURCE = "probe_mfma.hip"
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",
@@ -49,7 +52,8 @@ def _run(cmd, verbose):
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every HIP source (in parallel, one object each) and link LIB; always recompiles."""
+    """Compile every HIP source (in parallel, one object each) and link LIB, and
+    build PROBE_LIB; always recompiles."""
     from concurrent.futures import ThreadPoolExecutor
 
     cc = hipcc()
@@ -57,15 +61,18 @@ def build(verbose: bool = False) -> str:
     objs = [os.path.join(CSRC, s[:-4] + ".%s.o" % tag) for s in SOURCES]
     flags = [f for f in HIPCC_FLAGS if f != "-shared"]
     jobs = [[cc, *flags, "-c", os.path.join(CSRC, s), "-o", o] for s, o in zip(SOURCES, objs)]
-    workers = max(1, min(len(jobs), len(os.sched_getaffinity(0)), 8))
     tmp = LIB + ".tmp" + tag
+    ptmp = PROBE_LIB + ".tmp" + tag
+    jobs.append([cc, *HIPCC_FLAGS, os.path.join(CSRC, PROBE_SOURCE), "-o", ptmp])
+    workers = max(1, min(len(jobs), len(os.sched_getaffinity(0)), 8))
     try:
         with ThreadPoolExecutor(workers) as ex:
             list(ex.map(lambda c: _run(c, verbose), jobs))
         _run([cc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
         os.replace(tmp, LIB)
+        os.replace(ptmp, PROBE_LIB)
     finally:
-        for o in objs + [tmp]:
+        for o in objs + [tmp, ptmp]:
             if os.path.exists(o):
                 os.remove(o)
     return LIB
