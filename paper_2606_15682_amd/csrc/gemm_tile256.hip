@@ -476,17 +476,19 @@ __device__ __forceinline__ void store_tile(const v16f (&acc)[4][4], const TileGe
     }
 }
 
-// Position of the load stream: stage s of virtual tile v.
+// Position of the load stream: stage s of virtual tile v (the mapping is
+// evaluated only for tiles that exist: past the last one its group size
+// would be zero).
 template <class C>
 struct LoadPos {
     int64_t v;
     int s;
     TileGeo g;
-    __device__ __forceinline__ void advance(int nst, int64_t G, int64_t M, int64_t N) {
+    __device__ __forceinline__ void advance(int nst, int64_t G, int64_t M, int64_t N, int64_t T) {
         if (++s == nst) {
             s = 0;
             v += G;
-            g = tile_geo(v, M, N);
+            if (v < T) g = tile_geo(v, M, N);
         }
     }
 };
@@ -521,10 +523,10 @@ __device__ __forceinline__ void nv_persistent(uint8_t *smem, int64_t M, int64_t 
     {
         StageIssue<C> i0 = issue_at(ld, smem);
         i0.template region<0, 1>();
-        ld.advance(nst, G, M, N);
+        ld.advance(nst, G, M, N, T);
         StageIssue<C> i1 = issue_at(ld, smem + C::STAGE);
         i1.template region<0, 1>();
-        ld.advance(nst, G, M, N);
+        ld.advance(nst, G, M, N, T);
         if (total > 1) wait_vmcnt<C::LPS>();
         else wait_vmcnt<0>();
     }
@@ -555,7 +557,7 @@ __device__ __forceinline__ void nv_persistent(uint8_t *smem, int64_t M, int64_t 
             const uint8_t *nbuf = smem + ((gs + 1) & 1) * C::STAGE;
             StageIssue<C> issue = issue_at(ld, buf);    // stage gs + 2
             nv_region<C, 0, NT>(acc, st, buf, nbuf, ln, issue);
-            ld.advance(nst, G, M, N);
+            ld.advance(nst, G, M, N, T);
         }
         store_tile(acc, tile_geo(v, M, N), M, N, wm, wn, lane, scale, y, y_bf16, ldy);
     }

@@ -10,7 +10,7 @@ stream must never evaluate the mapping for an id at or past the tile count:
 the mapping divides by a zero group size there, or yields a tile with no rows,
 and a clamped row of -1 turns the 32-bit offset into one about 4 GiB past the
 operand.  The kernel's stream reuses the workgroup's first tile for loads past
-its last one (MXFP4) or issues none (NVFP4).
+its last one (MXFP4), or issues none and leaves the mapping unevaluated (NVFP4).
 """
 import pytest
 
