@@ -141,7 +141,8 @@ static reqat_status run_kv4(const void *x, int64_t rows, int64_t cols, int64_t l
     }
     hipError_t e = launch_kv4(fake ? kFakeQuant : kCodes, reinterpret_cast<const uint16_t *>(x), rows, cols, ldx,
                               shift, codes, scales, reinterpret_cast<uint16_t *>(y), ldy, tensor_scale, compute,
-                              reinterpret_cast<uint32_t *>(workspace), s);
+                              reinterpret_cast<uint32_t *>(workspace), compute ? quant_seg_table(workspace) : nullptr,
+                              s);
     return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
 }
 

@@ -57,11 +57,13 @@ hipError_t launch_gemm_w4a16(int64_t M, int64_t N, int64_t K, const uint16_t *x,
                              const uint8_t *w_codes, const uint8_t *w_scales, void *y, bool y_bf16,
                              int64_t ldy, float *workspace, hipStream_t stream);
 
-// KV4 (E1M2 elements, E4M3 block scales of 16, FP32 global scale) of x - shift;
-// `computed` runs the absmax pass into `partials` first (<= kMaxPartials).
+// KV4 (E1M2 elements, E4M3 block scales of 16, FP32 global scale) of x - shift.
+// A computed g takes one pass over x and a fix-up kernel when the segment
+// table (one uint16 per 64 blocks) has room for the tensor, else an absmax pass
+// into `partials` (<= kMaxPartials) and then the quantizer.
 hipError_t launch_kv4(QuantOut out, const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx, const float *shift,
                       uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy, float *gptr, bool computed,
-                      uint32_t *partials, hipStream_t stream);
+                      uint32_t *partials, uint16_t *seg_table, hipStream_t stream);
 
 // SEM loss: per-row statistics ([T][4]: H, NLL, lse, 0), weights [T], loss[4]
 // (L, L_SFT, L_ent, tau); backward writes dL/dlogits.  V % 8 == 0.

@@ -196,6 +196,112 @@ __device__ __forceinline__ uint32_t e1m2_mag_f32(float a, float S) {
     return m;
 }
 
+// The global scale g as the element paths use it: the FP32 path needs a
+// power of two in [2^-126, 2^100] (every computed g is a power of two), so
+// that every threshold and decoded value is exact in FP32.
+struct Kv4G {
+    float g;
+    double gd;
+    bool f32;
+    int kg;
+};
+
+__device__ __forceinline__ Kv4G kv4_make_g(float g) {
+    Kv4G G;
+    G.g = g;
+    G.gd = (double)g;
+    const uint32_t gb = bits_from_f32(g);
+    G.f32 = (gb & 0x807FFFFFu) == 0u && gb >= 0x00800000u && gb <= ((100u + 127u) << 23);
+    G.kg = (int)(gb >> 23) - 127;
+    return G;
+}
+
+// Largest finite |d| of a block (FP32 pattern; 0 when none).
+__device__ __forceinline__ uint32_t kv4_finite_max(const float (&d)[16]) {
+    uint32_t m = 0u;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        const uint32_t a = bits_from_f32(d[j]) & 0x7FFFFFFFu;
+        if (a < 0x7F800000u && a > m) m = a;
+    }
+    return m;
+}
+
+// Quantizes block blk (its 16 shifted values d, am = the largest |d| pattern,
+// NaN and Inf included) under G and stores codes and scale byte, or the
+// fake-quant values; returns the scale byte.
+template <int OUT>
+__device__ __forceinline__ uint32_t kv4_emit(const float (&d)[16], uint32_t am, int64_t blk, int64_t nb, bool narrow,
+                                             const Kv4G &G, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
+                                             uint16_t *__restrict__ y, int64_t ldy) {
+    const bool bad = am >= 0x7F800000u;
+    const uint32_t sbyte = bad ? 0x7Fu
+                           : am == 0u ? 0u
+                           : G.f32 ? kv4_scale_byte_f32(f32_from_bits(am), G.g, G.kg)
+                                   : kv4_scale_byte((double)f32_from_bits(am), G.gd);
+    const double S = (double)e4m3_value(sbyte) * G.gd;
+    const float Sf = e4m3_value(sbyte) * G.g;               // exact on the FP32 path
+    uint32_t c[16];
+    if (G.f32) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const uint32_t sign = (bits_from_f32(d[j]) >> 28) & 8u;
+            c[j] = bad ? 0u : (sbyte == 0u ? sign : (e1m2_mag_f32(__builtin_fabsf(d[j]), Sf) | sign));
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const uint32_t sign = (bits_from_f32(d[j]) >> 28) & 8u;
+            c[j] = bad ? 0u : (sbyte == 0u ? sign : (e1m2_mag(__builtin_fabs((double)d[j]), S) | sign));
+        }
+    }
+    if (OUT == kCodes) {
+        uint32_t lo = 0, hi = 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            lo |= c[j] << (4 * j);
+            hi |= c[8 + j] << (4 * j);
+        }
+        *reinterpret_cast<uint2 *>(codes + blk * 8) = make_uint2(lo, hi);
+        scales[blk] = (uint8_t)sbyte;
+    } else {
+        const int64_t r = narrow ? (int64_t)((uint32_t)blk / (uint32_t)nb) : blk / nb;
+        uint32_t o[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            uint32_t h[2];
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                const uint32_t cc = c[2 * i + k];
+                uint32_t mag;
+                if (G.f32) {
+                    const float v = 0.5f * (float)(cc & 7u) * (sbyte == 0u ? 0.0f : Sf);
+                    mag = bf16_rne_from_float(v);
+                } else {
+                    const double v = 0.5 * (double)(cc & 7u) * (sbyte == 0u ? 0.0 : S);
+                    mag = bf16_rne_from_double(v);
+                }
+                h[k] = bad ? 0x7FC0u : (mag | ((cc & 8u) << 12));
+            }
+            o[i] = h[0] | (h[1] << 16);
+        }
+        uint4 *dst = reinterpret_cast<uint4 *>(y + r * ldy + (blk - r * nb) * 16);
+        dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
+        dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
+    }
+    return sbyte;
+}
+
+__device__ __forceinline__ uint32_t kv4_block_max(const float (&d)[16]) {
+    uint32_t am = 0u;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        const uint32_t a = bits_from_f32(d[j]) & 0x7FFFFFFFu;
+        am = am > a ? am : a;
+    }
+    return am;
+}
+
 template <int OUT, int SRC>
 __global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
     const uint16_t *__restrict__ x, int64_t rows, int64_t cols, int64_t ldx, const float *__restrict__ shift,
@@ -222,12 +328,7 @@ __global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
     } else {
         g = *gptr;
     }
-    const double gd = (double)g;
-    // FP32 element path: g a power of two in [2^-126, 2^100] (a computed g
-    // always is), so every threshold and decoded value is exact in FP32
-    const uint32_t gb = bits_from_f32(g);
-    const bool f32 = (gb & 0x807FFFFFu) == 0u && gb >= 0x00800000u && gb <= ((100u + 127u) << 23);
-    const int kg = (int)(gb >> 23) - 127;
+    const Kv4G G = kv4_make_g(g);
 
     const int64_t nb = cols / 16, total = rows * nb;
     const bool narrow = total < (int64_t(1) << 32);
@@ -235,66 +336,169 @@ __global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
          blk += (int64_t)gridDim.x * kThreads) {
         float d[16];
         kv4_load<SRC>(x, shift, lds_shift, blk, nb, ldx, narrow, d);
-        uint32_t am = 0u;
+        kv4_emit<OUT>(d, kv4_block_max(d), blk, nb, narrow, G, codes, scales, y, ldy);
+    }
+}
+
+__device__ __forceinline__ uint32_t kv4_wave_min(uint32_t v) {
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const uint32_t a = bits_from_f32(d[j]) & 0x7FFFFFFFu;
-            am = am > a ? am : a;
-        }
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint32_t o = __shfl_xor(v, off, 64);
+        v = v < o ? v : o;
+    }
+    return v;
+}
+
+// One pass over x for a computed g.  g needs the amax of all of d, known only
+// once every block is read, so each segment of 64 consecutive blocks (the 64
+// lanes of a wave in one step) is quantized under its own reference g_r: the
+// global-scale rule applied to the segment's largest finite |d| (g_r <= g,
+// both powers of two).  Dividing g by a power of two only moves the exponent
+// of the smallest E4M3 scale s with amax <= 3.5 s g, so codes, s g and
+// fake-quant values under g_r equal those under g for every block whose scale
+// under g is still a normal E4M3 value; kv4_fixup_kernel lowers the scale
+// exponents by log2(g / g_r) and re-quantizes from x only the blocks whose
+// scale would leave the normal range.  The segment table records log2(g_r) +
+// 127 (0 for a segment with no non-zero finite value) and the smallest scale
+// exponent field among the segment's non-zero finite blocks; partials get the
+// workgroup's largest finite |d|.
+template <int OUT, int SRC>
+__global__ __launch_bounds__(kThreads) void kv4_quantize_deferred_kernel(
+    const uint16_t *__restrict__ x, int64_t rows, int64_t cols, int64_t ldx, const float *__restrict__ shift,
+    uint8_t *__restrict__ codes, uint8_t *__restrict__ scales, uint16_t *__restrict__ y, int64_t ldy,
+    uint32_t *__restrict__ partials, uint16_t *__restrict__ seg_table) {
+    __shared__ float4 lds_shift[SRC == kShiftLdsSrc ? kShiftLds / 4 : 1];
+    if (SRC == kShiftLdsSrc) kv4_stage_shift(shift, cols, lds_shift);
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t nb = cols / 16, total = rows * nb;
+    const bool narrow = total < (int64_t(1) << 32);
+    uint32_t mloc = 0u;
+    // segment base / 64 (wave-uniform): the blocks a lane takes are those of kv4_quantize_kernel
+    for (int64_t base = ((int64_t)blockIdx.x * 4 + wave) * 64; base < total;
+         base += (int64_t)gridDim.x * kThreads) {
+        const int64_t blk = base + lane;
+        const bool act = blk < total;
+        float d[16];
+        kv4_load<SRC>(x, shift, lds_shift, act ? blk : total - 1, nb, ldx, narrow, d);   // in range, unused past the end
+        uint32_t am = act ? kv4_block_max(d) : 0u;
         const bool bad = am >= 0x7F800000u;
-        const uint32_t sbyte = bad ? 0x7Fu
-                               : am == 0u ? 0u
-                               : f32 ? kv4_scale_byte_f32(f32_from_bits(am), g, kg)
-                                     : kv4_scale_byte((double)f32_from_bits(am), gd);
-        const double S = (double)e4m3_value(sbyte) * gd;
-        const float Sf = e4m3_value(sbyte) * g;             // exact on the FP32 path
-        uint32_t c[16];
-        if (f32) {
+        const uint32_t fm = bad ? kv4_finite_max(d) : am;
+        mloc = mloc > fm ? mloc : fm;
+        const uint32_t segmax = kv4_wave_max(fm);
+        const Kv4G Gr = kv4_make_g(kv4_global_scale(segmax));
+        uint32_t sbyte = 0u;
+        if (act) sbyte = kv4_emit<OUT>(d, am, blk, nb, narrow, Gr, codes, scales, y, ldy);
+        const bool live = act && am != 0u && !bad;
+        const uint32_t emin = kv4_wave_min(live ? sbyte >> 3 : 0xFFu);
+        if (lane == 0) seg_table[base / 64] = segmax ? (uint16_t)((uint32_t)(Gr.kg + 127) | (emin << 8)) : (uint16_t)0;
+    }
+    __shared__ uint32_t red[kThreads / 64];
+    mloc = kv4_wave_max(mloc);
+    if (lane == 0) red[wave] = mloc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t r = red[0];
+        for (int i = 1; i < kThreads / 64; ++i) r = r > red[i] ? r : red[i];
+        partials[blockIdx.x] = r;
+    }
+}
+
+// Subtracts sub (= sh << 3, a lowering of the exponent field by sh) from each
+// of the four scale bytes in v except 0x00 (zero block) and 0x7F (NaN block),
+// whose meaning does not depend on g.  Every other byte has an exponent field
+// > sh, so no byte borrows from its neighbour.
+__device__ __forceinline__ uint32_t kv4_lower_bytes(uint32_t v, uint32_t sub) {
+    const uint32_t z = ~(((v & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | v | 0x7F7F7F7Fu);   // 0x80 where a byte is 0x00
+    const uint32_t t = v ^ 0x7F7F7F7Fu;
+    const uint32_t n = ~(((t & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | t | 0x7F7F7F7Fu);   // 0x80 where a byte is 0x7F
+    const uint32_t mask = 0x01010101u & ~((z | n) >> 7);
+    return v - mask * sub;
+}
+
+// Second kernel of the one-pass quantizer: folds the partials into g,
+// publishes it, and corrects every segment whose reference scale differs from
+// g by 2^sh, one lane per segment: when the segment's smallest exponent field
+// exceeds sh, every block keeps a normal scale and only its scale bytes are
+// lowered (codes output; fake-quant values stand).  Otherwise the wave walks
+// such segments, one lane per block, lowering the bytes that stay normal and
+// re-quantizing the other blocks from x under g (fake-quant output, with no
+// scale bytes to tell them apart: every block of the segment).  The shift is
+// read from global memory (only re-quantized blocks need it).
+template <int OUT>
+__global__ __launch_bounds__(kThreads) void kv4_fixup_kernel(
+    const uint16_t *__restrict__ x, int64_t rows, int64_t cols, int64_t ldx, const float *__restrict__ shift,
+    uint8_t *__restrict__ codes, uint8_t *__restrict__ scales, uint16_t *__restrict__ y, int64_t ldy, float *gptr,
+    const uint32_t *__restrict__ partials, int nparts, const uint16_t *__restrict__ seg_table) {
+    const int lane = threadIdx.x & 63;
+    const int64_t nb = cols / 16, total = rows * nb;
+    const int64_t nseg = (total + 63) / 64;
+    const bool narrow = total < (int64_t(1) << 32);
+    __shared__ uint32_t red[kThreads / 64];
+    uint32_t m = 0u;
+    for (int i = threadIdx.x; i < nparts; i += kThreads) {
+        const uint32_t p = partials[i];
+        m = m > p ? m : p;
+    }
+    m = kv4_wave_max(m);
+    if (lane == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    uint32_t r = red[0];
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const uint32_t sign = (bits_from_f32(d[j]) >> 28) & 8u;
-                c[j] = bad ? 0u : (sbyte == 0u ? sign : (e1m2_mag_f32(__builtin_fabsf(d[j]), Sf) | sign));
-            }
-        } else {
+    for (int i = 1; i < kThreads / 64; ++i) r = r > red[i] ? r : red[i];
+    const Kv4G G = kv4_make_g(kv4_global_scale(r));
+    if (blockIdx.x == 0 && threadIdx.x == 0) *gptr = G.g;
+
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    for (int64_t s0 = (int64_t)blockIdx.x * kThreads + (threadIdx.x & ~63); s0 < nseg; s0 += stride) {
+        const int64_t seg = s0 + lane;
+        const uint32_t e = seg < nseg ? seg_table[seg] : 0u;
+        int sh = 0;
+        bool redo = false;
+        if (e != 0u) sh = G.kg - ((int)(e & 0xFFu) - 127);
+        if (sh > 0) {
+            redo = (int)(e >> 8) <= sh;
+            if (OUT == kCodes && !redo) {
+                const uint32_t sub = (uint32_t)sh << 3;
+                const int64_t n = total - seg * 64;
+                if (n >= 64) {
+                    uint4 *p = reinterpret_cast<uint4 *>(scales + seg * 64);
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const uint32_t sign = (bits_from_f32(d[j]) >> 28) & 8u;
-                c[j] = bad ? 0u : (sbyte == 0u ? sign : (e1m2_mag(__builtin_fabs((double)d[j]), S) | sign));
+                    for (int i = 0; i < 4; ++i) {
+                        const uint4 v = p[i];
+                        p[i] = make_uint4(kv4_lower_bytes(v.x, sub), kv4_lower_bytes(v.y, sub),
+                                          kv4_lower_bytes(v.z, sub), kv4_lower_bytes(v.w, sub));
+                    }
+                } else {
+                    for (int64_t i = 0; i < n; ++i)
+                        scales[seg * 64 + i] = (uint8_t)kv4_lower_bytes(scales[seg * 64 + i], sub);
+                }
             }
         }
-        if (OUT == kCodes) {
-            uint32_t lo = 0, hi = 0;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                lo |= c[j] << (4 * j);
-                hi |= c[8 + j] << (4 * j);
-            }
-            *reinterpret_cast<uint2 *>(codes + blk * 8) = make_uint2(lo, hi);
-            scales[blk] = (uint8_t)sbyte;
-        } else {
-            const int64_t r = narrow ? (int64_t)((uint32_t)blk / (uint32_t)nb) : blk / nb;
-            uint32_t o[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                uint32_t h[2];
-#pragma unroll
-                for (int k = 0; k < 2; ++k) {
-                    const uint32_t cc = c[2 * i + k];
-                    uint32_t mag;
-                    if (f32) {
-                        const float v = 0.5f * (float)(cc & 7u) * (sbyte == 0u ? 0.0f : Sf);
-                        mag = bf16_rne_from_float(v);
-                    } else {
-                        const double v = 0.5 * (double)(cc & 7u) * (sbyte == 0u ? 0.0 : S);
-                        mag = bf16_rne_from_double(v);
+        uint64_t flags = __ballot(redo);
+        while (flags) {
+            const int l = __builtin_ctzll(flags);
+            flags &= flags - 1;
+            const int lsh = __shfl(sh, l, 64);
+            const int64_t blk = (s0 + l) * 64 + lane;
+            if (blk < total) {
+                bool requant = true;
+                if (OUT == kCodes) {
+                    const uint32_t b = scales[blk];
+                    if (b == 0u || b == 0x7Fu) {
+                        requant = false;
+                    } else if ((int)(b >> 3) > lsh) {
+                        scales[blk] = (uint8_t)(b - ((uint32_t)lsh << 3));
+                        requant = false;
                     }
-                    h[k] = bad ? 0x7FC0u : (mag | ((cc & 8u) << 12));
                 }
-                o[i] = h[0] | (h[1] << 16);
+                if (requant) {
+                    float d[16];
+                    if (shift) kv4_load<kShiftGlobal>(x, shift, nullptr, blk, nb, ldx, narrow, d);
+                    else kv4_load<kNoShift>(x, shift, nullptr, blk, nb, ldx, narrow, d);
+                    kv4_emit<OUT>(d, kv4_block_max(d), blk, nb, narrow, G, codes, scales, y, ldy);
+                }
             }
-            uint4 *dst = reinterpret_cast<uint4 *>(y + r * ldy + (blk - r * nb) * 16);
-            dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
-            dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
         }
     }
 }
@@ -303,13 +507,37 @@ __global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
 
 hipError_t launch_kv4(QuantOut out, const uint16_t *x, int64_t rows, int64_t cols, int64_t ldx, const float *shift,
                       uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy, float *gptr, bool computed,
-                      uint32_t *partials, hipStream_t stream) {
+                      uint32_t *partials, uint16_t *seg_table, hipStream_t stream) {
     const int64_t total = rows * (cols / 16);
     if (total == 0) return hipSuccess;
     int64_t grid = (total + kThreads - 1) / kThreads;
     if (grid > kMaxKvGroups) grid = kMaxKvGroups;
+    const int64_t nseg = (total + 63) / 64;
+    const bool deferred = computed && seg_table != nullptr && nseg <= kMaxSegments;
     auto run = [&](auto src_c) {
         constexpr int SRC = decltype(src_c)::value;
+        if (deferred) {
+            // one pass over x under per-segment reference scales, then the fix-up
+            if (out == kCodes)
+                hipLaunchKernelGGL((kv4_quantize_deferred_kernel<kCodes, SRC>), dim3((unsigned)grid), dim3(kThreads), 0,
+                                   stream, x, rows, cols, ldx, shift, codes, scales, y, ldy, partials, seg_table);
+            else
+                hipLaunchKernelGGL((kv4_quantize_deferred_kernel<kFakeQuant, SRC>), dim3((unsigned)grid),
+                                   dim3(kThreads), 0, stream, x, rows, cols, ldx, shift, codes, scales, y, ldy,
+                                   partials, seg_table);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            int64_t fgrid = (nseg + kThreads - 1) / kThreads;
+            if (fgrid > kMaxKvGroups) fgrid = kMaxKvGroups;
+            if (out == kCodes)
+                hipLaunchKernelGGL(kv4_fixup_kernel<kCodes>, dim3((unsigned)fgrid), dim3(kThreads), 0, stream, x, rows,
+                                   cols, ldx, shift, codes, scales, y, ldy, gptr, partials, (int)grid, seg_table);
+            else
+                hipLaunchKernelGGL(kv4_fixup_kernel<kFakeQuant>, dim3((unsigned)fgrid), dim3(kThreads), 0, stream, x,
+                                   rows, cols, ldx, shift, codes, scales, y, ldy, gptr, partials, (int)grid,
+                                   seg_table);
+            return hipGetLastError();
+        }
         if (computed) {
             hipLaunchKernelGGL(kv4_absmax_kernel<SRC>, dim3((unsigned)grid), dim3(kThreads), 0, stream, x, rows, cols,
                                ldx, shift, partials);

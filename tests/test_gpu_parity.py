@@ -340,6 +340,27 @@ def test_kv4_exhaustive_patterns_and_specials():
     assert_kv4_parity(_rand(45, 320, 19, "student_t"), np.linspace(-2, 2, 320).astype(np.float32), ldx_pad=24)
 
 
+@pytest.mark.parametrize("shifted", [False, True])
+def test_kv4_one_pass_segments(shifted):
+    """A computed g runs one pass under per-segment reference scales (64 blocks
+    = 4 rows of 256 channels here) and a fix-up.  Segment k is scaled by
+    2^-(3k mod 41), so the fix-up lowers some segments' scale exponents and
+    re-quantizes the blocks of others whose scales would leave the normal E4M3
+    range; plus an all-zero segment, a segment of NaN blocks whose finite
+    elements still count for g, and a final partial segment (2080 blocks)."""
+    log("kv4 one-pass segments shifted=%s" % shifted)
+    R, C = 130, 256
+    v = indep.bf16_values(_rand(R, C, 77, "student_t"))
+    for k in range(R // 4 + 1):
+        v[4 * k:4 * k + 4] *= 2.0 ** -(3 * k % 41)
+    v[8:12] = 0.0                                          # an all-zero segment
+    v[20:24, ::16] = np.nan                                # every block of this segment has a NaN
+    v[21, 5] = 300.0                                       # a finite element of a NaN block sets g
+    xb = indep.to_bf16_bits(v)
+    shift = np.random.default_rng(5).normal(0.0, 0.5, C).astype(np.float32) if shifted else None
+    assert_kv4_parity(xb, shift)
+
+
 def test_kv4_empty_writes_unit_scale():
     log("kv4 empty")
     x = torch.empty((0, 128), dtype=torch.bfloat16, device=DEV)
