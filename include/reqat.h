@@ -239,7 +239,9 @@ reqat_status reqat_quantize_kv4(const void *x, int64_t rows, int64_t cols, int64
 /*
  * Fake-quant of the KV4 quantization above: y[r][c] = RN_bf16(E1M2(code) * s * g)
  * in the shifted domain (NaN for a non-finite block).  y [rows][ldy] bfloat16,
- * 16-byte aligned, ldy % 8 == 0, ldy >= cols.
+ * 16-byte aligned, ldy % 8 == 0, ldy >= cols.  In place under the rules of
+ * reqat_fakequant_fp4 for NVFP4: not with REQAT_TS_COMPUTE, whose fix-up
+ * re-reads x.
  */
 reqat_status reqat_fakequant_kv4(const void *x, int64_t rows, int64_t cols, int64_t ldx, const float *shift,
                                  void *y, int64_t ldy, float *tensor_scale, reqat_tscale_mode ts, void *workspace,
