@@ -290,16 +290,17 @@ int row_tile(int64_t M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
 
 }  // namespace
 
-// K splits: enough workgroups to cover the chip (>= 512) when the weight
-// rows alone give fewer than 256, at most 8 and at most one chunk each.
+// K splits: enough workgroups to cover the chip (REQAT_W16_TARGET) when the
+// weight rows alone give fewer than 256, at most REQAT_W16_KSMAX, and at most
+// one pair of chunks each (splits start at even chunks).
 int gemm_w4a16_splits(int64_t M, int64_t N, int64_t K) {
     const int64_t rows = 64 * REQAT_W16_NT;
     const int64_t base = ((N + rows - 1) / rows) * ((M + 16 * row_tile(M) - 1) / (16 * row_tile(M)));
-    const int64_t nch = K / 128;
-    if (base >= 256 || nch <= 1) return 1;
+    const int64_t npair = K / 256;
+    if (base >= 256 || npair <= 1) return 1;
     int64_t ks = (REQAT_W16_TARGET + base - 1) / base;
     if (ks > REQAT_W16_KSMAX) ks = REQAT_W16_KSMAX;
-    if (ks > nch) ks = nch;
+    if (ks > npair) ks = npair;
     return (int)ks;
 }
 

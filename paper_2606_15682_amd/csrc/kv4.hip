@@ -133,6 +133,29 @@ __device__ __forceinline__ float kv4_global_scale(uint32_t am) {
     return f32_from_bits((uint32_t)(k + 127) << 23);
 }
 
+// The largest of the first nparts partial maxima (<= kMaxKvGroups), for the
+// whole workgroup: every thread's loads are issued before any is waited on.
+__device__ __forceinline__ uint32_t kv4_fold_partials(const uint32_t *__restrict__ partials, int nparts) {
+    __shared__ uint32_t red[kThreads / 64];
+    constexpr int kPer = (kMaxKvGroups + kThreads - 1) / kThreads;
+    uint32_t p[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int i = (int)threadIdx.x + j * kThreads;
+        p[j] = i < nparts ? partials[i] : 0u;
+    }
+    uint32_t m = 0u;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) m = m > p[j] ? m : p[j];
+    m = kv4_wave_max(m);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    uint32_t r = red[0];
+#pragma unroll
+    for (int i = 1; i < kThreads / 64; ++i) r = r > red[i] ? r : red[i];
+    return r;
+}
+
 // Smallest positive finite E4M3 s with amax <= 3.5 * s * g (0x7E when none).
 __device__ __forceinline__ uint32_t kv4_scale_byte(double a, double g) {
     uint32_t b = e4m3_ceil_byte(a / (3.5 * g));
@@ -311,19 +334,7 @@ __global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
     if (SRC == kShiftLdsSrc) kv4_stage_shift(shift, cols, lds_shift);
     float g;
     if (computed) {
-        __shared__ uint32_t red[kThreads / 64];
-        uint32_t m = 0;
-        for (int i = threadIdx.x; i < nparts; i += kThreads) {
-            const uint32_t p = partials[i];
-            m = m > p ? m : p;
-        }
-        m = kv4_wave_max(m);
-        if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
-        __syncthreads();
-        uint32_t r = red[0];
-#pragma unroll
-        for (int i = 1; i < kThreads / 64; ++i) r = r > red[i] ? r : red[i];
-        g = kv4_global_scale(r);
+        g = kv4_global_scale(kv4_fold_partials(partials, nparts));
         if (blockIdx.x == 0 && threadIdx.x == 0) *gptr = g;
     } else {
         g = *gptr;
@@ -434,25 +445,29 @@ __global__ __launch_bounds__(kThreads) void kv4_fixup_kernel(
     const int64_t nb = cols / 16, total = rows * nb;
     const int64_t nseg = (total + 63) / 64;
     const bool narrow = total < (int64_t(1) << 32);
-    __shared__ uint32_t red[kThreads / 64];
-    uint32_t m = 0u;
-    for (int i = threadIdx.x; i < nparts; i += kThreads) {
-        const uint32_t p = partials[i];
-        m = m > p ? m : p;
-    }
-    m = kv4_wave_max(m);
-    if (lane == 0) red[threadIdx.x >> 6] = m;
-    __syncthreads();
-    uint32_t r = red[0];
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    const int64_t first = (int64_t)blockIdx.x * kThreads + (threadIdx.x & ~63);
+    // a lane's table entry and (codes output) its segment's 64 scale bytes
+    auto fetch = [&](int64_t seg, uint32_t &e, uint4 (&v)[4]) {
+        e = 0u;
+        if (seg < nseg) {
+            e = seg_table[seg];
+            if (OUT == kCodes && total - seg * 64 >= 64) {
+                const uint4 *p = reinterpret_cast<const uint4 *>(scales + seg * 64);
 #pragma unroll
-    for (int i = 1; i < kThreads / 64; ++i) r = r > red[i] ? r : red[i];
-    const Kv4G G = kv4_make_g(kv4_global_scale(r));
+                for (int i = 0; i < 4; ++i) v[i] = p[i];
+            }
+        }
+    };
+    uint32_t e;
+    uint4 v[4] = {};
+    fetch(first + lane, e, v);                          // its latency overlaps the fold
+    const Kv4G G = kv4_make_g(kv4_global_scale(kv4_fold_partials(partials, nparts)));
     if (blockIdx.x == 0 && threadIdx.x == 0) *gptr = G.g;
 
-    const int64_t stride = (int64_t)gridDim.x * kThreads;
-    for (int64_t s0 = (int64_t)blockIdx.x * kThreads + (threadIdx.x & ~63); s0 < nseg; s0 += stride) {
+    for (int64_t s0 = first; s0 < nseg; s0 += stride) {
+        if (s0 != first) fetch(s0 + lane, e, v);
         const int64_t seg = s0 + lane;
-        const uint32_t e = seg < nseg ? seg_table[seg] : 0u;
         int sh = 0;
         bool redo = false;
         if (e != 0u) sh = G.kg - ((int)(e & 0xFFu) - 127);
@@ -464,11 +479,9 @@ __global__ __launch_bounds__(kThreads) void kv4_fixup_kernel(
                 if (n >= 64) {
                     uint4 *p = reinterpret_cast<uint4 *>(scales + seg * 64);
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const uint4 v = p[i];
-                        p[i] = make_uint4(kv4_lower_bytes(v.x, sub), kv4_lower_bytes(v.y, sub),
-                                          kv4_lower_bytes(v.z, sub), kv4_lower_bytes(v.w, sub));
-                    }
+                    for (int i = 0; i < 4; ++i)
+                        p[i] = make_uint4(kv4_lower_bytes(v[i].x, sub), kv4_lower_bytes(v[i].y, sub),
+                                          kv4_lower_bytes(v[i].z, sub), kv4_lower_bytes(v[i].w, sub));
                 } else {
                     for (int64_t i = 0; i < n; ++i)
                         scales[seg * 64 + i] = (uint8_t)kv4_lower_bytes(scales[seg * 64 + i], sub);

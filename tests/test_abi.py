@@ -379,12 +379,14 @@ def test_binding_checks_workspace_sizes(trapped):
     _raises_before_device(lambda: reqat.linear(x, NV, wc, ws_, g, ws=_u8(need - 1)), match="ws")
     _raises_before_device(lambda: reqat.linear(x, NV, wc, ws_, g, ws=torch.zeros(need)), match="ws")
     _raises_before_device(lambda: reqat.linear(x, NV, wc, _u8(32, 8), g), match="w_scales")
-    mc, ms = _u8(5120, 128), _u8(5120, 8)
-    need16 = reqat.reqat_w4a16_workspace_bytes(16, 5120, 256)
-    assert need16 > 0
-    _raises_before_device(lambda: reqat.gemm_w4a16(x, mc, ms, ws=_u8(need16 - 4)), match="ws")
-    _raises_before_device(lambda: reqat.gemm_w4a16(x, mc, _u8(5120, 16)), match="w_scales")
-    _raises_before_device(lambda: reqat.gemm_w4a16(x, mc, ms, out=torch.zeros(16, 5120, dtype=torch.bfloat16)),
+    x5 = torch.zeros(16, 512, dtype=torch.bfloat16)
+    mc, ms = _u8(5120, 256), _u8(5120, 16)
+    need16 = reqat.reqat_w4a16_workspace_bytes(16, 5120, 512)      # K split in two (one pair of chunks each)
+    assert need16 == 4 * 2 * 16 * 5120
+    assert reqat.reqat_w4a16_workspace_bytes(16, 5120, 256) == 0     # a single pair of chunks: no split
+    _raises_before_device(lambda: reqat.gemm_w4a16(x5, mc, ms, ws=_u8(need16 - 4)), match="ws")
+    _raises_before_device(lambda: reqat.gemm_w4a16(x5, mc, _u8(5120, 32)), match="w_scales")
+    _raises_before_device(lambda: reqat.gemm_w4a16(x5, mc, ms, out=torch.zeros(16, 5120, dtype=torch.bfloat16)),
                           match="out")
 
 
