@@ -160,6 +160,7 @@ __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
         constexpr int kTurn = 2 * kDepth;                      // steps per unrolled loop turn
         constexpr int kGroups = kTurn / 4;                      // scale-group ring slots
         static_assert(kTurn % XG == 0 && kDepth % 2 == 0, "loop turn of whole x groups and code pairs");
+        static_assert(kDepth % 4 == 0, "scale dwords cover four chunks: the prologue loads kDepth / 4 of them");
         v4u xv[XG][MT];                                         // the next x group in flight
         v4u wq[kDepth][NT];
         uint32_t sq[kGroups][NT];                               // scale dwords of 4-chunk groups
