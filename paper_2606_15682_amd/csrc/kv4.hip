@@ -250,21 +250,10 @@ __device__ __forceinline__ uint32_t kv4_finite_max(const float (&d)[16]) {
     return m;
 }
 
-// Quantizes block blk (its 16 shifted values d, am = the largest |d| pattern,
-// NaN and Inf included) under G and stores codes and scale byte, or the
-// fake-quant values; returns the scale byte.
-template <int OUT>
-__device__ __forceinline__ uint32_t kv4_emit(const float (&d)[16], uint32_t am, int64_t blk, int64_t nb, bool narrow,
-                                             const Kv4G &G, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
-                                             uint16_t *__restrict__ y, int64_t ldy) {
-    const bool bad = am >= 0x7F800000u;
-    const uint32_t sbyte = bad ? 0x7Fu
-                           : am == 0u ? 0u
-                           : G.f32 ? kv4_scale_byte_f32(f32_from_bits(am), G.g, G.kg)
-                                   : kv4_scale_byte((double)f32_from_bits(am), G.gd);
-    const double S = (double)e4m3_value(sbyte) * G.gd;
-    const float Sf = e4m3_value(sbyte) * G.g;               // exact on the FP32 path
-    uint32_t c[16];
+// Exact element codes of one block (sign in bit 3, magnitude 0..7) by
+// threshold comparisons: FP32 thresholds for a power-of-two g, FP64 otherwise.
+__device__ __forceinline__ void kv4_exact_codes(const float (&d)[16], bool bad, uint32_t sbyte, const Kv4G &G,
+                                                double S, float Sf, uint32_t (&c)[16]) {
     if (G.f32) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
@@ -278,12 +267,74 @@ __device__ __forceinline__ uint32_t kv4_emit(const float (&d)[16], uint32_t am, 
             c[j] = bad ? 0u : (sbyte == 0u ? sign : (e1m2_mag(__builtin_fabs((double)d[j]), S) | sign));
         }
     }
-    if (OUT == kCodes) {
-        uint32_t lo = 0, hi = 0;
+}
+
+// Packs eight codes (sign in bit 3, magnitude 0..7 = |c|) of the integral
+// values c[0..8) into a word, code j in bits 4j..4j+3: magnitudes converted
+// into bytes (even j in one word, odd j in another), signs gathered from the
+// top bytes of the FP32 patterns.
+__device__ __forceinline__ uint32_t kv4_pack8(const float *c) {
+    uint32_t pe = 0u, po = 0u;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            lo |= c[j] << (4 * j);
-            hi |= c[8 + j] << (4 * j);
+    for (int k = 0; k < 4; ++k) {
+        pe = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_fabsf(c[2 * k]), k, pe);
+        po = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_fabsf(c[2 * k + 1]), k, po);
+    }
+    // top byte of c[2k] (resp. c[2k+1]) into byte k; 0x0C selects a zero byte
+    const uint32_t se = __builtin_amdgcn_perm(bits_from_f32(c[2]), bits_from_f32(c[0]), 0x0C0C0703u) |
+                        __builtin_amdgcn_perm(bits_from_f32(c[6]), bits_from_f32(c[4]), 0x07030C0Cu);
+    const uint32_t so = __builtin_amdgcn_perm(bits_from_f32(c[3]), bits_from_f32(c[1]), 0x0C0C0703u) |
+                        __builtin_amdgcn_perm(bits_from_f32(c[7]), bits_from_f32(c[5]), 0x07030C0Cu);
+    return (pe | (po << 4)) | ((se >> 4) & 0x08080808u) | (so & 0x80808080u);
+}
+
+// Quantizes block blk (its 16 shifted values d, am = the largest |d| pattern,
+// NaN and Inf included) under G and stores codes and scale byte, or the
+// fake-quant values; returns the scale byte.
+//
+// Fast path (power-of-two g, finite block, H = s g / 2 zero or a normal FP32
+// value, am <= 7 H, i.e. the scale did not saturate): the code magnitude is
+// the integer nearest |d| / H, ties to even (at most 7).  q = d * rcp(H) is
+// within 2^-19 of d / H (the reciprocal's ulp and one rounding, |q| <= 7), so
+// rint(q) is the code with d's sign (-0 for a small negative d) unless d / H
+// lies within 2^-19 of a half-integer; q - rint(q) is exact, and a block with
+// some |q - rint(q)| >= 0.5 - 2^-17 takes the threshold path instead.  The
+// fake-quant value c * H has at most 7 significant bits and is normal or
+// zero, so its top 16 bits are the bfloat16 value.
+template <int OUT>
+__device__ __forceinline__ uint32_t kv4_emit(const float (&d)[16], uint32_t am, int64_t blk, int64_t nb, bool narrow,
+                                             const Kv4G &G, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
+                                             uint16_t *__restrict__ y, int64_t ldy) {
+    const bool bad = am >= 0x7F800000u;
+    const uint32_t sbyte = bad ? 0x7Fu
+                           : am == 0u ? 0u
+                           : G.f32 ? kv4_scale_byte_f32(f32_from_bits(am), G.g, G.kg)
+                                   : kv4_scale_byte((double)f32_from_bits(am), G.gd);
+    const float Sf = e4m3_value(sbyte) * G.g;               // exact on the FP32 path
+    const float H = 0.5f * Sf;
+    const bool fast_ok = G.f32 && !bad && (sbyte == 0u || (H >= 0x1p-126f && f32_from_bits(am) <= 7.0f * H));
+    const float rh = (fast_ok && sbyte != 0u) ? __builtin_amdgcn_rcpf(H) : 0.0f;
+    float cf[16];
+    float emax = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        const float q = d[j] * rh;
+        cf[j] = __builtin_rintf(q);
+        emax = __builtin_fmaxf(emax, __builtin_fabsf(q - cf[j]));
+    }
+    const bool exact = !fast_ok || emax >= 0.5f - 0x1p-17f;
+    if (OUT == kCodes) {
+        uint32_t lo = kv4_pack8(cf), hi = kv4_pack8(cf + 8);
+        if (exact) {
+            uint32_t c[16];
+            kv4_exact_codes(d, bad, sbyte, G, (double)e4m3_value(sbyte) * G.gd, Sf, c);
+            lo = 0;
+            hi = 0;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                lo |= c[j] << (4 * j);
+                hi |= c[8 + j] << (4 * j);
+            }
         }
         *reinterpret_cast<uint2 *>(codes + blk * 8) = make_uint2(lo, hi);
         scales[blk] = (uint8_t)sbyte;
@@ -291,22 +342,30 @@ __device__ __forceinline__ uint32_t kv4_emit(const float (&d)[16], uint32_t am, 
         const int64_t r = narrow ? (int64_t)((uint32_t)blk / (uint32_t)nb) : blk / nb;
         uint32_t o[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            uint32_t h[2];
+        for (int i = 0; i < 8; ++i)   // bytes 2, 3 of each product: the bfloat16 patterns
+            o[i] = __builtin_amdgcn_perm(bits_from_f32(cf[2 * i + 1] * H), bits_from_f32(cf[2 * i] * H), 0x07060302u);
+        if (exact) {
+            const double S = (double)e4m3_value(sbyte) * G.gd;
+            uint32_t c[16];
+            kv4_exact_codes(d, bad, sbyte, G, S, Sf, c);
 #pragma unroll
-            for (int k = 0; k < 2; ++k) {
-                const uint32_t cc = c[2 * i + k];
-                uint32_t mag;
-                if (G.f32) {
-                    const float v = 0.5f * (float)(cc & 7u) * (sbyte == 0u ? 0.0f : Sf);
-                    mag = bf16_rne_from_float(v);
-                } else {
-                    const double v = 0.5 * (double)(cc & 7u) * (sbyte == 0u ? 0.0 : S);
-                    mag = bf16_rne_from_double(v);
+            for (int i = 0; i < 8; ++i) {
+                uint32_t h[2];
+#pragma unroll
+                for (int k = 0; k < 2; ++k) {
+                    const uint32_t cc = c[2 * i + k];
+                    uint32_t mag;
+                    if (G.f32) {
+                        const float v = 0.5f * (float)(cc & 7u) * (sbyte == 0u ? 0.0f : Sf);
+                        mag = bf16_rne_from_float(v);
+                    } else {
+                        const double v = 0.5 * (double)(cc & 7u) * (sbyte == 0u ? 0.0 : S);
+                        mag = bf16_rne_from_double(v);
+                    }
+                    h[k] = bad ? 0x7FC0u : (mag | ((cc & 8u) << 12));
                 }
-                h[k] = bad ? 0x7FC0u : (mag | ((cc & 8u) << 12));
+                o[i] = h[0] | (h[1] << 16);
             }
-            o[i] = h[0] | (h[1] << 16);
         }
         uint4 *dst = reinterpret_cast<uint4 *>(y + r * ldy + (blk - r * nb) * 16);
         dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
@@ -315,14 +374,13 @@ __device__ __forceinline__ uint32_t kv4_emit(const float (&d)[16], uint32_t am, 
     return sbyte;
 }
 
+// Largest |d| of a block as an FP32 pattern.  The IEEE maximum propagates NaN,
+// so a block with a NaN or an infinity gives a pattern >= 0x7F800000.
 __device__ __forceinline__ uint32_t kv4_block_max(const float (&d)[16]) {
-    uint32_t am = 0u;
+    float m = 0.0f;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-        const uint32_t a = bits_from_f32(d[j]) & 0x7FFFFFFFu;
-        am = am > a ? am : a;
-    }
-    return am;
+    for (int j = 0; j < 16; ++j) m = __builtin_elementwise_maximum(m, __builtin_fabsf(d[j]));
+    return bits_from_f32(m);
 }
 
 template <int OUT, int SRC>
@@ -351,13 +409,25 @@ __global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
     }
 }
 
-__device__ __forceinline__ uint32_t kv4_wave_min(uint32_t v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        const uint32_t o = __shfl_xor(v, off, 64);
-        v = v < o ? v : o;
-    }
-    return v;
+// Largest (kMax) or smallest v over the 64 lanes of a wave (all active), as a
+// wave-uniform value.  DPP row shifts by 1, 2, 4, 8 leave each row's extreme
+// in its lane 15; row_bcast:15 and row_bcast:31 carry it across rows to lane
+// 63.  Lanes with no source keep their own value (the operation is idempotent).
+template <int kCtrl, int kRows>
+__device__ __forceinline__ uint32_t kv4_dpp(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, kCtrl, kRows, 0xF, false);
+}
+
+template <bool kMax>
+__device__ __forceinline__ uint32_t kv4_wave_reduce(uint32_t v) {
+    auto op = [](uint32_t a, uint32_t b) { return kMax ? (a > b ? a : b) : (a < b ? a : b); };
+    v = op(v, kv4_dpp<0x111, 0xF>(v));   // row_shr:1
+    v = op(v, kv4_dpp<0x112, 0xF>(v));   // row_shr:2
+    v = op(v, kv4_dpp<0x114, 0xF>(v));   // row_shr:4
+    v = op(v, kv4_dpp<0x118, 0xF>(v));   // row_shr:8
+    v = op(v, kv4_dpp<0x142, 0xA>(v));   // row_bcast:15 into rows 1 and 3
+    v = op(v, kv4_dpp<0x143, 0xC>(v));   // row_bcast:31 into rows 2 and 3
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
 // One pass over x for a computed g.  g needs the amax of all of d, known only
@@ -396,12 +466,12 @@ __global__ __launch_bounds__(kThreads) void kv4_quantize_deferred_kernel(
         const bool bad = am >= 0x7F800000u;
         const uint32_t fm = bad ? kv4_finite_max(d) : am;
         mloc = mloc > fm ? mloc : fm;
-        const uint32_t segmax = kv4_wave_max(fm);
+        const uint32_t segmax = kv4_wave_reduce<true>(fm);
         const Kv4G Gr = kv4_make_g(kv4_global_scale(segmax));
         uint32_t sbyte = 0u;
         if (act) sbyte = kv4_emit<OUT>(d, am, blk, nb, narrow, Gr, codes, scales, y, ldy);
         const bool live = act && am != 0u && !bad;
-        const uint32_t emin = kv4_wave_min(live ? sbyte >> 3 : 0xFFu);
+        const uint32_t emin = kv4_wave_reduce<false>(live ? sbyte >> 3 : 0xFFu);
         if (lane == 0) seg_table[base / 64] = segmax ? (uint16_t)((uint32_t)(Gr.kg + 127) | (emin << 8)) : (uint16_t)0;
     }
     __shared__ uint32_t red[kThreads / 64];

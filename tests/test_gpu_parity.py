@@ -361,6 +361,43 @@ def test_kv4_one_pass_segments(shifted):
     assert_kv4_parity(xb, shift)
 
 
+def _kv4_midpoint_targets():
+    """FP32 values at and next to the E1M2 rounding midpoints.  Block b sets
+    its amax to 7 H (H = s g / 2 for the scale s it gets, any of the eight
+    E4M3 mantissas), the other 15 elements are +-((k + 1/2) H + j ulp),
+    k = 0..6, j = -2..2: exact ties and values one or two FP32 ulps away."""
+    vals = []
+    combos = [(k, j) for k in range(7) for j in range(-2, 3)]
+    for m in range(8, 16):
+        for e in (-9, -3, 0, 5):
+            H = np.float32(m / 8.0 * 2.0 ** e)
+            for b0 in range(0, len(combos), 15):
+                blk = [np.float32(7.0) * H]
+                for i, (k, j) in enumerate(combos[b0:b0 + 15]):
+                    t = np.float32((k + 0.5) * H)
+                    for _ in range(abs(j)):
+                        t = np.nextafter(t, np.float32(np.inf if j > 0 else -np.inf), dtype=np.float32)
+                    blk.append(-t if i % 2 else t)
+                blk += [np.float32(0.0)] * (16 - len(blk))
+                vals += blk
+    return np.array(vals, np.float32)
+
+
+@pytest.mark.parametrize("g", [None, 1.0, 2.0 ** -3])
+def test_kv4_rounding_near_midpoints(g):
+    """d = x - shift with x = +-0 makes d any FP32 value, so the elements sit
+    exactly on, or one or two ulps beside, the midpoints between codes."""
+    log("kv4 near-midpoint rounding g=%s" % g)
+    t = _kv4_midpoint_targets()
+    C = t.size
+    x = np.zeros((3, C), np.uint16)
+    x[1] = 0x8000
+    x[2] = indep.to_bf16_bits(np.random.default_rng(3).normal(0.0, 2.0 ** -12, C))
+    assert_kv4_parity(x, -t, g=g)
+    wide = np.zeros((2, 4224), np.uint16)                      # shift read from global memory (> 4096 channels)
+    assert_kv4_parity(wide, -np.resize(t, 4224), g=g)
+
+
 def test_kv4_empty_writes_unit_scale():
     log("kv4 empty")
     x = torch.empty((0, 128), dtype=torch.bfloat16, device=DEV)
