@@ -110,3 +110,55 @@ def test_step_graph_replays_match_eager(fmt, M, N, K):
             assert torch.equal(got.view(torch.uint8), want.view(torch.uint8)), \
                 f"replay {rep}: output {i} differs from the eager step"
     log("graph replays match")
+
+
+def test_kv4_graph_replays_match_eager():
+    """KV4 quantize (computed g: one pass + fix-up, and a given g) and
+    fake-quant of shifted keys, captured and replayed."""
+    T, C = 300, 1024
+    log(f"graph kv4 T={T} C={C}")
+    gen = torch.Generator().manual_seed(77)
+    mu = (torch.randn(C, generator=gen) * 2.0).to(DEV)
+    def keys(seed):
+        g2 = torch.Generator().manual_seed(seed)
+        return (torch.randn(T, C, generator=g2) + mu.cpu()).to(torch.bfloat16).to(DEV)
+    def bufs():
+        return [torch.empty((T, C // 2), dtype=torch.uint8, device=DEV),
+                torch.empty((T, C // 16), dtype=torch.uint8, device=DEV),
+                torch.empty(1, dtype=torch.float32, device=DEV),
+                torch.empty((T, C), dtype=torch.bfloat16, device=DEV),
+                torch.empty(1, dtype=torch.float32, device=DEV),
+                torch.empty((T, C // 2), dtype=torch.uint8, device=DEV),
+                torch.empty((T, C // 16), dtype=torch.uint8, device=DEV)]
+    gq = torch.tensor([2.0 ** -7], dtype=torch.float32, device=DEV)
+    def step(k, b):
+        reqat.quantize_kv4(k, mu, out=(b[0], b[1]), g_out=b[2])
+        reqat.fakequant_kv4(k, mu, out=b[3], g_out=b[4])
+        reqat.quantize_kv4(k, mu, tensor_scale=gq, out=(b[5], b[6]))
+    k1, k2 = keys(1), keys(2)
+    b1, b2 = bufs(), bufs()
+    reqat.workspace(torch.device(DEV))
+    step(k1, b1)
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in b1]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step(k1, b1)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step(k1, b1)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in b1:
+            t.fill_(0xA5) if t.dtype == torch.uint8 else t.fill_(float("nan"))
+        step(k2, b2)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (got, want) in enumerate(zip(b1, ref)):
+            assert torch.equal(got.view(torch.uint8), want.view(torch.uint8)), \
+                f"replay {rep}: kv4 output {i} differs from the eager step"
+    log("kv4 graph replays match")
