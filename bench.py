@@ -349,11 +349,17 @@ def bench_w4a16(args, w):
     wsp = torch.empty(max(1, reqat.reqat_w4a16_workspace_bytes(M, N, K)), dtype=torch.uint8, device=dev)
     flops = 2.0 * M * N * K
     nbytes = N * K * (0.5 + 1.0 / 32) + M * K * 2.0 + M * N * 2.0       # W codes + scales, x, Y (bf16)
-    # rotate through copies of the weights (> 512 MB in all): every step streams them from HBM
+    # rotate through copies of the weights (> 512 MB in all): every step streams them from HBM.
+    # Served weights are stored once in the product's packed image (pack_w4a16,
+    # untimed, like the quantization); the product from the row-major codes is context.
     ncp = n_copies(N * K * (0.5 + 1.0 / 32), args)
     copies = [(wc0.clone(), ws0.clone()) for _ in range(ncp)]
+    packed = [reqat.pack_w4a16(a, b) for a, b in copies]
 
     def step(i):
+        reqat.gemm_w4a16_packed(x, packed[i], N, out_dtype=torch.bfloat16, out=y, ws=wsp)
+
+    def step_rowmajor(i):
         wc, ws = copies[i]
         reqat.gemm_w4a16(x, wc, ws, out_dtype=torch.bfloat16, out=y, ws=wsp)
 
@@ -362,9 +368,11 @@ def bench_w4a16(args, w):
     ms_eager, ms_eager_dev = timed_rotation(step, ncp, args)
     ms_step = graph_rotation_ms(step, ncp, args)
     ms_kernel = ms_step
+    ms_rowmajor = graph_rotation_ms(step_rowmajor, ncp, args)
     # context: the same weights every step (they then sit in the Infinity Cache)
     _, ms_resident = timed_rotation(lambda i: step(0), ncp, args)
     gbs = nbytes / (ms_kernel * 1e-3) / 1e9
+    ksplit = reqat.reqat_w4a16_workspace_bytes(M, N, K) // (4 * M * N)   # FP32 partial sums per split
     out = {
         "metric": METRIC,
         "value": round(nbytes / (ms_step * 1e-3) / 1e9, 1),
@@ -380,15 +388,21 @@ def bench_w4a16(args, w):
         "data": "synthetic (seeded; Student-t or Gaussian-with-outlier activations, N(0,0.02) weights)",
         "config": {"workload": w.name, "M": M, "N": N, "K": K, "format": "mxfp4 weights, bf16 activations",
                    "gemm_out": "bf16", "global_batch": M, "parallelism": "single GPU",
-                   "step": "W4A16 GEMM (weights pre-quantized, untimed), each step on another of %d weight "
-                           "copies (%.0f MB in all, twice the Infinity Cache), the %d steps captured in one "
+                   "step": "W4A16 GEMM (weights pre-quantized and packed, untimed), each step on another of %d "
+                           "weight copies (%.0f MB in all, twice the Infinity Cache), the %d steps captured in one "
                            "HIP graph, time per step" % (ncp, ncp * N * K * (0.5 + 1.0 / 32) / 1e6, ncp)},
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK["hbm"], "unit": "GB/s",
                      "frac": round(gbs / PEAK["hbm"], 4), "traffic": None,
-                     "kernel": "gemm_w4a16_kernel (MXFP4 W4A16, algorithmic bytes %d)" % int(nbytes)},
-        "kernels": {"gemm_w4a16": {"ms": round(ms_kernel, 4), "GB/s": round(gbs, 1),
-                                   "TFLOP/s": round(flops / (ms_kernel * 1e-3) / 1e12, 2),
-                                   "note": "per launch in the graph, weights from HBM (rotating copies)"},
+                     "kernel": "gemm_w4a16_kernel on the packed weight image%s (MXFP4 W4A16, algorithmic bytes %d)"
+                               % (" + gemm_w4a16_reduce (K split %d ways)" % ksplit if ksplit > 1 else "",
+                                  int(nbytes))},
+        "kernels": {"gemm_w4a16_packed": {"ms": round(ms_kernel, 4), "GB/s": round(gbs, 1),
+                                          "TFLOP/s": round(flops / (ms_kernel * 1e-3) / 1e12, 2),
+                                          "note": "per launch in the graph, weights from HBM (rotating copies)"},
+                    "gemm_w4a16_rowmajor": {"ms": round(ms_rowmajor, 4),
+                                            "GB/s": round(nbytes / (ms_rowmajor * 1e-3) / 1e9, 1),
+                                            "note": "context: the same product from the row-major codes and "
+                                                    "scales (reqat_gemm_w4a16), per launch in the graph"},
                     "eager": {"ms": round(ms_eager, 4), "device_ms": round(ms_eager_dev, 4),
                               "note": "context: eager launches from Python, wall clock and HIP-event time"},
                     "cache_resident": {"ms": round(ms_resident, 4),

@@ -66,7 +66,7 @@
 extern "C" {
 #endif
 
-#define REQAT_ABI_VERSION 9
+#define REQAT_ABI_VERSION 10
 
 /* The enums travel as C ints.  Compiled as C++ they get int as their fixed
  * underlying type, so any int a caller passes is a value the library may
@@ -213,6 +213,39 @@ reqat_status reqat_gemm_w4a16(int64_t M, int64_t N, int64_t K, const void *x, in
 
 /* Bytes of workspace reqat_gemm_w4a16 needs for an M x N x K product (0: none; 0 on bad arguments). */
 size_t reqat_w4a16_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+/*
+ * Packed W4A16 weight image (weights are fixed in W4A16 serving, so they are
+ * re-laid out once, when loaded): the MXFP4 weights of reqat_gemm_w4a16 in
+ * the order its matrix-core tiles consume them, so that the product reads
+ * each wave's weights as contiguous 1 KB runs instead of 64 bytes from each
+ * of 16 rows.  Rows go in groups of 16 (the last padded with zero codes and
+ * scales), K in chunks of 128 elements; with G = ceil(N / 16), C = K / 128:
+ *   bytes [0, 1024 G C): unit (g, c) at 1024 (g C + c) holds, at byte
+ *     16 (r + 16 q) + i, byte 16 q + i of chunk c of row 16 g + r, i.e.
+ *     w_codes[16 g + r][64 c + 16 q + i]  (r < 16, q < 4, i < 16);
+ *   bytes [1024 G C, 1088 G C): unit (g, c) at 1024 G C + 64 (g C + c) holds,
+ *     at byte 4 r + j, w_scales[16 g + r][4 c + j]  (j < 4).
+ * reqat_w4a16_packed_bytes: the image's size, 1088 G C (0 on bad arguments:
+ * N < 0, K < 0 or K % 128).
+ * reqat_pack_w4a16: writes the image of w_codes [N][K/2] (16-byte aligned) and
+ * w_scales [N][K/32] (4-byte aligned) into `packed` (16-byte aligned, not
+ * overlapping them), on `stream`.  A pure re-layout: no value changes.
+ * Errors: REQAT_E_SHAPE (N < 0, K < 0, K % 128), REQAT_E_NULL, REQAT_E_ALIGN.
+ */
+size_t reqat_w4a16_packed_bytes(int64_t N, int64_t K);
+reqat_status reqat_pack_w4a16(const uint8_t *w_codes, const uint8_t *w_scales, int64_t N, int64_t K, void *packed,
+                              void *stream);
+
+/*
+ * reqat_gemm_w4a16 on the packed image of its weights (same result, bit for
+ * bit: the same splits and the same order of operations).  packed: the
+ * reqat_w4a16_packed_bytes(N, K) bytes reqat_pack_w4a16 wrote (16-byte
+ * aligned).  Other arguments, requirements, workspace and errors as
+ * reqat_gemm_w4a16.
+ */
+reqat_status reqat_gemm_w4a16_packed(int64_t M, int64_t N, int64_t K, const void *x, int64_t ldx, const void *packed,
+                                     void *y, reqat_dtype y_dtype, int64_t ldy, void *workspace, void *stream);
 
 /*
  * KV-cache quantization of the NVFP4 W4A4KV4 setting: E1M2 elements (the KV4

@@ -227,7 +227,43 @@ reqat_status reqat_gemm_w4a16(int64_t M, int64_t N, int64_t K, const void *x, in
         return REQAT_E_ALIGN;
     if (reinterpret_cast<uintptr_t>(y) & (y_dtype == REQAT_DT_BF16 ? 1u : 3u)) return REQAT_E_ALIGN;
     if (reinterpret_cast<uintptr_t>(workspace) & 3u) return REQAT_E_ALIGN;
-    hipError_t e = launch_gemm_w4a16(M, N, K, reinterpret_cast<const uint16_t *>(x), ldx, w_codes, w_scales, y,
+    hipError_t e = launch_gemm_w4a16(M, N, K, reinterpret_cast<const uint16_t *>(x), ldx, w_codes, w_scales, false,
+                                     y, y_dtype == REQAT_DT_BF16, ldy, reinterpret_cast<float *>(workspace),
+                                     reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
+}
+
+size_t reqat_w4a16_packed_bytes(int64_t N, int64_t K) {
+    if (N < 0 || K < 0 || K % 128) return 0;
+    return w4a16_packed_bytes(N, K);
+}
+
+reqat_status reqat_pack_w4a16(const uint8_t *w_codes, const uint8_t *w_scales, int64_t N, int64_t K, void *packed,
+                              void *stream) {
+    if (N < 0 || K < 0 || K % 128) return REQAT_E_SHAPE;
+    if (N == 0 || K == 0) return REQAT_OK;
+    if (!w_codes || !w_scales || !packed) return REQAT_E_NULL;
+    if (!aligned16(w_codes) || (reinterpret_cast<uintptr_t>(w_scales) & 3u) || !aligned16(packed))
+        return REQAT_E_ALIGN;
+    hipError_t e = launch_w4a16_pack(w_codes, w_scales, N, K, reinterpret_cast<uint8_t *>(packed),
+                                     reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
+}
+
+reqat_status reqat_gemm_w4a16_packed(int64_t M, int64_t N, int64_t K, const void *x, int64_t ldx, const void *packed,
+                                     void *y, reqat_dtype y_dtype, int64_t ldy, void *workspace, void *stream) {
+    if (y_dtype != REQAT_DT_F32 && y_dtype != REQAT_DT_BF16) return REQAT_E_ENUM;
+    if (M < 0 || N < 0 || K < 0) return REQAT_E_SHAPE;
+    if (K % 128 || ldx < K || ldy < N) return REQAT_E_SHAPE;
+    if (M == 0 || N == 0) return REQAT_OK;
+    if (!y || (K > 0 && (!x || !packed))) return REQAT_E_NULL;
+    if (gemm_w4a16_workspace_bytes(M, N, K) > 0 && !workspace) return REQAT_E_NULL;
+    if (K > 0 && (!aligned16(x) || ldx % 8 || !aligned16(packed))) return REQAT_E_ALIGN;
+    if (reinterpret_cast<uintptr_t>(y) & (y_dtype == REQAT_DT_BF16 ? 1u : 3u)) return REQAT_E_ALIGN;
+    if (reinterpret_cast<uintptr_t>(workspace) & 3u) return REQAT_E_ALIGN;
+    const uint8_t *pc = reinterpret_cast<const uint8_t *>(packed);
+    const uint8_t *ps = pc + (size_t)((N + 15) / 16) * (size_t)(K / 128) * 1024u;
+    hipError_t e = launch_gemm_w4a16(M, N, K, reinterpret_cast<const uint16_t *>(x), ldx, pc, ps, true, y,
                                      y_dtype == REQAT_DT_BF16, ldy, reinterpret_cast<float *>(workspace),
                                      reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;

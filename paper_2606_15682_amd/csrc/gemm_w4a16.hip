@@ -89,7 +89,7 @@ __device__ __forceinline__ v8bf decode_step(const v4u &w, uint32_t sb, int s) {
 // thread per 16-row tile), stored to LDS and read by all four waves; each LDS
 // fragment feeds NT MFMAs.  With one split the results go to y; otherwise to the FP32 partial
 // sums part[ks][m][n], added in split order by gemm_w4a16_reduce.
-template <int MT, int NT, int kDepth, int XG>
+template <int MT, int NT, int kDepth, int XG, bool kPacked>
 __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
     int64_t M, int64_t N, int64_t K, const uint16_t *__restrict__ x, int64_t ldx,
     const uint8_t *__restrict__ w_codes, const uint8_t *__restrict__ w_scales, void *__restrict__ y,
@@ -104,6 +104,11 @@ __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
     int64_t nrow[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) nrow[t] = (n0 + 16 * t + r) < N ? (n0 + 16 * t + r) : N - 1;
+    // packed image: 16-row group of each tile (past the last group: the last, never stored)
+    const int64_t ngrp = (N + 15) / 16;
+    int64_t grp[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) grp[t] = (n0 / 16 + t) < ngrp ? (n0 / 16 + t) : ngrp - 1;
     const int ks = blockIdx.y;
     const int64_t m0 = (int64_t)blockIdx.z * 16 * MT;
     const int64_t nch = K / 128;
@@ -127,18 +132,22 @@ __global__ __launch_bounds__(kThreads) void gemm_w4a16_kernel(
         for (int mt = 0; mt < MT; ++mt) *reinterpret_cast<v4u *>(&xs[buf][16 * mt + xr][128 * u + xc]) = v[mt];
     };
     // the lane's 32 codes (MX block kg of the chunk) of each of its weight rows
+    // (packed: the 1 KB of group grp, chunk c, in lane order)
     auto load_w = [&](int64_t c, v4u (&v)[NT]) {
 #pragma unroll
         for (int t = 0; t < NT; ++t)
-            v[t] = *reinterpret_cast<const v4u *>(w_codes + nrow[t] * (K / 2) + (c * 4 + kg) * 16);
+            v[t] = kPacked ? *reinterpret_cast<const v4u *>(w_codes + ((grp[t] * nch + c) << 10) + lane * 16)
+                           : *reinterpret_cast<const v4u *>(w_codes + nrow[t] * (K / 2) + (c * 4 + kg) * 16);
     };
     // Scale bytes of four chunks in one load: lane (r, kg) takes the dword of
     // chunk c + kg (its four blocks' E8M0 bytes; K % 128 == 0 keeps it
     // aligned); the lanes of chunk c + u read it from lane r + 16u.
+    // (packed: the 64 scale bytes of group grp, chunk c, four per row)
     auto load_s = [&](int64_t c, uint32_t (&v)[NT]) {
 #pragma unroll
         for (int t = 0; t < NT; ++t)
-            v[t] = *reinterpret_cast<const uint32_t *>(w_scales + nrow[t] * (K / 32) + c * 4);
+            v[t] = kPacked ? *reinterpret_cast<const uint32_t *>(w_scales + ((grp[t] * nch + c) << 6) + r * 4)
+                           : *reinterpret_cast<const uint32_t *>(w_scales + nrow[t] * (K / 32) + c * 4);
     };
 
     v4f acc[MT][NT];
@@ -268,7 +277,7 @@ __global__ __launch_bounds__(kThreads) void gemm_w4a16_reduce(int64_t M, int64_t
 
 template <int MT>
 hipError_t launch_mt(int64_t M, int64_t N, int64_t K, const uint16_t *x, int64_t ldx, const uint8_t *w_codes,
-                     const uint8_t *w_scales, void *y, bool y_bf16, int64_t ldy, int KS, float *part,
+                     const uint8_t *w_scales, bool packed, void *y, bool y_bf16, int64_t ldy, int KS, float *part,
                      hipStream_t stream) {
     constexpr int NT = REQAT_W16_NT;
     const dim3 grid((unsigned)((N + 64 * NT - 1) / (64 * NT)), (unsigned)KS,
@@ -276,8 +285,12 @@ hipError_t launch_mt(int64_t M, int64_t N, int64_t K, const uint16_t *x, int64_t
     // chunks in flight per wave (8 measured no faster than 4)
     constexpr int kDepth = MT == 1 ? REQAT_W16_DEPTH1 : 4;
     constexpr int XG = MT == 1 ? REQAT_W16_XG : 1;
-    hipLaunchKernelGGL((gemm_w4a16_kernel<MT, NT, kDepth, XG>), grid, dim3(kThreads), 0, stream, M, N, K, x, ldx, w_codes,
-                       w_scales, y, (int)y_bf16, ldy, KS, part);
+    if (packed)
+        hipLaunchKernelGGL((gemm_w4a16_kernel<MT, NT, kDepth, XG, true>), grid, dim3(kThreads), 0, stream, M, N, K, x,
+                           ldx, w_codes, w_scales, y, (int)y_bf16, ldy, KS, part);
+    else
+        hipLaunchKernelGGL((gemm_w4a16_kernel<MT, NT, kDepth, XG, false>), grid, dim3(kThreads), 0, stream, M, N, K,
+                           x, ldx, w_codes, w_scales, y, (int)y_bf16, ldy, KS, part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || KS == 1) return e;
     int64_t rgrid = (M * N + kThreads - 1) / kThreads;
@@ -289,7 +302,46 @@ hipError_t launch_mt(int64_t M, int64_t N, int64_t K, const uint16_t *x, int64_t
 
 int row_tile(int64_t M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
 
+// Packed weight image (one thread per 16 code bytes, and per scale dword):
+// unit (G, c) of 16-row group G and 128-element chunk c holds 1024 code bytes,
+// piece q (bytes 16q .. 16q+15 of the chunk) of row 16G + r at byte
+// 16 (r + 16 q), then, in the scale part, that row's four E8M0 bytes of the
+// chunk at byte 4 r.  Rows past N are zero.
+__global__ __launch_bounds__(kThreads) void w4a16_pack_kernel(const uint8_t *__restrict__ codes,
+                                                              const uint8_t *__restrict__ scales, int64_t N,
+                                                              int64_t K, uint8_t *__restrict__ packed) {
+    const int64_t nch = K / 128, units = (N + 15) / 16 * nch;
+    uint8_t *pscales = packed + (units << 10);
+    for (int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x; p < units * 64;
+         p += (int64_t)gridDim.x * kThreads) {
+        const int64_t u = p >> 6, g = u / nch, c = u - g * nch;
+        const int l = (int)(p & 63), r = l & 15, q = l >> 4;
+        const int64_t row = 16 * g + r;
+        v4u v = v4u{0u, 0u, 0u, 0u};
+        uint32_t sc = 0u;
+        if (row < N) {
+            v = *reinterpret_cast<const v4u *>(codes + row * (K / 2) + c * 64 + q * 16);
+            sc = *reinterpret_cast<const uint32_t *>(scales + row * (K / 32) + c * 4);
+        }
+        *reinterpret_cast<v4u *>(packed + (u << 10) + l * 16) = v;
+        if (q == 0) *reinterpret_cast<uint32_t *>(pscales + (u << 6) + r * 4) = sc;
+    }
+}
+
 }  // namespace
+
+size_t w4a16_packed_bytes(int64_t N, int64_t K) { return (size_t)((N + 15) / 16) * (size_t)(K / 128) * 1088u; }
+
+hipError_t launch_w4a16_pack(const uint8_t *codes, const uint8_t *scales, int64_t N, int64_t K, uint8_t *packed,
+                             hipStream_t stream) {
+    const int64_t pieces = (N + 15) / 16 * (K / 128) * 64;
+    if (pieces == 0) return hipSuccess;
+    int64_t grid = (pieces + kThreads - 1) / kThreads;
+    if (grid > 8192) grid = 8192;
+    hipLaunchKernelGGL(w4a16_pack_kernel, dim3((unsigned)grid), dim3(kThreads), 0, stream, codes, scales, N, K,
+                       packed);
+    return hipGetLastError();
+}
 
 // K splits: enough workgroups to cover the chip (REQAT_W16_TARGET) when the
 // weight rows alone give fewer than 256, at most REQAT_W16_KSMAX, and at most
@@ -311,14 +363,14 @@ size_t gemm_w4a16_workspace_bytes(int64_t M, int64_t N, int64_t K) {
 }
 
 hipError_t launch_gemm_w4a16(int64_t M, int64_t N, int64_t K, const uint16_t *x, int64_t ldx,
-                             const uint8_t *w_codes, const uint8_t *w_scales, void *y, bool y_bf16,
+                             const uint8_t *w_codes, const uint8_t *w_scales, bool packed, void *y, bool y_bf16,
                              int64_t ldy, float *workspace, hipStream_t stream) {
     if (M == 0 || N == 0) return hipSuccess;
     const int ks = gemm_w4a16_splits(M, N, K);
     switch (row_tile(M)) {
-    case 1: return launch_mt<1>(M, N, K, x, ldx, w_codes, w_scales, y, y_bf16, ldy, ks, workspace, stream);
-    case 2: return launch_mt<2>(M, N, K, x, ldx, w_codes, w_scales, y, y_bf16, ldy, ks, workspace, stream);
-    default: return launch_mt<4>(M, N, K, x, ldx, w_codes, w_scales, y, y_bf16, ldy, ks, workspace, stream);
+    case 1: return launch_mt<1>(M, N, K, x, ldx, w_codes, w_scales, packed, y, y_bf16, ldy, ks, workspace, stream);
+    case 2: return launch_mt<2>(M, N, K, x, ldx, w_codes, w_scales, packed, y, y_bf16, ldy, ks, workspace, stream);
+    default: return launch_mt<4>(M, N, K, x, ldx, w_codes, w_scales, packed, y, y_bf16, ldy, ks, workspace, stream);
     }
 }
 

@@ -53,9 +53,14 @@ hipError_t launch_quantize_rht(QuantOut out, const uint16_t *x, int64_t rows, in
 // `workspace` holds gemm_w4a16_workspace_bytes(M, N, K) bytes of split-K partial sums.
 int gemm_w4a16_splits(int64_t M, int64_t N, int64_t K);
 size_t gemm_w4a16_workspace_bytes(int64_t M, int64_t N, int64_t K);
+// packed: w_codes / w_scales are the code and scale parts of the packed image
+// that launch_w4a16_pack writes (w4a16_packed_bytes(N, K) bytes).
 hipError_t launch_gemm_w4a16(int64_t M, int64_t N, int64_t K, const uint16_t *x, int64_t ldx,
-                             const uint8_t *w_codes, const uint8_t *w_scales, void *y, bool y_bf16,
+                             const uint8_t *w_codes, const uint8_t *w_scales, bool packed, void *y, bool y_bf16,
                              int64_t ldy, float *workspace, hipStream_t stream);
+size_t w4a16_packed_bytes(int64_t N, int64_t K);
+hipError_t launch_w4a16_pack(const uint8_t *codes, const uint8_t *scales, int64_t N, int64_t K, uint8_t *packed,
+                             hipStream_t stream);
 
 // KV4 (E1M2 elements, E4M3 block scales of 16, FP32 global scale) of x - shift.
 // A computed g takes one pass over x and a fix-up kernel when the segment

@@ -55,6 +55,9 @@ SIGNATURES = {
     "reqat_fakequant_kv4": (_INT, [_VP, _I64, _I64, _I64, _VP, _VP, _I64, _VP, _INT, _VP, _VP]),
     "reqat_gemm_w4a16": (_INT, [_I64, _I64, _I64, _VP, _I64, _VP, _VP, _VP, _INT, _I64, _VP, _VP]),
     "reqat_w4a16_workspace_bytes": (ctypes.c_size_t, [_I64, _I64, _I64]),
+    "reqat_w4a16_packed_bytes": (ctypes.c_size_t, [_I64, _I64]),
+    "reqat_pack_w4a16": (_INT, [_VP, _VP, _I64, _I64, _VP, _VP]),
+    "reqat_gemm_w4a16_packed": (_INT, [_I64, _I64, _I64, _VP, _I64, _VP, _VP, _INT, _I64, _VP, _VP]),
     "reqat_quantize_mxfp4_rht": (_INT, [_VP, _I64, _I64, _I64, ctypes.c_uint32, _VP, _VP, _VP]),
     "reqat_fakequant_mxfp4_rht": (_INT, [_VP, _I64, _I64, _I64, ctypes.c_uint32, _VP, _I64, _VP]),
     "reqat_workspace_bytes": (ctypes.c_size_t, []),
@@ -142,6 +145,18 @@ def reqat_gemm_w4a16(M, N, K, x, ldx, w_codes, w_scales, y, y_dtype, ldy, worksp
 
 def reqat_w4a16_workspace_bytes(M, N, K) -> int:
     return load().reqat_w4a16_workspace_bytes(M, N, K)
+
+
+def reqat_w4a16_packed_bytes(N, K) -> int:
+    return load().reqat_w4a16_packed_bytes(N, K)
+
+
+def reqat_pack_w4a16(w_codes, w_scales, N, K, packed, stream):
+    return load().reqat_pack_w4a16(w_codes, w_scales, N, K, packed, stream)
+
+
+def reqat_gemm_w4a16_packed(M, N, K, x, ldx, packed, y, y_dtype, ldy, workspace, stream):
+    return load().reqat_gemm_w4a16_packed(M, N, K, x, ldx, packed, y, y_dtype, ldy, workspace, stream)
 
 
 def reqat_quantize_mxfp4_rht(x, rows, cols, ldx, signs, codes, scales, stream):
@@ -491,6 +506,51 @@ def gemm_w4a16(x: torch.Tensor, w_codes, w_scales, out_dtype=torch.float32, out=
     st = reqat_gemm_w4a16(M, N, K, x.data_ptr(), ldx, w_codes.data_ptr(), w_scales.data_ptr(), y.data_ptr(),
                           dt, ldy, _ptr(ws), _stream(x.device))
     _check(st, "reqat_gemm_w4a16")
+    return y
+
+
+def pack_w4a16(w_codes, w_scales, out=None):
+    """Packed weight image of MXFP4 weights (codes [N, K/2], scales [N, K/32])
+    for gemm_w4a16_packed: a uint8 tensor of reqat_w4a16_packed_bytes(N, K)."""
+    if w_codes.dim() != 2:
+        raise ValueError("w_codes must be 2-D")
+    N, K = w_codes.shape[0], w_codes.shape[1] * 2
+    if K % 128:
+        raise ValueError("K must be a multiple of 128")
+    _packed_u8(w_codes, N, K // 2, w_codes.device, "w_codes")
+    _packed_u8(w_scales, N, K // 32, w_codes.device, "w_scales")
+    nbytes = reqat_w4a16_packed_bytes(N, K)
+    packed = out if out is not None else torch.empty(max(nbytes, 16), dtype=torch.uint8, device=w_codes.device)
+    if packed.dtype != torch.uint8 or not packed.is_contiguous() or packed.numel() < nbytes \
+            or packed.device != w_codes.device:
+        raise ValueError("out must be a contiguous uint8 tensor of at least %d bytes on the weights' device" % nbytes)
+    _require_cuda(w_codes, "w_codes")
+    st = reqat_pack_w4a16(w_codes.data_ptr(), w_scales.data_ptr(), N, K, packed.data_ptr(), _stream(w_codes.device))
+    _check(st, "reqat_pack_w4a16")
+    return packed
+
+
+def gemm_w4a16_packed(x: torch.Tensor, packed, N, out_dtype=torch.float32, out=None, ws=None):
+    """gemm_w4a16 on the packed image (pack_w4a16) of N x K weights: same result, bit for bit."""
+    M, K, ldx = _x2d(x)
+    if K % 128:
+        raise ValueError("K must be a multiple of 128")
+    nbytes_w = reqat_w4a16_packed_bytes(N, K)
+    if packed.dtype != torch.uint8 or not packed.is_contiguous() or packed.numel() < nbytes_w \
+            or packed.device != x.device:
+        raise ValueError("packed must be the contiguous uint8 image of %d bytes on x's device" % nbytes_w)
+    dt = _dtype_arg(out_dtype)
+    y = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=x.device)
+    ldy = _out2d(y, M, N, out_dtype, x.device, "out")
+    nbytes = reqat_w4a16_workspace_bytes(M, N, K)
+    if ws is None and nbytes:
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
+    if ws is not None:
+        _workspace_arg(ws, nbytes, x.device)
+    _require_cuda(x, 'x')
+    st = reqat_gemm_w4a16_packed(M, N, K, x.data_ptr(), ldx, packed.data_ptr(), y.data_ptr(), dt, ldy, _ptr(ws),
+                                 _stream(x.device))
+    _check(st, "reqat_gemm_w4a16_packed")
     return y
 
 

@@ -81,7 +81,7 @@ def test_probe_library_is_separate_and_launch_only():
 
 
 def test_small_queries(lib):
-    assert reqat.reqat_abi_version() == 9
+    assert reqat.reqat_abi_version() == 10
     assert reqat.reqat_workspace_bytes() == 4 * 4096 + 2 * (1 << 19)   # partials + segment table
     for s in range(8):
         assert reqat.reqat_status_str(s).startswith(reqat.STATUS[s])
@@ -195,6 +195,48 @@ def test_w4a16_validation(lib):
     assert g16(x=P + 2) == E_ALIGN and g16(ldx=132) == E_ALIGN and g16(wc=P + 8) == E_ALIGN
     assert g16(ws=P + 2) == E_ALIGN and g16(ws=P + 1) == E_ALIGN
     assert g16(y=P + 2) == E_ALIGN and g16(y=P + 1, dt=1) == E_ALIGN
+
+
+def test_w4a16_packed_validation(lib):
+    """Packed weight image: size 1088 bytes per (16-row group, 128-element
+    chunk), host-side argument checks of the pack and of the packed product."""
+    assert reqat.reqat_w4a16_packed_bytes(5120, 27648) == 320 * 216 * 1088
+    assert reqat.reqat_w4a16_packed_bytes(17, 256) == 2 * 2 * 1088        # a partial last group is padded
+    assert reqat.reqat_w4a16_packed_bytes(16, 100) == 0 and reqat.reqat_w4a16_packed_bytes(-1, 128) == 0
+    assert reqat.reqat_w4a16_packed_bytes(0, 128) == 0 and reqat.reqat_w4a16_packed_bytes(16, 0) == 0
+    pk = lambda wc=P, ws=P, N=8, K=128, out=P: reqat.reqat_pack_w4a16(wc, ws, N, K, out, None)
+    assert pk(K=96) == E_SHAPE and pk(N=-1) == E_SHAPE
+    assert pk(N=0, wc=None, ws=None, out=None) == 0 and pk(K=0, wc=None, ws=None, out=None) == 0
+    assert pk(wc=None) == E_NULL and pk(ws=None) == E_NULL and pk(out=None) == E_NULL
+    assert pk(wc=P + 8) == E_ALIGN and pk(ws=P + 2) == E_ALIGN and pk(out=P + 4) == E_ALIGN
+    gp = lambda M=4, N=8, K=128, x=P, ldx=128, w=P, y=P, dt=0, ldy=8, wk=None: reqat.reqat_gemm_w4a16_packed(
+        M, N, K, x, ldx, w, y, dt, ldy, wk, None)
+    assert gp(M=16, N=5120, K=27648, ldx=27648, ldy=5120) == E_NULL  # needs the workspace
+    assert gp(dt=5) == E_ENUM
+    assert gp(M=-1) == E_SHAPE and gp(K=96, ldx=96) == E_SHAPE and gp(ldx=64) == E_SHAPE and gp(ldy=4) == E_SHAPE
+    assert gp(M=0, x=None, w=None, y=None) == 0 and gp(N=0, y=None) == 0
+    assert gp(y=None) == E_NULL and gp(x=None) == E_NULL and gp(w=None) == E_NULL
+    assert gp(x=P + 2) == E_ALIGN and gp(ldx=132) == E_ALIGN and gp(w=P + 8) == E_ALIGN
+    assert gp(y=P + 2) == E_ALIGN and gp(y=P + 1, dt=1) == E_ALIGN
+
+
+def test_binding_w4a16_packed_checks(trapped):
+    x5 = torch.zeros(16, 512, dtype=torch.bfloat16)
+    mc, ms = _u8(5120, 256), _u8(5120, 16)
+    nb = reqat.reqat_w4a16_packed_bytes(5120, 512)
+    with pytest.raises(TypeError, match="CUDA"):
+        reqat.pack_w4a16(mc, ms, out=_u8(nb))
+    _raises_before_device(lambda: reqat.pack_w4a16(mc, ms, out=_u8(nb - 1)), match="out")
+    _raises_before_device(lambda: reqat.pack_w4a16(mc, _u8(5120, 8)), match="w_scales")
+    _raises_before_device(lambda: reqat.pack_w4a16(_u8(5120, 48), _u8(5120, 3)), match="multiple of 128")
+    need16 = reqat.reqat_w4a16_workspace_bytes(16, 5120, 512)
+    with pytest.raises(TypeError, match="CUDA"):
+        reqat.gemm_w4a16_packed(x5, _u8(nb), 5120, ws=_u8(need16))
+    _raises_before_device(lambda: reqat.gemm_w4a16_packed(x5, _u8(nb - 16), 5120), match="packed")
+    _raises_before_device(lambda: reqat.gemm_w4a16_packed(x5, _u8(nb), 5120, ws=_u8(need16 - 4)), match="ws")
+    _raises_before_device(lambda: reqat.gemm_w4a16_packed(x5, _u8(nb), 5120,
+                                                          out=torch.zeros(16, 5120, dtype=torch.bfloat16)),
+                          match="out")
 
 
 def test_kv4_validation(lib):

@@ -217,14 +217,19 @@ def test_fullsize_rotated_mxfp4_activations():
 @pytest.mark.parametrize("idx", [6, 7])
 def test_fullsize_w4a16_decode(idx):
     """W4A16 decode shapes at full size: weights quantized to MXFP4 by the oracle,
-    the product checked on sampled outputs (plus corners) against the FP64 oracle."""
+    the product checked on sampled outputs (plus corners) against the FP64 oracle,
+    and the product from the packed weight image equal to it bit for bit."""
     w = wl.WORKLOADS[idx]
     log("full-size W4A16 workload %d: %s" % (idx, w.name))
     xb, wb = wl.bf16_bits(wl.make_x(w)), wl.bf16_bits(wl.make_w(w))
     wc, ws, _ = oracle.quantize(oracle.FMT_MXFP4, wb)
     t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
-    y = reqat.gemm_w4a16(wl.from_bits(xb).to(DEV), t(wc), t(ws), out_dtype=torch.float32)
+    xt, wct, wst = wl.from_bits(xb).to(DEV), t(wc), t(ws)
+    y = reqat.gemm_w4a16(xt, wct, wst, out_dtype=torch.float32)
+    # the packed weight image (the layout the bench streams): same result bit for bit
+    yp = reqat.gemm_w4a16_packed(xt, reqat.pack_w4a16(wct, wst), w.N, out_dtype=torch.float32)
     torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int32), yp.view(torch.int32)), "packed W4A16 product differs"
     rng = np.random.default_rng(idx)
     ms = np.concatenate([rng.integers(0, w.M, 2000), [0, 0, w.M - 1, w.M - 1]])
     ns = np.concatenate([rng.integers(0, w.N, 2000), [0, w.N - 1, 0, w.N - 1]])

@@ -679,16 +679,45 @@ def test_gemm_nan_block_propagates(fmt):
 
 # ------------------------------------------------------------------ W4A16
 
+def _w4a16_pack_ref(wc, ws):
+    """The packed W4A16 weight image as the header defines it, by numpy
+    indexing: 16-row groups (zero-padded), 128-element chunks; per unit (g, c)
+    1024 code bytes (piece q of row r at 16 (r + 16 q)) and, after all code
+    units, 64 scale bytes (row r's four bytes at 4 r)."""
+    N, Kh = wc.shape
+    G, C = -(-N // 16), Kh // 64
+    cp = np.zeros((G * 16, Kh), np.uint8)
+    cp[:N] = wc
+    sp = np.zeros((G * 16, ws.shape[1]), np.uint8)
+    sp[:N] = ws
+    codes = cp.reshape(G, 16, C, 4, 16).transpose(0, 2, 3, 1, 4).reshape(-1)    # [g][c][q][r][i]
+    scales = sp.reshape(G, 16, C, 4).transpose(0, 2, 1, 3).reshape(-1)          # [g][c][r][j]
+    return np.concatenate([codes, scales])
+
+
 def run_w4a16(xb, wc, ws):
+    """Parity of reqat_gemm_w4a16 with the oracle (FP32 and BF16 outputs), and
+    the packed path: the image equals the header's layout, the packed product
+    equals the unpacked one bit for bit."""
     M, K = xb.shape
     N = wc.shape[0]
     t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
     xt = wl.from_bits(xb).to(DEV)
+    packed = torch.full((max(reqat.reqat_w4a16_packed_bytes(N, K), 16),), 0xA5, dtype=torch.uint8, device=DEV)
+    reqat.pack_w4a16(t(wc), t(ws), out=packed)
+    torch.cuda.synchronize()
+    pref = _w4a16_pack_ref(wc, ws)
+    assert np.array_equal(packed.cpu().numpy()[:pref.size], pref), "packed image differs from the documented layout"
     outs = []
     for dt, poison in ((torch.float32, float("nan")), (torch.float32, 0.0), (torch.bfloat16, float("nan"))):
         y = torch.full((M, N), poison, dtype=dt, device=DEV)
         reqat.gemm_w4a16(xt, t(wc), t(ws), out_dtype=dt, out=y)
+        yp = torch.full((M, N), poison, dtype=dt, device=DEV)
+        reqat.gemm_w4a16_packed(xt, packed, N, out_dtype=dt, out=yp)
         torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.uint8) if dt == torch.bfloat16 else y.view(torch.int32),
+                           yp.view(torch.uint8) if dt == torch.bfloat16 else yp.view(torch.int32)), \
+            "packed product differs from the unpacked one"
         outs.append(y.float().cpu().numpy().astype(np.float64))
     assert np.array_equal(outs[0], outs[1], equal_nan=True), "poison visible or nondeterministic"
     ms, ns = np.arange(M).repeat(N), np.tile(np.arange(N), M)
