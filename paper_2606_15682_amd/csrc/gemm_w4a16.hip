@@ -40,7 +40,7 @@ typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 #define REQAT_W16_NT 1
 #endif
 #ifndef REQAT_W16_KSMAX
-#define REQAT_W16_KSMAX 8
+#define REQAT_W16_KSMAX 12
 #endif
 
 #ifndef REQAT_W16_DEPTH1
@@ -50,7 +50,7 @@ typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 #define REQAT_W16_TARGET 1024
 #endif
 #ifndef REQAT_W16_XG
-#define REQAT_W16_XG 4
+#define REQAT_W16_XG 2
 #endif
 
 constexpr int kThreads = 256;          // four waves
