@@ -31,22 +31,33 @@ if ROOT not in sys.path:
 METRIC = "W4A4 GEMM TFLOPS & % FP4 MFMA peak (prefill); quantize/decode HBM GB/s"
 GEMM_SOURCES = ["paper_2606_15682_amd/csrc/gemm_tile256.hip", "paper_2606_15682_amd/csrc/gemm.hip",
                 "paper_2606_15682_amd/csrc/fp4_device.h"]
+# the sources a committed traffic summary was measured on, per kind of row
+TRAFFIC_SOURCES = {
+    "gemm": GEMM_SOURCES,
+    "w4a16": ["paper_2606_15682_amd/csrc/gemm_w4a16.hip", "paper_2606_15682_amd/csrc/fp4_device.h"],
+    "kv4": ["paper_2606_15682_amd/csrc/kv4.hip", "paper_2606_15682_amd/csrc/fp4_device.h"],
+}
 
 
-def gemm_source_hash() -> str:
+def source_hash(kind: str = "gemm") -> str:
     import hashlib
     h = hashlib.sha256()
-    for rel in GEMM_SOURCES:
+    for rel in TRAFFIC_SOURCES[kind]:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 
 
-def profiled_traffic(fmt_name: str, workload: int):
-    """HBM bytes per GEMM launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
-    summary (each counter scaled by its reading for a plain copy of known size);
-    None when there is no summary or the GEMM sources changed since it was taken."""
-    path = os.path.join(ROOT, "profiles", "gemm_%s_workload%d_traffic.txt" % (fmt_name, workload))
+def gemm_source_hash() -> str:
+    return source_hash("gemm")
+
+
+def profiled_traffic_file(name: str, kind: str):
+    """HBM bytes per launch (or per step, as the summary states) from the
+    committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary profiles/<name> (each
+    counter scaled by its reading for a plain copy of known size); None when
+    there is no summary or the row's sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
         return None
     kv = {}
@@ -55,12 +66,19 @@ def profiled_traffic(fmt_name: str, workload: int):
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 kv[k.strip()] = v.strip()
-    if kv.get("gemm_source_sha256") != gemm_source_hash():
+    if kv.get("source_sha256", kv.get("gemm_source_sha256")) != source_hash(kind):
         return None
     try:
         return float(kv["traffic_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def profiled_traffic(fmt_name: str, workload: int):
+    """Traffic of the tile GEMM of a prefill workload (see profiled_traffic_file)."""
+    return profiled_traffic_file("gemm_%s_workload%d_traffic.txt" % (fmt_name, workload), "gemm")
+
+
 PEAK = {"fp4": 10100.0, "f16": 2500.0, "hbm": 8000.0}   # TFLOP/s, TFLOP/s, GB/s (MI355X published)
 # workloads timed as a decode step (quantize X + product, weights quantized once,
 # untimed); the others run the whole step (quantize and fake-quant both operands)
@@ -392,7 +410,8 @@ def bench_w4a16(args, w):
                            "weight copies (%.0f MB in all, twice the Infinity Cache), the %d steps captured in one "
                            "HIP graph, time per step" % (ncp, ncp * N * K * (0.5 + 1.0 / 32) / 1e6, ncp)},
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK["hbm"], "unit": "GB/s",
-                     "frac": round(gbs / PEAK["hbm"], 4), "traffic": None,
+                     "frac": round(gbs / PEAK["hbm"], 4),
+                     "traffic": profiled_traffic_file("w4a16_mxfp4_workload%d_traffic.txt" % args.workload, "w4a16"),
                      "kernel": "gemm_w4a16_kernel on the packed weight image%s (MXFP4 W4A16, algorithmic bytes %d)"
                                % (" + gemm_w4a16_reduce (K split %d ways)" % ksplit if ksplit > 1 else "",
                                   int(nbytes))},
@@ -615,7 +634,8 @@ def bench_kv4(args, w):
                            "step on another of %d key copies (%.0f MB in all, twice the Infinity Cache); the %d "
                            "steps captured in one HIP graph, time per step" % (ncp, ncp * T * C * 2 / 1e6, ncp)},
         "roofline": {"bound": "hbm", "achieved": round(gbs(q_bytes, ms_q), 1), "peak": PEAK["hbm"],
-                     "unit": "GB/s", "frac": round(gbs(q_bytes, ms_q) / PEAK["hbm"], 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(gbs(q_bytes, ms_q) / PEAK["hbm"], 4),
+                     "traffic": profiled_traffic_file("kv4_workload%d_traffic.txt" % args.workload, "kv4"),
                      "kernel": "kv4_quantize_deferred_kernel + kv4_fixup_kernel (algorithmic bytes %d)" % int(q_bytes)},
         "kernels": {"quantize_kv4_computed_g": {"ms": round(ms_q, 4), "GB/s": round(gbs(q_bytes, ms_q), 1)},
                     "quantize_kv4_given_g": {"ms": round(ms_given, 4), "GB/s": round(gbs(q_bytes, ms_given), 1)},
