@@ -36,6 +36,8 @@ TRAFFIC_SOURCES = {
     "gemm": GEMM_SOURCES,
     "w4a16": ["paper_2606_15682_amd/csrc/gemm_w4a16.hip", "paper_2606_15682_amd/csrc/fp4_device.h"],
     "kv4": ["paper_2606_15682_amd/csrc/kv4.hip", "paper_2606_15682_amd/csrc/fp4_device.h"],
+    "skinny": ["paper_2606_15682_amd/csrc/gemm_skinny.hip", "paper_2606_15682_amd/csrc/fp4_device.h"],
+    "sem": ["paper_2606_15682_amd/csrc/sem.hip"],
 }
 
 
@@ -522,7 +524,9 @@ def bench_decode(args, w):
                            "Infinity Cache); the %d steps captured in one HIP graph, time per step"
                            % (ncp, ncp * w_bytes / 1e6, ncp)},
         "roofline": {"bound": "hbm", "achieved": round(gbs_gemm, 1), "peak": PEAK["hbm"], "unit": "GB/s",
-                     "frac": round(gbs_gemm / PEAK["hbm"], 4), "traffic": None,
+                     "frac": round(gbs_gemm / PEAK["hbm"], 4),
+                     "traffic": profiled_traffic_file("gemm_skinny_%s_workload%d_traffic.txt" % (w.fmt, args.workload),
+                                                      "skinny"),
                      "kernel": "gemm_skinny_kernel (%s W4A4 GEMM, M <= 64; algorithmic bytes %d)"
                                % (w.fmt, int(gemm_bytes))},
         "kernels": {"linear_step_eager": {"ms": round(ms_eager, 4), "device_ms": round(ms_dev, 4),
@@ -726,7 +730,8 @@ def bench_sem(args, w):
         "config": {"workload": w.name, "tokens": T, "vocab": V, "global_batch": T, "parallelism": "single GPU",
                    "step": "SEM loss forward + backward (bfloat16 gradient)"},
         "roofline": {"bound": "hbm", "achieved": round(gbs_bwd, 1), "peak": PEAK["hbm"], "unit": "GB/s",
-                     "frac": round(gbs_bwd / PEAK["hbm"], 4), "traffic": None,
+                     "frac": round(gbs_bwd / PEAK["hbm"], 4),
+                     "traffic": profiled_traffic_file("sem_workload%d_traffic.txt" % args.workload, "sem"),
                      "kernel": "sem_backward_kernel (reads T*V*2 B of logits, writes T*V*2 B of gradient)"},
         "kernels": {"sem_forward": {"ms": round(fwd, 4), "GB/s": round(b_fwd / (fwd * 1e-3) / 1e9, 1)},
                     "sem_backward": {"ms": round(bwd, 4), "GB/s": round(gbs_bwd, 1)}},
@@ -919,7 +924,9 @@ def main():
         gbs = gemm_bytes / (per["gemm"] * 1e-3) / 1e9
         kern["gemm"]["GB/s"] = round(gbs, 1)
         roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK["hbm"], "unit": "GB/s",
-                    "frac": round(gbs / PEAK["hbm"], 4), "traffic": None,
+                    "frac": round(gbs / PEAK["hbm"], 4),
+                    "traffic": profiled_traffic_file("gemm_skinny_%s_workload%d_traffic.txt"
+                                                     % (w.fmt, args.workload), "skinny"),
                     "kernel": "gemm_skinny_kernel (%s W4A4 GEMM, M <= 64; algorithmic bytes %d)"
                               % (w.fmt, int(gemm_bytes))}
     else:
