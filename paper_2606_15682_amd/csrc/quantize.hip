@@ -189,17 +189,6 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
     uint16_t *__restrict__ seg_table) {
     constexpr int B = FMT == kMX ? 32 : 16;
 
-    GScale G = make_gscale(1.0f);
-    if (FMT == kNV && GM == kGFold) {
-        G = make_gscale(fold_partials(partials, nparts));
-        if (blockIdx.x == 0 && threadIdx.x == 0) *gptr = G.g;
-    } else if (FMT == kNV && GM == kGLocal) {
-        G = make_gscale(local_global_scale<kThreads>(x, rows, cols, ldx));
-        if (blockIdx.x == 0 && threadIdx.x == 0) *gptr = G.g;
-    } else if (FMT == kNV && GM == kGFixed) {
-        G = make_gscale(*gptr);
-    }
-
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t nb = cols / B;
@@ -228,10 +217,25 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
         }
     };
 
+    // kGLocal: the first step's blocks are requested together with the amax
+    // pass (the grid gives a wave at most two segments, launched with U = 2,
+    // so this is the wave's only step): one memory round trip for both.
+    uint32_t wfirst[U][B / 2];
+    if (GM == kGLocal && s_begin < s_end) load_step(s_begin, wfirst);
+
+    GScale G = make_gscale(1.0f);
+    if (FMT == kNV && GM == kGFold) {
+        G = make_gscale(fold_partials(partials, nparts));
+        if (blockIdx.x == 0 && threadIdx.x == 0) *gptr = G.g;
+    } else if (FMT == kNV && GM == kGLocal) {
+        G = make_gscale(local_global_scale<kThreads>(x, rows, cols, ldx));
+        if (blockIdx.x == 0 && threadIdx.x == 0) *gptr = G.g;
+    } else if (FMT == kNV && GM == kGFixed) {
+        G = make_gscale(*gptr);
+    }
+
     uint32_t mloc = 0;                                  // kGDeferred: finite max of this lane's elements
-    for (int64_t s = s_begin; s < s_end; s += step * U) {
-        uint32_t wc[U][B / 2];
-        load_step(s, wc);
+    auto run_step = [&](int64_t s, const uint32_t (&wc)[U][B / 2]) {
         uint32_t am[U];
         int64_t blk[U];
         bool act[U];
@@ -287,6 +291,16 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
                         segmax[u] ? (uint16_t)((uint32_t)(Gs[u].kg + 127) | (emin << 8)) : (uint16_t)0;
             }
         }
+    };
+    int64_t s = s_begin;
+    if (GM == kGLocal && s < s_end) {
+        run_step(s, wfirst);
+        s += step * U;
+    }
+    for (; s < s_end; s += step * U) {
+        uint32_t wc[U][B / 2];
+        load_step(s, wc);
+        run_step(s, wc);
     }
 
     if (GM == kGDeferred) {
@@ -731,8 +745,8 @@ hipError_t launch_fmt_out(GSrc gsrc, bool local, bool deferred, int grid, const 
                           int64_t cols, int64_t ldx, uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy,
                           float *gptr, uint32_t *partials, int nparts, uint16_t *seg_table, hipStream_t stream) {
     constexpr int U = OUT == kCodes ? REQAT_Q_UCODES : OUT == kFakeQuant ? REQAT_Q_UFQ : REQAT_Q_UBOTH;
-    if (FMT == kNV && local)
-        return launch_loop<FMT, OUT, kGLocal, U>(grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr, partials,
+    if (FMT == kNV && local)   // two segments per step: one step per wave (see quantize_kernel)
+        return launch_loop<FMT, OUT, kGLocal, 2>(grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr, partials,
                                                 nparts, seg_table, stream);
     if (FMT == kNV && deferred)
         return launch_loop<FMT, OUT, kGDeferred, U>(grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr,
