@@ -133,6 +133,12 @@ static reqat_status run_kv4(const void *x, int64_t rows, int64_t cols, int64_t l
                                   tensor_scale, ts, workspace, fake);
     if (st != REQAT_OK) return st;
     if (shift && (reinterpret_cast<uintptr_t>(shift) & 15u)) return REQAT_E_ALIGN;
+    if (fake && overlaps(x, span_bf16(rows, cols, ldx), y, span_bf16(rows, cols, ldy))) {
+        // in place only when x is not read again after y is written: every
+        // block is read before its values are stored, but a computed g's
+        // fix-up re-quantizes some blocks from x
+        if (ts == REQAT_TS_COMPUTE || x != y || ldx != ldy) return REQAT_E_UNSUPPORTED;
+    }
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const bool compute = ts == REQAT_TS_COMPUTE;
     if (rows == 0 || cols == 0) {

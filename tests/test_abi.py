@@ -248,6 +248,9 @@ def test_kv4_validation(lib):
     assert kq(ts_ptr=None) == E_NULL and kq(ws=None) == E_NULL and kq(c=None) == E_NULL
     assert kq(sh=P + 4) == E_ALIGN and kq(x=P + 2) == E_ALIGN and kq(ldx=68) == E_ALIGN
     assert kf(ldy=32) == E_SHAPE and kf(y=None) == E_NULL and kf(sh=P + 8) == E_ALIGN
+    # in place (y is x) only with a given g: a computed g's fix-up re-reads x
+    kfw = lambda y=P, ts=0: reqat.reqat_fakequant_kv4(P, 4, 64, 64, None, y, 64, P, ts, P + 65536, None)
+    assert kfw(y=P, ts=0) == E_UNSUP and kfw(y=P + 64, ts=1) == E_UNSUP
 
 
 def test_sem_validation(lib):

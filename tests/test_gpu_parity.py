@@ -398,6 +398,23 @@ def test_kv4_rounding_near_midpoints(g):
     assert_kv4_parity(wide, -np.resize(t, 4224), g=g)
 
 
+@pytest.mark.parametrize("g", [2.0 ** -6, 0.0123456789])
+def test_kv4_fakequant_in_place(g):
+    """KV4 fake-quant in place (y is x) with a given g, as the header allows:
+    each block is read once before its values are written (FP32 element path
+    for the power-of-two g, FP64 for the other)."""
+    log("kv4 fake-quant in place g=%r" % g)
+    xb = _rand(37, 512, 78, "normal", outliers=4)
+    shift = np.random.default_rng(9).normal(0.0, 1.0, 512).astype(np.float32)
+    g = float(np.float32(g))
+    oy, _ = oracle.kv4_fakequant(xb, shift, g)
+    xt = wl.from_bits(xb).to(DEV)
+    reqat.fakequant_kv4(xt, torch.from_numpy(shift).to(DEV), tensor_scale=torch.tensor([g], dtype=torch.float32,
+                                                                                      device=DEV), out=xt)
+    torch.cuda.synchronize()
+    assert np.array_equal(wl.bf16_bits(xt.cpu()), oy)
+
+
 def test_kv4_empty_writes_unit_scale():
     log("kv4 empty")
     x = torch.empty((0, 128), dtype=torch.bfloat16, device=DEV)
