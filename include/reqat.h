@@ -231,7 +231,8 @@ size_t reqat_w4a16_workspace_bytes(int64_t M, int64_t N, int64_t K);
  * reqat_pack_w4a16: writes the image of w_codes [N][K/2] (16-byte aligned) and
  * w_scales [N][K/32] (4-byte aligned) into `packed` (16-byte aligned, not
  * overlapping them), on `stream`.  A pure re-layout: no value changes.
- * Errors: REQAT_E_SHAPE (N < 0, K < 0, K % 128), REQAT_E_NULL, REQAT_E_ALIGN.
+ * Errors: REQAT_E_SHAPE (N < 0, K < 0, K % 128), REQAT_E_NULL, REQAT_E_ALIGN,
+ * REQAT_E_UNSUPPORTED (packed overlaps w_codes or w_scales).
  */
 size_t reqat_w4a16_packed_bytes(int64_t N, int64_t K);
 reqat_status reqat_pack_w4a16(const uint8_t *w_codes, const uint8_t *w_scales, int64_t N, int64_t K, void *packed,

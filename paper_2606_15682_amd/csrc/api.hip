@@ -251,6 +251,10 @@ reqat_status reqat_pack_w4a16(const uint8_t *w_codes, const uint8_t *w_scales, i
     if (!w_codes || !w_scales || !packed) return REQAT_E_NULL;
     if (!aligned16(w_codes) || (reinterpret_cast<uintptr_t>(w_scales) & 3u) || !aligned16(packed))
         return REQAT_E_ALIGN;
+    const size_t pbytes = w4a16_packed_bytes(N, K);
+    if (overlaps(packed, pbytes, w_codes, (size_t)N * (size_t)(K / 2)) ||
+        overlaps(packed, pbytes, w_scales, (size_t)N * (size_t)(K / 32)))
+        return REQAT_E_UNSUPPORTED;
     hipError_t e = launch_w4a16_pack(w_codes, w_scales, N, K, reinterpret_cast<uint8_t *>(packed),
                                      reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;

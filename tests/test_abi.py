@@ -209,6 +209,9 @@ def test_w4a16_packed_validation(lib):
     assert pk(N=0, wc=None, ws=None, out=None) == 0 and pk(K=0, wc=None, ws=None, out=None) == 0
     assert pk(wc=None) == E_NULL and pk(ws=None) == E_NULL and pk(out=None) == E_NULL
     assert pk(wc=P + 8) == E_ALIGN and pk(ws=P + 2) == E_ALIGN and pk(out=P + 4) == E_ALIGN
+    # the image must not overlap the weights (8 x 128: 512 code bytes, 32 scale bytes, a 1088-byte image)
+    far = P + (1 << 20)
+    assert pk(wc=P, ws=far, out=P + 256) == E_UNSUP and pk(wc=far, ws=P + 1024, out=P) == E_UNSUP
     gp = lambda M=4, N=8, K=128, x=P, ldx=128, w=P, y=P, dt=0, ldy=8, wk=None: reqat.reqat_gemm_w4a16_packed(
         M, N, K, x, ldx, w, y, dt, ldy, wk, None)
     assert gp(M=16, N=5120, K=27648, ldx=27648, ldy=5120) == E_NULL  # needs the workspace
