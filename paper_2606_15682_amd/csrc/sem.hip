@@ -14,8 +14,10 @@
 // H = log S - A / S, lse = m + log S, NLL = lse - z_y.  exp(x) is
 // v_exp_f32(x * log2 e).  HBM-bound: the logits are read once.
 // sem_batch_kernel: one workgroup; H_min by reduction, the two order
-// statistics by radix selection on the FP32 patterns (exact, deterministic),
-// the weights and the three loss sums (FP64, fixed order).
+// statistics by radix selection on the FP32 patterns (exact, deterministic;
+// up to 8192 tokens the keys stay in registers and the second statistic
+// follows from the first in one counting pass), the weights and the three
+// loss sums (FP64, fixed order).
 // sem_backward_kernel: one workgroup per row, logits read once more, gradient
 // written as bfloat16 (round to nearest even) or FP32.
 #include "fp4_device.h"
@@ -137,6 +139,24 @@ __device__ __forceinline__ uint32_t fkey(float f) {
 
 constexpr int kBatchThreads = 1024;
 
+// Adds one to hist[bin] for each active lane.  Entropies cluster, so in the
+// high-digit passes most lanes of a wave share a bin: the lanes with the first
+// active lane's bin are counted with one atomic, the others add theirs alone
+// (a 64-way same-address atomic serialises in the LDS).
+__device__ __forceinline__ void hist_add(uint32_t *hist, bool active, uint32_t bin) {
+    const uint64_t act = __ballot(active);
+    if (act == 0) return;
+    const int first = __builtin_ctzll(act);
+    const uint32_t lb = (uint32_t)__shfl((int)bin, first, 64);
+    const bool same = active && bin == lb;
+    const uint64_t group = __ballot(same);
+    if (same) {
+        if ((int)(threadIdx.x & 63) == first) atomicAdd(&hist[lb], (uint32_t)__builtin_popcountll(group));
+    } else if (active) {
+        atomicAdd(&hist[bin], 1u);
+    }
+}
+
 // k-th smallest (0-based) of the T entropies, by 4 passes of 8-bit radix selection.
 __device__ uint32_t select_key(const float *__restrict__ stats, int64_t T, int64_t k, uint32_t *hist,
                                uint32_t *scan, uint32_t *sel) {
@@ -145,9 +165,10 @@ __device__ uint32_t select_key(const float *__restrict__ stats, int64_t T, int64
         const int shift = 24 - 8 * pass;
         for (int i = threadIdx.x; i < 256; i += kBatchThreads) hist[i] = 0;
         __syncthreads();
-        for (int64_t t = threadIdx.x; t < T; t += kBatchThreads) {
-            const uint32_t key = fkey(stats[4 * t]);
-            if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 0xFFu], 1u);
+        for (int64_t t0 = 0; t0 < T; t0 += kBatchThreads) {      // whole waves, so the ballots see every lane
+            const int64_t t = t0 + threadIdx.x;
+            const uint32_t key = t < T ? fkey(stats[4 * t]) : 0u;
+            hist_add(hist, t < T && (key & mask) == prefix, (key >> shift) & 0xFFu);
         }
         __syncthreads();
         // exclusive prefix sums of the 256 counts (Hillis-Steele in LDS, the
@@ -184,6 +205,100 @@ __device__ uint32_t select_key(const float *__restrict__ stats, int64_t T, int64
     return prefix;
 }
 
+// Entropies a thread holds in registers for the batch kernel: a batch of up
+// to kBatchThreads * kKeyCache tokens is read from memory once; larger ones
+// take select_key above, which re-reads the keys in every pass.
+constexpr int kKeyCache = 8;
+
+// Inclusive prefix sum over threads 0..255 of c (the 256 bin counts), four
+// waves of 64: shuffles within each wave, then the totals of the waves
+// before it (one barrier).  Threads past 255 pass 0 and get unused values.
+__device__ __forceinline__ uint32_t bins_inclusive_scan(uint32_t c, uint32_t *wsum) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    uint32_t v = c;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t u = __shfl_up(v, off, 64);
+        if (lane >= off) v += u;
+    }
+    if (w < 4 && lane == 63) wsum[w] = v;
+    __syncthreads();
+    uint32_t base = 0;
+    for (int i = 0; i < w && i < 4; ++i) base += wsum[i];
+    return v + base;
+}
+
+// k-th smallest (0-based) of the n keys held kKeyCache per thread (key j of
+// thread t is entry t + j * kBatchThreads), by 4 passes of 8-bit radix
+// selection: the same key select_key finds, without re-reading memory.
+__device__ uint32_t select_key_cached(const uint32_t (&keys)[kKeyCache], int64_t n, int64_t k, uint32_t *hist,
+                                      uint32_t *wsum, uint32_t *sel) {
+    uint32_t prefix = 0, mask = 0;
+    for (int pass = 0; pass < 4; ++pass) {
+        const int shift = 24 - 8 * pass;
+        if (threadIdx.x < 256) hist[threadIdx.x] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kKeyCache; ++j) {
+            const int64_t t = threadIdx.x + (int64_t)j * kBatchThreads;
+            hist_add(hist, t < n && (keys[j] & mask) == prefix, (keys[j] >> shift) & 0xFFu);
+        }
+        __syncthreads();
+        const uint32_t c = threadIdx.x < 256 ? hist[threadIdx.x] : 0u;
+        const uint32_t incl = bins_inclusive_scan(c, wsum);
+        if (threadIdx.x < 256) {
+            const int64_t below = (int64_t)(incl - c);
+            if (c != 0 && k >= below && k < below + (int64_t)c) {
+                sel[0] = threadIdx.x;
+                sel[1] = (uint32_t)below;
+            }
+        }
+        __syncthreads();
+        const uint32_t digit = sel[0];
+        k -= (int64_t)sel[1];
+        prefix |= digit << shift;
+        mask |= 0xFFu << shift;
+        __syncthreads();                           // sel, wsum and hist are reused
+    }
+    return prefix;
+}
+
+// The (k+1)-th smallest key given the k-th, klo: klo again when at least k + 2
+// keys are <= klo, else the smallest key above klo (one pass: a count and a
+// minimum over the cached keys).
+__device__ uint32_t next_key_cached(const uint32_t (&keys)[kKeyCache], int64_t n, int64_t k, uint32_t klo,
+                                    uint32_t *wsum) {
+    uint32_t cnt = 0, mn = 0xFFFFFFFFu;
+#pragma unroll
+    for (int j = 0; j < kKeyCache; ++j) {
+        const int64_t t = threadIdx.x + (int64_t)j * kBatchThreads;
+        if (t < n) {
+            cnt += keys[j] <= klo ? 1u : 0u;
+            if (keys[j] > klo && keys[j] < mn) mn = keys[j];
+        }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        cnt += __shfl_xor(cnt, off, 64);
+        const uint32_t o = __shfl_xor(mn, off, 64);
+        mn = o < mn ? o : mn;
+    }
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    if (lane == 0) {
+        wsum[w] = cnt;
+        wsum[kBatchThreads / 64 + w] = mn;
+    }
+    __syncthreads();
+    uint64_t total = 0;
+    uint32_t m = 0xFFFFFFFFu;
+    for (int i = 0; i < kBatchThreads / 64; ++i) {
+        total += wsum[i];
+        m = wsum[kBatchThreads / 64 + i] < m ? wsum[kBatchThreads / 64 + i] : m;
+    }
+    __syncthreads();
+    return (int64_t)total >= k + 2 ? klo : m;
+}
+
 __device__ __forceinline__ float unkey(uint32_t key) {
     return f32_from_bits((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
 }
@@ -192,13 +307,30 @@ __global__ __launch_bounds__(kBatchThreads) void sem_batch_kernel(const float *_
                                                                   float lambda, float eps,
                                                                   float *__restrict__ weights,
                                                                   float *__restrict__ loss) {
-    __shared__ uint32_t hist[256], scan[256], sel[2];
+    __shared__ uint32_t hist[256], scan[256], sel[2], wsum[2 * (kBatchThreads / 64)];
     __shared__ double dred[2][kBatchThreads / 64];
     __shared__ float fred[kBatchThreads / 64];
 
-    // H_min
+    // H_min; a batch of at most kBatchThreads * kKeyCache tokens keeps its
+    // entropies' keys in registers for the selection below
+    const bool cached = T <= (int64_t)kBatchThreads * kKeyCache;
+    uint32_t keys[kKeyCache];
     float hmin = __builtin_inff();
-    for (int64_t t = threadIdx.x; t < T; t += kBatchThreads) hmin = fminf(hmin, stats[4 * t]);
+    if (cached) {
+        float h[kKeyCache];
+#pragma unroll
+        for (int j = 0; j < kKeyCache; ++j) {
+            const int64_t t = threadIdx.x + (int64_t)j * kBatchThreads;
+            h[j] = t < T ? stats[4 * t] : __builtin_inff();
+        }
+#pragma unroll
+        for (int j = 0; j < kKeyCache; ++j) {
+            hmin = fminf(hmin, h[j]);
+            keys[j] = fkey(h[j]);
+        }
+    } else {
+        for (int64_t t = threadIdx.x; t < T; t += kBatchThreads) hmin = fminf(hmin, stats[4 * t]);
+    }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) hmin = fminf(hmin, __shfl_xor(hmin, off, 64));
     if ((threadIdx.x & 63) == 0) fred[threadIdx.x >> 6] = hmin;
@@ -211,8 +343,15 @@ __global__ __launch_bounds__(kBatchThreads) void sem_batch_kernel(const float *_
     const double q = 0.75 * (double)(T - 1);
     const int64_t lo = (int64_t)q;
     const int64_t hi = lo + 1 < T ? lo + 1 : T - 1;
-    const double hlo = (double)unkey(select_key(stats, T, lo, hist, scan, sel));
-    const double hhi = hi == lo ? hlo : (double)unkey(select_key(stats, T, hi, hist, scan, sel));
+    double hlo, hhi;
+    if (cached) {
+        const uint32_t klo = select_key_cached(keys, T, lo, hist, wsum, sel);
+        hlo = (double)unkey(klo);
+        hhi = hi == lo ? hlo : (double)unkey(next_key_cached(keys, T, lo, klo, wsum));
+    } else {
+        hlo = (double)unkey(select_key(stats, T, lo, hist, scan, sel));
+        hhi = hi == lo ? hlo : (double)unkey(select_key(stats, T, hi, hist, scan, sel));
+    }
     const double tau = hlo + (q - (double)lo) * (hhi - hlo);
     const double denom = tau - (double)hmin + (double)eps;
 

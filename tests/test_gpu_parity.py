@@ -467,6 +467,35 @@ def test_sem_loss_parity(T, V):
     run_sem_case(T, V, T + V)
 
 
+def _tau_from_entropies(H, T):
+    """The 75th percentile the batch kernel defines, from its own FP32 entropies:
+    linear interpolation at q = 0.75 (T - 1) between the order statistics at
+    floor(q) and floor(q) + 1, in FP64, rounded to FP32."""
+    hs = np.sort(H.astype(np.float32)).astype(np.float64)
+    q = 0.75 * (T - 1)
+    lo = int(q)
+    hi = min(lo + 1, T - 1)
+    return np.float32(hs[lo] + (q - lo) * (hs[hi] - hs[lo]))
+
+
+@pytest.mark.parametrize("T,dup", [(4096, 1), (4097, 37), (1000, 1000), (8192, 5), (8193, 3), (9001, 1)])
+def test_sem_batch_order_statistics_exact(T, dup):
+    """tau (loss[3]) equals, bit for bit, the interpolated 75th percentile of the
+    kernel's own entropies: batches held in registers (T <= 8192) and larger
+    ones, distinct entropies and runs of equal ones (rows repeated dup times,
+    so both order statistics can fall in one run or straddle two)."""
+    log("sem batch order statistics T=%d dup=%d" % (T, dup))
+    rng = np.random.default_rng(T + dup)
+    V = 64
+    base = indep.to_bf16_bits(rng.normal(0.0, 2.0, (-(-T // dup), V)))
+    zb = np.repeat(base, dup, axis=0)[:T]
+    tg = rng.integers(0, V, T).astype(np.int32)
+    loss, stats, _ = reqat.sem_loss(wl.from_bits(zb).to(DEV), torch.from_numpy(tg).to(DEV), 0.5, 1e-6)
+    torch.cuda.synchronize()
+    H = stats.cpu().numpy()[:, 0]
+    assert np.float32(loss.cpu().numpy()[3]) == _tau_from_entropies(H, T)
+
+
 def test_sem_loss_low_entropy_rows():
     log("sem loss with near-deterministic rows")
     run_sem_case(33, 1024, 7, std=12.0)           # peaked softmax rows: entropies near zero
