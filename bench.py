@@ -215,6 +215,9 @@ def practical_ceilings(x=None, wt=None, steps=10):
     torch.cuda.synchronize()
     ms = ev[0].elapsed_time(ev[1]) / steps
     out["copy_GBps"] = round(2.0 * n * 4 / (ms * 1e-3) / 1e9, 1)
+    read = read_probe_gbps(src)
+    if read is not None:
+        out["read_GBps"] = read
     del src, dst
     if x is not None and wt is not None and x.shape[0] > 64:
         # W^T made contiguous: a plain (non-batched) NN product
@@ -233,9 +236,44 @@ def practical_ceilings(x=None, wt=None, steps=10):
         out["bf16_library_gemm_ms"] = round(ms, 4)
         del b, y
     torch.cuda.empty_cache()
-    out["note"] = ("device copy of 1 GiB (read + write bytes); torch.mm of the same bfloat16 "
-                   "operands, unquantized (vendor GEMM)")
+    out["note"] = ("device copy of 1 GiB (read + write bytes); read-only stream of 1 GiB (libreqat_probe.so); "
+                   "torch.mm of the same bfloat16 operands, unquantized (vendor GEMM)")
     return out
+
+
+def read_probe_gbps(buf, steps: int = 10):
+    """Context: the read-only HBM stream rate of libreqat_probe.so's read probe
+    over the 1 GiB device tensor `buf` (2048 workgroups, 16-byte loads); None
+    when the probe library is not built."""
+    import ctypes
+
+    import torch
+
+    from paper_2606_15682_amd import build as pbuild
+    if not os.path.exists(pbuild.PROBE_LIB):
+        return None
+    lib = ctypes.CDLL(pbuild.PROBE_LIB)
+    lib.reqat_probe_read.restype = ctypes.c_int
+    lib.reqat_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+    blocks = 2048
+    out = torch.empty(blocks * 256, dtype=torch.int32, device=buf.device)
+    nbytes = buf.numel() * buf.element_size()
+    st = torch.cuda.current_stream(buf.device).cuda_stream
+
+    def launch():
+        if lib.reqat_probe_read(buf.data_ptr(), nbytes, out.data_ptr(), blocks, st) != 0:
+            raise RuntimeError("reqat_probe_read failed")
+
+    launch()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(steps):
+        launch()
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / steps
+    return round(nbytes / (ms * 1e-3) / 1e9, 1)
 
 
 def mfma_probe_tflops(kind: int, ops, warmup: int = 10, reps: int = 20, iters: int = 1500) -> float:

@@ -1,5 +1,6 @@
-// Matrix-core rate probe for gfx950 (measurement context, not part of the
-// product path; built into its own library, libreqat_probe.so).
+// Rate probes for gfx950 (measurement context, not part of the product path;
+// built into their own library, libreqat_probe.so): the matrix-core rate
+// (reqat_probe_mfma) and the read-only HBM stream rate (reqat_probe_read).
 //
 // The products' rooflines are quoted against the nominal MFMA peaks, but the
 // rate the chip sustains depends on the operand bits: under random-looking
@@ -65,9 +66,35 @@ __global__ __launch_bounds__(kThreads, 1) void probe_mfma_kernel(const uint32_t 
     out[blockIdx.x * kThreads + threadIdx.x] = s;
 }
 
+// Read-only stream: one 16-byte load per thread per iteration of a
+// grid-stride loop, folded by XOR so that no load is dead; each thread writes
+// its fold.  (Four loads per iteration a grid-stride apart measured 19% slower
+// on gfx950, four consecutive 1 KB wave pieces 4% slower.)
+__global__ __launch_bounds__(kThreads) void probe_read_kernel(const uint4 *__restrict__ p, int64_t n16,
+                                                              uint32_t *__restrict__ out) {
+    uint32_t acc = 0u;
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n16; i += (int64_t)gridDim.x * kThreads) {
+        const uint4 a = p[i];
+        acc ^= a.x ^ a.y ^ a.z ^ a.w;
+    }
+    out[(int64_t)blockIdx.x * kThreads + threadIdx.x] = acc;
+}
+
 }  // namespace
 
 extern "C" {
+
+// Enqueues one read of `bytes` bytes (a multiple of 16; p 16-byte aligned)
+// by `blocks` workgroups of 256 threads on `stream`; out: blocks * 256
+// uint32 of device memory, whose XOR is the XOR of every 32-bit word read.
+// Returns 0, or the HIP error code of the launch (1 for a bad argument).
+int reqat_probe_read(const void *p, int64_t bytes, void *out, int blocks, void *stream) {
+    if (!p || !out || bytes <= 0 || bytes % 16 || blocks <= 0 || (reinterpret_cast<uintptr_t>(p) & 15u)) return 1;
+    hipLaunchKernelGGL(probe_read_kernel, dim3(blocks), dim3(kThreads), 0, reinterpret_cast<hipStream_t>(stream),
+                       static_cast<const uint4 *>(p), bytes / 16, static_cast<uint32_t *>(out));
+    return (int)hipGetLastError();
+}
+
 
 // Enqueues one probe launch of `blocks` workgroups (256 threads each) running
 // `iters` rounds of 16 MFMAs per wave on `stream`.  ops: 8 KB of device

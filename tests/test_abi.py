@@ -65,15 +65,17 @@ def test_library_imports_no_allocation_copy_or_sync(lib):
 
 
 def test_probe_library_is_separate_and_launch_only():
-    """The matrix-core rate probe (bench.py context) lives in its own library:
+    """The rate probes (bench.py context) live in their own library:
     libreqat exports none of it, and it launches kernels and nothing else."""
     from paper_2606_15682_amd import build as pbuild
     if not os.path.exists(pbuild.PROBE_LIB):
         pytest.skip("libreqat_probe.so not built")
     nm = lambda *a: subprocess.run(["nm", "-D", *a], capture_output=True, text=True, check=True).stdout
     exported = set(re.findall(r"\sT\s(\S+)", nm("--defined-only", pbuild.PROBE_LIB)))
-    assert "reqat_probe_mfma" in exported
-    assert "reqat_probe_mfma" not in set(re.findall(r"\sT\s(\S+)", nm("--defined-only", reqat.LIB_PATH)))
+    product = set(re.findall(r"\sT\s(\S+)", nm("--defined-only", reqat.LIB_PATH)))
+    for name in ("reqat_probe_mfma", "reqat_probe_read"):
+        assert name in exported
+        assert name not in product
     imported = {x.split("@")[0] for x in re.findall(r"\sU\s(\S+)", nm("--undefined-only", pbuild.PROBE_LIB))}
     hip = {x for x in imported if x.lower().startswith(("hip", "__hip", "hsa"))}
     assert hip <= {"hipLaunchKernel", "hipGetLastError", "__hipPushCallConfiguration", "__hipPopCallConfiguration",
