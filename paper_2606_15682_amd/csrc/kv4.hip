@@ -29,6 +29,12 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kMaxKvGroups = kMaxPartials;
+#ifndef REQAT_KV4_U
+#define REQAT_KV4_U 2
+#endif
+// Adjacent 64-block segments per wave step in the quantize kernels, their
+// loads all issued before any block is computed.
+constexpr int kKvU = REQAT_KV4_U;
 // Shift vectors of up to this many channels are staged in LDS once per
 // workgroup: read per block from global memory, the 64 shift bytes of a
 // 16-channel block would double the bytes the vector memory path moves.
@@ -401,11 +407,22 @@ __global__ __launch_bounds__(kThreads) void kv4_quantize_kernel(
 
     const int64_t nb = cols / 16, total = rows * nb;
     const bool narrow = total < (int64_t(1) << 32);
-    for (int64_t blk = (int64_t)blockIdx.x * kThreads + threadIdx.x; blk < total;
-         blk += (int64_t)gridDim.x * kThreads) {
-        float d[16];
-        kv4_load<SRC>(x, shift, lds_shift, blk, nb, ldx, narrow, d);
-        kv4_emit<OUT>(d, kv4_block_max(d), blk, nb, narrow, G, codes, scales, y, ldy);
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    // a wave step: kKvU adjacent segments of 64 blocks, one block per lane each
+    for (int64_t base = ((int64_t)blockIdx.x * 4 + wave) * (64 * kKvU); base < total;
+         base += (int64_t)gridDim.x * 4 * 64 * kKvU) {
+        float d[kKvU][16];
+#pragma unroll
+        for (int u = 0; u < kKvU; ++u) {
+            const int64_t blk = base + 64 * u + lane;
+            kv4_load<SRC>(x, shift, lds_shift, blk < total ? blk : total - 1, nb, ldx, narrow, d[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kKvU; ++u) {
+            const int64_t blk = base + 64 * u + lane;
+            if (blk < total) kv4_emit<OUT>(d[u], kv4_block_max(d[u]), blk, nb, narrow, G, codes, scales, y, ldy);
+        }
     }
 }
 
@@ -455,24 +472,34 @@ __global__ __launch_bounds__(kThreads) void kv4_quantize_deferred_kernel(
     const int64_t nb = cols / 16, total = rows * nb;
     const bool narrow = total < (int64_t(1) << 32);
     uint32_t mloc = 0u;
-    // segment base / 64 (wave-uniform): the blocks a lane takes are those of kv4_quantize_kernel
-    for (int64_t base = ((int64_t)blockIdx.x * 4 + wave) * 64; base < total;
-         base += (int64_t)gridDim.x * kThreads) {
-        const int64_t blk = base + lane;
-        const bool act = blk < total;
-        float d[16];
-        kv4_load<SRC>(x, shift, lds_shift, act ? blk : total - 1, nb, ldx, narrow, d);   // in range, unused past the end
-        uint32_t am = act ? kv4_block_max(d) : 0u;
-        const bool bad = am >= 0x7F800000u;
-        const uint32_t fm = bad ? kv4_finite_max(d) : am;
-        mloc = mloc > fm ? mloc : fm;
-        const uint32_t segmax = kv4_wave_reduce<true>(fm);
-        const Kv4G Gr = kv4_make_g(kv4_global_scale(segmax));
-        uint32_t sbyte = 0u;
-        if (act) sbyte = kv4_emit<OUT>(d, am, blk, nb, narrow, Gr, codes, scales, y, ldy);
-        const bool live = act && am != 0u && !bad;
-        const uint32_t emin = kv4_wave_reduce<false>(live ? sbyte >> 3 : 0xFFu);
-        if (lane == 0) seg_table[base / 64] = segmax ? (uint16_t)((uint32_t)(Gr.kg + 127) | (emin << 8)) : (uint16_t)0;
+    // a wave step: kKvU adjacent segments (base / 64 + u, wave-uniform), as in kv4_quantize_kernel
+    for (int64_t base = ((int64_t)blockIdx.x * 4 + wave) * (64 * kKvU); base < total;
+         base += (int64_t)gridDim.x * 4 * 64 * kKvU) {
+        float d[kKvU][16];
+#pragma unroll
+        for (int u = 0; u < kKvU; ++u) {
+            const int64_t blk = base + 64 * u + lane;
+            kv4_load<SRC>(x, shift, lds_shift, blk < total ? blk : total - 1, nb, ldx, narrow, d[u]);   // in range
+        }
+#pragma unroll
+        for (int u = 0; u < kKvU; ++u) {
+            if (base + 64 * u >= total) break;                     // wave-uniform: no such segment
+            const int64_t blk = base + 64 * u + lane;
+            const bool act = blk < total;
+            const uint32_t am = act ? kv4_block_max(d[u]) : 0u;
+            const bool bad = am >= 0x7F800000u;
+            const uint32_t fm = bad ? kv4_finite_max(d[u]) : am;
+            mloc = mloc > fm ? mloc : fm;
+            const uint32_t segmax = kv4_wave_reduce<true>(fm);
+            const Kv4G Gr = kv4_make_g(kv4_global_scale(segmax));
+            uint32_t sbyte = 0u;
+            if (act) sbyte = kv4_emit<OUT>(d[u], am, blk, nb, narrow, Gr, codes, scales, y, ldy);
+            const bool live = act && am != 0u && !bad;
+            const uint32_t emin = kv4_wave_reduce<false>(live ? sbyte >> 3 : 0xFFu);
+            if (lane == 0)
+                seg_table[base / 64 + u] =
+                    segmax ? (uint16_t)((uint32_t)(Gr.kg + 127) | (emin << 8)) : (uint16_t)0;
+        }
     }
     __shared__ uint32_t red[kThreads / 64];
     mloc = kv4_wave_max(mloc);
@@ -593,8 +620,10 @@ hipError_t launch_kv4(QuantOut out, const uint16_t *x, int64_t rows, int64_t col
                       uint32_t *partials, uint16_t *seg_table, hipStream_t stream) {
     const int64_t total = rows * (cols / 16);
     if (total == 0) return hipSuccess;
-    int64_t grid = (total + kThreads - 1) / kThreads;
+    int64_t grid = (total + kThreads - 1) / kThreads;             // absmax pass: one block per lane
     if (grid > kMaxKvGroups) grid = kMaxKvGroups;
+    int64_t qgrid = (total + kThreads * kKvU - 1) / (kThreads * kKvU);   // quantize kernels: kKvU per lane
+    if (qgrid > kMaxKvGroups) qgrid = kMaxKvGroups;
     const int64_t nseg = (total + 63) / 64;
     const bool deferred = computed && seg_table != nullptr && nseg <= kMaxSegments;
     auto run = [&](auto src_c) {
@@ -602,10 +631,10 @@ hipError_t launch_kv4(QuantOut out, const uint16_t *x, int64_t rows, int64_t col
         if (deferred) {
             // one pass over x under per-segment reference scales, then the fix-up
             if (out == kCodes)
-                hipLaunchKernelGGL((kv4_quantize_deferred_kernel<kCodes, SRC>), dim3((unsigned)grid), dim3(kThreads), 0,
+                hipLaunchKernelGGL((kv4_quantize_deferred_kernel<kCodes, SRC>), dim3((unsigned)qgrid), dim3(kThreads), 0,
                                    stream, x, rows, cols, ldx, shift, codes, scales, y, ldy, partials, seg_table);
             else
-                hipLaunchKernelGGL((kv4_quantize_deferred_kernel<kFakeQuant, SRC>), dim3((unsigned)grid),
+                hipLaunchKernelGGL((kv4_quantize_deferred_kernel<kFakeQuant, SRC>), dim3((unsigned)qgrid),
                                    dim3(kThreads), 0, stream, x, rows, cols, ldx, shift, codes, scales, y, ldy,
                                    partials, seg_table);
             hipError_t e = hipGetLastError();
@@ -614,10 +643,10 @@ hipError_t launch_kv4(QuantOut out, const uint16_t *x, int64_t rows, int64_t col
             if (fgrid > kMaxKvGroups) fgrid = kMaxKvGroups;
             if (out == kCodes)
                 hipLaunchKernelGGL(kv4_fixup_kernel<kCodes>, dim3((unsigned)fgrid), dim3(kThreads), 0, stream, x, rows,
-                                   cols, ldx, shift, codes, scales, y, ldy, gptr, partials, (int)grid, seg_table);
+                                   cols, ldx, shift, codes, scales, y, ldy, gptr, partials, (int)qgrid, seg_table);
             else
                 hipLaunchKernelGGL(kv4_fixup_kernel<kFakeQuant>, dim3((unsigned)fgrid), dim3(kThreads), 0, stream, x,
-                                   rows, cols, ldx, shift, codes, scales, y, ldy, gptr, partials, (int)grid,
+                                   rows, cols, ldx, shift, codes, scales, y, ldy, gptr, partials, (int)qgrid,
                                    seg_table);
             return hipGetLastError();
         }
@@ -628,11 +657,11 @@ hipError_t launch_kv4(QuantOut out, const uint16_t *x, int64_t rows, int64_t col
             if (e != hipSuccess) return e;
         }
         if (out == kCodes)
-            hipLaunchKernelGGL((kv4_quantize_kernel<kCodes, SRC>), dim3((unsigned)grid), dim3(kThreads), 0, stream, x,
+            hipLaunchKernelGGL((kv4_quantize_kernel<kCodes, SRC>), dim3((unsigned)qgrid), dim3(kThreads), 0, stream, x,
                                rows, cols, ldx, shift, codes, scales, y, ldy, gptr, (int)computed, partials,
                                (int)grid);
         else
-            hipLaunchKernelGGL((kv4_quantize_kernel<kFakeQuant, SRC>), dim3((unsigned)grid), dim3(kThreads), 0,
+            hipLaunchKernelGGL((kv4_quantize_kernel<kFakeQuant, SRC>), dim3((unsigned)qgrid), dim3(kThreads), 0,
                                stream, x, rows, cols, ldx, shift, codes, scales, y, ldy, gptr, (int)computed,
                                partials, (int)grid);
         return hipGetLastError();
