@@ -10,14 +10,18 @@
 // Every decision compares d (FP32, exact in FP64) with products of at most
 // 31 significant bits, so FP64 comparisons decide exactly; with a power-of-two
 // g (every computed g) the element thresholds have at most 8 bits and the
-// comparisons run in FP32, exactly as well.
+// comparisons run in FP32, exactly as well.  With a power-of-two g the codes
+// are normally taken by rounding d * rcp(s g / 2) (see kv4_emit), and the
+// threshold comparisons run only for blocks that rounding cannot decide.
 //
-// One lane per 16-channel block in a grid-stride loop; the shift vector is
-// staged in LDS once per workgroup (up to kShiftLds channels; from global
-// memory beyond).  With a power-of-two g the scale byte is computed in FP32
-// as well, with an exact correction step.  A computed g takes
-// two passes: the partial maxima of |d| per workgroup, then the quantizer,
-// whose workgroups fold them.
+// One lane per 16-channel block; a wave step takes kKvU adjacent segments of
+// 64 blocks.  The shift vector is staged in LDS once per workgroup (up to
+// kShiftLds channels; from global memory beyond).  With a power-of-two g the
+// scale byte is computed in FP32 as well, with an exact correction step.  A
+// computed g takes one pass over x under per-segment reference scales and a
+// fix-up kernel (kv4_quantize_deferred_kernel, kv4_fixup_kernel); a tensor
+// beyond the segment table takes two passes instead (the partial maxima of
+// |d| per workgroup, then the quantizer, whose workgroups fold them).
 #include <type_traits>
 
 #include "fp4_device.h"
