@@ -14,8 +14,15 @@
 // waves read it, so every activation byte read from L2 serves 64 weight rows
 // (reading it per wave, for 16 rows, made the L2 reads four times the weight
 // bytes and capped the rate near 1 TB/s).  With few weight rows the K range
-// is split over more workgroups (>= 512 in total) whose FP32 partial sums a
-// second kernel adds in split order (deterministic).
+// is split over more workgroups (>= 1024 in total, at most 12 splits) whose
+// FP32 partial sums a second kernel adds in split order (deterministic).
+//
+// The weights come row-major (codes [N][K/2], scales [N][K/32]) or as the
+// packed image of w4a16_pack_kernel: per 16-row group and 128-element chunk,
+// the 1 KB of codes in the order the lanes below load them, then (after all
+// code units) the 64 scale bytes, so that a wave's chunk is one contiguous
+// 1 KB load instead of 64 bytes from each of 16 rows.  The two layouts differ
+// only in the load addresses (kPacked); the arithmetic is the same.
 //
 // In a chunk, lane l takes the 32-element MX block kg = l / 16 of weight row
 // l % 16 (16 code bytes + its scale byte) and the same 32 K positions of

@@ -1,10 +1,10 @@
 // Block quantizer, fake-quant and tensor absmax kernels for gfx950.
 //
 // Quantize: a lane owns one scale block at a time (16 bfloat16 = 32 B for
-// NVFP4, 32 = 64 B for MXFP4) and walks the blocks in a grid-stride loop, so
-// the block absmax, the scale and the rounding are computed once per block
-// with no cross-lane traffic, and per-thread set-up (global scale) is paid
-// once.  Consecutive lanes own consecutive blocks, so every wave-wide 16-byte
+// NVFP4, 32 = 64 B for MXFP4); a wave takes U adjacent segments of 64 blocks
+// per step and the grid's waves sweep the tensor front to back, so the block
+// absmax, the scale and the rounding are computed once per block with no
+// cross-lane traffic, and per-thread set-up (global scale) is paid once.  Consecutive lanes own consecutive blocks, so every wave-wide 16-byte
 // load covers whole 128-byte lines; codes leave as one 8-byte (NVFP4) or
 // 16-byte (MXFP4) store per lane and scales as one byte per lane.
 //
