@@ -492,9 +492,10 @@ def bench_w4a16(args, w):
 
 def bench_decode(args, w):
     """Decode step of the W4A4 layer (M <= 64 activation rows): quantize X and
-    multiply by weights that were quantized once, untimed (served weights are
-    stored quantized), in one reqat_linear_w4a4 call.  Bound by HBM: the
-    weights stream once per step."""
+    multiply by weights that were quantized and packed once, untimed (served
+    weights are stored quantized, in the decode product's packed image), in one
+    reqat_linear_w4a4_packed call.  Bound by HBM: the weights stream once per
+    step.  The same step on the row-major weights is context."""
     import numpy as np
     import torch
 
@@ -520,8 +521,12 @@ def bench_decode(args, w):
     # step streams its weights from HBM, as a model's layers do
     ncp = n_copies(w_bytes, args)
     copies = [(wc0.clone(), wsc0.clone()) for _ in range(ncp)]
+    packed = [reqat.pack_w4a4(a, b, fmt) for a, b in copies]
 
     def step(i):
+        reqat.linear_packed(x, fmt, packed[i], N, gw, out_dtype=torch.bfloat16, out=y, g_out=gl, ws=lws)
+
+    def step_rowmajor(i):
         wc, wsc = copies[i]
         reqat.linear(x, fmt, wc, wsc, gw, out_dtype=torch.bfloat16, out=y, g_out=gl, ws=lws)
 
@@ -531,16 +536,21 @@ def bench_decode(args, w):
     # graph (each on its own weight copy), per step; eager launches are context.
     ms_eager, ms_dev = timed_rotation(step, ncp, args)
     ms_step = graph_rotation_ms(step, ncp, args)
+    ms_step_rowmajor = graph_rotation_ms(step_rowmajor, ncp, args)
     _, ms_resident = timed_rotation(lambda i: step(0), ncp, args)
 
     # the product alone (activation codes from one quantize), timed apart, also over the copies
     xc, xs, gx = reqat.quantize(x, fmt)
 
     def gemm_step(i):
+        reqat.gemm_packed(fmt, xc, xs, gx, packed[i], N, gw, out_dtype=torch.bfloat16, out=y)
+
+    def gemm_step_rowmajor(i):
         wc, wsc = copies[i]
         reqat.gemm(fmt, xc, xs, gx, wc, wsc, gw, out_dtype=torch.bfloat16, out=y)
 
     ms_gemm = graph_rotation_ms(gemm_step, ncp, args)
+    ms_gemm_rowmajor = graph_rotation_ms(gemm_step_rowmajor, ncp, args)
     gbs_gemm = gemm_bytes / (ms_gemm * 1e-3) / 1e9
     out = {
         "metric": METRIC,
@@ -557,23 +567,31 @@ def bench_decode(args, w):
         "data": "synthetic (seeded; Gaussian activations with outlier channels, N(0,0.02) weights)",
         "config": {"workload": w.name, "M": M, "N": N, "K": K, "format": w.fmt, "gemm_out": "bf16",
                    "global_batch": M, "parallelism": "single GPU",
-                   "step": "quantize X + W4A4 GEMM in one reqat_linear_w4a4 call (weights quantized once, "
-                           "untimed), each step on another of %d weight copies (%.0f MB in all, twice the "
-                           "Infinity Cache); the %d steps captured in one HIP graph, time per step"
+                   "step": "quantize X + W4A4 GEMM in one reqat_linear_w4a4_packed call (weights quantized "
+                           "and packed once, untimed), each step on another of %d weight copies (%.0f MB in all, "
+                           "twice the Infinity Cache); the %d steps captured in one HIP graph, time per step"
                            % (ncp, ncp * w_bytes / 1e6, ncp)},
         "roofline": {"bound": "hbm", "achieved": round(gbs_gemm, 1), "peak": PEAK["hbm"], "unit": "GB/s",
                      "frac": round(gbs_gemm / PEAK["hbm"], 4),
                      "traffic": profiled_traffic_file("gemm_skinny_%s_workload%d_traffic.txt" % (w.fmt, args.workload),
                                                       "skinny"),
-                     "kernel": "gemm_skinny_kernel (%s W4A4 GEMM, M <= 64; algorithmic bytes %d)"
-                               % (w.fmt, int(gemm_bytes))},
-        "kernels": {"linear_step_eager": {"ms": round(ms_eager, 4), "device_ms": round(ms_dev, 4),
+                     "kernel": "gemm_skinny_kernel on the packed weight image (%s W4A4 GEMM, M <= 64; "
+                               "algorithmic bytes %d)" % (w.fmt, int(gemm_bytes))},
+        "kernels": {"linear_step_rowmajor": {"ms": round(ms_step_rowmajor, 4),
+                                             "GB/s": round(step_bytes / (ms_step_rowmajor * 1e-3) / 1e9, 1),
+                                             "note": "context: the same step from the row-major weights "
+                                                     "(reqat_linear_w4a4), per step in the graph"},
+                    "gemm_rowmajor": {"ms": round(ms_gemm_rowmajor, 4),
+                                      "GB/s": round(gemm_bytes / (ms_gemm_rowmajor * 1e-3) / 1e9, 1),
+                                      "note": "context: the product from the row-major weights (reqat_gemm_w4a4), "
+                                              "per launch in the graph"},
+                    "linear_step_eager": {"ms": round(ms_eager, 4), "device_ms": round(ms_dev, 4),
                                           "GB/s": round(step_bytes / (ms_eager * 1e-3) / 1e9, 1),
                                           "note": "context: eager launches from Python (bound by the launch "
                                                   "rate); wall clock and HIP-event time per step"},
                     "gemm": {"ms": round(ms_gemm, 4), "GB/s": round(gbs_gemm, 1),
                              "TFLOP/s": round(2.0 * M * N * K / (ms_gemm * 1e-3) / 1e12, 2),
-                             "note": "product alone over the weight copies, %d launches in one HIP graph, "
+                             "note": "product alone on the packed image over the weight copies, %d launches in one HIP graph, "
                                      "per launch (HIP events around the replays)" % ncp},
                     "cache_resident_step": {"ms": round(ms_resident, 4),
                                             "GB/s": round(step_bytes / (ms_resident * 1e-3) / 1e9, 1),

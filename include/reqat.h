@@ -66,7 +66,7 @@
 extern "C" {
 #endif
 
-#define REQAT_ABI_VERSION 10
+#define REQAT_ABI_VERSION 11
 
 /* The enums travel as C ints.  Compiled as C++ they get int as their fixed
  * underlying type, so any int a caller passes is a value the library may
@@ -359,6 +359,55 @@ reqat_status reqat_linear_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K
                                const uint8_t *w_scales, const float *w_tensor_scale,
                                void *y, reqat_dtype y_dtype, int64_t ldy, void *workspace,
                                void *stream);
+
+/*
+ * Packed decode weight image (weights are fixed in serving, so they can be
+ * re-laid out once, when loaded): the weights of reqat_gemm_w4a4 in the order
+ * the decode-shaped product (M <= 64) consumes them, so that each of its
+ * weight loads reads 1 KB of consecutive bytes instead of 64 bytes from each
+ * of 16 rows.  Rows go in groups of 16 (the last padded with zero codes and
+ * scales), K in chunks of 256 elements (when K % 256 == 128 the last chunk's
+ * second half is zero); with G = ceil(N / 16), C = ceil(K / 256) and
+ * S = 16 (NVFP4) or 8 (MXFP4) scale bytes per row and chunk:
+ *   bytes [0, 2048 G C): unit (g, c) at 2048 (g C + c) holds, at byte
+ *     1024 h + 16 (r + 16 q) + i, w_codes[16 g + r][128 c + 32 q + 16 h + i]
+ *     (h < 2, r < 16, q < 4, i < 16);
+ *   bytes [2048 G C, (2048 + 16 S) G C): unit (g, c) at 2048 G C + 16 S (g C + c)
+ *     holds, at byte (S / 4)(r + 16 q) + j, w_scales[16 g + r][S c + (S / 4) q + j]
+ *     (j < S / 4).
+ * reqat_w4a4_packed_bytes: the image's size, (2048 + 16 S) G C (0 on bad
+ * arguments: unknown format, N < 0, K < 0 or K % 128).
+ * reqat_pack_w4a4: writes the image of w_codes [N][K/2] and w_scales [N][K/B]
+ * (both 16-byte aligned, as for reqat_gemm_w4a4) into `packed` (16-byte
+ * aligned, not overlapping them), on `stream`.  A pure re-layout: no value
+ * changes; the weights' tensor scale stays with the caller.
+ * Errors: REQAT_E_ENUM, REQAT_E_SHAPE (N < 0, K < 0, K % 128), REQAT_E_NULL,
+ * REQAT_E_ALIGN, REQAT_E_UNSUPPORTED (packed overlaps w_codes or w_scales).
+ */
+size_t reqat_w4a4_packed_bytes(reqat_format fmt, int64_t N, int64_t K);
+reqat_status reqat_pack_w4a4(reqat_format fmt, const uint8_t *w_codes, const uint8_t *w_scales, int64_t N, int64_t K,
+                             void *packed, void *stream);
+
+/*
+ * reqat_gemm_w4a4 and reqat_linear_w4a4 (the 4-bit GEMM of Sec. 5.3) for
+ * decode-shaped products (1 <= M <= 64) on the packed image of the weights (same results, bit for
+ * bit: the same kernel and order of operations, only the weight addresses
+ * differ).  packed: the reqat_w4a4_packed_bytes(fmt, N, K) bytes
+ * reqat_pack_w4a4 wrote for the same format (16-byte aligned); it takes the
+ * place of b_codes / b_scales (w_codes / w_scales).  Other arguments,
+ * requirements, workspace and errors as the row-major calls, plus
+ * REQAT_E_UNSUPPORTED for M > 64.
+ */
+reqat_status reqat_gemm_w4a4_packed(reqat_format fmt, int64_t M, int64_t N, int64_t K,
+                                    const uint8_t *a_codes, const uint8_t *a_scales,
+                                    const float *a_tensor_scale, const void *packed,
+                                    const float *b_tensor_scale, void *y, reqat_dtype y_dtype, int64_t ldy,
+                                    void *stream);
+reqat_status reqat_linear_w4a4_packed(reqat_format fmt, int64_t M, int64_t N, int64_t K,
+                                      const void *x, int64_t ldx, float *x_tensor_scale,
+                                      reqat_tscale_mode ts, const void *packed,
+                                      const float *w_tensor_scale, void *y, reqat_dtype y_dtype, int64_t ldy,
+                                      void *workspace, void *stream);
 
 /* Bytes of workspace reqat_linear_w4a4 needs for M x K activations (0 on bad arguments). */
 size_t reqat_linear_workspace_bytes(reqat_format fmt, int64_t M, int64_t K);

@@ -365,7 +365,7 @@ reqat_status check_linear(reqat_format fmt, int64_t M, int64_t N, int64_t K, con
 reqat_status run_linear(reqat_format fmt, int64_t M, int64_t N, int64_t K, const void *x, int64_t ldx,
                         float *x_tensor_scale, reqat_tscale_mode ts, const uint8_t *w_codes,
                         const uint8_t *w_scales, const float *w_tensor_scale, void *y, reqat_dtype y_dtype,
-                        int64_t ldy, void *workspace, void *stream) {
+                        int64_t ldy, void *workspace, void *stream, bool packed = false) {
     const bool nv = fmt == REQAT_FMT_NVFP4;
     uint8_t *ws = reinterpret_cast<uint8_t *>(workspace);
     uint8_t *a_codes = ws + round256(sizeof(uint32_t) * kMaxPartials);
@@ -382,10 +382,20 @@ reqat_status run_linear(reqat_format fmt, int64_t M, int64_t N, int64_t K, const
     reqat_status st = run_quant(fmt, x, M, K, ldx, a_codes, a_scales, nullptr, 0, x_tensor_scale, ts,
                                 workspace, nseg <= kMaxSegments ? table : nullptr, nseg, stream, kCodes);
     if (st != REQAT_OK) return st;
-    hipError_t e = launch_gemm(nv ? kNV : kMX, M, N, K, a_codes, a_scales, x_tensor_scale, w_codes,
-                               w_scales, w_tensor_scale, y, y_dtype == REQAT_DT_BF16, ldy,
-                               reinterpret_cast<hipStream_t>(stream));
+    hipError_t e = packed && K > 0
+                       ? launch_gemm_skinny(nv ? kNV : kMX, M, N, K, a_codes, a_scales, x_tensor_scale, w_codes,
+                                            w_scales, w_tensor_scale, y, y_dtype == REQAT_DT_BF16, ldy, true,
+                                            reinterpret_cast<hipStream_t>(stream))
+                       : launch_gemm(nv ? kNV : kMX, M, N, K, a_codes, a_scales, x_tensor_scale, w_codes,
+                                     w_scales, w_tensor_scale, y, y_dtype == REQAT_DT_BF16, ldy,
+                                     reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
+}
+
+// Code and scale parts of a packed decode image (reqat_pack_w4a4).
+const uint8_t *packed_scales(const void *packed, int64_t N, int64_t K) {
+    const size_t code_bytes = (size_t)((N + 15) / 16) * (size_t)((K + 255) / 256) * 2048u;
+    return reinterpret_cast<const uint8_t *>(packed) + code_bytes;
 }
 
 }  // namespace
@@ -406,6 +416,74 @@ reqat_status reqat_linear_w4a4(reqat_format fmt, int64_t M, int64_t N, int64_t K
                       ldy, workspace, stream);
 }
 
+size_t reqat_w4a4_packed_bytes(reqat_format fmt, int64_t N, int64_t K) {
+    if (!fmt_ok(fmt) || N < 0 || K < 0 || K % 128) return 0;
+    return skinny_packed_bytes(fmt == REQAT_FMT_NVFP4 ? kNV : kMX, N, K);
+}
+
+reqat_status reqat_pack_w4a4(reqat_format fmt, const uint8_t *w_codes, const uint8_t *w_scales, int64_t N, int64_t K,
+                             void *packed, void *stream) {
+    if (!fmt_ok(fmt)) return REQAT_E_ENUM;
+    if (N < 0 || K < 0 || K % 128) return REQAT_E_SHAPE;
+    if (N == 0 || K == 0) return REQAT_OK;
+    if (!w_codes || !w_scales || !packed) return REQAT_E_NULL;
+    if (!aligned16(w_codes) || !aligned16(w_scales) || !aligned16(packed)) return REQAT_E_ALIGN;
+    const Fmt f = fmt == REQAT_FMT_NVFP4 ? kNV : kMX;
+    const size_t pbytes = skinny_packed_bytes(f, N, K);
+    if (overlaps(packed, pbytes, w_codes, (size_t)N * (size_t)(K / 2)) ||
+        overlaps(packed, pbytes, w_scales, (size_t)N * (size_t)(K / block_of(fmt))))
+        return REQAT_E_UNSUPPORTED;
+    hipError_t e = launch_skinny_pack(f, w_codes, w_scales, N, K, reinterpret_cast<uint8_t *>(packed),
+                                      reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
+}
+
+reqat_status reqat_gemm_w4a4_packed(reqat_format fmt, int64_t M, int64_t N, int64_t K, const uint8_t *a_codes,
+                                    const uint8_t *a_scales, const float *a_tensor_scale, const void *packed,
+                                    const float *b_tensor_scale, void *y, reqat_dtype y_dtype, int64_t ldy,
+                                    void *stream) {
+    if (!fmt_ok(fmt)) return REQAT_E_ENUM;
+    if (y_dtype != REQAT_DT_F32 && y_dtype != REQAT_DT_BF16) return REQAT_E_ENUM;
+    if (M < 0 || N < 0 || K < 0) return REQAT_E_SHAPE;
+    if (K % 128) return REQAT_E_SHAPE;
+    if (ldy < N) return REQAT_E_SHAPE;
+    const bool nv = fmt == REQAT_FMT_NVFP4;
+    if (!nv && (a_tensor_scale || b_tensor_scale)) return REQAT_E_UNSUPPORTED;
+    if (nv && (!a_tensor_scale || !b_tensor_scale)) return REQAT_E_NULL;
+    if (M > 64) return REQAT_E_UNSUPPORTED;
+    if (M == 0 || N == 0) return REQAT_OK;
+    if (!y) return REQAT_E_NULL;
+    if (K > 0 && (!a_codes || !a_scales || !packed)) return REQAT_E_NULL;
+    if (reinterpret_cast<uintptr_t>(y) & (y_dtype == REQAT_DT_BF16 ? 1u : 3u)) return REQAT_E_ALIGN;
+    if (K > 0 && (!aligned16(a_codes) || !aligned16(a_scales) || !aligned16(packed))) return REQAT_E_ALIGN;
+    if (nv && ((reinterpret_cast<uintptr_t>(a_tensor_scale) & 3u) ||
+               (reinterpret_cast<uintptr_t>(b_tensor_scale) & 3u)))
+        return REQAT_E_ALIGN;
+    const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    // K == 0: the generic product writes zeros and reads no operand
+    hipError_t e = K > 0 ? launch_gemm_skinny(nv ? kNV : kMX, M, N, K, a_codes, a_scales, a_tensor_scale,
+                                              reinterpret_cast<const uint8_t *>(packed),
+                                              packed_scales(packed, N, K), b_tensor_scale, y,
+                                              y_dtype == REQAT_DT_BF16, ldy, true, st)
+                         : launch_gemm(nv ? kNV : kMX, M, N, 0, nullptr, nullptr, a_tensor_scale, nullptr, nullptr,
+                                       b_tensor_scale, y, y_dtype == REQAT_DT_BF16, ldy, st);
+    return e == hipSuccess ? REQAT_OK : REQAT_E_HIP;
+}
+
+reqat_status reqat_linear_w4a4_packed(reqat_format fmt, int64_t M, int64_t N, int64_t K, const void *x,
+                                      int64_t ldx, float *x_tensor_scale, reqat_tscale_mode ts, const void *packed,
+                                      const float *w_tensor_scale, void *y, reqat_dtype y_dtype, int64_t ldy,
+                                      void *workspace, void *stream) {
+    const uint8_t *pc = reinterpret_cast<const uint8_t *>(packed);
+    reqat_status st = check_linear(fmt, M, N, K, x, ldx, x_tensor_scale, ts, pc, pc, w_tensor_scale, y, y_dtype,
+                                   ldy);
+    if (st != REQAT_OK) return st;
+    if (M > 64) return REQAT_E_UNSUPPORTED;
+    if (!workspace) return REQAT_E_NULL;
+    if (reinterpret_cast<uintptr_t>(workspace) & 255u) return REQAT_E_ALIGN;
+    return run_linear(fmt, M, N, K, x, ldx, x_tensor_scale, ts, pc, pc ? packed_scales(packed, N, K) : nullptr,
+                      w_tensor_scale, y, y_dtype, ldy, workspace, stream, true);
+}
 
 }  // extern "C"
 

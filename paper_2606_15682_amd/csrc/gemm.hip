@@ -202,7 +202,7 @@ hipError_t launch_gemm(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *
                                    y_bf16, ldy, stream);
     if (M <= 64 && K > 0)
         return launch_gemm_skinny(fmt, M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16,
-                                  ldy, stream);
+                                  ldy, false, stream);
     dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)), block(kThreads);
     if (fmt == kMX)
         hipLaunchKernelGGL(gemm_w4a4_kernel<kMX>, grid, block, 0, stream, M, N, K, a_codes, a_scales,

@@ -57,8 +57,11 @@ struct Chunk {
 // Loads chunk c of the lane's rows.  The row pointers exclude the lane's
 // offset in the chunk; a lane past K loads the chunk's first elements (always
 // in range) and mul_chunk discards them, so every load is unconditional and
-// no select waits on a load before the chunk is multiplied.
-template <int FMT, int MT>
+// no select waits on a load before the chunk is multiplied.  kPacked: bc / bs
+// point at the lane's place in the workgroup's first unit of the packed image
+// (units of a row group are consecutive; the 2 KB of codes are two 1 KB
+// halves, one per load), where a lane past K finds zeros.
+template <int FMT, int MT, bool kPacked>
 __device__ __forceinline__ void load_chunk(Chunk<MT> &q, int64_t c, int g, int64_t K,
                                            const uint8_t *const (&ac)[MT], const uint8_t *const (&as)[MT],
                                            const uint8_t *bc, const uint8_t *bs) {
@@ -74,10 +77,11 @@ __device__ __forceinline__ void load_chunk(Chunk<MT> &q, int64_t c, int g, int64
         if constexpr (FMT == kMX) q.sa[mt] = *reinterpret_cast<const uint16_t *>(as[mt] + so);
         else q.sa[mt] = *reinterpret_cast<const uint32_t *>(as[mt] + so);
     }
-    q.b0 = *reinterpret_cast<const uint4 *>(bc + co);
-    q.b1 = *reinterpret_cast<const uint4 *>(bc + co + 16);
-    if constexpr (FMT == kMX) q.sb = *reinterpret_cast<const uint16_t *>(bs + so);
-    else q.sb = *reinterpret_cast<const uint32_t *>(bs + so);
+    const int64_t bco = kPacked ? 2048 * c : co, bso = kPacked ? 16 * SB * c : so;
+    q.b0 = *reinterpret_cast<const uint4 *>(bc + bco);
+    q.b1 = *reinterpret_cast<const uint4 *>(bc + bco + (kPacked ? 1024 : 16));
+    if constexpr (FMT == kMX) q.sb = *reinterpret_cast<const uint16_t *>(bs + bso);
+    else q.sb = *reinterpret_cast<const uint32_t *>(bs + bso);
 }
 
 __device__ __forceinline__ v8i as_v8i(uint4 q) {
@@ -144,7 +148,7 @@ __device__ __forceinline__ void mul_chunk(v4f (&acc)[MT], const Chunk<MT> &q) {
     }
 }
 
-template <int FMT, int MT>
+template <int FMT, int MT, bool kPacked>
 __global__ __launch_bounds__(kThreads) void gemm_skinny_kernel(
     int64_t M, int64_t N, int64_t K, const uint8_t *__restrict__ a_codes,
     const uint8_t *__restrict__ a_scales, const float *__restrict__ ga,
@@ -168,8 +172,17 @@ __global__ __launch_bounds__(kThreads) void gemm_skinny_kernel(
         ac[mt] = a_codes + row * cpr;
         as[mt] = a_scales + row * spr;
     }
-    const int64_t brow = (n0 + r) < N ? n0 + r : N - 1;
-    const uint8_t *bc = b_codes + brow * cpr, *bs = b_scales + brow * spr;
+    const uint8_t *bc, *bs;
+    if constexpr (kPacked) {
+        // b_codes / b_scales: the code and scale parts of the packed image
+        constexpr int SU = FMT == kMX ? 128 : 256;  // scale bytes per unit
+        bc = b_codes + (int64_t)blockIdx.x * nch * 2048 + lane * 16;
+        bs = b_scales + (int64_t)blockIdx.x * nch * SU + lane * (SU / 64);
+    } else {
+        const int64_t brow = (n0 + r) < N ? n0 + r : N - 1;
+        bc = b_codes + brow * cpr;
+        bs = b_scales + brow * spr;
+    }
 
     v4f acc[MT];
 #pragma unroll
@@ -178,14 +191,14 @@ __global__ __launch_bounds__(kThreads) void gemm_skinny_kernel(
     Chunk<MT> q[kDepth];
 #pragma unroll
     for (int j = 0; j < kDepth; ++j)
-        if (j < my) load_chunk<FMT, MT>(q[j], c0 + j, g, K, ac, as, bc, bs);
+        if (j < my) load_chunk<FMT, MT, kPacked>(q[j], c0 + j, g, K, ac, as, bc, bs);
     for (int64_t i0 = 0; i0 < my; i0 += kDepth) {
 #pragma unroll
         for (int j = 0; j < kDepth; ++j) {
             const int64_t i = i0 + j;
             if (i < my) {
                 mul_chunk<FMT, MT>(acc, q[j]);
-                if (i + kDepth < my) load_chunk<FMT, MT>(q[j], c0 + i + kDepth, g, K, ac, as, bc, bs);
+                if (i + kDepth < my) load_chunk<FMT, MT, kPacked>(q[j], c0 + i + kDepth, g, K, ac, as, bc, bs);
             }
         }
     }
@@ -211,24 +224,62 @@ __global__ __launch_bounds__(kThreads) void gemm_skinny_kernel(
     }
 }
 
-template <int FMT, int MT>
+// Packed image of skinny_pack_kernel: per 16-row group g and 256-element chunk
+// c (unit u = g C + c, C = ceil(K / 256)), 2 KB of codes at 2048 u, in the
+// order the lanes load them: byte 1024 h + 16 l + i is code byte
+// 128 c + 32 (l / 16) + 16 h + i of row 16 g + l % 16; after all code units,
+// 16 SB scale bytes per unit at 2048 G C + 16 SB u: byte (SB / 4) l + j is
+// scale byte SB c + (SB / 4)(l / 16) + j of that row (SB = 16 NV, 8 MX).
+// Rows past N and elements past K are zero.
+template <int FMT>
+__global__ __launch_bounds__(256) void skinny_pack_kernel(const uint8_t *__restrict__ codes,
+                                                          const uint8_t *__restrict__ scales, int64_t N, int64_t K,
+                                                          uint8_t *__restrict__ packed) {
+    constexpr int SB = FMT == kMX ? 8 : 16;     // scale bytes per row per chunk
+    constexpr int LSB = SB / 4;                 // scale bytes per lane per chunk
+    const int64_t nch = (K + 255) / 256, units = (N + 15) / 16 * nch;
+    const int64_t cpr = K / 2, spr = K / (FMT == kMX ? 32 : 16);
+    uint8_t *pscales = packed + units * 2048;
+    for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < units * 128; p += (int64_t)gridDim.x * 256) {
+        const int64_t u = p >> 7, g = u / nch, c = u - g * nch;
+        const int h = (int)(p >> 6) & 1, l = (int)(p & 63), q = l >> 4;
+        const int64_t row = 16 * g + (l & 15), cb = 128 * c + 32 * q + 16 * h, sb = SB * c + LSB * q;
+        uint4 v = uint4{0u, 0u, 0u, 0u};
+        if (row < N && cb < cpr) v = *reinterpret_cast<const uint4 *>(codes + row * cpr + cb);
+        *reinterpret_cast<uint4 *>(packed + u * 2048 + h * 1024 + l * 16) = v;
+        if (h == 0) {
+            const bool in = row < N && sb < spr;
+            if constexpr (FMT == kMX)
+                *reinterpret_cast<uint16_t *>(pscales + u * 128 + l * 2) =
+                    in ? *reinterpret_cast<const uint16_t *>(scales + row * spr + sb) : (uint16_t)0;
+            else
+                *reinterpret_cast<uint32_t *>(pscales + u * 256 + l * 4) =
+                    in ? *reinterpret_cast<const uint32_t *>(scales + row * spr + sb) : 0u;
+        }
+    }
+}
+
+template <int FMT, int MT, bool kPacked>
 hipError_t launch(int64_t M, int64_t N, int64_t K, const uint8_t *a_codes, const uint8_t *a_scales,
                   const float *ga, const uint8_t *b_codes, const uint8_t *b_scales, const float *gb, void *y,
                   bool y_bf16, int64_t ldy, hipStream_t stream) {
     const dim3 grid((unsigned)((N + kRows - 1) / kRows)), block(kThreads);
-    hipLaunchKernelGGL((gemm_skinny_kernel<FMT, MT>), grid, block, 0, stream, M, N, K, a_codes, a_scales, ga,
-                       b_codes, b_scales, gb, y, (int)y_bf16, ldy);
+    hipLaunchKernelGGL((gemm_skinny_kernel<FMT, MT, kPacked>), grid, block, 0, stream, M, N, K, a_codes, a_scales,
+                       ga, b_codes, b_scales, gb, y, (int)y_bf16, ldy);
     return hipGetLastError();
 }
 
-template <int FMT>
+template <int FMT, bool kPacked>
 hipError_t launch_fmt(int64_t M, int64_t N, int64_t K, const uint8_t *a_codes, const uint8_t *a_scales,
                       const float *ga, const uint8_t *b_codes, const uint8_t *b_scales, const float *gb, void *y,
                       bool y_bf16, int64_t ldy, hipStream_t stream) {
-    if (M <= 16) return launch<FMT, 1>(M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16, ldy, stream);
-    if (M <= 32) return launch<FMT, 2>(M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16, ldy, stream);
-    if (M <= 48) return launch<FMT, 3>(M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16, ldy, stream);
-    return launch<FMT, 4>(M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16, ldy, stream);
+    if (M <= 16)
+        return launch<FMT, 1, kPacked>(M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16, ldy, stream);
+    if (M <= 32)
+        return launch<FMT, 2, kPacked>(M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16, ldy, stream);
+    if (M <= 48)
+        return launch<FMT, 3, kPacked>(M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16, ldy, stream);
+    return launch<FMT, 4, kPacked>(M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16, ldy, stream);
 }
 
 }  // namespace
@@ -236,11 +287,34 @@ hipError_t launch_fmt(int64_t M, int64_t N, int64_t K, const uint8_t *a_codes, c
 hipError_t launch_gemm_skinny(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *a_codes,
                               const uint8_t *a_scales, const float *ga, const uint8_t *b_codes,
                               const uint8_t *b_scales, const float *gb, void *y, bool y_bf16, int64_t ldy,
-                              hipStream_t stream) {
+                              bool packed, hipStream_t stream) {
     if (M < 1 || M > 64 || K <= 0 || K % 128) return hipErrorInvalidValue;
     if (fmt == kMX)
-        return launch_fmt<kMX>(M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16, ldy, stream);
-    return launch_fmt<kNV>(M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16, ldy, stream);
+        return packed ? launch_fmt<kMX, true>(M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16, ldy,
+                                              stream)
+                      : launch_fmt<kMX, false>(M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16, ldy,
+                                               stream);
+    return packed ? launch_fmt<kNV, true>(M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16, ldy,
+                                          stream)
+                  : launch_fmt<kNV, false>(M, N, K, a_codes, a_scales, ga, b_codes, b_scales, gb, y, y_bf16, ldy,
+                                           stream);
+}
+
+size_t skinny_packed_bytes(Fmt fmt, int64_t N, int64_t K) {
+    return (size_t)((N + 15) / 16) * (size_t)((K + 255) / 256) * (fmt == kMX ? 2176u : 2304u);
+}
+
+hipError_t launch_skinny_pack(Fmt fmt, const uint8_t *codes, const uint8_t *scales, int64_t N, int64_t K,
+                              uint8_t *packed, hipStream_t stream) {
+    const int64_t pieces = (N + 15) / 16 * ((K + 255) / 256) * 128;
+    if (pieces == 0) return hipSuccess;
+    const int64_t blocks = (pieces + 255) / 256;
+    const dim3 grid((unsigned)(blocks < 4096 ? blocks : 4096)), block(256);
+    if (fmt == kMX)
+        hipLaunchKernelGGL(skinny_pack_kernel<kMX>, grid, block, 0, stream, codes, scales, N, K, packed);
+    else
+        hipLaunchKernelGGL(skinny_pack_kernel<kNV>, grid, block, 0, stream, codes, scales, N, K, packed);
+    return hipGetLastError();
 }
 
 }  // namespace reqat

@@ -80,11 +80,16 @@ hipError_t launch_sem_backward(const uint16_t *logits, int64_t T, int64_t V, int
                                bool grad_bf16, int64_t ldg, hipStream_t stream);
 
 bool gemm_tile256_supported(Fmt fmt, int64_t M, int64_t N, int64_t K, int64_t ldy);
-// Skinny product for M <= 64 (K % 128 == 0, K > 0).
+// Skinny product for M <= 64 (K % 128 == 0, K > 0).  packed: b_codes / b_scales
+// are the code and scale parts of the image launch_skinny_pack writes
+// (skinny_packed_bytes(fmt, N, K) bytes; the scales start 2048 G C bytes in).
 hipError_t launch_gemm_skinny(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *a_codes,
                               const uint8_t *a_scales, const float *ga, const uint8_t *b_codes,
                               const uint8_t *b_scales, const float *gb, void *y, bool y_bf16, int64_t ldy,
-                              hipStream_t stream);
+                              bool packed, hipStream_t stream);
+size_t skinny_packed_bytes(Fmt fmt, int64_t N, int64_t K);
+hipError_t launch_skinny_pack(Fmt fmt, const uint8_t *codes, const uint8_t *scales, int64_t N, int64_t K,
+                              uint8_t *packed, hipStream_t stream);
 
 hipError_t launch_gemm_tile256(Fmt fmt, int64_t M, int64_t N, int64_t K, const uint8_t *a_codes,
                                const uint8_t *a_scales, const float *ga, const uint8_t *b_codes,

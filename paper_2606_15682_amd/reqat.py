@@ -46,6 +46,11 @@ SIGNATURES = {
     "reqat_linear_w4a4": (_INT, [_INT, _I64, _I64, _I64, _VP, _I64, _VP, _INT, _VP, _VP, _VP, _VP,
                                  _INT, _I64, _VP, _VP]),
     "reqat_linear_workspace_bytes": (ctypes.c_size_t, [_INT, _I64, _I64]),
+    "reqat_w4a4_packed_bytes": (ctypes.c_size_t, [_INT, _I64, _I64]),
+    "reqat_pack_w4a4": (_INT, [_INT, _VP, _VP, _I64, _I64, _VP, _VP]),
+    "reqat_gemm_w4a4_packed": (_INT, [_INT, _I64, _I64, _I64, _VP, _VP, _VP, _VP, _VP, _VP, _INT, _I64, _VP]),
+    "reqat_linear_w4a4_packed": (_INT, [_INT, _I64, _I64, _I64, _VP, _I64, _VP, _INT, _VP, _VP, _VP, _INT, _I64,
+                                        _VP, _VP]),
     "reqat_linear_w4a4_noalloc": (_INT, [_INT, _I64, _I64, _I64, _VP, _I64, _VP, _INT, _VP, _VP, _VP, _VP,
                                          _INT, _I64, _VP]),
     "reqat_sem_loss": (_INT, [_VP, _I64, _I64, _I64, _VP, ctypes.c_float, ctypes.c_float, _VP, _VP, _VP, _VP]),
@@ -165,6 +170,24 @@ def reqat_quantize_mxfp4_rht(x, rows, cols, ldx, signs, codes, scales, stream):
 
 def reqat_fakequant_mxfp4_rht(x, rows, cols, ldx, signs, y, ldy, stream):
     return load().reqat_fakequant_mxfp4_rht(x, rows, cols, ldx, signs, y, ldy, stream)
+
+
+def reqat_w4a4_packed_bytes(fmt, N, K) -> int:
+    return load().reqat_w4a4_packed_bytes(fmt, N, K)
+
+
+def reqat_pack_w4a4(fmt, w_codes, w_scales, N, K, packed, stream):
+    return load().reqat_pack_w4a4(fmt, w_codes, w_scales, N, K, packed, stream)
+
+
+def reqat_gemm_w4a4_packed(fmt, M, N, K, a_codes, a_scales, a_ts, packed, b_ts, y, y_dtype, ldy, stream):
+    return load().reqat_gemm_w4a4_packed(fmt, M, N, K, a_codes, a_scales, a_ts, packed, b_ts, y, y_dtype, ldy,
+                                         stream)
+
+
+def reqat_linear_w4a4_packed(fmt, M, N, K, x, ldx, x_ts, ts, packed, w_ts, y, y_dtype, ldy, workspace, stream):
+    return load().reqat_linear_w4a4_packed(fmt, M, N, K, x, ldx, x_ts, ts, packed, w_ts, y, y_dtype, ldy,
+                                           workspace, stream)
 
 
 def reqat_linear_workspace_bytes(fmt, M, K) -> int:
@@ -583,6 +606,85 @@ def linear(x: torch.Tensor, fmt, w_codes, w_scales, w_g, x_tensor_scale=None, ou
                            w_scales.data_ptr(), _ptr(w_g), y.data_ptr(), dt, ldy, ws.data_ptr(),
                            _stream(x.device))
     _check(st, "reqat_linear_w4a4")
+    return y, g
+
+
+def pack_w4a4(w_codes, w_scales, fmt, out=None):
+    """Packed decode image of W4A4 weights (codes [N, K/2], scales [N, K/B]) for
+    gemm_packed / linear_packed: a uint8 tensor of reqat_w4a4_packed_bytes(fmt, N, K)."""
+    B = BLOCK[_fmt_arg(fmt)]
+    if w_codes.dim() != 2:
+        raise ValueError("w_codes must be 2-D")
+    N, K = w_codes.shape[0], w_codes.shape[1] * 2
+    if K % 128:
+        raise ValueError("K must be a multiple of 128")
+    _packed_u8(w_codes, N, K // 2, w_codes.device, "w_codes")
+    _packed_u8(w_scales, N, K // B, w_codes.device, "w_scales")
+    nbytes = reqat_w4a4_packed_bytes(fmt, N, K)
+    packed = out if out is not None else torch.empty(max(nbytes, 16), dtype=torch.uint8, device=w_codes.device)
+    _packed_image_arg(packed, nbytes, w_codes.device, "out")
+    _require_cuda(w_codes, "w_codes")
+    st = reqat_pack_w4a4(fmt, w_codes.data_ptr(), w_scales.data_ptr(), N, K, packed.data_ptr(),
+                         _stream(w_codes.device))
+    _check(st, "reqat_pack_w4a4")
+    return packed
+
+
+def _packed_image_arg(packed, nbytes, device, name):
+    if not isinstance(packed, torch.Tensor) or packed.dtype != torch.uint8 or not packed.is_contiguous() \
+            or packed.numel() < nbytes or packed.device != device:
+        raise ValueError("%s must be a contiguous uint8 tensor of at least %d bytes on %s" % (name, nbytes, device))
+
+
+def gemm_packed(fmt, a_codes, a_scales, a_g, packed, N, b_g, out_dtype=torch.float32, out=None):
+    """gemm() for M <= 64 on the packed image (pack_w4a4) of N x K weights: same result, bit for bit."""
+    B = BLOCK[_fmt_arg(fmt)]
+    dev = a_codes.device
+    if a_codes.dim() != 2:
+        raise ValueError("codes must be 2-D")
+    M, K = a_codes.shape[0], a_codes.shape[1] * 2
+    if K % 128:
+        raise ValueError("K must be a multiple of 128")
+    if M > 64:
+        raise ValueError("the packed image serves products with M <= 64")
+    _packed_u8(a_codes, M, K // 2, dev, "a_codes")
+    _packed_u8(a_scales, M, K // B, dev, "a_scales")
+    _packed_image_arg(packed, reqat_w4a4_packed_bytes(fmt, N, K), dev, "packed")
+    _scale_arg(a_g, fmt, dev, "a_g")
+    _scale_arg(b_g, fmt, dev, "b_g")
+    dt = _dtype_arg(out_dtype)
+    y = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=dev)
+    ldy = _out2d(y, M, N, out_dtype, dev, "out")
+    _require_cuda(a_codes, 'a_codes')
+    st = reqat_gemm_w4a4_packed(fmt, M, N, K, a_codes.data_ptr(), a_scales.data_ptr(), _ptr(a_g), packed.data_ptr(),
+                                _ptr(b_g), y.data_ptr(), dt, ldy, _stream(dev))
+    _check(st, "reqat_gemm_w4a4_packed")
+    return y
+
+
+def linear_packed(x: torch.Tensor, fmt, packed, N, w_g, x_tensor_scale=None, out_dtype=torch.bfloat16,
+                  out=None, g_out=None, ws=None):
+    """linear() for M <= 64 on the packed image (pack_w4a4) of N x K weights.  Returns (Y, g_x)."""
+    M, K, ldx = _x2d(x)
+    _fmt_arg(fmt)
+    if K % 128:
+        raise ValueError("K must be a multiple of 128")
+    if M > 64:
+        raise ValueError("the packed image serves products with M <= 64")
+    _packed_image_arg(packed, reqat_w4a4_packed_bytes(fmt, N, K), x.device, "packed")
+    _scale_arg(w_g, fmt, x.device, "w_g")
+    dt = _dtype_arg(out_dtype)
+    y = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=x.device)
+    ldy = _out2d(y, M, N, out_dtype, x.device, "out")
+    g, ts = _gscale(fmt, x, x_tensor_scale, g_out)
+    nbytes = reqat_linear_workspace_bytes(fmt, M, K)
+    if ws is None:
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
+    _workspace_arg(ws, nbytes, x.device)
+    _require_cuda(x, 'x')
+    st = reqat_linear_w4a4_packed(fmt, M, N, K, x.data_ptr(), ldx, _ptr(g), ts, packed.data_ptr(), _ptr(w_g),
+                                  y.data_ptr(), dt, ldy, ws.data_ptr(), _stream(x.device))
+    _check(st, "reqat_linear_w4a4_packed")
     return y, g
 
 

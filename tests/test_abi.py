@@ -83,7 +83,7 @@ def test_probe_library_is_separate_and_launch_only():
 
 
 def test_small_queries(lib):
-    assert reqat.reqat_abi_version() == 10
+    assert reqat.reqat_abi_version() == 11
     assert reqat.reqat_workspace_bytes() == 4 * 4096 + 2 * (1 << 19)   # partials + segment table
     for s in range(8):
         assert reqat.reqat_status_str(s).startswith(reqat.STATUS[s])
@@ -242,6 +242,72 @@ def test_binding_w4a16_packed_checks(trapped):
     _raises_before_device(lambda: reqat.gemm_w4a16_packed(x5, _u8(nb), 5120,
                                                           out=torch.zeros(16, 5120, dtype=torch.bfloat16)),
                           match="out")
+
+
+def test_w4a4_packed_validation(lib):
+    """Packed decode image: 2048 code bytes and 16 S scale bytes (S = 16 NVFP4,
+    8 MXFP4) per (16-row group, 256-element chunk); host-side argument checks of
+    the pack and of the packed product and linear layer (none reaches a launch)."""
+    nb = lambda N, K, fmt=NV: reqat.reqat_w4a4_packed_bytes(fmt, N, K)
+    assert nb(8960, 1536) == 560 * 6 * 2304 and nb(8960, 1536, MX) == 560 * 6 * 2176
+    assert nb(17, 384) == 2 * 2 * 2304                  # partial last group, half last chunk: padded
+    assert nb(16, 100) == 0 and nb(-1, 128) == 0 and nb(0, 128) == 0 and nb(16, 0) == 0 and nb(16, 128, 7) == 0
+    pk = lambda fmt=NV, wc=P, ws=P, N=8, K=128, out=P: reqat.reqat_pack_w4a4(fmt, wc, ws, N, K, out, None)
+    assert pk(fmt=7) == E_ENUM
+    assert pk(K=96) == E_SHAPE and pk(N=-1) == E_SHAPE
+    assert pk(N=0, wc=None, ws=None, out=None) == 0 and pk(K=0, wc=None, ws=None, out=None) == 0
+    assert pk(wc=None) == E_NULL and pk(ws=None) == E_NULL and pk(out=None) == E_NULL
+    assert pk(wc=P + 8) == E_ALIGN and pk(ws=P + 8) == E_ALIGN and pk(out=P + 4) == E_ALIGN
+    # the image must not overlap the weights (NVFP4 8 x 128: 512 code bytes, 64 scale bytes, a 2304-byte image)
+    far = P + (1 << 20)
+    assert pk(wc=P, ws=far, out=P + 256) == E_UNSUP and pk(wc=far, ws=P + 1024, out=P) == E_UNSUP
+    gp = lambda fmt=NV, M=4, N=8, K=128, a=P, sa=P, ag=P, w=P, bg=P, y=P, dt=0, ldy=8: \
+        reqat.reqat_gemm_w4a4_packed(fmt, M, N, K, a, sa, ag, w, bg, y, dt, ldy, None)
+    assert gp(fmt=7) == E_ENUM and gp(dt=5) == E_ENUM
+    assert gp(M=-1) == E_SHAPE and gp(K=96) == E_SHAPE and gp(ldy=4) == E_SHAPE
+    assert gp(M=65) == E_UNSUP and gp(fmt=MX) == E_UNSUP and gp(ag=None) == E_NULL and gp(bg=None) == E_NULL
+    assert gp(M=0, a=None, sa=None, w=None, y=None) == 0 and gp(N=0, y=None) == 0
+    assert gp(y=None) == E_NULL and gp(a=None) == E_NULL and gp(sa=None) == E_NULL and gp(w=None) == E_NULL
+    assert gp(a=P + 8) == E_ALIGN and gp(sa=P + 8) == E_ALIGN and gp(w=P + 8) == E_ALIGN
+    assert gp(y=P + 2) == E_ALIGN and gp(y=P + 1, dt=1) == E_ALIGN and gp(ag=P + 2) == E_ALIGN
+    lp = lambda fmt=NV, M=4, N=8, K=128, x=P, ldx=128, xg=P, ts=1, w=P, wg=P, y=P, dt=0, ldy=8, wk=P: \
+        reqat.reqat_linear_w4a4_packed(fmt, M, N, K, x, ldx, xg, ts, w, wg, y, dt, ldy, wk, None)
+    assert lp(fmt=7) == E_ENUM and lp(ts=5) == E_ENUM and lp(dt=5) == E_ENUM
+    assert lp(K=96, ldx=96) == E_SHAPE and lp(ldx=64) == E_SHAPE
+    assert lp(M=65) == E_UNSUP and lp(fmt=MX) == E_UNSUP
+    assert lp(wk=None) == E_NULL and lp(w=None) == E_NULL and lp(x=None) == E_NULL and lp(wg=None) == E_NULL
+    assert lp(wk=P + 16) == E_ALIGN and lp(w=P + 8) == E_ALIGN and lp(x=P + 2) == E_ALIGN
+    assert lp(M=0, x=None, w=None, y=None) == 0          # a given g: nothing to write, nothing launched
+
+
+def test_binding_w4a4_packed_checks(trapped):
+    mc, ms = _u8(8960, 768), _u8(8960, 96)
+    nb = reqat.reqat_w4a4_packed_bytes(NV, 8960, 1536)
+    with pytest.raises(TypeError, match="CUDA"):
+        reqat.pack_w4a4(mc, ms, NV, out=_u8(nb))
+    _raises_before_device(lambda: reqat.pack_w4a4(mc, ms, NV, out=_u8(nb - 1)), match="out")
+    _raises_before_device(lambda: reqat.pack_w4a4(mc, _u8(8960, 48), NV), match="w_scales")
+    _raises_before_device(lambda: reqat.pack_w4a4(mc, ms, 7), match="format")
+    _raises_before_device(lambda: reqat.pack_w4a4(_u8(8960, 48), _u8(8960, 6), NV), match="multiple of 128")
+    g = torch.ones(1, dtype=torch.float32)
+    a, sa = _u8(16, 768), _u8(16, 96)
+    with pytest.raises(TypeError, match="CUDA"):
+        reqat.gemm_packed(NV, a, sa, g, _u8(nb), 8960, g.clone())
+    _raises_before_device(lambda: reqat.gemm_packed(NV, a, sa, g, _u8(nb - 16), 8960, g.clone()), match="packed")
+    _raises_before_device(lambda: reqat.gemm_packed(NV, _u8(65, 768), _u8(65, 96), g, _u8(nb), 8960, g.clone()),
+                          match="M <= 64")
+    _raises_before_device(lambda: reqat.gemm_packed(NV, a, _u8(16, 48), g, _u8(nb), 8960, g.clone()),
+                          match="a_scales")
+    _raises_before_device(lambda: reqat.gemm_packed(NV, a, sa, g, _u8(nb), 8960, g.clone(),
+                                                    out=torch.zeros(16, 8960, dtype=torch.bfloat16)), match="out")
+    x = torch.zeros(16, 1536, dtype=torch.bfloat16)
+    ws = _u8(reqat.reqat_linear_workspace_bytes(NV, 16, 1536))
+    with pytest.raises(TypeError, match="CUDA"):
+        reqat.linear_packed(x, NV, _u8(nb), 8960, g, ws=ws)
+    _raises_before_device(lambda: reqat.linear_packed(x, NV, _u8(nb - 16), 8960, g, ws=ws), match="packed")
+    _raises_before_device(lambda: reqat.linear_packed(torch.zeros(65, 1536, dtype=torch.bfloat16), NV, _u8(nb),
+                                                      8960, g, ws=ws), match="M <= 64")
+    _raises_before_device(lambda: reqat.linear_packed(x, NV, _u8(nb), 8960, g, ws=ws[:-1]), match="ws")
 
 
 def test_kv4_validation(lib):

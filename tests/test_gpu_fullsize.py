@@ -47,6 +47,14 @@ def _check_gemm(w, fmt, ofmt, q, out_dtype, npts=2000, seed=0):
     reqat.gemm(fmt, xc, xs, xg, wc, ws, wg, out_dtype=out_dtype, out=y)
     torch.cuda.synchronize()
     assert not torch.isnan(y).any().item(), "unwritten or NaN outputs"
+    if w.M <= 64:
+        # the packed decode image (the layout the bench streams): same product bit for bit
+        yp = torch.full((w.M, w.N), float("nan"), dtype=out_dtype, device=DEV)
+        reqat.gemm_packed(fmt, xc, xs, xg, reqat.pack_w4a4(wc, ws, fmt), w.N, wg, out_dtype=out_dtype, out=yp)
+        torch.cuda.synchronize()
+        iv = torch.int32 if out_dtype == torch.float32 else torch.int16
+        assert torch.equal(y.view(iv), yp.view(iv)), "packed decode product differs"
+        log("  packed decode image: same product bit for bit")
     rng = np.random.default_rng(seed)
     ms = np.concatenate([rng.integers(0, w.M, npts), [0, 0, w.M - 1, w.M - 1]])
     ns = np.concatenate([rng.integers(0, w.N, npts), [0, w.N - 1, 0, w.N - 1]])

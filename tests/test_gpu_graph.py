@@ -2,7 +2,8 @@
 
 The library allocates nothing, records no memset and never synchronises, so
 a caller may capture its calls.  A captured step (fused quantize + fake-quant
-of X and W with computed global scales, the product, the one-call linear)
+of X and W with computed global scales, the product, the one-call linear and,
+for decode-sized X, the packed weight image and the linear call on it)
 is replayed several times, with other eager library work and host
 synchronisation between replays and its outputs overwritten before each
 replay; every replay must reproduce the eager outputs bit for bit.  Eager
@@ -41,7 +42,10 @@ def _buffers(fmt, M, N, K):
             "yl": torch.empty((M, N), dtype=torch.bfloat16, device=DEV),
             "gl": torch.empty(1, dtype=torch.float32, device=DEV),
             "lws": torch.empty(max(reqat.reqat_linear_workspace_bytes(fmt, M, K), 16), dtype=torch.uint8,
-                               device=DEV)}
+                               device=DEV),
+            "pk": torch.empty(max(reqat.reqat_w4a4_packed_bytes(fmt, N, K), 16), dtype=torch.uint8, device=DEV),
+            "yp": torch.empty((M, N), dtype=torch.bfloat16, device=DEV),
+            "gp": torch.empty(1, dtype=torch.float32, device=DEV)}
 
 
 def _step(fmt, x, w, b):
@@ -54,6 +58,10 @@ def _step(fmt, x, w, b):
     reqat.gemm(fmt, xc, xs, xg if nv else None, wc, ws, wg if nv else None, out_dtype=torch.bfloat16, out=b["y"])
     reqat.linear(x, fmt, wc, ws, wg if nv else None, out_dtype=torch.bfloat16, out=b["yl"],
                  g_out=b["gl"] if nv else None, ws=b["lws"])
+    if x.shape[0] <= 64:
+        reqat.pack_w4a4(wc, ws, fmt, out=b["pk"])
+        reqat.linear_packed(x, fmt, b["pk"], w.shape[0], wg if nv else None, out_dtype=torch.bfloat16,
+                            out=b["yp"], g_out=b["gp"] if nv else None, ws=b["lws"])
 
 
 def _flat(fmt, b):
@@ -63,6 +71,8 @@ def _flat(fmt, b):
     for k in ("x", "w"):
         out += list(b[k][:3]) + ([b[k][3]] if nv else [])
     out += [b["y"], b["yl"]] + ([b["gl"]] if nv else [])
+    if b["y"].shape[0] <= 64:
+        out += [b["pk"], b["yp"]] + ([b["gp"]] if nv else [])
     return out
 
 
@@ -78,6 +88,7 @@ def _scramble(fmt, b):
 @pytest.mark.parametrize("M,N,K", [(300, 520, 1024), (16, 768, 512)])
 def test_step_graph_replays_match_eager(fmt, M, N, K):
     log(f"graph step fmt={fmt} M={M} N={N} K={K}")
+    nv = int(fmt == reqat.NVFP4)
     x, w = _inputs(M, N, K, seed=1000 + 7 * M + fmt)
     b = _buffers(fmt, M, N, K)
     reqat.workspace(torch.device(DEV))                  # library workspace exists before capture
@@ -100,6 +111,9 @@ def test_step_graph_replays_match_eager(fmt, M, N, K):
         _step(fmt, x, w, b)
     torch.cuda.synchronize()
 
+    if M <= 64:
+        assert torch.equal(ref[-1 - nv].view(torch.uint8), ref[-3 - 2 * nv].view(torch.uint8)), \
+            "linear on the packed image differs from the row-major linear"
     for rep in range(3):
         _scramble(fmt, b)
         _step(fmt, x2, w2, b2)

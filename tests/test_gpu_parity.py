@@ -665,6 +665,46 @@ def check_gemm_points(fmt, ac, as_, ga, bc, bs, gb, y32, ybf, ms, ns):
         assert np.all(np.abs(gb_ - rb) <= ulp + GEMM_TOL * aref[ok])
 
 
+def _w4a4_pack_ref(bc, bs, fmt):
+    """The packed decode image as the header defines it, by numpy indexing:
+    16-row groups and 256-element chunks (zero-padded); per unit (g, c) 2048
+    code bytes (half h of piece q of row r at 1024 h + 16 (r + 16 q)) and,
+    after all code units, 16 S scale bytes (piece q of row r at (S/4)(r + 16 q))."""
+    N, Kh = bc.shape
+    S = 16 if fmt == NV else 8
+    G, C = -(-N // 16), -(-Kh // 128)
+    cp = np.zeros((G * 16, C * 128), np.uint8)
+    cp[:N, :Kh] = bc
+    sp = np.zeros((G * 16, C * S), np.uint8)
+    sp[:N, :bs.shape[1]] = bs
+    codes = cp.reshape(G, 16, C, 4, 2, 16).transpose(0, 2, 4, 3, 1, 5).reshape(-1)   # [g][c][h][q][r][i]
+    scales = sp.reshape(G, 16, C, 4, S // 4).transpose(0, 2, 3, 1, 4).reshape(-1)    # [g][c][q][r][j]
+    return np.concatenate([codes, scales])
+
+
+def check_gemm_packed(fmt, ac, as_, ga, bc, bs, gb):
+    """M <= 64: the packed decode image equals the header's layout, and the
+    product on it equals the row-major product bit for bit (FP32 and BF16)."""
+    M, N, K = ac.shape[0], bc.shape[0], ac.shape[1] * 2
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    nb = reqat.reqat_w4a4_packed_bytes(fmt, N, K)
+    packed = torch.full((max(nb, 16),), 0xA5, dtype=torch.uint8, device=DEV)
+    reqat.pack_w4a4(t(bc), t(bs), fmt, out=packed)
+    torch.cuda.synchronize()
+    pref = _w4a4_pack_ref(bc, bs, fmt)
+    assert pref.size == nb
+    assert np.array_equal(packed.cpu().numpy()[:nb], pref), "packed image differs from the documented layout"
+    gat = None if fmt == MX else torch.tensor([ga], dtype=torch.float32, device=DEV)
+    gbt = None if fmt == MX else torch.tensor([gb], dtype=torch.float32, device=DEV)
+    for dt, iv in ((torch.float32, torch.int32), (torch.bfloat16, torch.int16)):
+        y = torch.full((M, N), float("nan"), dtype=dt, device=DEV)
+        reqat.gemm(fmt, t(ac), t(as_), gat, t(bc), t(bs), gbt, out_dtype=dt, out=y)
+        yp = torch.full((M, N), float("nan"), dtype=dt, device=DEV)
+        reqat.gemm_packed(fmt, t(ac), t(as_), gat, packed, N, gbt, out_dtype=dt, out=yp)
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(iv), yp.view(iv)), "packed product differs from the row-major one"
+
+
 def run_gemm_case(fmt, M, N, K, seed, dist="normal", wstd=0.02, g=(None, None), all_points=True):
     xa = _rand(M, K, seed, dist, outliers=max(1, K // 100))
     xb = _rand(N, K, seed + 7, "normal", std=wstd)
@@ -681,6 +721,8 @@ def run_gemm_case(fmt, M, N, K, seed, dist="normal", wstd=0.02, g=(None, None), 
         ms = np.concatenate([rng.integers(0, M, 3000), [0, M - 1, M - 1, 0]])
         ns = np.concatenate([rng.integers(0, N, 3000), [0, N - 1, 0, N - 1]])
     check_gemm_points(fmt, ac, as_, ga, bc, bs, gb, y1, yb, ms, ns)
+    if M <= 64:
+        check_gemm_packed(fmt, ac, as_, ga, bc, bs, gb)
 
 
 @pytest.mark.parametrize("fmt", [NV, MX])
@@ -887,7 +929,8 @@ def test_decode_linear_equals_two_launch_path(fmt, M, K, given):
     """The linear call on decode-sized activations: its outputs, the activation
     codes and scales it leaves in its workspace, and g are bitwise those of
     quantize() then gemm(), also with NaN blocks, an all-zero row, subnormal and
-    huge values."""
+    huge values; the linear call on the packed weight image gives the same
+    outputs and g bit for bit."""
     log("decode linear vs two launches fmt=%d M=%d K=%d given=%s" % (fmt, M, K, given))
     N = 700
     xa = _rand(M, K, 91 + M, "student_t", outliers=max(1, K // 100))
@@ -915,6 +958,14 @@ def test_decode_linear_equals_two_launch_path(fmt, M, K, given):
             assert float(g1.cpu()[0]) == float(g2.cpu()[0])
         iv = torch.int32 if dt == torch.float32 else torch.int16
         assert torch.equal(y1.view(iv), y2.view(iv)), "outputs differ"
+        y3 = torch.full((M, N), float("nan"), dtype=dt, device=DEV)
+        ws3 = torch.full((reqat.reqat_linear_workspace_bytes(fmt, M, K),), 0xCD, dtype=torch.uint8, device=DEV)
+        _, g3 = reqat.linear_packed(x, fmt, reqat.pack_w4a4(t(bc), t(bs), fmt), N, wg, x_tensor_scale=gx,
+                                    out_dtype=dt, out=y3, ws=ws3)
+        torch.cuda.synchronize()
+        assert torch.equal(y1.view(iv), y3.view(iv)), "packed linear differs"
+        if fmt == NV:
+            assert float(g3.cpu()[0]) == float(g1.cpu()[0])
 
 
 # ------------------------------------------------------- strided operands
