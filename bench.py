@@ -41,12 +41,42 @@ TRAFFIC_SOURCES = {
 }
 
 
+def code_text(src: str) -> str:
+    """C/C++ source with its comments and blank lines removed and trailing
+    blanks stripped: what a compiled kernel depends on, so that an edit of a
+    comment leaves a measurement taken on the source valid.  (String and
+    character literals are copied whole, so a // inside one is kept.)"""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if c in "\"'":
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        elif src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    lines = (ln.rstrip() for ln in "".join(out).split("\n"))
+    return "\n".join(ln for ln in lines if ln)
+
+
 def source_hash(kind: str = "gemm") -> str:
+    """SHA-256 of the code (code_text) of the sources a row's traffic summary
+    was measured on."""
     import hashlib
     h = hashlib.sha256()
     for rel in TRAFFIC_SOURCES[kind]:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+            h.update(code_text(f.read()).encode("utf-8"))
     return h.hexdigest()
 
 

@@ -16,6 +16,16 @@
 // 8.2 -> 5.7 us on the 16 x 8960 x 1536 decode product.  Loads run up to
 // kDepth chunks ahead of the chunk being multiplied.
 //
+// From row-major weights each 16-byte weight load of a wave still touches 16
+// rows (64 scattered bytes of each row's line).  Served weights can instead
+// be re-laid out once into a packed image (skinny_pack_kernel) in which a
+// unit of 16 rows x 256 elements holds the 2 KB of codes in lane order and,
+// after all code units, its scale bytes in lane order: every weight load of
+// a wave is then 1 KB (codes) or 256 / 128 bytes (scales) of consecutive
+// bytes (kPacked; 6.2 -> 5.2 us on the decode product above, weights from
+// HBM).  Only the weight addresses differ, so both forms give the same
+// result bit for bit.
+//
 // Operands go to the 16 x 16 MFMAs in the layout the loads produce: in step s
 // a lane feeds elements 8s .. 8s+7 (NV, v_mfma_f32_16x16x32_f16) or the
 // 32-block s (MX, v_mfma_scale_f32_16x16x128_f8f6f4) of its 64; A and B use
