@@ -176,3 +176,56 @@ def test_kv4_graph_replays_match_eager():
             assert torch.equal(got.view(torch.uint8), want.view(torch.uint8)), \
                 f"replay {rep}: kv4 output {i} differs from the eager step"
     log("kv4 graph replays match")
+
+
+@pytest.mark.parametrize("M,N,K", [(16, 640, 4096), (5, 1536, 1024)])
+def test_w4a16_graph_replays_match_eager(M, N, K):
+    """W4A16 product (row-major and packed weights) captured and replayed.
+    640 rows give 10 workgroups, so K is split and the FP32 partial sums meet
+    in the workspace through the reduction kernel; 1536 rows are not split."""
+    log(f"graph w4a16 M={M} N={N} K={K}")
+    gen = torch.Generator().manual_seed(5 + M)
+    w = (torch.randn(N, K, generator=gen) * 0.02).to(torch.bfloat16).to(DEV)
+    wc, ws, _ = reqat.quantize(w, reqat.MXFP4)
+    packed = reqat.pack_w4a16(wc, ws)
+    x1 = (torch.randn(M, K, generator=gen) * 2.0).to(torch.bfloat16).to(DEV)
+    x2 = (torch.randn(M, K, generator=gen) * 2.0).to(torch.bfloat16).to(DEV)
+    nws = max(reqat.reqat_w4a16_workspace_bytes(M, N, K), 16)
+    if N == 640:
+        assert reqat.reqat_w4a16_workspace_bytes(M, N, K) > 0, "expected a split product"
+
+    def bufs():
+        return {"y": torch.empty((M, N), dtype=torch.bfloat16, device=DEV),
+                "yp": torch.empty((M, N), dtype=torch.float32, device=DEV),
+                "ws": torch.empty(nws, dtype=torch.uint8, device=DEV)}
+
+    def step(x, b):
+        reqat.gemm_w4a16(x, wc, ws, out_dtype=torch.bfloat16, out=b["y"], ws=b["ws"])
+        reqat.gemm_w4a16_packed(x, packed, N, out_dtype=torch.float32, out=b["yp"], ws=b["ws"])
+
+    b1, b2 = bufs(), bufs()
+    step(x1, b1)
+    torch.cuda.synchronize()
+    ref = [b1["y"].clone(), b1["yp"].clone()]
+    assert torch.equal(ref[0], ref[1].to(torch.bfloat16)), "packed and row-major products differ"
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step(x1, b1)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step(x1, b1)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        b1["y"].fill_(float("nan"))
+        b1["yp"].fill_(float("nan"))
+        b1["ws"].fill_(0xA5)
+        step(x2, b2)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(b1["y"].view(torch.int16), ref[0].view(torch.int16)), f"replay {rep}: bf16 output differs"
+        assert torch.equal(b1["yp"].view(torch.int32), ref[1].view(torch.int32)), f"replay {rep}: fp32 output differs"
+    log("graph replays match")
