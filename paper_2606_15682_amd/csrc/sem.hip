@@ -9,10 +9,11 @@
 //     dL/dz_tj = (scale / T) [(p_j - [j == y_t]) - lambda w_t p_j (log p_j + H_t)].
 //
 // sem_rows_kernel: one 256-thread workgroup per row, one pass over the row with
-// a running maximum m, S = sum exp(z - m) and A = sum exp(z - m) (z - m) per
-// thread (rescaled when m grows), merged in a fixed tree order; then
-// H = log S - A / S, lse = m + log S, NLL = lse - z_y.  exp(x) is
-// v_exp_f32(x * log2 e).  HBM-bound: the logits are read once.
+// a running maximum m and, in base-2 units (mb = m log2 e, t = z log2 e - mb
+// in one fused multiply-add, 2^t by v_exp_f32), S = sum 2^t and
+// A = sum 2^t t per thread (rescaled when m grows), merged in a fixed tree
+// order; then H = ln 2 (log2 S - A / S), lse = ln 2 (mb + log2 S),
+// NLL = lse - z_y.  The logits are read once.
 // sem_batch_kernel: one workgroup; H_min by reduction, the two order
 // statistics by radix selection on the FP32 patterns (exact, deterministic;
 // up to 8192 tokens the keys stay in registers and the second statistic
@@ -33,40 +34,47 @@ constexpr float kLn2 = 0.6931471805599453f;
 
 __device__ __forceinline__ float exp_fast(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
 
+// Running softmax state of a slice of a row, in base-2 units: mb = RN(m log2 e)
+// for the largest logit m seen so far, S = sum 2^t and A = sum 2^t t over the
+// slice with t = RN(z log2 e - mb) (one fused multiply-add per logit), so that
+// 2^t = exp(z - mb / log2 e).  Then ln sum exp(z) = ln 2 (mb + log2 S) and the
+// entropy H = ln 2 (log2 S - A / S), whatever mb is.
 struct Online {
-    float m, S, A;   // running max, sum of exp(z - m), sum of exp(z - m) (z - m)
+    float m, mb, S, A;
 };
 
 // Merge two partial states.
 __device__ __forceinline__ Online merge(Online a, Online b) {
     if (b.m > a.m) { Online t = a; a = b; b = t; }
     if (b.S == 0.0f) return a;                     // b empty (m = -inf)
-    const float d = b.m - a.m;                     // <= 0
-    const float f = exp_fast(d);
+    const float d = b.mb - a.mb;                   // <= 0
+    const float f = __builtin_amdgcn_exp2f(d);
     a.A = a.A + f * (b.A + d * b.S);
     a.S = a.S + f * b.S;
     return a;
 }
 
+// Adds eight finite logits (the header requires finite logits).
 __device__ __forceinline__ void add8(Online &o, const float (&z)[8]) {
-    float mx = z[0];
-#pragma unroll
-    for (int i = 1; i < 8; ++i) mx = mx > z[i] ? mx : z[i];
+    const float mx = __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(z[0], z[1]), __builtin_fmaxf(z[2], z[3])),
+                                     __builtin_fmaxf(__builtin_fmaxf(z[4], z[5]), __builtin_fmaxf(z[6], z[7])));
     if (mx > o.m) {
+        const float mxb = mx * kLog2e;
         if (o.S != 0.0f) {
-            const float d = o.m - mx;
-            const float f = exp_fast(d);
+            const float d = o.mb - mxb;
+            const float f = __builtin_amdgcn_exp2f(d);
             o.A = f * (o.A + d * o.S);
             o.S = f * o.S;
         }
         o.m = mx;
+        o.mb = mxb;
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        const float t = z[i] - o.m;
-        const float e = exp_fast(t);
+        const float t = __builtin_fmaf(z[i], kLog2e, -o.mb);
+        const float e = __builtin_amdgcn_exp2f(t);
         o.S += e;
-        o.A += e * t;
+        o.A = __builtin_fmaf(e, t, o.A);
     }
 }
 
@@ -85,7 +93,7 @@ __global__ __launch_bounds__(kThreads) void sem_rows_kernel(const uint16_t *__re
     const int64_t t = blockIdx.x;
     const uint4 *row = reinterpret_cast<const uint4 *>(logits + t * ld);
     const int64_t nv = V / 8;
-    Online o{-__builtin_inff(), 0.0f, 0.0f};
+    Online o{-__builtin_inff(), -__builtin_inff(), 0.0f, 0.0f};
     int64_t i = threadIdx.x;
     for (; i + 3 * kThreads < nv; i += 4 * kThreads) {
         uint4 v[4];
@@ -106,26 +114,28 @@ __global__ __launch_bounds__(kThreads) void sem_rows_kernel(const uint16_t *__re
     // fixed-order tree: within the wave by xor shuffles, then the four waves in LDS
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
-        Online b{__shfl_xor(o.m, off, 64), __shfl_xor(o.S, off, 64), __shfl_xor(o.A, off, 64)};
+        Online b{__shfl_xor(o.m, off, 64), __shfl_xor(o.mb, off, 64), __shfl_xor(o.S, off, 64),
+                 __shfl_xor(o.A, off, 64)};
         o = merge(o, b);
     }
-    __shared__ float red[3][kThreads / 64];
+    __shared__ float red[4][kThreads / 64];
     if ((threadIdx.x & 63) == 0) {
         red[0][threadIdx.x >> 6] = o.m;
-        red[1][threadIdx.x >> 6] = o.S;
-        red[2][threadIdx.x >> 6] = o.A;
+        red[1][threadIdx.x >> 6] = o.mb;
+        red[2][threadIdx.x >> 6] = o.S;
+        red[3][threadIdx.x >> 6] = o.A;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        Online r{red[0][0], red[1][0], red[2][0]};
-        for (int w = 1; w < kThreads / 64; ++w) r = merge(r, Online{red[0][w], red[1][w], red[2][w]});
-        const float logS = __builtin_amdgcn_logf(r.S) * kLn2;
-        const float lse = r.m + logS;
+        Online r{red[0][0], red[1][0], red[2][0], red[3][0]};
+        for (int w = 1; w < kThreads / 64; ++w) r = merge(r, Online{red[0][w], red[1][w], red[2][w], red[3][w]});
+        const float log2S = __builtin_amdgcn_logf(r.S);
+        const float lse = (r.mb + log2S) * kLn2;
         const int32_t y = targets[t];
         const bool ok = y >= 0 && (int64_t)y < V;  // a target outside [0, V) gives NaN, reads nothing
         const float zy = ok ? f32_from_bits((uint32_t)logits[t * ld + y] << 16) : __builtin_nanf("");
-        stats[4 * t + 0] = logS - r.A / r.S;       // H
-        stats[4 * t + 1] = lse - zy;               // NLL
+        stats[4 * t + 0] = (log2S - r.A / r.S) * kLn2;   // H
+        stats[4 * t + 1] = lse - zy;                      // NLL
         stats[4 * t + 2] = lse;
         stats[4 * t + 3] = 0.0f;
     }
