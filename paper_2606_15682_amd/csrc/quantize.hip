@@ -223,7 +223,7 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
     };
 
     // kGLocal: the first step's blocks are requested together with the amax
-    // pass (the grid gives a wave at most two segments, launched with U = 2,
+    // pass (the grid gives each wave at most one segment, launched with U = 1,
     // so this is the wave's only step): one memory round trip for both.
     uint32_t wfirst[U][B / 2];
     if (GM == kGLocal && s_begin < s_end) load_step(s_begin, wfirst);
@@ -750,8 +750,8 @@ hipError_t launch_fmt_out(GSrc gsrc, bool local, bool deferred, int grid, const 
                           int64_t cols, int64_t ldx, uint8_t *codes, uint8_t *scales, uint16_t *y, int64_t ldy,
                           float *gptr, uint32_t *partials, int nparts, uint16_t *seg_table, hipStream_t stream) {
     constexpr int U = OUT == kCodes ? REQAT_Q_UCODES : OUT == kFakeQuant ? REQAT_Q_UFQ : REQAT_Q_UBOTH;
-    if (FMT == kNV && local)   // two segments per step: one step per wave (see quantize_kernel)
-        return launch_loop<FMT, OUT, kGLocal, 2>(grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr, partials,
+    if (FMT == kNV && local)   // one segment per wave, one step (see quantize_kernel)
+        return launch_loop<FMT, OUT, kGLocal, 1>(grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr, partials,
                                                 nparts, seg_table, stream);
     if (FMT == kNV && deferred)
         return launch_loop<FMT, OUT, kGDeferred, U>(grid, x, rows, cols, ldx, codes, scales, y, ldy, gptr,
@@ -818,6 +818,9 @@ hipError_t launch_quantize(Fmt fmt, QuantOut out, const uint16_t *x, int64_t row
     int64_t grid = (nseg + 4 * kSegPerWave - 1) / (4 * kSegPerWave);
     if (grid > kMaxGroups) grid = kMaxGroups;
     if (grid < 1) grid = 1;
+    // small tensor: one segment per wave (at most 16 workgroups, each reading
+    // all of x for the amax) keeps each wave's chain of block arithmetic short
+    if (local) grid = (nseg + 3) / 4;
     if (deferred) nparts = (int)grid;
     hipError_t e;
     auto run = [&](auto fmt_c, auto out_c) {
