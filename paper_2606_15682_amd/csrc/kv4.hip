@@ -33,6 +33,13 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kMaxKvGroups = kMaxPartials;
+// Workgroups of the quantize kernels (grid-stride beyond): four per CU, so a
+// wave takes several steps.  Each workgroup stages the shift vector in LDS and
+// the one-pass kernel writes one partial maximum per workgroup, which the
+// fix-up folds; on 32768 x 1024 keys this cap took the computed-g quantize
+// from 31.5 to 28.2 us and its fake-quant from 36.9 to 32.0 us (4096 or 512
+// workgroups were slower).
+constexpr int kMaxKvQuantGroups = 1024;
 #ifndef REQAT_KV4_U
 #define REQAT_KV4_U 2
 #endif
@@ -627,7 +634,7 @@ hipError_t launch_kv4(QuantOut out, const uint16_t *x, int64_t rows, int64_t col
     int64_t grid = (total + kThreads - 1) / kThreads;             // absmax pass: one block per lane
     if (grid > kMaxKvGroups) grid = kMaxKvGroups;
     int64_t qgrid = (total + kThreads * kKvU - 1) / (kThreads * kKvU);   // quantize kernels: kKvU per lane
-    if (qgrid > kMaxKvGroups) qgrid = kMaxKvGroups;
+    if (qgrid > kMaxKvQuantGroups) qgrid = kMaxKvQuantGroups;
     const int64_t nseg = (total + 63) / 64;
     const bool deferred = computed && seg_table != nullptr && nseg <= kMaxSegments;
     auto run = [&](auto src_c) {
