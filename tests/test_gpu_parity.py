@@ -730,10 +730,14 @@ def run_gemm_case(fmt, M, N, K, seed, dist="normal", wstd=0.02, g=(None, None), 
                                    (256, 384, 1024), (5, 300, 128), (300, 520, 768),
                                    (257, 256, 2048), (512, 1000, 1280), (48, 100, 1152),
                                    (64, 40, 640), (33, 17, 128), (2, 8960, 1536),
-                                   (100, 96, 384), (200, 130, 1152), (65, 300, 128)])
+                                   (100, 96, 384), (200, 130, 1152), (65, 300, 128),
+                                   (20, 150, 640), (32, 96, 384)])
 def test_gemm_parity(fmt, M, N, K):
     """(100, 96, 384), (200, 130, 1152) and (65, 300, 128): K % 256 == 128 with
-    M > 64, which NVFP4 runs on the 128 x 128 register-staged kernel."""
+    M > 64, which NVFP4 runs on the 128 x 128 register-staged kernel.
+    (20, 150, 640) and (32, 96, 384): two 16-row activation tiles in the
+    decode-shaped product, row-major and packed, with a ragged N and half a
+    256-element chunk at the end of K."""
     log("gemm parity fmt=%d M=%d N=%d K=%d" % (fmt, M, N, K))
     run_gemm_case(fmt, M, N, K, seed=M * 31 + N * 7 + K, dist="student_t")
 
@@ -924,7 +928,8 @@ def test_linear_parity(fmt, M, N, K, given):
 
 
 @pytest.mark.parametrize("fmt", [NV, MX])
-@pytest.mark.parametrize("M,K,given", [(16, 1536, False), (16, 1536, True), (64, 1024, False), (7, 2944, False)])
+@pytest.mark.parametrize("M,K,given", [(16, 1536, False), (16, 1536, True), (64, 1024, False), (7, 2944, False),
+                                       (24, 2048, False)])
 def test_decode_linear_equals_two_launch_path(fmt, M, K, given):
     """The linear call on decode-sized activations: its outputs, the activation
     codes and scales it leaves in its workspace, and g are bitwise those of
