@@ -14,8 +14,9 @@
 // waves read it, so every activation byte read from L2 serves 64 weight rows
 // (reading it per wave, for 16 rows, made the L2 reads four times the weight
 // bytes and capped the rate near 1 TB/s).  With few weight rows the K range
-// is split over more workgroups (>= 1024 in total, at most 12 splits) whose
-// FP32 partial sums a second kernel adds in split order (deterministic).
+// is split over more workgroups (about two per CU, spread evenly, else up to
+// 1024 in total; at most 12 splits) whose FP32 partial sums a second kernel
+// adds in split order (deterministic).
 //
 // The weights come row-major (codes [N][K/2], scales [N][K/32]) or as the
 // packed image of w4a16_pack_kernel: per 16-row group and 128-element chunk,
@@ -350,18 +351,29 @@ hipError_t launch_w4a16_pack(const uint8_t *codes, const uint8_t *scales, int64_
     return hipGetLastError();
 }
 
-// K splits: enough workgroups to cover the chip (REQAT_W16_TARGET) when the
-// weight rows alone give fewer than 256, at most REQAT_W16_KSMAX, and at most
-// one pair of chunks each (splits start at even chunks).
+// K splits, when the weight rows alone give fewer workgroups than CUs: the
+// fewest splits (fewest FP32 partials to add) that give about two workgroups
+// per CU, spread evenly (the average CU has at least 90% of the busiest CU's
+// count, so no CU runs a round alone); when no split count up to
+// REQAT_W16_KSMAX does, enough to reach REQAT_W16_TARGET workgroups.  At most
+// REQAT_W16_KSMAX splits and one pair of chunks each (splits start at even
+// chunks).  On 16 x 5120 x 27648 (80 row groups) the first rule picks 6:
+// 20.3 us against 21.6 for 12 and 24.5 for 4, which leaves a quarter of the
+// CUs with one workgroup more than the rest.  The split depends on the shape
+// alone, never on the device, so results are deterministic.
 int gemm_w4a16_splits(int64_t M, int64_t N, int64_t K) {
+    constexpr int64_t kCUs = 256;
     const int64_t rows = 64 * REQAT_W16_NT;
     const int64_t base = ((N + rows - 1) / rows) * ((M + 16 * row_tile(M) - 1) / (16 * row_tile(M)));
     const int64_t npair = K / 256;
-    if (base >= 256 || npair <= 1) return 1;
+    if (base >= kCUs || npair <= 1) return 1;
+    const int64_t kmax = REQAT_W16_KSMAX < npair ? REQAT_W16_KSMAX : npair;
+    for (int64_t ks = 2; ks <= kmax; ++ks) {
+        const int64_t wg = base * ks, busiest = (wg + kCUs - 1) / kCUs;
+        if (10 * wg >= 18 * kCUs && 10 * wg >= 9 * busiest * kCUs) return (int)ks;
+    }
     int64_t ks = (REQAT_W16_TARGET + base - 1) / base;
-    if (ks > REQAT_W16_KSMAX) ks = REQAT_W16_KSMAX;
-    if (ks > npair) ks = npair;
-    return (int)ks;
+    return (int)(ks < kmax ? ks : kmax);
 }
 
 size_t gemm_w4a16_workspace_bytes(int64_t M, int64_t N, int64_t K) {
