@@ -183,8 +183,12 @@ def test_rotated_quantize_validation(lib):
 def test_w4a16_validation(lib):
     g16 = lambda M=4, N=8, K=128, x=P, ldx=128, wc=P, ws=P, y=P, dt=0, ldy=8, wk=None: reqat.reqat_gemm_w4a16(
         M, N, K, x, ldx, wc, ws, y, dt, ldy, wk, None)
-    # 80 weight tiles of 64 rows in a 16 x 5120 x 27648 product: K split 12 ways (FP32 partials)
-    assert reqat.reqat_w4a16_workspace_bytes(16, 5120, 27648) == 4 * 12 * 16 * 5120
+    # K splits (FP32 partials): the fewest that give about two workgroups per CU,
+    # spread evenly (80 weight tiles of 64 rows: 6 ways, 480 workgroups; 64 tiles:
+    # 8 ways, 512), else enough for 1024 workgroups (10 tiles: 12 ways, the cap)
+    assert reqat.reqat_w4a16_workspace_bytes(16, 5120, 27648) == 4 * 6 * 16 * 5120
+    assert reqat.reqat_w4a16_workspace_bytes(32, 4096, 8192) == 4 * 8 * 32 * 4096
+    assert reqat.reqat_w4a16_workspace_bytes(16, 640, 4096) == 4 * 12 * 16 * 640
     assert reqat.reqat_w4a16_workspace_bytes(16, 27648, 5120) == 0
     assert reqat.reqat_w4a16_workspace_bytes(4, 8, 128) == 0          # a single chunk: no split
     assert reqat.reqat_w4a16_workspace_bytes(4, 8, 100) == 0
