@@ -884,6 +884,34 @@ def test_gemm_k_zero_writes_zeros():
     torch.cuda.synchronize()
     assert torch.all(y == 0).item()
 
+def test_packed_decode_edge_cases():
+    """The packed decode calls at the edges: K = 0 writes zeros (no operand is
+    read), M = 0 with a computed activation scale writes g = 1, N = 0 leaves
+    the output alone."""
+    log("packed decode edge cases")
+    stream = torch.cuda.current_stream().cuda_stream
+    z = torch.zeros(16, dtype=torch.uint8, device=DEV)
+    y = torch.full((4, 8), float("nan"), dtype=torch.float32, device=DEV)
+    assert reqat.reqat_gemm_w4a4_packed(MX, 4, 8, 0, z.data_ptr(), z.data_ptr(), None, z.data_ptr(), None,
+                                        y.data_ptr(), reqat.DT_F32, 8, stream) == 0
+    torch.cuda.synchronize()
+    assert torch.all(y == 0).item()
+    one = torch.ones(1, dtype=torch.float32, device=DEV)
+    g = torch.full((1,), float("nan"), dtype=torch.float32, device=DEV)
+    x = torch.zeros(16, dtype=torch.bfloat16, device=DEV)
+    ws = torch.zeros(256, dtype=torch.uint8, device=DEV)
+    assert reqat.reqat_linear_w4a4_packed(NV, 0, 8, 128, x.data_ptr(), 128, g.data_ptr(), reqat.TS_COMPUTE,
+                                          z.data_ptr(), one.data_ptr(), y.data_ptr(), reqat.DT_F32, 8,
+                                          ws.data_ptr(), stream) == 0
+    torch.cuda.synchronize()
+    assert float(g.cpu()[0]) == 1.0
+    y.fill_(float("nan"))
+    assert reqat.reqat_linear_w4a4_packed(NV, 4, 0, 128, x.data_ptr(), 128, g.data_ptr(), reqat.TS_GIVEN,
+                                          z.data_ptr(), one.data_ptr(), y.data_ptr(), reqat.DT_F32, 8,
+                                          ws.data_ptr(), stream) == 0
+    torch.cuda.synchronize()
+    assert torch.isnan(y).all().item()
+
 # ------------------------------------------------------------------ linear (quantize X + GEMM)
 
 @pytest.mark.parametrize("fmt", [NV, MX])
