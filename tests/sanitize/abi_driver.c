@@ -79,6 +79,37 @@ int main(void)
     EXPECT(reqat_linear_w4a4_noalloc(NV, 1 << 20, 8, 5120, P, 5120, F, REQAT_TS_COMPUTE, U, U, F, P, REQAT_DT_F32,
                                      8, 0),
            REQAT_E_TOO_LARGE);
+    /* packed weight images: sizes, and every rejection before a launch (overlap included) */
+    if (reqat_w4a16_packed_bytes(17, 256) != 2 * 2 * 1088 || reqat_w4a16_packed_bytes(16, 100) != 0) ++fails;
+    if (reqat_w4a4_packed_bytes(NV, 8960, 1536) != (size_t)560 * 6 * 2304 ||
+        reqat_w4a4_packed_bytes(MX, 17, 384) != (size_t)2 * 2 * 2176 ||
+        reqat_w4a4_packed_bytes((reqat_format)7, 16, 128) != 0 || reqat_w4a4_packed_bytes(NV, -1, 128) != 0)
+        ++fails;
+    EXPECT(reqat_pack_w4a16(U, U, 8, 96, P, 0), REQAT_E_SHAPE);
+    EXPECT(reqat_pack_w4a16(0, U, 8, 128, P, 0), REQAT_E_NULL);
+    EXPECT(reqat_pack_w4a16(U, U + 2, 8, 128, U + 4096, 0), REQAT_E_ALIGN);
+    EXPECT(reqat_pack_w4a16(U, U + 4096, 8, 128, U + 256, 0), REQAT_E_UNSUPPORTED);
+    EXPECT(reqat_gemm_w4a16_packed(4, 8, 128, P, 128, 0, P, REQAT_DT_F32, 8, 0, 0), REQAT_E_NULL);
+    EXPECT(reqat_pack_w4a4((reqat_format)7, U, U, 8, 128, P, 0), REQAT_E_ENUM);
+    EXPECT(reqat_pack_w4a4(NV, U, U, 8, 96, P, 0), REQAT_E_SHAPE);
+    EXPECT(reqat_pack_w4a4(NV, U, 0, 8, 128, P, 0), REQAT_E_NULL);
+    EXPECT(reqat_pack_w4a4(NV, U, U + 8, 8, 128, U + 8192, 0), REQAT_E_ALIGN);
+    EXPECT(reqat_pack_w4a4(NV, U, U + 8192, 8, 128, U + 256, 0), REQAT_E_UNSUPPORTED);
+    EXPECT(reqat_pack_w4a4(MX, U + 8192, U, 8, 128, U + 16, 0), REQAT_E_UNSUPPORTED);
+    EXPECT(reqat_gemm_w4a4_packed(NV, 65, 8, 128, U, U, F, P, F, P, REQAT_DT_F32, 8, 0), REQAT_E_UNSUPPORTED);
+    EXPECT(reqat_gemm_w4a4_packed(MX, 4, 8, 128, U, U, F, P, 0, P, REQAT_DT_F32, 8, 0), REQAT_E_UNSUPPORTED);
+    EXPECT(reqat_gemm_w4a4_packed(NV, 4, 8, 128, U, U, F, 0, F, P, REQAT_DT_F32, 8, 0), REQAT_E_NULL);
+    EXPECT(reqat_gemm_w4a4_packed(NV, 4, 8, 128, U, U, F, U + 8, F, P, REQAT_DT_F32, 8, 0), REQAT_E_ALIGN);
+    EXPECT(reqat_gemm_w4a4_packed(NV, 4, 8, 128, U, U, F, P, F, P, REQAT_DT_F32, 4, 0), REQAT_E_SHAPE);
+    EXPECT(reqat_linear_w4a4_packed(NV, 65, 8, 128, P, 128, F, REQAT_TS_GIVEN, P, F, P, REQAT_DT_F32, 8, P, 0),
+           REQAT_E_UNSUPPORTED);
+    EXPECT(reqat_linear_w4a4_packed(NV, 4, 8, 128, P, 128, F, REQAT_TS_GIVEN, P, F, P, REQAT_DT_F32, 8, 0, 0),
+           REQAT_E_NULL);
+    EXPECT(reqat_linear_w4a4_packed(NV, 4, 8, 128, P, 128, F, REQAT_TS_GIVEN, P, F, P, REQAT_DT_F32, 8,
+                                    (char *)P + 16, 0),
+           REQAT_E_ALIGN);
+    EXPECT(reqat_linear_w4a4_packed(NV, 4, 8, 128, P, 128, F, (reqat_tscale_mode)3, P, F, P, REQAT_DT_F32, 8, P, 0),
+           REQAT_E_ENUM);
     if (fails) {
         printf("%d failures\n", fails);
         return 1;
